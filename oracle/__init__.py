@@ -1,0 +1,21 @@
+"""Plain, slow, float64 CPU oracle of the Flow-GRPO SDE rollout of a flow-matching DiT.
+
+TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the benchmark's
+CPU-baseline leg may import or call anything here.  The product path (the HIP
+library and its Python binding) never imports this package, and this package
+imports nothing from the product: the two share no code.  The only common
+ground is the seeded input generator, which holds none of the method's
+arithmetic; every function here receives plain numpy arrays.
+
+Modules:
+  sde        -- time grid, sigma schedules (Table 1), the SDE / ODE step (Eq. 1)
+                and the Gaussian transition log-probability (Sec. 3.1)
+  advantage  -- group-normalised advantages, weighted-sum and GDPO-style
+                multi-reward aggregation (Sec. 2.3)
+  dit        -- the DiT velocity field v_theta(x_t, c, t): norms, modulation,
+                RoPE, plain-softmax attention, dual-stream, single-stream and
+                WAN blocks, embedders, final layer
+  rollout    -- the K-step rollout loop with mixed ODE/SDE steps (Sec. 3.1,
+                MixGRPO), per-step log-probs and final advantages
+"""
+from . import advantage, dit, rollout, sde  # noqa: F401
