@@ -1,0 +1,75 @@
+/*
+ * ff_ops.h -- kernel-level entry points of libff.so.
+ *
+ * These expose the building blocks that ff_dit_forward composes, so each can
+ * be checked and timed on its own at full shape.  Conventions (ownership,
+ * asynchrony on `stream`, host-side validation, status codes, ff_last_error)
+ * are those of ff.h.  All tensors are device memory, row-major, of `dtype`
+ * (FF_F32 or FF_BF16) unless stated otherwise.
+ */
+#ifndef FF_OPS_H
+#define FF_OPS_H
+
+#include "ff.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { FF_EPI_BIAS = 0, FF_EPI_GELU = 1, FF_EPI_GATED = 2 };
+
+/* Linear layer out = epi(A W^T + bias) of the DiT blocks.
+ *   A [M, K] (row stride lda), W [N, K] (nn.Linear layout, row stride K),
+ *   bias [N] or NULL, out [M, N] (row stride ldo).
+ *   FF_EPI_BIAS:  out = A W^T + bias
+ *   FF_EPI_GELU:  out = GELU_tanh(A W^T + bias) on columns >= gelu_from
+ *                 (earlier columns get A W^T + bias)
+ *   FF_EPI_GATED: out = resid + gate[m / rows_per_sample] * (A W^T + bias), the
+ *                 adaLN-gated residual; gate float32 [*, gate_ld], resid
+ *                 [M, N] (row stride ldr) may alias out.
+ * Accumulation is float32.  bf16 requires K % 64 == 0 and lda, ldo, ldr % 8 == 0. */
+int ff_linear(const void* A, int64_t lda, const void* W, const void* bias, void* out, int64_t ldo,
+              int64_t M, int64_t N, int64_t K, int32_t epi, int64_t gelu_from, const float* gate,
+              int64_t gate_ld, const void* resid, int64_t ldr, int64_t rows_per_sample, int32_t dtype,
+              void* stream);
+
+/* Attention O = softmax(Q K^T / sqrt(d)) V, no mask.
+ *   Q [B, heads, n_q, d], K [B, heads, n_kv, d];
+ *   V: bf16 takes V transposed, [B, heads, d, n_kv]; f32 takes [B, heads, n_kv, d].
+ *   out [B, n_q, heads*d] (token-major, heads concatenated).
+ * bf16: d == 128, n_kv % 8 == 0.  f32: d <= 64. */
+int ff_attention(const void* Q, const void* K, const void* V, void* out, int64_t B, int64_t heads,
+                 int64_t n_q, int64_t n_kv, int64_t head_dim, int32_t dtype, void* stream);
+
+/* y = Norm(x) (1 + scale[b]) + shift[b] per row, b = row / rows_per_sample.
+ * x, y [rows, H]; shift, scale float32 rows of stride mod_ld (either may be NULL);
+ * norm_kind FF_NORM_RMS or FF_NORM_LN (no affine), statistics in float32. */
+int ff_norm_modulate(const void* x, void* y, int64_t rows, int64_t H, const float* shift,
+                     const float* scale, int64_t mod_ld, int64_t rows_per_sample, int32_t norm_kind,
+                     float eps, int32_t dtype, void* stream);
+
+/* Per-head RMSNorm (weights q_w, k_w of [d]) and RoPE of one token stream, with
+ * relayout into the joint attention layout.
+ *   qkv [B, n_tok, 3*heads*d] (Q | K | V per row);
+ *   rope: float32 pairs [n_tok, d/2, 2] = (cos, sin), or NULL for no rotation;
+ *   Q, K out [B, heads, n_joint, d] at token offset tok_offset;
+ *   V out transposed [B, heads, d, n_joint] (bf16) or [B, heads, n_joint, d] (f32). */
+int ff_qk_norm_rope(const void* qkv, int64_t B, int64_t n_tok, int64_t heads, int64_t head_dim,
+                    const void* q_w, const void* k_w, float eps, const float* rope, void* Q, void* K,
+                    void* V, int64_t n_joint, int64_t tok_offset, int32_t dtype, void* stream);
+
+/* RoPE (cos, sin) table for a (frames, rows, cols) grid: out float32 [N, d/2, 2],
+ * pair i of band a turning by pos_a * theta^(-2i/axes[a]) (float64 math). */
+int ff_rope_table(float* out, const int32_t grid[3], int32_t head_dim, const int32_t axes[3],
+                  double theta, void* stream);
+
+/* out[b, n] = act_out(sum_k W[n,k] act_in(in[b,k]) + bias[n]) for skinny batches
+ * (the adaLN modulation and embedding MLPs).  in float32 [B, K], out float32
+ * [B, N], W of dtype [N, K]; act: 0 none, 1 SiLU, 2 GELU_tanh. */
+int ff_skinny_linear(const float* in, const void* W, const void* bias, float* out, int64_t B, int64_t N,
+                     int64_t K, int32_t act_in, int32_t act_out, int32_t dtype, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FF_OPS_H */

@@ -1,0 +1,290 @@
+// Joint (text + image) attention O = softmax(Q K^T / sqrt(d)) V, non-causal.
+//
+// bf16, d = 128: a flash-style kernel with online softmax in float32.  Each
+// wave owns 32 queries; a workgroup of WAVES waves shares 64-key tiles of K
+// and V^T staged through LDS (double-buffered, the next tile's global loads in
+// flight during the current tile's math).  Both products are computed
+// transposed on MFMA 32x32x16:
+//   S^T (keys x queries) = K Q^T        A = K rows (LDS), B = Q (registers)
+//   O^T (d x queries)   += V^T P^T      A = V^T rows (LDS), B = P (registers)
+// so a lane always holds one query (lane % 32): the running max, the running
+// sum and the rescale of O are lane-local, and the only cross-lane step per
+// tile is one exchange of the row max between the two lane halves.
+// K rows are fed to the first MFMA in an order that swaps bits 2 and 3 of the
+// row index; with it, the 8 scores a lane holds for a 16-key slice are keys
+// 16s + 8(lane/32) + 0..7 in order, exactly the B-operand slots of the second
+// MFMA, so P goes from accumulators to operands without any shuffle.
+//
+// float32 (any d <= 64): one thread per query with the same online softmax,
+// for the small float32 configuration.
+#include <cmath>
+
+#include "dev.h"
+#include "ff_internal.h"
+
+namespace ff {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+struct AttnParams {
+  int64_t B, heads, n_q, n_kv;
+  const bf16_t* Q; const bf16_t* K; const bf16_t* Vt;
+  bf16_t* out0; bf16_t* out1; int64_t split; int64_t ldo;
+  float scale_log2;
+};
+
+constexpr int D = 128;
+constexpr int KT = 64;                   // keys per tile
+constexpr int K_STAGE = KT * D * 2;      // bytes of one K tile (64 rows x 256 B)
+constexpr int V_STAGE = D * KT * 2;      // bytes of one V^T tile (128 rows x 128 B)
+
+// LDS position of 16-byte chunk c of K row r (16 chunks per 256-byte row).
+__device__ __forceinline__ int k_off(int r, int c) {
+  const int f = (r & 3) | ((r >> 1) & 4);
+  return r * 256 + ((c ^ f) << 4);
+}
+// LDS position of 16-byte chunk c of V^T row r (8 chunks per 128-byte row).
+__device__ __forceinline__ int v_off(int r, int c) { return r * 128 + ((c ^ (r & 7)) << 4); }
+
+template <int WAVES>
+__global__ __launch_bounds__(WAVES * 64, 2) void attn_bf16_d128(AttnParams p) {
+  constexpr int THREADS = WAVES * 64;
+  constexpr int K_LOADS = KT * 16 / THREADS;   // 16-byte chunks per thread per K tile
+  constexpr int V_LOADS = D * 8 / THREADS;
+  __shared__ __attribute__((aligned(16))) char smem[2 * (K_STAGE + V_STAGE)];
+
+  // Workgroup -> (query tile, batch*head): ids are regrouped so the query
+  // tiles of one (b, h) run on one XCD and share its L2.
+  const int64_t nqt = (p.n_q + 32 * WAVES - 1) / (32 * WAVES);
+  const int64_t total = nqt * p.B * p.heads;
+  const int64_t pid = blockIdx.x;
+  const int64_t full = total / 8 * 8;
+  const int64_t lid = pid < full ? (pid % 8) * (full / 8) + pid / 8 : pid;
+  const int64_t qt = lid % nqt, bh = lid / nqt;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int ql = lane & 31, g = lane >> 5;
+  const int64_t q0 = qt * 32 * WAVES + wave * 32;
+
+  const bf16_t* Kb = p.K + bh * p.n_kv * D;
+  const bf16_t* Vb = p.Vt + bh * D * p.n_kv;
+
+  // Q fragments: query q0 + ql, d slots 16t + 8g .. +7.
+  bf16x8_t qf[8];
+  {
+    int64_t q = q0 + ql;
+    if (q >= p.n_q) q = p.n_q - 1;
+    const bf16_t* qp = p.Q + (bh * p.n_q + q) * D + 8 * g;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) qf[t] = *reinterpret_cast<const bf16x8_t*>(qp + 16 * t);
+  }
+
+  uint4 rk[K_LOADS], rv[V_LOADS];
+  auto load_tile = [&](int64_t kv0) {
+#pragma unroll
+    for (int i = 0; i < K_LOADS; ++i) {
+      const int e = tid + i * THREADS;
+      const int r = e >> 4, c = e & 15;
+      int64_t key = kv0 + r;
+      if (key >= p.n_kv) key = p.n_kv - 1;
+      rk[i] = *reinterpret_cast<const uint4*>(Kb + key * D + c * 8);
+    }
+#pragma unroll
+    for (int i = 0; i < V_LOADS; ++i) {
+      const int e = tid + i * THREADS;
+      const int r = e >> 3, c = e & 7;
+      const int64_t col = kv0 + c * 8;
+      if (col < p.n_kv) rv[i] = *reinterpret_cast<const uint4*>(Vb + r * p.n_kv + col);
+      else rv[i] = make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+  auto store_tile = [&](int buf) {
+    char* Ks = smem + buf * (K_STAGE + V_STAGE);
+    char* Vs = Ks + K_STAGE;
+#pragma unroll
+    for (int i = 0; i < K_LOADS; ++i) {
+      const int e = tid + i * THREADS;
+      *reinterpret_cast<uint4*>(Ks + k_off(e >> 4, e & 15)) = rk[i];
+    }
+#pragma unroll
+    for (int i = 0; i < V_LOADS; ++i) {
+      const int e = tid + i * THREADS;
+      *reinterpret_cast<uint4*>(Vs + v_off(e >> 3, e & 7)) = rv[i];
+    }
+  };
+
+  f32x16_t o[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[i][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  // Row of K fed to MFMA row rho: bits 2 and 3 swapped.
+  const int krow = (ql & ~12) | ((ql & 4) << 1) | ((ql & 8) >> 1);
+
+  const int64_t ntiles = (p.n_kv + KT - 1) / KT;
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+
+  for (int64_t it = 0; it < ntiles; ++it) {
+    const int buf = it & 1;
+    const int64_t kv0 = it * KT;
+    if (it + 1 < ntiles) load_tile(kv0 + KT);
+    const char* Ks = smem + buf * (K_STAGE + V_STAGE);
+    const char* Vs = Ks + K_STAGE;
+
+    f32x16_t s[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(Ks + k_off(32 * kb + krow, 2 * t + g));
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[t], s[kb], 0, 0, 0);
+      }
+
+    // s[kb][8u + j] is the score of key kv0 + 32kb + 16u + 8g + j for query q0 + ql.
+    float mx = -INFINITY;
+    const bool tail = kv0 + KT > p.n_kv;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float v = s[kb][r] * p.scale_log2;
+        if (tail) {
+          const int64_t key = kv0 + 32 * kb + 16 * (r >> 3) + 8 * g + (r & 7);
+          if (key >= p.n_kv) v = -INFINITY;
+        }
+        s[kb][r] = v;
+        mx = fmaxf(mx, v);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = exp2f(m_run - m_new);
+    m_run = m_new;
+    float lsum = 0.f;
+    bf16x8_t pf[4];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float e = exp2f(s[kb][8 * u + j] - m_new);
+          lsum += e;
+          pf[2 * kb + u][j] = static_cast<__bf16>(e);
+        }
+    l_run = l_run * alpha + lsum;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
+
+#pragma unroll
+    for (int sl = 0; sl < 4; ++sl)
+#pragma unroll
+      for (int db = 0; db < 4; ++db) {
+        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(Vs + v_off(32 * db + ql, 2 * sl + g));
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[sl], o[db], 0, 0, 0);
+      }
+
+    if (it + 1 < ntiles) store_tile(buf ^ 1);
+    __syncthreads();
+  }
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const float inv = 1.0f / l_tot;
+  const int64_t q = q0 + ql;
+  if (q >= p.n_q) return;
+  const int64_t b = bh / p.heads, h = bh % p.heads;
+  bf16_t* row;
+  if (q < p.split) row = p.out0 + (b * p.split + q) * p.ldo;
+  else row = p.out1 + (b * (p.n_q - p.split) + (q - p.split)) * p.ldo;
+  row += h * D;
+  // o[db][4u + j] is O[q, 32db + 8u + 4g + j].
+#pragma unroll
+  for (int db = 0; db < 4; ++db)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      uint2 w;
+      w.x = uint32_t(f2bf(o[db][4 * u] * inv)) | (uint32_t(f2bf(o[db][4 * u + 1] * inv)) << 16);
+      w.y = uint32_t(f2bf(o[db][4 * u + 2] * inv)) | (uint32_t(f2bf(o[db][4 * u + 3] * inv)) << 16);
+      *reinterpret_cast<uint2*>(row + 32 * db + 8 * u + 4 * g) = w;
+    }
+}
+
+// ------------------------------------------------------------------ float32
+struct AttnF32Params {
+  int64_t B, heads, n_q, n_kv, d;
+  const float* Q; const float* K; const float* V;   // V not transposed: [B, h, n_kv, d]
+  float* out0; float* out1; int64_t split; int64_t ldo;
+  float scale;
+};
+
+__global__ __launch_bounds__(64) void attn_f32_kernel(AttnF32Params p) {
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * 64 + threadIdx.x;
+  const int64_t bh = blockIdx.y;
+  if (q >= p.n_q) return;
+  constexpr int MAXD = 64;
+  float qv[MAXD], acc[MAXD];
+  const int d = static_cast<int>(p.d);
+  const float* qp = p.Q + (bh * p.n_q + q) * d;
+  for (int i = 0; i < d; ++i) { qv[i] = qp[i]; acc[i] = 0.f; }
+  float m = -INFINITY, l = 0.f;
+  for (int64_t k = 0; k < p.n_kv; ++k) {
+    const float* kp = p.K + (bh * p.n_kv + k) * d;
+    float sc = 0.f;
+    for (int i = 0; i < d; ++i) sc = fmaf(qv[i], kp[i], sc);
+    sc *= p.scale;
+    const float mn = fmaxf(m, sc);
+    const float alpha = expf(m - mn), e = expf(sc - mn);
+    l = l * alpha + e;
+    const float* vp = p.V + (bh * p.n_kv + k) * d;
+    for (int i = 0; i < d; ++i) acc[i] = fmaf(e, vp[i], acc[i] * alpha);
+    m = mn;
+  }
+  const int64_t b = bh / p.heads, h = bh % p.heads;
+  float* row = q < p.split ? p.out0 + (b * p.split + q) * p.ldo
+                           : p.out1 + (b * (p.n_q - p.split) + (q - p.split)) * p.ldo;
+  row += h * d;
+  for (int i = 0; i < d; ++i) row[i] = acc[i] / l;
+}
+
+}  // namespace
+
+int attention(const AttnArgs& a, hipStream_t s) {
+  if (a.B == 0 || a.n_q == 0) return FF_OK;
+  const double flops = 4.0 * a.B * a.heads * static_cast<double>(a.n_q) * a.n_kv * a.d;
+  const double esz = static_cast<double>(dtype_size(a.dtype));
+  const double bytes = esz * a.B * a.heads * a.d * (2.0 * a.n_q + 2.0 * a.n_kv);
+  if (a.dtype == FF_BF16) {
+    if (a.d != D) return fail(FF_EUNSUPPORTED, "attention: bf16 head_dim %lld (128 required)", (long long)a.d);
+    if (a.n_kv % 8 != 0) return fail(FF_EUNSUPPORTED, "attention: bf16 n_kv=%lld must be a multiple of 8", (long long)a.n_kv);
+    AttnParams p{a.B, a.heads, a.n_q, a.n_kv,
+                 static_cast<const bf16_t*>(a.Q), static_cast<const bf16_t*>(a.K), static_cast<const bf16_t*>(a.Vt),
+                 static_cast<bf16_t*>(a.out0), static_cast<bf16_t*>(a.out1), a.split, a.ldo,
+                 static_cast<float>(a.scale * 1.4426950408889634)};
+    constexpr int WAVES = 4;
+    const int64_t tiles = (a.n_q + 32 * WAVES - 1) / (32 * WAVES) * a.B * a.heads;
+    LaunchScope ls("attn_bf16_d128", s, flops, bytes);
+    hipLaunchKernelGGL(attn_bf16_d128<WAVES>, dim3(static_cast<unsigned>(tiles)), dim3(WAVES * 64), 0, s, p);
+    return ls.status();
+  }
+  if (a.d > 64) return fail(FF_EUNSUPPORTED, "attention: f32 head_dim %lld > 64", (long long)a.d);
+  AttnF32Params p{a.B, a.heads, a.n_q, a.n_kv, a.d,
+                  static_cast<const float*>(a.Q), static_cast<const float*>(a.K), static_cast<const float*>(a.Vt),
+                  static_cast<float*>(a.out0), static_cast<float*>(a.out1), a.split, a.ldo, a.scale};
+  LaunchScope ls("attn_f32", s, flops, bytes);
+  hipLaunchKernelGGL(attn_f32_kernel, dim3(static_cast<unsigned>((a.n_q + 63) / 64), static_cast<unsigned>(a.B * a.heads)),
+                     dim3(64), 0, s, p);
+  return ls.status();
+}
+
+}  // namespace ff

@@ -1,0 +1,100 @@
+// Device-side helpers shared by the kernels: bf16 conversion, vector loads, reductions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace ff {
+
+typedef uint16_t bf16_t;   // bfloat16 storage word
+
+__device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float(uint32_t(h) << 16); }
+
+// Round to nearest, ties to even; NaN stays NaN.
+__device__ __forceinline__ bf16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return bf16_t((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return bf16_t(u >> 16);
+}
+
+// Scalar load/store of a dtype element as float.
+template <bool BF16>
+__device__ __forceinline__ float ld1(const void* p, int64_t i) {
+  if constexpr (BF16) return bf2f(static_cast<const bf16_t*>(p)[i]);
+  else return static_cast<const float*>(p)[i];
+}
+template <bool BF16>
+__device__ __forceinline__ void st1(void* p, int64_t i, float v) {
+  if constexpr (BF16) static_cast<bf16_t*>(p)[i] = f2bf(v);
+  else static_cast<float*>(p)[i] = v;
+}
+// Value after rounding to the storage dtype.
+template <bool BF16>
+__device__ __forceinline__ float round_dt(float v) {
+  if constexpr (BF16) return bf2f(f2bf(v));
+  else return v;
+}
+
+// 8 consecutive elements (16 bytes of bf16 or 32 bytes of f32) as floats.
+template <bool BF16>
+__device__ __forceinline__ void ld8(const void* p, int64_t i, float (&o)[8]) {
+  if constexpr (BF16) {
+    uint4 u = *reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(p) + i);
+    uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      o[2 * j] = __uint_as_float(w[j] << 16);
+      o[2 * j + 1] = __uint_as_float(w[j] & 0xffff0000u);
+    }
+  } else {
+    const float4* q = reinterpret_cast<const float4*>(static_cast<const float*>(p) + i);
+    float4 a = q[0], b = q[1];
+    o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
+    o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+  }
+}
+template <bool BF16>
+__device__ __forceinline__ void st8(void* p, int64_t i, const float (&v)[8]) {
+  if constexpr (BF16) {
+    uint4 u;
+    u.x = uint32_t(f2bf(v[0])) | (uint32_t(f2bf(v[1])) << 16);
+    u.y = uint32_t(f2bf(v[2])) | (uint32_t(f2bf(v[3])) << 16);
+    u.z = uint32_t(f2bf(v[4])) | (uint32_t(f2bf(v[5])) << 16);
+    u.w = uint32_t(f2bf(v[6])) | (uint32_t(f2bf(v[7])) << 16);
+    *reinterpret_cast<uint4*>(static_cast<bf16_t*>(p) + i) = u;
+  } else {
+    float4* q = reinterpret_cast<float4*>(static_cast<float*>(p) + i);
+    q[0] = make_float4(v[0], v[1], v[2], v[3]);
+    q[1] = make_float4(v[4], v[5], v[6], v[7]);
+  }
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+__device__ __forceinline__ float silu_f(float x) { return x / (1.0f + __expf(-x)); }
+
+// GELU, tanh approximation, with tanh(u) = 1 - 2 / (exp(2u) + 1).
+__device__ __forceinline__ float gelu_tanh_f(float x) {
+  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
+  float u = k0 * fmaf(0.044715f * x, x * x, x);
+  float t = 1.0f - 2.0f / (__expf(2.0f * u) + 1.0f);
+  return 0.5f * x * (1.0f + t);
+}
+
+}  // namespace ff

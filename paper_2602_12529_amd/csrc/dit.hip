@@ -1,0 +1,559 @@
+// DiT velocity forward v_theta(x_t, c, t): model handle, parameter table,
+// workspace plan and the launch sequence of the dual-stream, single-stream and
+// WAN blocks (block structure as documented in include/ff.h).
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "ff_internal.h"
+
+using namespace ff;
+
+namespace {
+
+struct TensorSpec {
+  std::string name;
+  int64_t s0, s1;   // s1 = 0 for 1-D
+};
+
+void lin(std::vector<TensorSpec>& t, const std::string& p, int64_t out, int64_t in) {
+  t.push_back({p + ".w", out, in});
+  t.push_back({p + ".b", out, 0});
+}
+
+std::vector<TensorSpec> tensor_table(const ff_dit_config& c) {
+  std::vector<TensorSpec> t;
+  const int64_t H = c.hidden, F = c.mlp_hidden, d = c.head_dim;
+  const bool latent = c.io_mode == FF_IO_LATENT;
+  if (c.model == FF_MODEL_MMDIT) {
+    if (latent) {
+      lin(t, "temb.fc1", H, 256);
+      lin(t, "temb.fc2", H, H);
+      if (c.pooled_dim) {
+        lin(t, "pooled.fc1", H, c.pooled_dim);
+        lin(t, "pooled.fc2", H, H);
+      }
+      lin(t, "x_in", H, c.in_channels);
+      lin(t, "txt_in", H, c.txt_dim);
+    }
+    for (int i = 0; i < c.n_dual; ++i)
+      for (const char* s : {"img", "txt"}) {
+        std::string p = "dual." + std::to_string(i) + "." + s + ".";
+        lin(t, p + "mod", 6 * H, H);
+        lin(t, p + "qkv", 3 * H, H);
+        t.push_back({p + "q_norm.w", d, 0});
+        t.push_back({p + "k_norm.w", d, 0});
+        lin(t, p + "o", H, H);
+        lin(t, p + "mlp1", F, H);
+        lin(t, p + "mlp2", H, F);
+      }
+    for (int j = 0; j < c.n_single; ++j) {
+      std::string p = "single." + std::to_string(j) + ".";
+      lin(t, p + "mod", 3 * H, H);
+      lin(t, p + "lin1", 3 * H + F, H);
+      t.push_back({p + "q_norm.w", d, 0});
+      t.push_back({p + "k_norm.w", d, 0});
+      lin(t, p + "lin2", H, H + F);
+    }
+    if (latent) {
+      lin(t, "final.mod", 2 * H, H);
+      lin(t, "final.proj", c.in_channels, H);
+    }
+  } else {
+    if (latent) {
+      lin(t, "temb.fc1", H, 256);
+      lin(t, "temb.fc2", H, H);
+      lin(t, "temb.proj", 6 * H, H);
+      lin(t, "x_in", H, c.in_channels);
+      lin(t, "txt_in.fc1", H, c.txt_dim);
+      lin(t, "txt_in.fc2", H, H);
+    }
+    for (int i = 0; i < c.n_wan; ++i) {
+      std::string p = "wan." + std::to_string(i) + ".";
+      t.push_back({p + "mod", 6, H});
+      lin(t, p + "sa.qkv", 3 * H, H);
+      t.push_back({p + "sa.q_norm.w", H, 0});
+      t.push_back({p + "sa.k_norm.w", H, 0});
+      lin(t, p + "sa.o", H, H);
+      t.push_back({p + "ca.norm.w", H, 0});
+      t.push_back({p + "ca.norm.b", H, 0});
+      lin(t, p + "ca.q", H, H);
+      lin(t, p + "ca.kv", 2 * H, H);
+      t.push_back({p + "ca.q_norm.w", H, 0});
+      t.push_back({p + "ca.k_norm.w", H, 0});
+      lin(t, p + "ca.o", H, H);
+      lin(t, p + "ffn1", F, H);
+      lin(t, p + "ffn2", H, F);
+    }
+    if (latent) {
+      lin(t, "final.mod", 2 * H, H);
+      lin(t, "final.proj", c.in_channels, H);
+    }
+  }
+  return t;
+}
+
+int check_config(const ff_dit_config* c) {
+  if (!c) return fail(FF_EINVAL, "ff_dit: null config");
+  if (c->model != FF_MODEL_MMDIT && c->model != FF_MODEL_WAN) return fail(FF_EINVAL, "ff_dit: bad model %d", c->model);
+  if (c->io_mode != FF_IO_LATENT && c->io_mode != FF_IO_HIDDEN) return fail(FF_EINVAL, "ff_dit: bad io_mode %d", c->io_mode);
+  if (c->dtype != FF_F32 && c->dtype != FF_BF16) return fail(FF_EINVAL, "ff_dit: bad dtype %d", c->dtype);
+  if (c->n_dual < 0 || c->n_single < 0 || c->n_wan < 0) return fail(FF_EINVAL, "ff_dit: negative block count");
+  if (c->hidden <= 0 || c->heads <= 0 || c->head_dim <= 0 || c->mlp_hidden <= 0)
+    return fail(FF_EINVAL, "ff_dit: non-positive size");
+  if (static_cast<int64_t>(c->heads) * c->head_dim != c->hidden)
+    return fail(FF_EINVAL, "ff_dit: hidden %d != heads %d * head_dim %d", c->hidden, c->heads, c->head_dim);
+  if (c->head_dim % 2) return fail(FF_EINVAL, "ff_dit: head_dim must be even");
+  for (int a = 0; a < 3; ++a)
+    if (c->rope_axes[a] < 0 || c->rope_axes[a] % 2) return fail(FF_EINVAL, "ff_dit: rope axis widths must be even and >= 0");
+  if (c->rope_axes[0] + c->rope_axes[1] + c->rope_axes[2] != c->head_dim)
+    return fail(FF_EINVAL, "ff_dit: rope axes must sum to head_dim");
+  if (!(c->rope_theta > 0) || !(c->norm_eps > 0)) return fail(FF_EINVAL, "ff_dit: rope_theta and norm_eps must be > 0");
+  if (c->norm_kind != FF_NORM_RMS && c->norm_kind != FF_NORM_LN) return fail(FF_EINVAL, "ff_dit: bad norm_kind");
+  if (c->io_mode == FF_IO_LATENT && (c->in_channels <= 0 || c->txt_dim <= 0))
+    return fail(FF_EINVAL, "ff_dit: latent mode needs in_channels and txt_dim");
+  if (c->pooled_dim < 0) return fail(FF_EINVAL, "ff_dit: negative pooled_dim");
+  if (c->dtype == FF_BF16) {
+    if (c->head_dim != 128) return fail(FF_EUNSUPPORTED, "ff_dit: bf16 attention needs head_dim 128");
+    const int64_t ks[] = {c->hidden, c->mlp_hidden, c->io_mode == FF_IO_LATENT ? c->in_channels : 64,
+                          c->io_mode == FF_IO_LATENT ? c->txt_dim : 64};
+    for (int64_t k : ks)
+      if (k % 64) return fail(FF_EUNSUPPORTED, "ff_dit: bf16 layer widths must be multiples of 64 (got %lld)", (long long)k);
+    if (c->pooled_dim % 8) return fail(FF_EUNSUPPORTED, "ff_dit: pooled_dim must be a multiple of 8");
+  } else {
+    if (c->head_dim > 64) return fail(FF_EUNSUPPORTED, "ff_dit: f32 attention needs head_dim <= 64");
+    if (c->hidden % 8 || c->mlp_hidden % 8 || c->pooled_dim % 8)
+      return fail(FF_EUNSUPPORTED, "ff_dit: f32 widths must be multiples of 8");
+  }
+  return FF_OK;
+}
+
+struct Lin {
+  const void* w = nullptr;
+  const void* b = nullptr;
+};
+struct Stream {
+  Lin mod, qkv, o, mlp1, mlp2;
+  const void* qn = nullptr;
+  const void* kn = nullptr;
+};
+struct Single {
+  Lin mod, lin1, lin2;
+  const void* qn = nullptr;
+  const void* kn = nullptr;
+};
+
+}  // namespace
+
+struct ff_dit {
+  ff_dit_config cfg;
+  std::vector<const void*> ptr;
+  Lin temb1, temb2, pooled1, pooled2, x_in, txt_in, final_mod, final_proj;
+  std::vector<Stream> dual_img, dual_txt;
+  std::vector<Single> single;
+};
+
+namespace {
+
+// Workspace plan: byte offsets of every buffer of one forward.
+struct Plan {
+  int64_t B, Ni, Nt, N, P;
+  size_t rope, temb_in, c, tmp, condB, cond32, mods, ximg, xtxt, joint, y, qkv, q, k, vt, o, u, txth, total;
+};
+
+Plan plan(const ff_dit& m, int64_t B, const int32_t grid[3], int64_t n_txt, int64_t n_prompts) {
+  const ff_dit_config& c = m.cfg;
+  Plan p{};
+  p.B = B;
+  p.Ni = static_cast<int64_t>(grid[0]) * grid[1] * grid[2];
+  p.Nt = n_txt;
+  p.N = p.Ni + p.Nt;
+  p.P = n_prompts;
+  const int64_t H = c.hidden, F = c.mlp_hidden;
+  const size_t es = dtype_size(c.dtype);
+  const bool latent = c.io_mode == FF_IO_LATENT;
+  Carver cv(nullptr, 0);
+  auto take = [&](size_t bytes) { void* q = cv.take(bytes); (void)q; return cv.off - bytes; };
+  p.rope = take(static_cast<size_t>(p.Ni) * (c.head_dim / 2) * 8);
+  p.temb_in = take(static_cast<size_t>(B) * 256 * 4);
+  p.c = take(static_cast<size_t>(B) * H * 4);
+  p.tmp = take(static_cast<size_t>(B) * H * 4);
+  p.condB = take(static_cast<size_t>(B) * (c.pooled_dim > H ? c.pooled_dim : H) * es);
+  p.cond32 = take(static_cast<size_t>(B) * (c.pooled_dim > H ? c.pooled_dim : H) * 4);
+  p.mods = take(static_cast<size_t>(2) * B * 6 * H * 4);
+  p.ximg = take(latent ? static_cast<size_t>(B) * p.Ni * H * es : 0);
+  p.xtxt = take(static_cast<size_t>(B) * p.Nt * H * es);
+  p.joint = take(c.n_single ? static_cast<size_t>(B) * p.N * H * es : 0);
+  p.y = take(static_cast<size_t>(B) * p.N * H * es);
+  p.qkv = take(static_cast<size_t>(B) * p.N * (3 * H + (c.n_single ? F : 0)) * es);
+  p.q = take(static_cast<size_t>(B) * p.N * H * es);
+  p.k = take(static_cast<size_t>(B) * p.N * H * es);
+  p.vt = take(static_cast<size_t>(B) * p.N * H * es);
+  p.o = take(static_cast<size_t>(B) * p.N * H * es);
+  p.u = take(static_cast<size_t>(B) * (p.Ni > p.Nt ? p.Ni : p.Nt) * F * es);
+  p.txth = take(latent ? static_cast<size_t>(p.P) * p.Nt * H * es : 0);
+  p.total = round_up(cv.off, 256);
+  return p;
+}
+
+inline char* at(void* ws, size_t off) { return static_cast<char*>(ws) + off; }
+
+GemmArgs gemm_args(int dtype, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, Lin l, void* out,
+                   int64_t ldo, int epi) {
+  GemmArgs g{};
+  g.dtype = dtype;
+  g.M = M; g.N = N; g.K = K;
+  g.A1 = A; g.lda1 = lda; g.K1 = K;
+  g.A2 = nullptr; g.lda2 = 0;
+  g.W = l.w; g.ldw = K;
+  g.bias = l.b;
+  g.out = out; g.ldo = ldo;
+  g.epi = epi;
+  g.gelu_from = 0;
+  g.rows_per_sample = M;
+  return g;
+}
+
+NormArgs norm_args(const ff_dit_config& c, int64_t rows, const void* x, void* y, const float* shift,
+                   const float* scale, int64_t mod_ld, int64_t rows_per_sample) {
+  NormArgs a{};
+  a.dtype = c.dtype;
+  a.rows = rows; a.H = c.hidden;
+  a.x = x; a.ldx = c.hidden;
+  a.y = y; a.ldy = c.hidden;
+  a.norm_kind = c.norm_kind;
+  a.eps = static_cast<float>(c.norm_eps);
+  a.shift = shift; a.scale = scale; a.mod_ld = mod_ld;
+  a.w = nullptr; a.bias = nullptr;
+  a.rows_per_sample = rows_per_sample;
+  return a;
+}
+
+SkinnyArgs skinny_args(int dtype, int64_t B, int64_t N, int64_t K, const float* in, int act_in, Lin l, float* out,
+                       int accumulate = 0, int act_out = ACT_NONE) {
+  SkinnyArgs s{};
+  s.dtype = dtype;
+  s.B = B; s.N = N; s.K = K;
+  s.in = in; s.ldi = K; s.act_in = act_in;
+  s.W = l.w; s.bias = l.b;
+  s.out = out; s.ldo = N;
+  s.accumulate = accumulate;
+  s.act_out = act_out;
+  return s;
+}
+
+// QK norm + RoPE + relayout for one stream's rows: source row of token i of sample b is
+// b * src_rows + src_off + i.
+int qkv_stream(const ff_dit_config& c, const Plan& p, void* ws, const void* qkv_base, int64_t ld, int64_t src_rows,
+               int64_t src_off, int64_t n_tok, int64_t tok_offset, const void* qn, const void* kn, bool rope,
+               hipStream_t s) {
+  const size_t es = dtype_size(c.dtype);
+  const char* base = static_cast<const char*>(qkv_base) + src_off * ld * es;
+  QkvArgs a{};
+  a.dtype = c.dtype;
+  a.B = p.B; a.n_tok = n_tok; a.tok_offset = tok_offset; a.n_joint = p.N;
+  a.heads = c.heads; a.d = c.head_dim;
+  a.q = base; a.k = base + c.hidden * es; a.v = base + 2 * c.hidden * es;
+  a.ld = ld;
+  a.q_w = qn; a.k_w = kn;
+  a.full_width_norm = 0;
+  a.apply_norm = 1;
+  a.eps = static_cast<float>(c.norm_eps);
+  a.rope = rope ? reinterpret_cast<const float2*>(at(ws, p.rope)) : nullptr;
+  a.Q = at(ws, p.q); a.Kd = at(ws, p.k); a.Vt = at(ws, p.vt);
+  a.v_transposed = c.dtype == FF_BF16;
+  a.src_rows = src_rows;
+  return qk_norm_rope(a, s);
+}
+
+int attention_joint(const ff_dit_config& c, const Plan& p, void* ws, void* out_txt, void* out_img, hipStream_t s) {
+  AttnArgs a{};
+  a.dtype = c.dtype;
+  a.B = p.B; a.heads = c.heads; a.d = c.head_dim;
+  a.n_q = p.N; a.n_kv = p.N;
+  a.Q = at(ws, p.q); a.K = at(ws, p.k); a.Vt = at(ws, p.vt);
+  a.out0 = out_txt; a.out1 = out_img; a.split = p.Nt; a.ldo = c.hidden;
+  a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(c.head_dim)));
+  return attention(a, s);
+}
+
+// One dual-stream block.  cur[s] is the stream's current residual (input of the block);
+// dst[s] receives the updated residual (may equal cur[s]).
+int dual_block(const ff_dit& m, const Plan& p, void* ws, int i, const float* c32, const void* cur[2], void* dst[2],
+               hipStream_t s) {
+  const ff_dit_config& c = m.cfg;
+  const int64_t H = c.hidden, F = c.mlp_hidden;
+  const size_t es = dtype_size(c.dtype);
+  const Stream* st[2] = {&m.dual_txt[i], &m.dual_img[i]};
+  const int64_t rows[2] = {p.B * p.Nt, p.B * p.Ni};
+  const int64_t ntok[2] = {p.Nt, p.Ni};
+  const int64_t y_off[2] = {0, p.B * p.Nt * H};    // Y / O rows: txt rows first, then img rows
+  float* mods[2] = {reinterpret_cast<float*>(at(ws, p.mods)), reinterpret_cast<float*>(at(ws, p.mods)) + p.B * 6 * H};
+  char* Y = at(ws, p.y);
+  char* O = at(ws, p.o);
+  char* QKV = at(ws, p.qkv);
+  for (int k = 0; k < 2; ++k) {
+    FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 6 * H, H, c32, ACT_SILU, st[k]->mod, mods[k]), s));
+    FF_TRY(norm_modulate(norm_args(c, rows[k], cur[k], Y + y_off[k] * es, mods[k], mods[k] + H, 6 * H, ntok[k]), s));
+    char* qkv_k = QKV + (k == 0 ? 0 : p.B * p.Nt * 3 * H * es);
+    FF_TRY(gemm(gemm_args(c.dtype, rows[k], 3 * H, H, Y + y_off[k] * es, H, st[k]->qkv, qkv_k, 3 * H, EPI_NONE), s));
+    FF_TRY(qkv_stream(c, p, ws, qkv_k, 3 * H, ntok[k], 0, ntok[k], k == 0 ? 0 : p.Nt, st[k]->qn, st[k]->kn, k == 1, s));
+  }
+  FF_TRY(attention_joint(c, p, ws, O, O + p.B * p.Nt * H * es, s));
+  for (int k = 0; k < 2; ++k) {
+    GemmArgs g = gemm_args(c.dtype, rows[k], H, H, O + y_off[k] * es, H, st[k]->o, dst[k], H, EPI_GATED);
+    g.gate = mods[k] + 2 * H; g.gate_ld = 6 * H;
+    g.resid = cur[k]; g.ldr = H;
+    g.rows_per_sample = ntok[k];
+    FF_TRY(gemm(g, s));
+    FF_TRY(norm_modulate(norm_args(c, rows[k], dst[k], Y + y_off[k] * es, mods[k] + 3 * H, mods[k] + 4 * H, 6 * H, ntok[k]), s));
+    char* U = at(ws, p.u);
+    FF_TRY(gemm(gemm_args(c.dtype, rows[k], F, H, Y + y_off[k] * es, H, st[k]->mlp1, U, F, EPI_GELU), s));
+    GemmArgs g2 = gemm_args(c.dtype, rows[k], H, F, U, F, st[k]->mlp2, dst[k], H, EPI_GATED);
+    g2.gate = mods[k] + 5 * H; g2.gate_ld = 6 * H;
+    g2.resid = dst[k]; g2.ldr = H;
+    g2.rows_per_sample = ntok[k];
+    FF_TRY(gemm(g2, s));
+  }
+  return FF_OK;
+}
+
+// One single-stream block on the joint residual X [B, N, H] (txt rows first), in place.
+int single_block(const ff_dit& m, const Plan& p, void* ws, int j, const float* c32, void* X, hipStream_t s) {
+  const ff_dit_config& c = m.cfg;
+  const int64_t H = c.hidden, F = c.mlp_hidden, W1 = 3 * H + F;
+  const size_t es = dtype_size(c.dtype);
+  const Single& sb = m.single[j];
+  float* mods = reinterpret_cast<float*>(at(ws, p.mods));
+  const int64_t rows = p.B * p.N;
+  char* Y = at(ws, p.y);
+  char* H1 = at(ws, p.qkv);
+  char* O = at(ws, p.o);
+  FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 3 * H, H, c32, ACT_SILU, sb.mod, mods), s));
+  FF_TRY(norm_modulate(norm_args(c, rows, X, Y, mods, mods + H, 3 * H, p.N), s));
+  GemmArgs g1 = gemm_args(c.dtype, rows, W1, H, Y, H, sb.lin1, H1, W1, EPI_GELU);
+  g1.gelu_from = 3 * H;
+  FF_TRY(gemm(g1, s));
+  FF_TRY(qkv_stream(c, p, ws, H1, W1, p.N, 0, p.Nt, 0, sb.qn, sb.kn, false, s));
+  FF_TRY(qkv_stream(c, p, ws, H1, W1, p.N, p.Nt, p.Ni, p.Nt, sb.qn, sb.kn, true, s));
+  AttnArgs a{};
+  a.dtype = c.dtype;
+  a.B = p.B; a.heads = c.heads; a.d = c.head_dim;
+  a.n_q = p.N; a.n_kv = p.N;
+  a.Q = at(ws, p.q); a.K = at(ws, p.k); a.Vt = at(ws, p.vt);
+  a.out0 = O; a.out1 = O; a.split = p.N; a.ldo = H;
+  a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(c.head_dim)));
+  FF_TRY(attention(a, s));
+  GemmArgs g2 = gemm_args(c.dtype, rows, H, H + F, O, H, sb.lin2, X, H, EPI_GATED);
+  g2.K1 = H;
+  g2.A2 = H1 + 3 * H * es; g2.lda2 = W1;
+  g2.gate = mods + 2 * H; g2.gate_ld = 3 * H;
+  g2.resid = X; g2.ldr = H;
+  g2.rows_per_sample = p.N;
+  return gemm(g2, s);
+}
+
+int forward_mmdit(const ff_dit& m, const Plan& p, const void* x, const void* txt, const int32_t* txt_index,
+                  const void* cond, const float* t, const int32_t grid[3], void* v_out, void* txt_out, void* ws,
+                  hipStream_t s) {
+  const ff_dit_config& c = m.cfg;
+  const int64_t H = c.hidden;
+  const size_t es = dtype_size(c.dtype);
+  const bool latent = c.io_mode == FF_IO_LATENT;
+  float* c32 = reinterpret_cast<float*>(at(ws, p.c));
+  FF_TRY(rope_table(reinterpret_cast<float2*>(at(ws, p.rope)), grid, c.head_dim, c.rope_axes, c.rope_theta, s));
+
+  const void* cur[2];
+  void* dst[2];
+  if (latent) {
+    float* te = reinterpret_cast<float*>(at(ws, p.temb_in));
+    float* tmp = reinterpret_cast<float*>(at(ws, p.tmp));
+    FF_TRY(timestep_sinusoid(t, te, p.B, s));
+    FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, H, 256, te, ACT_NONE, m.temb1, tmp), s));
+    FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, H, H, tmp, ACT_SILU, m.temb2, c32), s));
+    if (c.pooled_dim) {
+      float* cond32 = reinterpret_cast<float*>(at(ws, p.cond32));
+      FF_TRY(gather_rows(c.dtype, cond, txt_index, p.P, at(ws, p.condB), p.B, 1, c.pooled_dim, s));
+      FF_TRY(cast_to_f32(c.dtype, at(ws, p.condB), cond32, p.B * c.pooled_dim, s));
+      FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, H, c.pooled_dim, cond32, ACT_NONE, m.pooled1, tmp), s));
+      FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, H, H, tmp, ACT_SILU, m.pooled2, c32, 1), s));
+    }
+    char* ximg = at(ws, p.ximg);
+    FF_TRY(gemm(gemm_args(c.dtype, p.B * p.Ni, H, c.in_channels, x, c.in_channels, m.x_in, ximg, H, EPI_NONE), s));
+    char* txth = at(ws, p.txth);
+    FF_TRY(gemm(gemm_args(c.dtype, p.P * p.Nt, H, c.txt_dim, txt, c.txt_dim, m.txt_in, txth, H, EPI_NONE), s));
+    FF_TRY(gather_rows(c.dtype, txth, txt_index, p.P, at(ws, p.xtxt), p.B, p.Nt, H, s));
+    cur[0] = at(ws, p.xtxt);
+    cur[1] = ximg;
+    dst[0] = at(ws, p.xtxt);
+    dst[1] = ximg;
+  } else {
+    FF_TRY(cast_to_f32(c.dtype, cond, c32, p.B * H, s));
+    cur[0] = txt;
+    cur[1] = x;
+    dst[0] = txt_out ? txt_out : static_cast<void*>(at(ws, p.xtxt));
+    dst[1] = v_out;
+  }
+
+  for (int i = 0; i < c.n_dual; ++i) {
+    FF_TRY(dual_block(m, p, ws, i, c32, cur, dst, s));
+    cur[0] = dst[0];
+    cur[1] = dst[1];
+  }
+  if (c.n_single) {
+    char* X = at(ws, p.joint);
+    const size_t row = static_cast<size_t>(H) * es;
+    FF_CHECK_HIP(hipMemcpy2DAsync(X, p.N * row, cur[0], p.Nt * row, p.Nt * row, p.B, hipMemcpyDeviceToDevice, s), "copy txt->joint");
+    FF_CHECK_HIP(hipMemcpy2DAsync(X + p.Nt * row, p.N * row, cur[1], p.Ni * row, p.Ni * row, p.B, hipMemcpyDeviceToDevice, s), "copy img->joint");
+    for (int j = 0; j < c.n_single; ++j) FF_TRY(single_block(m, p, ws, j, c32, X, s));
+    void* img_dst = latent ? static_cast<void*>(at(ws, p.ximg)) : v_out;
+    FF_CHECK_HIP(hipMemcpy2DAsync(img_dst, p.Ni * row, X + p.Nt * row, p.N * row, p.Ni * row, p.B, hipMemcpyDeviceToDevice, s), "copy joint->img");
+    if (!latent && txt_out)
+      FF_CHECK_HIP(hipMemcpy2DAsync(txt_out, p.Nt * row, X, p.N * row, p.Nt * row, p.B, hipMemcpyDeviceToDevice, s), "copy joint->txt");
+    cur[1] = img_dst;
+  } else if (!latent && c.n_dual == 0) {
+    // No blocks: outputs are the inputs.
+    FF_CHECK_HIP(hipMemcpyAsync(v_out, x, static_cast<size_t>(p.B) * p.Ni * H * es, hipMemcpyDeviceToDevice, s), "copy x");
+    if (txt_out)
+      FF_CHECK_HIP(hipMemcpyAsync(txt_out, txt, static_cast<size_t>(p.B) * p.Nt * H * es, hipMemcpyDeviceToDevice, s), "copy txt");
+  }
+
+  if (latent) {
+    float* mods = reinterpret_cast<float*>(at(ws, p.mods));
+    FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 2 * H, H, c32, ACT_SILU, m.final_mod, mods), s));
+    char* Y = at(ws, p.y);
+    FF_TRY(norm_modulate(norm_args(c, p.B * p.Ni, cur[1], Y, mods, mods + H, 2 * H, p.Ni), s));
+    FF_TRY(gemm(gemm_args(c.dtype, p.B * p.Ni, c.in_channels, H, Y, H, m.final_proj, v_out, c.in_channels, EPI_NONE), s));
+  }
+  return FF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ff_dit_num_tensors(const ff_dit_config* cfg, int64_t* n) {
+  FF_TRY(check_config(cfg));
+  if (!n) return fail(FF_EINVAL, "ff_dit_num_tensors: null output");
+  *n = static_cast<int64_t>(tensor_table(*cfg).size());
+  return FF_OK;
+}
+
+int ff_dit_tensor_info(const ff_dit_config* cfg, int64_t i, char* name, size_t name_cap, int64_t* shape0,
+                       int64_t* shape1) {
+  FF_TRY(check_config(cfg));
+  std::vector<TensorSpec> t = tensor_table(*cfg);
+  if (i < 0 || i >= static_cast<int64_t>(t.size())) return fail(FF_EINVAL, "ff_dit_tensor_info: index %lld out of range", (long long)i);
+  if (name) {
+    if (name_cap < t[i].name.size() + 1) return fail(FF_EINVAL, "ff_dit_tensor_info: name buffer too small");
+    memcpy(name, t[i].name.c_str(), t[i].name.size() + 1);
+  }
+  if (shape0) *shape0 = t[i].s0;
+  if (shape1) *shape1 = t[i].s1;
+  return FF_OK;
+}
+
+int ff_dit_create(const ff_dit_config* cfg, const void* const* tensors, int64_t n_tensors, ff_dit** out) {
+  FF_TRY(check_config(cfg));
+  if (cfg->model == FF_MODEL_WAN) return fail(FF_EUNSUPPORTED, "ff_dit_create: the WAN block is not implemented in this build");
+  if (!out) return fail(FF_EINVAL, "ff_dit_create: null output");
+  *out = nullptr;
+  std::vector<TensorSpec> t = tensor_table(*cfg);
+  if (n_tensors != static_cast<int64_t>(t.size()))
+    return fail(FF_EINVAL, "ff_dit_create: %lld tensors given, %zu expected", (long long)n_tensors, t.size());
+  if (!tensors) return fail(FF_EINVAL, "ff_dit_create: null tensor array");
+  std::unordered_map<std::string, const void*> by;
+  for (size_t i = 0; i < t.size(); ++i) {
+    if (!tensors[i]) return fail(FF_EINVAL, "ff_dit_create: tensor %zu (%s) is null", i, t[i].name.c_str());
+    if (!aligned16(tensors[i])) return fail(FF_EINVAL, "ff_dit_create: tensor %s not 16-byte aligned", t[i].name.c_str());
+    by[t[i].name] = tensors[i];
+  }
+  ff_dit* m = new ff_dit();
+  m->cfg = *cfg;
+  m->ptr.assign(tensors, tensors + n_tensors);
+  auto L = [&](const std::string& p) { Lin l; l.w = by[p + ".w"]; l.b = by[p + ".b"]; return l; };
+  if (cfg->io_mode == FF_IO_LATENT) {
+    m->temb1 = L("temb.fc1");
+    m->temb2 = L("temb.fc2");
+    if (cfg->pooled_dim) { m->pooled1 = L("pooled.fc1"); m->pooled2 = L("pooled.fc2"); }
+    m->x_in = L("x_in");
+    m->txt_in = L("txt_in");
+    m->final_mod = L("final.mod");
+    m->final_proj = L("final.proj");
+  }
+  for (int i = 0; i < cfg->n_dual; ++i)
+    for (int k = 0; k < 2; ++k) {
+      std::string p = "dual." + std::to_string(i) + (k == 0 ? ".img." : ".txt.");
+      Stream st;
+      st.mod = L(p + "mod"); st.qkv = L(p + "qkv"); st.o = L(p + "o");
+      st.mlp1 = L(p + "mlp1"); st.mlp2 = L(p + "mlp2");
+      st.qn = by[p + "q_norm.w"]; st.kn = by[p + "k_norm.w"];
+      (k == 0 ? m->dual_img : m->dual_txt).push_back(st);
+    }
+  for (int j = 0; j < cfg->n_single; ++j) {
+    std::string p = "single." + std::to_string(j) + ".";
+    Single sb;
+    sb.mod = L(p + "mod"); sb.lin1 = L(p + "lin1"); sb.lin2 = L(p + "lin2");
+    sb.qn = by[p + "q_norm.w"]; sb.kn = by[p + "k_norm.w"];
+    m->single.push_back(sb);
+  }
+  *out = m;
+  return FF_OK;
+}
+
+int ff_dit_destroy(ff_dit* m) {
+  delete m;
+  return FF_OK;
+}
+
+static int check_forward_shape(const ff_dit* m, int64_t B, const int32_t grid[3], int64_t n_txt, int64_t n_prompts) {
+  if (!m) return fail(FF_EINVAL, "ff_dit: null model");
+  if (!grid) return fail(FF_EINVAL, "ff_dit: null grid");
+  if (B < 1 || B > 65535) return fail(FF_EINVAL, "ff_dit: B=%lld outside [1, 65535]", (long long)B);
+  if (grid[0] < 1 || grid[1] < 1 || grid[2] < 1) return fail(FF_EINVAL, "ff_dit: grid entries must be >= 1");
+  if (n_txt < 1) return fail(FF_EINVAL, "ff_dit: n_txt must be >= 1");
+  if (n_prompts < 1) return fail(FF_EINVAL, "ff_dit: n_prompts must be >= 1");
+  const int64_t Ni = static_cast<int64_t>(grid[0]) * grid[1] * grid[2];
+  if (m->cfg.dtype == FF_BF16 && (Ni % 8 || n_txt % 8))
+    return fail(FF_EUNSUPPORTED, "ff_dit: bf16 token counts must be multiples of 8 (N_img=%lld, n_txt=%lld)", (long long)Ni, (long long)n_txt);
+  return FF_OK;
+}
+
+int ff_dit_workspace_size(const ff_dit* m, int64_t B, const int32_t grid[3], int64_t n_txt, int64_t n_prompts,
+                          size_t* bytes) {
+  FF_TRY(check_forward_shape(m, B, grid, n_txt, n_prompts));
+  if (!bytes) return fail(FF_EINVAL, "ff_dit_workspace_size: null output");
+  *bytes = plan(*m, B, grid, n_txt, n_prompts).total;
+  return FF_OK;
+}
+
+int ff_dit_forward(const ff_dit* m, const void* x, const void* txt, const int32_t* txt_index, int64_t n_prompts,
+                   const void* cond, const float* t, const int32_t grid[3], int64_t B, int64_t n_txt, void* v_out,
+                   void* txt_out, void* workspace, size_t ws_bytes, void* stream) {
+  FF_TRY(check_forward_shape(m, B, grid, n_txt, n_prompts));
+  const ff_dit_config& c = m->cfg;
+  if (!x || !txt || !v_out) return fail(FF_EINVAL, "ff_dit_forward: null x, txt or v_out");
+  if (!aligned16(x) || !aligned16(txt) || !aligned16(v_out) || (txt_out && !aligned16(txt_out)) ||
+      (cond && !aligned16(cond)))
+    return fail(FF_EINVAL, "ff_dit_forward: tensors must be 16-byte aligned");
+  if (c.io_mode == FF_IO_LATENT) {
+    if (!t) return fail(FF_EINVAL, "ff_dit_forward: latent mode needs t");
+    if (txt_out) return fail(FF_EINVAL, "ff_dit_forward: txt_out must be NULL in latent mode");
+    if (!txt_index && n_prompts != B) return fail(FF_EINVAL, "ff_dit_forward: txt_index NULL needs n_prompts == B");
+    if (c.pooled_dim && !cond) return fail(FF_EINVAL, "ff_dit_forward: pooled_dim > 0 needs cond");
+  } else {
+    if (!cond) return fail(FF_EINVAL, "ff_dit_forward: hidden mode needs cond");
+    if (txt_index || n_prompts != B) return fail(FF_EINVAL, "ff_dit_forward: hidden mode takes per-sample text (txt_index NULL, n_prompts == B)");
+  }
+  if (v_out == x || v_out == txt || (txt_out && (txt_out == x || txt_out == txt || txt_out == v_out)))
+    return fail(FF_EINVAL, "ff_dit_forward: outputs may not alias inputs");
+  Plan p = plan(*m, B, grid, n_txt, n_prompts);
+  if (!workspace || ws_bytes < p.total)
+    return fail(FF_EWORKSPACE, "ff_dit_forward: workspace of %zu bytes needed, %zu given", p.total, workspace ? ws_bytes : 0);
+  if (!aligned16(workspace)) return fail(FF_EINVAL, "ff_dit_forward: workspace must be 16-byte aligned");
+  return forward_mmdit(*m, p, x, txt, txt_index, cond, t, grid, v_out, txt_out, workspace, static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,164 @@
+// Internal declarations shared by the library's translation units (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <hip/hip_bf16.h>
+
+#include <cstdint>
+#include <cstdio>
+#include <string>
+
+#include "../../include/ff.h"
+
+namespace ff {
+
+// ----------------------------------------------------------------- errors
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int hip_status(hipError_t e, const char* what);   // FF_OK or FF_EHIP with message
+
+#define FF_CHECK_HIP(expr, what)                             \
+  do {                                                       \
+    hipError_t _e = (expr);                                  \
+    if (_e != hipSuccess) return ::ff::hip_status(_e, what); \
+  } while (0)
+
+#define FF_TRY(expr)               \
+  do {                             \
+    int _s = (expr);               \
+    if (_s != FF_OK) return _s;    \
+  } while (0)
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+inline size_t dtype_size(int dt) { return dt == FF_BF16 ? 2 : 4; }
+inline size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// ----------------------------------------------------------------- profiling
+// Wraps one kernel launch: records events when profiling is enabled and
+// checks the launch status.  `flops` / `bytes` are the launch's algorithmic
+// work, accumulated per kernel name.
+struct LaunchScope {
+  LaunchScope(const char* name, hipStream_t s, double flops, double bytes);
+  ~LaunchScope();
+  int status();   // FF_OK or FF_EHIP (checks hipGetLastError)
+ private:
+  const char* name_;
+  hipStream_t stream_;
+  double flops_, bytes_;
+  int slot_;
+};
+
+// ----------------------------------------------------------------- workspace carving
+struct Carver {
+  char* base;
+  size_t cap;
+  size_t off = 0;
+  Carver(void* b, size_t c) : base(static_cast<char*>(b)), cap(c) {}
+  void* take(size_t bytes) {
+    off = round_up(off, 256);
+    void* p = base ? base + off : nullptr;
+    off += bytes;
+    return p;
+  }
+};
+
+// ----------------------------------------------------------------- kernels (launchers)
+// All launchers return FF_OK or FF_EHIP and expect validated arguments.
+
+enum Epi : int {
+  EPI_NONE = 0,       // out = acc + bias
+  EPI_GELU = 1,       // out = gelu_tanh(acc + bias) for columns >= gelu_from, else acc + bias
+  EPI_GATED = 2,      // out = resid + gate[b] * (acc + bias)
+};
+
+struct GemmArgs {
+  int dtype;
+  int64_t M, N, K;
+  // A = [A1 | A2] along K: A1 [M, K1] (lda1), A2 [M, K-K1] (lda2); K1 == K when A2 unused
+  const void* A1; int64_t lda1; int64_t K1;
+  const void* A2; int64_t lda2;
+  const void* W; int64_t ldw;           // [N, K] row-major (nn.Linear weight)
+  const void* bias;                     // [N] or null
+  void* out; int64_t ldo;
+  int epi;
+  int64_t gelu_from;                    // EPI_GELU: first GELU column
+  const float* gate; int64_t gate_ld;   // EPI_GATED: gate[(m / rows_per_sample) * gate_ld + n]
+  const void* resid; int64_t ldr;       // EPI_GATED: residual (may alias out)
+  int64_t rows_per_sample;
+};
+int gemm(const GemmArgs& a, hipStream_t s);
+
+// out[b, n] (+)= sum_k W[n, k] * act(in[b, k]) + bias[n]; in/out float32, W of dtype.
+enum Act : int { ACT_NONE = 0, ACT_SILU = 1, ACT_GELU = 2 };
+struct SkinnyArgs {
+  int dtype;
+  int64_t B, N, K;
+  const float* in; int64_t ldi;
+  int act_in;                 // activation applied to the input
+  const void* W; const void* bias;
+  float* out; int64_t ldo;
+  int accumulate;             // 1: out += result
+  int act_out;                // activation applied to the result (before accumulate)
+};
+int skinny_linear(const SkinnyArgs& a, hipStream_t s);
+
+// y = Norm(x) * mul + add per row; row r belongs to sample r / rows_per_sample.
+// mul = (1 + scale[b]) (if scale) * w (if w); add = shift[b] (if shift) + bias (if bias)
+struct NormArgs {
+  int dtype;
+  int64_t rows, H;
+  const void* x; int64_t ldx;
+  void* y; int64_t ldy;
+  int norm_kind; float eps;
+  const float* shift; const float* scale; int64_t mod_ld;  // per-sample modulation (fp32)
+  const void* w; const void* bias;                         // per-column affine (dtype)
+  int64_t rows_per_sample;
+};
+int norm_modulate(const NormArgs& a, hipStream_t s);
+
+// Converts a float32 [rows, H] tensor to dtype (plain copy for F32) or dtype -> float32.
+int cast_to_f32(int dtype, const void* in, float* out, int64_t n, hipStream_t s);
+
+// Per-head QK RMSNorm + RoPE + relayout into the joint attention layout.
+struct QkvArgs {
+  int dtype;
+  int64_t B, n_tok, tok_offset, n_joint;   // tokens of this stream, position in the joint sequence
+  int64_t src_rows;                         // source rows per sample (token i of sample b is row b*src_rows+i)
+  int heads, d;
+  const void* q; const void* k; const void* v; int64_t ld;  // row stride of the packed source
+  const void* q_w; const void* k_w;        // RMSNorm weights ([d] per-head, or [H] full-width)
+  int full_width_norm;                      // 1: RMSNorm over all H before RoPE (WAN)
+  int apply_norm;                           // 0: no QK norm (cross-attention V/K handled by caller)
+  float eps;
+  const float2* rope;                       // [n_tok, d/2] (cos, sin) or null = no rotation
+  void* Q; void* Kd; void* Vt;              // Q, K [B, h, n_joint, d]; V transposed [B, h, d, n_joint]
+  int v_transposed;
+};
+int qk_norm_rope(const QkvArgs& a, hipStream_t s);
+
+// (cos, sin) table for a (frames, rows, cols) grid: [N, d/2] float2, computed in float64.
+int rope_table(float2* out, const int32_t grid[3], int d, const int32_t axes[3], double theta,
+               hipStream_t s);
+
+struct AttnArgs {
+  int dtype;
+  int64_t B, heads, d;
+  int64_t n_q, n_kv;
+  const void* Q; const void* K; const void* Vt;   // Q [B,h,n_q,d], K [B,h,n_kv,d], Vt [B,h,d,n_kv]
+  // output split by query index: q < split -> out0 rows, else out1 rows (token-major, ld = H)
+  void* out0; void* out1; int64_t split; int64_t ldo;
+  float scale;
+};
+int attention(const AttnArgs& a, hipStream_t s);
+
+// Gathers rows: out[b, j, :] = in[idx[b], j, :] (zero when idx out of range)
+int gather_rows(int dtype, const void* in, const int32_t* idx, int64_t n_src, void* out,
+                int64_t B, int64_t rows_per, int64_t width, hipStream_t s);
+
+// temb input: [cos | sin](1000 t * 10000^(-j/128)) -> float32 [B, 256]
+int timestep_sinusoid(const float* t, float* out, int64_t B, hipStream_t s);
+
+// out[b, i, :] (+)= in (float32 [B, ld]) broadcast: used for WAN modulation tables
+int add_table(const void* table, int dtype, const float* e, float* out, int64_t B, int64_t n,
+              hipStream_t s);
+
+}  // namespace ff

@@ -1,0 +1,368 @@
+// Bandwidth-bound DiT pieces: adaLN modulation vectors (skinny linear),
+// norm + modulate, per-head QK RMSNorm + RoPE + relayout, RoPE tables,
+// prompt broadcast and the sinusoidal timestep embedding.
+#include <cmath>
+
+#include "dev.h"
+#include "ff_internal.h"
+
+namespace ff {
+namespace {
+
+// ------------------------------------------------------------------ skinny linear
+// out[b, n] = act_out(sum_k W[n,k] act_in(in[b,k]) + bias[n]) (+ out[b, n] when accumulating).
+// A wave owns 8 output rows; lanes stride over K in 8-element chunks.  Bc <= 8 samples per launch.
+constexpr int kSkRows = 8;
+
+__device__ __forceinline__ float act_apply(int act, float x) {
+  if (act == ACT_SILU) return silu_f(x);
+  if (act == ACT_GELU) return gelu_tanh_f(x);
+  return x;
+}
+
+template <bool BF16, int BC>
+__global__ __launch_bounds__(256) void skinny_kernel(const float* __restrict__ in, int64_t ldi, int act_in,
+                                                     const void* __restrict__ W, const void* __restrict__ bias,
+                                                     float* __restrict__ out, int64_t ldo, int64_t N, int64_t K,
+                                                     int accumulate, int act_out) {
+  const int lane = threadIdx.x & 63;
+  const int64_t n0 = (static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6)) * kSkRows;
+  if (n0 >= N) return;
+  float acc[kSkRows][BC];
+#pragma unroll
+  for (int r = 0; r < kSkRows; ++r)
+#pragma unroll
+    for (int b = 0; b < BC; ++b) acc[r][b] = 0.f;
+  for (int64_t k = static_cast<int64_t>(lane) * 8; k < K; k += 512) {
+    float xin[BC][8];
+#pragma unroll
+    for (int b = 0; b < BC; ++b) {
+      const float4* q = reinterpret_cast<const float4*>(in + b * ldi + k);
+      float4 u = q[0], v = q[1];
+      float t[8] = {u.x, u.y, u.z, u.w, v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int j = 0; j < 8; ++j) xin[b][j] = act_apply(act_in, t[j]);
+    }
+#pragma unroll
+    for (int r = 0; r < kSkRows; ++r) {
+      const int64_t n = n0 + r < N ? n0 + r : N - 1;
+      float w[8];
+      ld8<BF16>(W, n * K + k, w);
+#pragma unroll
+      for (int b = 0; b < BC; ++b)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[r][b] = fmaf(w[j], xin[b][j], acc[r][b]);
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < kSkRows; ++r)
+#pragma unroll
+    for (int b = 0; b < BC; ++b) {
+      float s = wave_sum(acc[r][b]);
+      const int64_t n = n0 + r;
+      if (lane == 0 && n < N) {
+        float v = s + (bias ? ld1<BF16>(bias, n) : 0.f);
+        v = act_apply(act_out, v);
+        if (accumulate) v += out[b * ldo + n];
+        out[b * ldo + n] = v;
+      }
+    }
+}
+
+template <bool BF16>
+int skinny_dispatch(const SkinnyArgs& a, int64_t b0, int bc, hipStream_t s) {
+  dim3 grid(static_cast<unsigned>((a.N + 4 * kSkRows - 1) / (4 * kSkRows)));
+  const float* in = a.in + b0 * a.ldi;
+  float* out = a.out + b0 * a.ldo;
+#define FF_SK(BCV)                                                                                   \
+  case BCV:                                                                                         \
+    hipLaunchKernelGGL((skinny_kernel<BF16, BCV>), grid, dim3(256), 0, s, in, a.ldi, a.act_in, a.W, \
+                       a.bias, out, a.ldo, a.N, a.K, a.accumulate, a.act_out);                      \
+    break;
+  switch (bc) {
+    FF_SK(1) FF_SK(2) FF_SK(3) FF_SK(4) FF_SK(5) FF_SK(6) FF_SK(7) FF_SK(8)
+    default: return fail(FF_EUNSUPPORTED, "skinny_linear: chunk %d", bc);
+  }
+#undef FF_SK
+  return FF_OK;
+}
+
+// ------------------------------------------------------------------ norm + modulate
+// One wave per row.  NCH > 0: the row is held in registers as NCH chunks of 8
+// per lane (row width 512 * NCH, 16-byte aligned); NCH == 0: generic scalar path.
+template <bool BF16, int NCH>
+__global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (row >= a.rows) return;
+  const int64_t H = a.H;
+  const int64_t b = row / a.rows_per_sample;
+  const float invH = 1.0f / static_cast<float>(H);
+  const float* sh = a.shift ? a.shift + b * a.mod_ld : nullptr;
+  const float* sc = a.scale ? a.scale + b * a.mod_ld : nullptr;
+  auto finish = [&](int64_t j, float xn) {
+    float mul = sc ? 1.0f + sc[j] : 1.0f;
+    if (a.w) mul *= ld1<BF16>(a.w, j);
+    float add = sh ? sh[j] : 0.0f;
+    if (a.bias) add += ld1<BF16>(a.bias, j);
+    return fmaf(xn, mul, add);
+  };
+  if constexpr (NCH > 0) {
+    float v[NCH][8];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) ld8<BF16>(a.x, row * a.ldx + (c * 64 + lane) * 8, v[c]);
+    float mean = 0.f;
+    if (a.norm_kind == FF_NORM_LN) {
+      float s = 0.f;
+#pragma unroll
+      for (int c = 0; c < NCH; ++c)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) s += v[c][j];
+      mean = wave_sum(s) * invH;
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        float d = v[c][j] - mean;
+        ss = fmaf(d, d, ss);
+      }
+    const float rstd = rsqrtf(wave_sum(ss) * invH + a.eps);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      float o[8];
+      const int64_t j0 = (c * 64 + lane) * 8;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) o[j] = finish(j0 + j, (v[c][j] - mean) * rstd);
+      st8<BF16>(a.y, row * a.ldy + j0, o);
+    }
+  } else {
+    float mean = 0.f;
+    if (a.norm_kind == FF_NORM_LN) {
+      float s = 0.f;
+      for (int64_t j = lane; j < H; j += 64) s += ld1<BF16>(a.x, row * a.ldx + j);
+      mean = wave_sum(s) * invH;
+    }
+    float ss = 0.f;
+    for (int64_t j = lane; j < H; j += 64) {
+      float d = ld1<BF16>(a.x, row * a.ldx + j) - mean;
+      ss = fmaf(d, d, ss);
+    }
+    const float rstd = rsqrtf(wave_sum(ss) * invH + a.eps);
+    for (int64_t j = lane; j < H; j += 64)
+      st1<BF16>(a.y, row * a.ldy + j, finish(j, (ld1<BF16>(a.x, row * a.ldx + j) - mean) * rstd));
+  }
+}
+
+template <bool BF16>
+int norm_dispatch(const NormArgs& a, hipStream_t s) {
+  dim3 grid(static_cast<unsigned>((a.rows + 3) / 4));
+  int nch = 0;
+  const bool fits = a.H % 512 == 0 && a.ldx % 8 == 0 && a.ldy % 8 == 0 && aligned16(a.x) && aligned16(a.y);
+  if (BF16 && fits) nch = static_cast<int>(a.H / 512);
+  switch (nch) {
+#define FF_NM(N) case N: hipLaunchKernelGGL((norm_kernel<BF16, N>), grid, dim3(256), 0, s, a); break;
+    FF_NM(1) FF_NM(2) FF_NM(3) FF_NM(4) FF_NM(5) FF_NM(6) FF_NM(7) FF_NM(8)
+#undef FF_NM
+    default: hipLaunchKernelGGL((norm_kernel<BF16, 0>), grid, dim3(256), 0, s, a); break;
+  }
+  return FF_OK;
+}
+
+// ------------------------------------------------------------------ QK norm + RoPE + relayout
+// A block handles 64 tokens of one head of one sample; each wave walks 16
+// tokens, lane p owning the rotation pair (2p, 2p+1).  Q and K go to
+// [B, h, n_joint, d]; V goes transposed to [B, h, d, n_joint] through LDS so
+// its rows are written 128 bytes at a time.
+constexpr int kRopeTok = 64;
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void qk_rope_kernel(QkvArgs a) {
+  __shared__ float vs[kRopeTok][130];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t t0 = static_cast<int64_t>(blockIdx.x) * kRopeTok;
+  const int h = blockIdx.y;
+  const int64_t b = blockIdx.z;
+  const int d = a.d, half = d / 2;
+  const bool active = lane < half;
+  const float inv_d = 1.0f / static_cast<float>(d);
+  for (int tt = wave; tt < kRopeTok; tt += 4) {
+    const int64_t i = t0 + tt;
+    if (i >= a.n_tok) break;
+    const int64_t src = (b * a.src_rows + i) * a.ld + static_cast<int64_t>(h) * d + 2 * lane;
+    const int64_t jn = a.tok_offset + i;
+    const int64_t dst = ((b * a.heads + h) * a.n_joint + jn) * d + 2 * lane;
+    float2 cs = make_float2(1.f, 0.f);
+    if (a.rope && active) cs = a.rope[i * half + lane];
+#pragma unroll
+    for (int which = 0; which < 2; ++which) {
+      const void* srcp = which == 0 ? a.q : a.k;
+      const void* wn = which == 0 ? a.q_w : a.k_w;
+      void* dstp = which == 0 ? a.Q : a.Kd;
+      float x0 = 0.f, x1 = 0.f;
+      if (active) { x0 = ld1<BF16>(srcp, src); x1 = ld1<BF16>(srcp, src + 1); }
+      if (a.apply_norm) {
+        const float rstd = rsqrtf(wave_sum(x0 * x0 + x1 * x1) * inv_d + a.eps);
+        if (active) {
+          x0 = x0 * rstd * ld1<BF16>(wn, 2 * lane);
+          x1 = x1 * rstd * ld1<BF16>(wn, 2 * lane + 1);
+        }
+      }
+      if (active) {
+        const float y0 = x0 * cs.x - x1 * cs.y;
+        const float y1 = x0 * cs.y + x1 * cs.x;
+        st1<BF16>(dstp, dst, y0);
+        st1<BF16>(dstp, dst + 1, y1);
+      }
+    }
+    if (active) {
+      float v0 = ld1<BF16>(a.v, src), v1 = ld1<BF16>(a.v, src + 1);
+      if (a.v_transposed) {
+        vs[tt][2 * lane] = v0;
+        vs[tt][2 * lane + 1] = v1;
+      } else {
+        st1<BF16>(a.Vt, dst, v0);
+        st1<BF16>(a.Vt, dst + 1, v1);
+      }
+    }
+  }
+  if (!a.v_transposed) return;
+  __syncthreads();
+  // Vt[b, h, dd, tok_offset + t0 + tt]
+  const int64_t ntok = (a.n_tok - t0) < kRopeTok ? (a.n_tok - t0) : kRopeTok;
+  const int64_t col0 = a.tok_offset + t0;
+  for (int e = threadIdx.x; e < d * kRopeTok; e += 256) {
+    const int dd = e / kRopeTok, tt = e % kRopeTok;
+    if (tt < ntok) {
+      const int64_t o = ((b * a.heads + h) * d + dd) * a.n_joint + col0 + tt;
+      st1<BF16>(a.Vt, o, vs[tt][dd]);
+    }
+  }
+}
+
+__global__ void rope_table_kernel(float2* out, int64_t N, int rows, int cols, int half, int b0, int b1,
+                                  int w0, int w1, int w2, double theta) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= N * half) return;
+  const int64_t n = e / half;
+  const int p = static_cast<int>(e % half);
+  const int64_t pos[3] = {n / (static_cast<int64_t>(rows) * cols), (n / cols) % rows, n % cols};
+  int axis, i, width;
+  if (p < b0) { axis = 0; i = p; width = w0; }
+  else if (p < b1) { axis = 1; i = p - b0; width = w1; }
+  else { axis = 2; i = p - b1; width = w2; }
+  const double ang = static_cast<double>(pos[axis]) * pow(theta, -2.0 * i / width);
+  out[e] = make_float2(static_cast<float>(cos(ang)), static_cast<float>(sin(ang)));
+}
+
+template <bool BF16>
+__global__ void gather_kernel(const void* __restrict__ in, const int32_t* __restrict__ idx, int64_t n_src,
+                              void* __restrict__ out, int64_t per, int64_t total) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= total) return;
+  const int64_t b = e / per, r = e % per;
+  const int64_t src = idx ? idx[b] : b;
+  const float v = (src >= 0 && src < n_src) ? ld1<BF16>(in, src * per + r) : 0.f;
+  st1<BF16>(out, e, v);
+}
+
+__global__ void temb_kernel(const float* __restrict__ t, float* __restrict__ out, int64_t B) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= B * 128) return;
+  const int64_t b = e / 128;
+  const int j = static_cast<int>(e % 128);
+  const double arg = 1000.0 * static_cast<double>(t[b]) * pow(10000.0, -static_cast<double>(j) / 128.0);
+  out[b * 256 + j] = static_cast<float>(cos(arg));
+  out[b * 256 + 128 + j] = static_cast<float>(sin(arg));
+}
+
+template <bool BF16>
+__global__ void to_f32_kernel(const void* __restrict__ in, float* __restrict__ out, int64_t n) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e < n) out[e] = ld1<BF16>(in, e);
+}
+
+// out[b, r, j] = table[r, j] + e[b, r, j]  (WAN modulation: E_block + e(t))
+template <bool BF16>
+__global__ void add_table_kernel(const void* __restrict__ table, const float* __restrict__ e,
+                                 float* __restrict__ out, int64_t B, int64_t n) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= B * n) return;
+  out[i] = ld1<BF16>(table, i % n) + e[i];
+}
+
+unsigned blocks_for(int64_t n, int t = 256) { return static_cast<unsigned>((n + t - 1) / t); }
+
+}  // namespace
+
+int skinny_linear(const SkinnyArgs& a, hipStream_t s) {
+  if (a.B == 0 || a.N == 0) return FF_OK;
+  if (a.K % 8 != 0 || a.ldi % 4 != 0) return fail(FF_EUNSUPPORTED, "skinny_linear: K=%lld must be a multiple of 8", (long long)a.K);
+  LaunchScope ls("skinny_linear", s, 2.0 * a.B * a.N * a.K,
+                 static_cast<double>(dtype_size(a.dtype)) * a.N * a.K + 4.0 * a.B * (a.K + a.N));
+  for (int64_t b0 = 0; b0 < a.B; b0 += 8) {
+    const int bc = static_cast<int>(a.B - b0 < 8 ? a.B - b0 : 8);
+    FF_TRY(a.dtype == FF_BF16 ? skinny_dispatch<true>(a, b0, bc, s) : skinny_dispatch<false>(a, b0, bc, s));
+  }
+  return ls.status();
+}
+
+int norm_modulate(const NormArgs& a, hipStream_t s) {
+  if (a.rows == 0) return FF_OK;
+  LaunchScope ls("norm_modulate", s, 0.0, 2.0 * dtype_size(a.dtype) * a.rows * a.H);
+  FF_TRY(a.dtype == FF_BF16 ? norm_dispatch<true>(a, s) : norm_dispatch<false>(a, s));
+  return ls.status();
+}
+
+int qk_norm_rope(const QkvArgs& a, hipStream_t s) {
+  if (a.B == 0 || a.n_tok == 0) return FF_OK;
+  if (a.d > 128 || a.d % 2) return fail(FF_EUNSUPPORTED, "qk_norm_rope: head_dim %d", a.d);
+  dim3 grid(blocks_for(a.n_tok, kRopeTok), static_cast<unsigned>(a.heads), static_cast<unsigned>(a.B));
+  LaunchScope ls("qk_norm_rope", s, 0.0, 6.0 * dtype_size(a.dtype) * a.B * a.n_tok * a.heads * a.d);
+  if (a.dtype == FF_BF16) hipLaunchKernelGGL(qk_rope_kernel<true>, grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(qk_rope_kernel<false>, grid, dim3(256), 0, s, a);
+  return ls.status();
+}
+
+int rope_table(float2* out, const int32_t grid[3], int d, const int32_t axes[3], double theta, hipStream_t s) {
+  const int64_t N = static_cast<int64_t>(grid[0]) * grid[1] * grid[2];
+  const int half = d / 2;
+  LaunchScope ls("rope_table", s, 0.0, 8.0 * N * half);
+  hipLaunchKernelGGL(rope_table_kernel, dim3(blocks_for(N * half)), dim3(256), 0, s, out, N, grid[1], grid[2],
+                     half, axes[0] / 2, (axes[0] + axes[1]) / 2, axes[0], axes[1], axes[2], theta);
+  return ls.status();
+}
+
+int gather_rows(int dtype, const void* in, const int32_t* idx, int64_t n_src, void* out, int64_t B,
+                int64_t rows_per, int64_t width, hipStream_t s) {
+  const int64_t per = rows_per * width, total = B * per;
+  if (total == 0) return FF_OK;
+  LaunchScope ls("gather_rows", s, 0.0, 2.0 * dtype_size(dtype) * total);
+  if (dtype == FF_BF16) hipLaunchKernelGGL(gather_kernel<true>, dim3(blocks_for(total)), dim3(256), 0, s, in, idx, n_src, out, per, total);
+  else hipLaunchKernelGGL(gather_kernel<false>, dim3(blocks_for(total)), dim3(256), 0, s, in, idx, n_src, out, per, total);
+  return ls.status();
+}
+
+int timestep_sinusoid(const float* t, float* out, int64_t B, hipStream_t s) {
+  LaunchScope ls("timestep_sinusoid", s, 0.0, 4.0 * B * 257);
+  hipLaunchKernelGGL(temb_kernel, dim3(blocks_for(B * 128)), dim3(256), 0, s, t, out, B);
+  return ls.status();
+}
+
+int cast_to_f32(int dtype, const void* in, float* out, int64_t n, hipStream_t s) {
+  if (n == 0) return FF_OK;
+  LaunchScope ls("to_f32", s, 0.0, (dtype_size(dtype) + 4.0) * n);
+  if (dtype == FF_BF16) hipLaunchKernelGGL(to_f32_kernel<true>, dim3(blocks_for(n)), dim3(256), 0, s, in, out, n);
+  else hipLaunchKernelGGL(to_f32_kernel<false>, dim3(blocks_for(n)), dim3(256), 0, s, in, out, n);
+  return ls.status();
+}
+
+int add_table(const void* table, int dtype, const float* e, float* out, int64_t B, int64_t n, hipStream_t s) {
+  LaunchScope ls("add_table", s, 0.0, 8.0 * B * n);
+  if (dtype == FF_BF16) hipLaunchKernelGGL(add_table_kernel<true>, dim3(blocks_for(B * n)), dim3(256), 0, s, table, e, out, B, n);
+  else hipLaunchKernelGGL(add_table_kernel<false>, dim3(blocks_for(B * n)), dim3(256), 0, s, table, e, out, B, n);
+  return ls.status();
+}
+
+}  // namespace ff

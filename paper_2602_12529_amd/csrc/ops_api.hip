@@ -1,0 +1,146 @@
+// C ABI of the kernel-level building blocks (include/ff_ops.h): validation + dispatch.
+#include <cmath>
+
+#include "../../include/ff_ops.h"
+#include "ff_internal.h"
+
+using namespace ff;
+
+namespace {
+int check_dtype(const char* fn, int32_t dt) {
+  if (dt != FF_F32 && dt != FF_BF16) return fail(FF_EINVAL, "%s: bad dtype %d", fn, dt);
+  return FF_OK;
+}
+}  // namespace
+
+extern "C" {
+
+int ff_linear(const void* A, int64_t lda, const void* W, const void* bias, void* out, int64_t ldo, int64_t M,
+              int64_t N, int64_t K, int32_t epi, int64_t gelu_from, const float* gate, int64_t gate_ld,
+              const void* resid, int64_t ldr, int64_t rows_per_sample, int32_t dtype, void* stream) {
+  const char* fn = "ff_linear";
+  FF_TRY(check_dtype(fn, dtype));
+  if (M < 0 || N < 0 || K < 1) return fail(FF_EINVAL, "%s: bad shape M=%lld N=%lld K=%lld", fn, (long long)M, (long long)N, (long long)K);
+  if (M == 0 || N == 0) return FF_OK;
+  if (!A || !W || !out) return fail(FF_EINVAL, "%s: null A, W or out", fn);
+  if (lda < K || ldo < N) return fail(FF_EINVAL, "%s: lda < K or ldo < N", fn);
+  if (epi < FF_EPI_BIAS || epi > FF_EPI_GATED) return fail(FF_EINVAL, "%s: bad epilogue %d", fn, epi);
+  if (epi == FF_EPI_GATED) {
+    if (!gate || !resid) return fail(FF_EINVAL, "%s: gated epilogue needs gate and resid", fn);
+    if (rows_per_sample < 1 || gate_ld < N || ldr < N) return fail(FF_EINVAL, "%s: bad gate/resid layout", fn);
+  }
+  if (!aligned16(A) || !aligned16(W) || !aligned16(out)) return fail(FF_EINVAL, "%s: pointers must be 16-byte aligned", fn);
+  if (dtype == FF_BF16) {
+    if (K % 64) return fail(FF_EUNSUPPORTED, "%s: bf16 needs K %% 64 == 0 (K=%lld)", fn, (long long)K);
+    if (lda % 8) return fail(FF_EINVAL, "%s: bf16 needs lda %% 8 == 0", fn);
+  }
+  GemmArgs g{};
+  g.dtype = dtype;
+  g.M = M; g.N = N; g.K = K;
+  g.A1 = A; g.lda1 = lda; g.K1 = K; g.A2 = nullptr; g.lda2 = 0;
+  g.W = W; g.ldw = K; g.bias = bias;
+  g.out = out; g.ldo = ldo;
+  g.epi = epi; g.gelu_from = gelu_from;
+  g.gate = gate; g.gate_ld = gate_ld; g.resid = resid; g.ldr = ldr;
+  g.rows_per_sample = rows_per_sample > 0 ? rows_per_sample : M;
+  return gemm(g, static_cast<hipStream_t>(stream));
+}
+
+int ff_attention(const void* Q, const void* K, const void* V, void* out, int64_t B, int64_t heads, int64_t n_q,
+                 int64_t n_kv, int64_t head_dim, int32_t dtype, void* stream) {
+  const char* fn = "ff_attention";
+  FF_TRY(check_dtype(fn, dtype));
+  if (B < 0 || heads < 1 || n_q < 0 || n_kv < 1 || head_dim < 1) return fail(FF_EINVAL, "%s: bad shape", fn);
+  if (B == 0 || n_q == 0) return FF_OK;
+  if (!Q || !K || !V || !out) return fail(FF_EINVAL, "%s: null pointer", fn);
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(out)) return fail(FF_EINVAL, "%s: pointers must be 16-byte aligned", fn);
+  if (B * heads > (int64_t{1} << 31)) return fail(FF_EUNSUPPORTED, "%s: too many heads", fn);
+  AttnArgs a{};
+  a.dtype = dtype;
+  a.B = B; a.heads = heads; a.d = head_dim; a.n_q = n_q; a.n_kv = n_kv;
+  a.Q = Q; a.K = K; a.Vt = V;
+  a.out0 = out; a.out1 = out; a.split = n_q; a.ldo = heads * head_dim;
+  a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(head_dim)));
+  return attention(a, static_cast<hipStream_t>(stream));
+}
+
+int ff_norm_modulate(const void* x, void* y, int64_t rows, int64_t H, const float* shift, const float* scale,
+                     int64_t mod_ld, int64_t rows_per_sample, int32_t norm_kind, float eps, int32_t dtype,
+                     void* stream) {
+  const char* fn = "ff_norm_modulate";
+  FF_TRY(check_dtype(fn, dtype));
+  if (rows < 0 || H < 1) return fail(FF_EINVAL, "%s: bad shape", fn);
+  if (rows == 0) return FF_OK;
+  if (!x || !y) return fail(FF_EINVAL, "%s: null x or y", fn);
+  if (norm_kind != FF_NORM_RMS && norm_kind != FF_NORM_LN) return fail(FF_EINVAL, "%s: bad norm_kind", fn);
+  if (!(eps > 0.f)) return fail(FF_EINVAL, "%s: eps must be > 0", fn);
+  if ((shift || scale) && (rows_per_sample < 1 || mod_ld < H)) return fail(FF_EINVAL, "%s: bad modulation layout", fn);
+  NormArgs a{};
+  a.dtype = dtype;
+  a.rows = rows; a.H = H;
+  a.x = x; a.ldx = H; a.y = y; a.ldy = H;
+  a.norm_kind = norm_kind; a.eps = eps;
+  a.shift = shift; a.scale = scale; a.mod_ld = mod_ld;
+  a.w = nullptr; a.bias = nullptr;
+  a.rows_per_sample = rows_per_sample > 0 ? rows_per_sample : rows;
+  return norm_modulate(a, static_cast<hipStream_t>(stream));
+}
+
+int ff_qk_norm_rope(const void* qkv, int64_t B, int64_t n_tok, int64_t heads, int64_t head_dim, const void* q_w,
+                    const void* k_w, float eps, const float* rope, void* Q, void* K, void* V, int64_t n_joint,
+                    int64_t tok_offset, int32_t dtype, void* stream) {
+  const char* fn = "ff_qk_norm_rope";
+  FF_TRY(check_dtype(fn, dtype));
+  if (B < 0 || n_tok < 0 || heads < 1 || head_dim < 2 || head_dim % 2 || head_dim > 128)
+    return fail(FF_EINVAL, "%s: bad shape", fn);
+  if (tok_offset < 0 || tok_offset + n_tok > n_joint) return fail(FF_EINVAL, "%s: tokens outside the joint sequence", fn);
+  if (B == 0 || n_tok == 0) return FF_OK;
+  if (B > 65535 || heads > 65535) return fail(FF_EUNSUPPORTED, "%s: grid too large", fn);
+  if (!qkv || !q_w || !k_w || !Q || !K || !V) return fail(FF_EINVAL, "%s: null pointer", fn);
+  QkvArgs a{};
+  a.dtype = dtype;
+  a.B = B; a.n_tok = n_tok; a.tok_offset = tok_offset; a.n_joint = n_joint; a.src_rows = n_tok;
+  a.heads = static_cast<int>(heads); a.d = static_cast<int>(head_dim);
+  const size_t es = dtype_size(dtype), H = static_cast<size_t>(heads * head_dim);
+  a.q = qkv; a.k = static_cast<const char*>(qkv) + H * es; a.v = static_cast<const char*>(qkv) + 2 * H * es;
+  a.ld = static_cast<int64_t>(3 * H);
+  a.q_w = q_w; a.k_w = k_w; a.full_width_norm = 0; a.apply_norm = 1; a.eps = eps;
+  a.rope = reinterpret_cast<const float2*>(rope);
+  a.Q = Q; a.Kd = K; a.Vt = V;
+  a.v_transposed = dtype == FF_BF16;
+  return qk_norm_rope(a, static_cast<hipStream_t>(stream));
+}
+
+int ff_rope_table(float* out, const int32_t grid[3], int32_t head_dim, const int32_t axes[3], double theta,
+                  void* stream) {
+  const char* fn = "ff_rope_table";
+  if (!out || !grid || !axes) return fail(FF_EINVAL, "%s: null pointer", fn);
+  if (grid[0] < 1 || grid[1] < 1 || grid[2] < 1) return fail(FF_EINVAL, "%s: bad grid", fn);
+  if (head_dim < 2 || head_dim % 2 || axes[0] + axes[1] + axes[2] != head_dim || axes[0] % 2 || axes[1] % 2 ||
+      axes[2] % 2 || axes[0] < 0 || axes[1] < 0 || axes[2] < 0)
+    return fail(FF_EINVAL, "%s: axes must be even and sum to head_dim", fn);
+  if (!(theta > 0)) return fail(FF_EINVAL, "%s: theta must be > 0", fn);
+  return rope_table(reinterpret_cast<float2*>(out), grid, head_dim, axes, theta, static_cast<hipStream_t>(stream));
+}
+
+int ff_skinny_linear(const float* in, const void* W, const void* bias, float* out, int64_t B, int64_t N, int64_t K,
+                     int32_t act_in, int32_t act_out, int32_t dtype, void* stream) {
+  const char* fn = "ff_skinny_linear";
+  FF_TRY(check_dtype(fn, dtype));
+  if (B < 0 || N < 0 || K < 1) return fail(FF_EINVAL, "%s: bad shape", fn);
+  if (B == 0 || N == 0) return FF_OK;
+  if (!in || !W || !out) return fail(FF_EINVAL, "%s: null pointer", fn);
+  if (K % 8) return fail(FF_EUNSUPPORTED, "%s: K must be a multiple of 8", fn);
+  if (act_in < 0 || act_in > 2 || act_out < 0 || act_out > 2) return fail(FF_EINVAL, "%s: bad activation", fn);
+  if (!aligned16(in) || !aligned16(W)) return fail(FF_EINVAL, "%s: pointers must be 16-byte aligned", fn);
+  SkinnyArgs a{};
+  a.dtype = dtype;
+  a.B = B; a.N = N; a.K = K;
+  a.in = in; a.ldi = K; a.act_in = act_in;
+  a.W = W; a.bias = bias;
+  a.out = out; a.ldo = N;
+  a.accumulate = 0; a.act_out = act_out;
+  return skinny_linear(a, static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,115 @@
+"""The K-step Flow-GRPO rollout driven through the C ABI (Sec. 3.1).
+
+Host side: the uniform time grid t_k = 1 - k/K, the sigma schedule of Table 1
+(Flow-SDE with its t = 1 singularity evaluated with 1 - t_1, Dance-SDE, or
+ODE) and the MixGRPO step mask.  Device side (all in libff.so): the DiT
+velocity, the SDE step with its per-sample log-probability, the group
+advantages.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional, Sequence
+
+import torch
+
+from . import api
+from . import configs as C
+
+
+def time_grid(K: int) -> List[float]:
+    return [1.0 - k / K for k in range(K + 1)]
+
+
+def sigma_schedule(ts: Sequence[float], eta: float, kind: str = "flow", sde_steps=None) -> List[float]:
+    """sigma_k of each step k (0 on ODE steps); Table 1."""
+    out = []
+    for k in range(len(ts) - 1):
+        if sde_steps is not None and k not in sde_steps:
+            out.append(0.0)
+            continue
+        t = ts[k]
+        if kind == "flow":
+            tt = ts[1] if t >= 1.0 else t          # 1 - t is 0 at t = 1: use the next grid point
+            out.append(eta * math.sqrt(t / (1.0 - tt)))
+        elif kind == "dance":
+            out.append(float(eta))
+        elif kind == "ode":
+            out.append(0.0)
+        else:
+            raise ValueError(kind)
+    return out
+
+
+@dataclass
+class RolloutResult:
+    xs: List[torch.Tensor]
+    vs: List[torch.Tensor]
+    logp: Dict[int, torch.Tensor]
+    ts: List[float]
+    sigmas: List[float]
+    adv: Optional[torch.Tensor] = None
+    counts: Optional[torch.Tensor] = None
+
+
+class Rollout:
+    """Holds the model handle and the per-step buffers of one workload."""
+
+    def __init__(self, w: C.Workload, dit: api.Dit, device="cuda", keep_velocities: bool = True):
+        self.w = w
+        self.dit = dit
+        self.device = device
+        self.keep_v = keep_velocities
+        m = w.model
+        self.dt = api.torch_dtype(m.dtype)
+        B = w.batch
+        width = m.hidden if m.io_mode == C.IO_HIDDEN else m.in_channels
+        self.shape = (B, w.n_img, width)
+        n_prompts = B if m.io_mode == C.IO_HIDDEN else w.prompts
+        self.ws_dit = api.workspace(dit.workspace_size(B, w.grid, w.n_txt, n_prompts), device)
+        self.ws_sde = api.workspace(api.sde_workspace_size(B, w.latent_dim), device)
+        if w.fixed_step is not None:
+            self.ts = [w.fixed_step[0], w.fixed_step[1]]
+        else:
+            self.ts = time_grid(w.steps)
+        self.sigmas = sigma_schedule(self.ts, w.eta, "flow", w.sde_steps)
+        if w.fixed_step is not None:
+            t, tn = w.fixed_step
+            self.sigmas = [w.eta * math.sqrt(t / (1.0 - t))]
+
+    def run(self, x0, txt, eps_steps, cond=None, txt_index=None, txt_out=None) -> RolloutResult:
+        w, m = self.w, self.w.model
+        B = w.batch
+        x = x0
+        xs, vs, logp = [x0], [], {}
+        t_dev = torch.empty(B, dtype=torch.float32, device=self.device)
+        for k in range(len(self.ts) - 1):
+            t, tn, sigma = self.ts[k], self.ts[k + 1], self.sigmas[k]
+            v = torch.empty(self.shape, dtype=self.dt, device=self.device)
+            if m.io_mode == C.IO_LATENT:
+                t_dev.fill_(t)
+                self.dit.forward(x, txt, w.grid, v, t=t_dev, cond=cond, txt_index=txt_index, ws=self.ws_dit)
+            else:
+                self.dit.forward(x, txt, w.grid, v, cond=cond, txt_out=txt_out, ws=self.ws_dit)
+            x_next = torch.empty_like(x)
+            lp = None
+            if sigma > 0.0:
+                lp = torch.empty(B, dtype=torch.float64, device=self.device)
+                logp[k] = lp
+            api.sde_step(x, v, eps_steps[k], x_next, t, tn, sigma, logp=lp, ws=self.ws_sde)
+            if self.keep_v:
+                vs.append(v)
+            xs.append(x_next)
+            x = x_next
+        return RolloutResult(xs=xs, vs=vs, logp=logp, ts=list(self.ts), sigmas=list(self.sigmas))
+
+    def advantages(self, rewards, weights=None, mode: int = 0, eps: float = 1e-4):
+        B = self.w.batch
+        gid = (torch.arange(B, device=self.device, dtype=torch.int32) // self.w.group).contiguous()
+        n_groups = self.w.prompts
+        if weights is None:
+            weights = torch.ones(rewards.shape[1], dtype=torch.float32, device=self.device)
+        counts = torch.empty(n_groups, dtype=torch.int32, device=self.device)
+        adv = api.group_advantage(rewards, weights, gid, n_groups, mode, eps, counts=counts)
+        return adv, counts

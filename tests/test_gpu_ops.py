@@ -1,0 +1,185 @@
+"""GPU parity of the kernel-level entry points (ff_ops.h) against the oracle's pieces.
+
+Shapes span several tiles and ragged tails (M, N not multiples of the GEMM
+tile; token counts not multiples of the attention tile).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import dit as odit
+from paper_2602_12529_amd import configs as C
+
+from gpu_util import TOL, dev, host, normal, rel, say
+
+pytestmark = pytest.mark.gpu
+
+LIN = [
+    # M, N, K, dtype
+    (256, 256, 64, C.BF16), (300, 200, 128, C.BF16), (1000, 520, 192, C.BF16), (77, 64, 3072, C.BF16),
+    (513, 9216 // 8, 3072, C.BF16), (33, 20, 16, C.F32), (130, 70, 96, C.F32), (64, 256, 64, C.F32),
+]
+
+
+@pytest.mark.parametrize("M,N,K,dt", LIN)
+@pytest.mark.parametrize("epi", ["bias", "gelu", "gelu_from", "gated"])
+def test_linear_parity(gpu_lib, M, N, K, dt, epi):
+    say("linear", M, N, K, dt, epi)
+    a = normal(1, (M, K), dt)
+    w = normal(2, (N, K), dt, 0.05)
+    b = normal(3, (N,), dt, 0.1)
+    rps = max(1, M // 3)
+    nsamp = (M + rps - 1) // rps
+    gate = normal(4, (nsamp, N), C.F32)
+    resid = normal(5, (M, N), dt)
+    A, W, Bv = dev(a, dt), dev(w, dt), dev(b, dt)
+    out = torch.empty((M, N), dtype=A.dtype, device="cuda")
+    z = odit.f64(a) @ odit.f64(w).T + odit.f64(b)
+    kw = {}
+    if epi == "bias":
+        ref = z
+        code = gpu_lib.EPI_BIAS
+    elif epi in ("gelu", "gelu_from"):
+        g0 = 0 if epi == "gelu" else N // 3
+        ref = z.copy()
+        ref[:, g0:] = odit.gelu_tanh(z[:, g0:])
+        code = gpu_lib.EPI_GELU
+        kw["gelu_from"] = g0
+    else:
+        G = dev(gate, C.F32)
+        R = dev(resid, dt)
+        kw.update(gate=G, gate_ld=N, resid=R, rows_per_sample=rps)
+        ref = resid + gate[np.arange(M) // rps] * z
+        code = gpu_lib.EPI_GATED
+    gpu_lib.linear(A, W, Bv, out, epi=code, **kw)
+    torch.cuda.synchronize()
+    got = host(out)
+    err = rel(got, ref)
+    say("  rel", err)
+    assert err <= (2e-6 if dt == C.F32 else 6e-3)
+
+
+def test_linear_in_place_gated_residual(gpu_lib):
+    M, N, K = 256, 384, 128
+    a, w = normal(6, (M, K), C.BF16), normal(7, (N, K), C.BF16, 0.05)
+    x = normal(8, (M, N), C.BF16)
+    g = normal(9, (2, N), C.F32)
+    X = dev(x, C.BF16)
+    gpu_lib.linear(dev(a, C.BF16), dev(w, C.BF16), None, X, epi=gpu_lib.EPI_GATED, gate=dev(g), gate_ld=N, resid=X,
+                   rows_per_sample=128)
+    torch.cuda.synchronize()
+    ref = x + g[np.arange(M) // 128] * (odit.f64(a) @ odit.f64(w).T)
+    assert rel(host(X), ref) <= 6e-3
+
+
+ATT = [
+    # B, heads, n_q (= n_kv), dtype, d
+    (1, 1, 64, C.BF16, 128), (2, 3, 200, C.BF16, 128), (1, 2, 520, C.BF16, 128), (1, 2, 24, C.BF16, 128),
+    (1, 4, 4608, C.BF16, 128), (2, 4, 24, C.F32, 16), (1, 2, 77, C.F32, 64),
+]
+
+
+@pytest.mark.parametrize("B,h,N,dt,d", ATT)
+def test_attention_parity(gpu_lib, B, h, N, dt, d):
+    say("attention", B, h, N, dt, d)
+    q, k, v = (normal(20 + i, (B, h, N, d), dt) for i in range(3))
+    Q, K = dev(q, dt), dev(k, dt)
+    V = dev(v, dt)
+    Vin = V.transpose(-1, -2).contiguous() if dt == C.BF16 else V
+    out = torch.empty((B, N, h * d), dtype=Q.dtype, device="cuda")
+    gpu_lib.attention(Q, K, Vin, out)
+    torch.cuda.synchronize()
+    ref = odit.merge_heads(odit.attention(q, k, v))
+    err = rel(host(out), ref)
+    say("  rel", err)
+    assert err <= (1e-5 if dt == C.F32 else 1e-2)
+
+
+def test_attention_cross_shape(gpu_lib):
+    """Queries and keys of different lengths (n_kv with a 64-key tail)."""
+    B, h, nq, nkv, d = 1, 2, 300, 136, 128
+    q, k, v = normal(30, (B, h, nq, d), C.BF16), normal(31, (B, h, nkv, d), C.BF16), normal(32, (B, h, nkv, d), C.BF16)
+    out = torch.empty((B, nq, h * d), dtype=torch.bfloat16, device="cuda")
+    gpu_lib.attention(dev(q, C.BF16), dev(k, C.BF16), dev(v, C.BF16).transpose(-1, -2).contiguous(), out)
+    torch.cuda.synchronize()
+    assert rel(host(out), odit.merge_heads(odit.attention(q, k, v))) <= 1e-2
+
+
+NORM = [(37, 3072, C.BF16), (10, 64, C.F32), (9, 200, C.BF16), (8, 1536, C.BF16), (5, 96, C.F32)]
+
+
+@pytest.mark.parametrize("rows,H,dt", NORM)
+@pytest.mark.parametrize("kind", [C.NORM_RMS, C.NORM_LN])
+def test_norm_modulate_parity(gpu_lib, rows, H, dt, kind):
+    x = normal(40, (rows, H), dt, 2.0) + 0.3
+    x = x.astype(np.float32) if dt == C.F32 else x
+    rps = max(1, rows // 3)
+    ns = (rows + rps - 1) // rps
+    mod = normal(41, (ns, 3 * H), C.F32, 0.5)
+    X = dev(x, dt)
+    Y = torch.empty_like(X)
+    Mo = dev(mod)
+    gpu_lib.norm_modulate(X, Y, shift=Mo, scale=Mo[:, H:], mod_ld=3 * H, rows_per_sample=rps, norm_kind=kind)
+    torch.cuda.synchronize()
+    xin = host(X)
+    b = np.arange(rows) // rps
+    ref = odit.norm(xin, kind, 1e-6) * (1 + mod[b, H:2 * H]) + mod[b, :H]
+    assert rel(host(Y), ref) <= (1e-5 if dt == C.F32 else 6e-3)
+
+
+@pytest.mark.parametrize("dt", [C.BF16, C.F32], ids=["bf16", "f32"])
+def test_qk_norm_rope_parity(gpu_lib, dt):
+    B, heads, d = 2, 3, 128 if dt == C.BF16 else 16
+    axes = (16, 56, 56) if dt == C.BF16 else (4, 6, 6)
+    grid = (1, 10, 10)
+    n_tok, n_txt = 100, 8
+    n_joint = n_tok + n_txt
+    H = heads * d
+    qkv = normal(50, (B, n_tok, 3 * H), dt)
+    qw, kw = normal(51, (d,), dt, 0.02) + 1, normal(52, (d,), dt, 0.02) + 1
+    QKV = dev(qkv, dt)
+    Qo = torch.zeros((B, heads, n_joint, d), dtype=QKV.dtype, device="cuda")
+    Ko = torch.zeros_like(Qo)
+    Vo = torch.zeros((B, heads, d, n_joint) if dt == C.BF16 else (B, heads, n_joint, d), dtype=QKV.dtype, device="cuda")
+    rope = gpu_lib.rope_table(grid, d, axes)
+    gpu_lib.qk_norm_rope(QKV, heads, d, dev(qw, dt), dev(kw, dt), Qo, Ko, Vo, n_joint, n_txt, rope=rope)
+    torch.cuda.synchronize()
+    ang = odit.rope_angles(odit.grid_positions(grid), axes, 10000.0)
+    q = odit.split_heads(qkv[..., :H].astype(np.float64), heads)
+    k = odit.split_heads(qkv[..., H:2 * H].astype(np.float64), heads)
+    v = odit.split_heads(qkv[..., 2 * H:].astype(np.float64), heads)
+    qr = odit.apply_rope(odit.rms_norm(q, 1e-6) * qw, ang)
+    kr = odit.apply_rope(odit.rms_norm(k, 1e-6) * kw, ang)
+    tol = 1e-5 if dt == C.F32 else 6e-3
+    assert rel(host(Qo)[:, :, n_txt:], qr) <= tol
+    assert rel(host(Ko)[:, :, n_txt:], kr) <= tol
+    vg = host(Vo)
+    vg = np.swapaxes(vg, -1, -2) if dt == C.BF16 else vg
+    assert rel(vg[:, :, n_txt:], v) <= tol
+    assert np.all(host(Qo)[:, :, :n_txt] == 0)      # other stream's rows untouched
+
+
+def test_rope_table_parity(gpu_lib):
+    grid, axes = (3, 5, 7), (44, 42, 42)
+    t = gpu_lib.rope_table(grid, 128, axes)
+    torch.cuda.synchronize()
+    ang = odit.rope_angles(odit.grid_positions(grid), axes, 10000.0)
+    g = t.cpu().numpy().astype(np.float64)
+    assert np.max(np.abs(g[..., 0] - np.cos(ang))) <= 1e-6
+    assert np.max(np.abs(g[..., 1] - np.sin(ang))) <= 1e-6
+
+
+@pytest.mark.parametrize("B,N,K,dt,act", [(8, 200, 3072, C.BF16, 1), (3, 64, 256, C.F32, 0), (16, 100, 64, C.F32, 1),
+                                          (11, 520, 768, C.BF16, 2)])
+def test_skinny_linear_parity(gpu_lib, B, N, K, dt, act):
+    x = normal(60, (B, K), C.F32)
+    w, b = normal(61, (N, K), dt, 0.02), normal(62, (N,), dt, 0.02)
+    out = torch.empty((B, N), dtype=torch.float32, device="cuda")
+    gpu_lib.skinny_linear(dev(x), dev(w, dt), dev(b, dt), out, act_in=act)
+    torch.cuda.synchronize()
+    xa = odit.f64(x)
+    xa = {0: xa, 1: odit.silu(xa), 2: odit.gelu_tanh(xa)}[act]
+    ref = xa @ odit.f64(w).T + odit.f64(b)
+    assert rel(host(out), ref) <= 1e-5

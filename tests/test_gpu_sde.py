@@ -1,0 +1,122 @@
+"""GPU parity of ff_sde_step / ff_logprob / ff_group_advantage against the oracle."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import advantage as oadv
+from oracle import sde as osde
+from paper_2602_12529_amd import configs as C
+
+from gpu_util import LOGP_ABS, TOL, dev, host, normal, rel, say
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [(8, 256), (3, 1000), (1, 1), (2, 7), (5, 12345), (4, 65536), (2, 8 * 2048 + 8)]
+STEPS = [(1.0, 0.75, 0.7 * math.sqrt(1 / 0.25)), (0.6, 0.5, 0.7 * math.sqrt(1.5)), (0.25, 0.0, 0.4)]
+
+
+@pytest.mark.parametrize("dt", [C.F32, C.BF16], ids=["f32", "bf16"])
+@pytest.mark.parametrize("B,D", SHAPES)
+@pytest.mark.parametrize("t,tn,sigma", STEPS)
+def test_sde_step_parity(gpu_lib, dt, B, D, t, tn, sigma):
+    say("sde", dt, B, D, t, tn, sigma)
+    x, v, e = (normal(100 + i, (B, D), dt) for i in range(3))
+    X, V, E = dev(x, dt), dev(v, dt), dev(e, dt)
+    Xn = torch.empty_like(X)
+    lp = torch.empty(B, dtype=torch.float64, device="cuda")
+    gpu_lib.sde_step(X, V, E, Xn, t, tn, sigma, logp=lp)
+    lp2 = torch.empty_like(lp)
+    gpu_lib.logprob(X, V, Xn, lp2, t, tn, sigma)
+    Xn2 = torch.empty_like(X)
+    lp3 = torch.empty_like(lp)
+    gpu_lib.sde_step(X, V, E, Xn2, t, tn, sigma, logp=lp3)
+    torch.cuda.synchronize()
+    ref = osde.sde_step(x, v, e, t, tn, sigma)
+    got = host(Xn)
+    assert rel(got, ref) <= TOL[dt]
+    if dt == C.F32:
+        assert np.max(np.abs(got - ref)) <= 1e-5 * (1 + np.max(np.abs(ref)))
+    # the log-prob of the stored next latent (its rounding is part of the stored value)
+    lp_ref = osde.step_log_prob(x, v, got, t, tn, sigma)
+    assert np.max(np.abs(host(lp) - lp_ref)) <= LOGP_ABS
+    # recomputation and repetition are bitwise identical
+    assert torch.equal(lp, lp2) and torch.equal(lp, lp3) and torch.equal(Xn, Xn2)
+
+
+@pytest.mark.parametrize("dt", [C.F32, C.BF16], ids=["f32", "bf16"])
+def test_ode_step_and_no_logprob(gpu_lib, dt):
+    x, v = normal(7, (4, 999), dt), normal(8, (4, 999), dt)
+    X, V = dev(x, dt), dev(v, dt)
+    Xn = torch.empty_like(X)
+    gpu_lib.sde_step(X, V, X, Xn, 0.7, 0.6, 0.0)
+    torch.cuda.synchronize()
+    assert rel(host(Xn), osde.sde_step(x, v, None, 0.7, 0.6, 0.0)) <= TOL[dt]
+    with pytest.raises(gpu_lib.FFError):
+        gpu_lib.sde_step(X, V, X, Xn, 0.7, 0.6, 0.0, logp=torch.empty(4, dtype=torch.float64, device="cuda"))
+
+
+def test_logprob_at_mean_matches_closed_form(gpu_lib):
+    """x_next = mean exactly (eps = 0 in f32): logp = -D/2 log(2 pi sigma^2 |dt|) per sample."""
+    B, D = 3, 40000
+    x, v = normal(11, (B, D)), normal(12, (B, D))
+    X, V = dev(x), dev(v)
+    Xn = torch.empty_like(X)
+    lp = torch.empty(B, dtype=torch.float64, device="cuda")
+    t, tn, s = 0.8, 0.7, 1.1
+    gpu_lib.sde_step(X, V, torch.zeros_like(X), Xn, t, tn, s, logp=lp)
+    torch.cuda.synchronize()
+    closed = -0.5 * D * math.log(2 * math.pi * s * s * (t - tn))
+    assert np.max(np.abs(host(lp) - closed)) <= LOGP_ABS
+
+
+def test_sde_full_size_flux_block_shape(gpu_lib):
+    """The 1024^2 Flux hidden-state reading of the SDE step: B=8, D=4096*3072, bf16."""
+    B, D = 8, 4096 * 3072
+    t, tn = 0.6, 0.5
+    sigma = 0.7 * math.sqrt(t / (1 - t))
+    say("sde full size", B, D)
+    x, v, e = (normal(200 + i, (B, D), C.BF16) for i in range(3))
+    X, V, E = dev(x, C.BF16), dev(v, C.BF16), dev(e, C.BF16)
+    Xn = torch.empty_like(X)
+    lp = torch.empty(B, dtype=torch.float64, device="cuda")
+    gpu_lib.sde_step(X, V, E, Xn, t, tn, sigma, logp=lp)
+    torch.cuda.synchronize()
+    got = host(Xn)
+    assert rel(got, osde.sde_step(x, v, e, t, tn, sigma)) <= TOL[C.BF16]
+    lp_ref = osde.step_log_prob(x, v, got, t, tn, sigma)
+    assert np.max(np.abs(host(lp) - lp_ref)) <= LOGP_ABS
+
+
+# ------------------------------------------------------------------ advantages
+ADV_CASES = [
+    # N, K, n_groups, mode
+    (8, 1, 2, 0), (16, 1, 1, 0), (64, 3, 8, 0), (64, 3, 8, 1), (1000, 4, 100, 1), (1, 1, 1, 0), (4096, 1, 4096, 0),
+]
+
+
+@pytest.mark.parametrize("N,K,G,mode", ADV_CASES)
+def test_group_advantage_parity(gpu_lib, N, K, G, mode):
+    say("adv", N, K, G, mode)
+    rng = np.random.default_rng(N * 31 + K)
+    r = rng.uniform(0, 1, (N, K)).astype(np.float32)
+    w = rng.uniform(0.5, 2, K).astype(np.float32)
+    gid = rng.permutation(np.arange(N) % G).astype(np.int32)
+    adv = gpu_lib.group_advantage(dev(r), dev(w), torch.from_numpy(gid).cuda(), G, mode,
+                                  counts=(cnt := torch.empty(G, dtype=torch.int32, device="cuda")))
+    torch.cuda.synchronize()
+    ref, ref_cnt = oadv.group_advantages(r, w, gid, G, mode)
+    assert np.array_equal(cnt.cpu().numpy(), ref_cnt)
+    np.testing.assert_allclose(host(adv), ref, rtol=1e-5, atol=1e-5)
+
+
+def test_group_advantage_edge_cases(gpu_lib):
+    r = np.array([[2.0], [2.0], [2.0], [5.0], [1.0], [3.0]], dtype=np.float32)
+    gid = np.array([0, 0, 0, 1, 3, 9], dtype=np.int32)       # group 2 empty; id 9 out of range
+    cnt = torch.empty(4, dtype=torch.int32, device="cuda")
+    adv = gpu_lib.group_advantage(dev(r), dev(np.ones(1)), torch.from_numpy(gid).cuda(), 4, 0, counts=cnt)
+    torch.cuda.synchronize()
+    a = adv.cpu().numpy()
+    assert cnt.cpu().tolist() == [3, 1, 0, 1]
+    assert np.all(a[:5] == 0.0) and np.isnan(a[5])
