@@ -1,0 +1,214 @@
+"""Throughput of the Flow-GRPO rollout hot path on one MI355X.
+
+One step = one pass of the whole hot path over one batch: the DiT velocity
+forward (here one Flux-shaped dual-stream block, B = 8 samples of 4096 image
++ 512 text tokens, hidden 3072, bf16), the SDE step with its per-sample
+log-probability, and the group-normalised advantages.  Inputs are synthetic
+(seeded, N(0, 0.02) weights, N(0, 1) activations) and resident in HBM before
+timing starts.
+
+Prints one JSON line: steps/s (and latent tokens/s), the roofline of the
+dominant kernel measured with HIP events on its launch stream over the timed
+region, and the plain CPU oracle timed on a bounded sample of the same work.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload flux-block|tiny]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "SDE rollout steps/sec and latent tokens/sec per GPU; % bf16 MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3       # MI355X fp32 vector
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="flux-block", choices=["flux-block", "tiny"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-samples", type=int, default=1, help="samples of the batch the oracle times")
+    return ap.parse_args()
+
+
+def main() -> int:
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the rollout would shard by prompt groups with no communication until the advantages).",
+              file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2602_12529_amd import api
+    from paper_2602_12529_amd import configs as C
+    from paper_2602_12529_amd import rollout as R
+    from paper_2602_12529_amd import synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    api.load()
+    w = C.FLUX_BLOCK if args.workload == "flux-block" else C.TINY
+    m = w.model
+    dt = api.torch_dtype(m.dtype)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda().to(dt)
+    print(f"[bench] workload {w.name}: generating inputs", file=sys.stderr, flush=True)
+    W = synth.weights(w)
+    Wd = {k: dev(v) for k, v in W.items()}
+    txt, cond, x0 = synth.text_input(w), synth.cond_input(w), synth.x0(w)
+    eps = [synth.sde_noise(w, k) for k in range(len(R.time_grid(w.steps)) - 1)]
+    T, Cd, X0 = dev(txt), (dev(cond) if cond is not None else None), dev(x0)
+    E = [dev(e) for e in eps]
+    rewards = torch.from_numpy(synth.rewards(w)).cuda()
+    tidx = torch.from_numpy(synth.txt_index(w)).cuda() if m.io_mode == C.IO_LATENT else None
+    dit = api.Dit(m, Wd)
+    ro = R.Rollout(w, dit, keep_velocities=False)
+    txt_out = torch.empty_like(T) if m.io_mode == C.IO_HIDDEN else None
+
+    def step():
+        res = ro.run(X0, T, E, cond=Cd, txt_index=tidx, txt_out=txt_out)
+        ro.advantages(rewards)
+        return res
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    api.profile_reset()
+    api.profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    api.profile_enable(False)
+    prof = api.profile_read()
+    print(f"[bench] timed {args.steps} steps in {elapsed:.3f} s", file=sys.stderr, flush=True)
+
+    ms_per_step = 1e3 * elapsed / args.steps
+    steps_per_s = args.steps / elapsed
+    latent_tok_s = steps_per_s * w.batch * w.n_img
+
+    # Per-kernel achieved rates from HIP events over the timed region.
+    kernels = {}
+    for name, p in prof.items():
+        avg_ms = p["ms"] / max(p["launches"], 1)
+        k = {"launches_per_step": p["launches"] / args.steps, "avg_us": 1e3 * avg_ms,
+             "ms_per_step": p["ms"] / args.steps}
+        if p["flops"] > 0 and name.startswith(("gemm", "attn")):
+            k["tflops"] = p["flops"] / (p["ms"] * 1e-3) / 1e12
+            k["mfma_frac"] = k["tflops"] / (PEAK_BF16_TFLOPS if m.dtype == C.BF16 else PEAK_FP32_TFLOPS)
+        elif p["bytes"] > 0:
+            k["gbs"] = p["bytes"] / (p["ms"] * 1e-3) / 1e9
+            k["hbm_frac"] = k["gbs"] / PEAK_HBM_GBS
+        kernels[name] = k
+    block_flops = sum(p["flops"] for n, p in prof.items() if n.startswith(("gemm", "attn"))) / args.steps
+    dominant = max(prof, key=lambda n: prof[n]["ms"])
+    dp = prof[dominant]
+    compute_bound = dp["flops"] > 0 and dominant.startswith(("gemm", "attn"))
+    if compute_bound:
+        peak = PEAK_BF16_TFLOPS if m.dtype == C.BF16 else PEAK_FP32_TFLOPS
+        achieved = dp["flops"] / (dp["ms"] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
+                "traffic": None, "kernel": dominant,
+                "per_launch": {"flops": dp["flops"] / dp["launches"], "avg_us": 1e3 * dp["ms"] / dp["launches"]}}
+    else:
+        achieved = dp["bytes"] / (dp["ms"] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": achieved / PEAK_HBM_GBS, "traffic": None, "kernel": dominant,
+                "per_launch": {"bytes": dp["bytes"] / dp["launches"], "avg_us": 1e3 * dp["ms"] / dp["launches"]}}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, W, txt, cond, x0, eps, args.cpu_samples)
+
+    out = {
+        "metric": METRIC,
+        "value": steps_per_s,
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if m.dtype == C.BF16 else "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.batch, "img_tokens": w.n_img, "txt_tokens": w.n_txt,
+                   "hidden": m.hidden, "heads": m.heads, "head_dim": m.head_dim, "mlp_hidden": m.mlp_hidden,
+                   "dual_blocks": m.n_dual, "single_blocks": m.n_single, "sde_steps_per_step": len(ro.sigmas),
+                   "t": ro.ts[0], "t_next": ro.ts[1], "sigma": ro.sigmas[0]},
+        "latent_tokens_per_s": latent_tok_s,
+        "sample_steps_per_s": steps_per_s * w.batch,
+        "block_tflops": block_flops / (ms_per_step * 1e-3) / 1e12,
+        "block_mfma_frac": block_flops / (ms_per_step * 1e-3) / 1e12 /
+                           (PEAK_BF16_TFLOPS if m.dtype == C.BF16 else PEAK_FP32_TFLOPS),
+        "roofline": roof,
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def cpu_baseline(w, W, txt, cond, x0, eps, n_samples: int):
+    """The oracle (as it stands) on a bounded sample of the step: n_samples of the batch's samples
+    through the DiT forward, the SDE step and its log-prob, plus the advantages; scaled to steps/s."""
+    import numpy as np
+
+    from oracle import dit as odit
+    from oracle import rollout as orollout
+    from oracle import sde as osde
+    from paper_2602_12529_amd import configs as C
+    from paper_2602_12529_amd import rollout as R
+    from paper_2602_12529_amd import synth
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+    except Exception:  # pragma: no cover
+        threads = 1
+    m = w.model
+    ts = [w.fixed_step[0], w.fixed_step[1]] if w.fixed_step else R.time_grid(w.steps)
+    n = min(n_samples, w.batch)
+    print(f"[bench] cpu baseline: oracle on {n} of {w.batch} samples, {threads} threads", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    x = x0[:n].astype(np.float64)
+    tidx = synth.txt_index(w)[:n]
+    for k in range(len(ts) - 1):
+        t, tn = ts[k], ts[k + 1]
+        sigma = (w.eta * math.sqrt(t / (1 - t))) if w.fixed_step else R.sigma_schedule(ts, w.eta, "flow", w.sde_steps)[k]
+        if m.io_mode == C.IO_HIDDEN:
+            v, _ = odit.forward(m, W, x, txt[:n], cond=cond[:n], grid=w.grid)
+        else:
+            v = odit.forward(m, W, x, txt, t=np.full(n, t), cond=cond, txt_index=tidx, grid=w.grid)
+        xn = osde.sde_step(x, v, eps[k][:n], t, tn, sigma)
+        if sigma > 0:
+            osde.step_log_prob(x, v, xn, t, tn, sigma)
+        x = xn
+    orollout.advantages_for(synth.rewards(w), w.group)
+    el = time.perf_counter() - t0
+    per_step = el * (w.batch / n)
+    return {"value": 1.0 / per_step, "unit": "steps/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n} of {w.batch} samples of one step (DiT forward fp64, SDE step, log-prob, advantages), "
+                      f"{el:.1f} s measured, scaled by {w.batch}/{n} to the full batch"}
+
+
+if __name__ == "__main__":
+    sys.exit(main())

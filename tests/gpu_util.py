@@ -18,7 +18,7 @@ def dev(a, code=C.F32):
 
 
 def host(t):
-    return t.detach().float().cpu().numpy().astype(np.float64)
+    return t.detach().to(torch.float64).cpu().numpy()
 
 
 def rel(a, b):
