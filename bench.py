@@ -38,7 +38,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="flux-block", choices=["flux-block", "tiny"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-samples", type=int, default=1, help="samples of the batch the oracle times")
+    ap.add_argument("--cpu-samples", type=int, default=3, help="samples of the batch the oracle times")
     return ap.parse_args()
 
 

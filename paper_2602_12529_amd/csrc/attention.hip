@@ -40,13 +40,13 @@ constexpr int KT = 64;                   // keys per tile
 constexpr int K_STAGE = KT * D * 2;      // bytes of one K tile (64 rows x 256 B)
 constexpr int V_STAGE = D * KT * 2;      // bytes of one V^T tile (128 rows x 128 B)
 
-// LDS position of 16-byte chunk c of K row r (16 chunks per 256-byte row).
-__device__ __forceinline__ int k_off(int r, int c) {
-  const int f = (r & 3) | ((r >> 1) & 4);
-  return r * 256 + ((c ^ f) << 4);
-}
-// LDS position of 16-byte chunk c of V^T row r (8 chunks per 128-byte row).
-__device__ __forceinline__ int v_off(int r, int c) { return r * 128 + ((c ^ (r & 7)) << 4); }
+// LDS layouts.  gfx950's LDS serves 16-byte-per-lane reads for 16 lanes per
+// clock over 64 banks (256 bytes); the chunk swizzles below put the fragment
+// rows read by 16 consecutive lanes on 16 distinct bank groups.
+// 16-byte chunk c of K row r (16 chunks per 256-byte row).
+__device__ __forceinline__ int k_off(int r, int c) { return r * 256 + ((c ^ (r & 15)) << 4); }
+// 16-byte chunk c of V^T row r (8 chunks per 128-byte row).
+__device__ __forceinline__ int v_off(int r, int c) { return r * 128 + ((c ^ ((r >> 1) & 7)) << 4); }
 
 template <int WAVES>
 __global__ __launch_bounds__(WAVES * 64, 2) void attn_bf16_d128(AttnParams p) {

@@ -4,10 +4,12 @@
 // are both K-contiguous (nn.Linear layout).  A workgroup computes a BM x BN
 // tile; its waves split it into wave tiles of (BM/WAVES_M) x (BN/WAVES_N),
 // each a grid of 32x32 MFMA blocks.  K advances in slabs of 64 that are
-// staged global -> registers -> LDS with two LDS buffers (the next slab's
-// global loads are in flight while the current slab is multiplied).  Each
-// 128-byte LDS row holds 8 chunks of 16 bytes stored at chunk ^ (row & 7), so
-// the 16-byte fragment reads of 8 consecutive rows hit distinct banks.
+// staged into LDS with two buffers (the next slab's global loads are in
+// flight while the current slab is multiplied), either through registers or
+// with direct global->LDS loads.  gfx950's LDS serves a 16-byte-per-lane read
+// for 16 lanes per clock across 64 banks (256 bytes): each 128-byte LDS row
+// holds 8 chunks of 16 bytes stored at chunk ^ ((row >> 1) & 7), so the
+// fragment reads of 16 consecutive rows land on 16 distinct bank groups.
 // Tiles are ordered so that consecutive tiles of one XCD (workgroups are
 // dealt round-robin over the 8 XCDs) share A rows in that XCD's L2.
 //
@@ -16,6 +18,8 @@
 //
 // f32: a plain LDS-tiled FMA kernel with the same epilogues, for the float32
 // configurations.
+#include <cstdlib>
+
 #include "dev.h"
 #include "ff_internal.h"
 
@@ -24,6 +28,9 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_t;
+typedef __attribute__((address_space(1))) void glb_t;
 
 struct GemmParams {
   int64_t M, N, K;
@@ -36,6 +43,7 @@ struct GemmParams {
   const float* gate; int64_t gate_ld;
   const void* resid; int64_t ldr;
   int64_t rows_per_sample;
+  int vec_ok;   // 16-byte vector access of bias, gate, resid and out is aligned
 };
 
 template <bool BF16, int EPI>
@@ -71,7 +79,72 @@ __device__ __forceinline__ void tile_coords(int64_t pid, int64_t num_m, int64_t 
 
 constexpr int BK = 64;
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI>
+// Epilogue of one wave's FM x FN grid of 32x32 accumulator blocks.  Each block
+// goes through a per-wave 32 x 36 float scratch in LDS (the K loop is over, so
+// LDS is free) and comes back row-major: lane l owns row l/2, 16 consecutive
+// columns, so bias, gate and residual are read and the output written with
+// 16-byte vector accesses, one sample-index division per row.
+template <int EPI, int FM, int FN>
+__device__ __forceinline__ void epilogue_blocks(const GemmParams& p, const f32x16_t (&acc)[FM][FN], int64_t mw,
+                                                int64_t nw, float* scratch, int lane) {
+  const int frow = lane & 31, fhalf = lane >> 5;
+  const int rr = lane >> 1, cc = (lane & 1) * 16;
+  const bf16_t* bias = static_cast<const bf16_t*>(p.bias);
+  bf16_t* out = static_cast<bf16_t*>(p.out);
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) scratch[(8 * (r >> 2) + 4 * fhalf + (r & 3)) * 36 + frow] = acc[i][j][r];
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      float v[16];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 t = *reinterpret_cast<const float4*>(scratch + rr * 36 + cc + 4 * q);
+        v[4 * q] = t.x; v[4 * q + 1] = t.y; v[4 * q + 2] = t.z; v[4 * q + 3] = t.w;
+      }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      const int64_t m = mw + i * 32 + rr;
+      const int64_t n = nw + j * 32 + cc;
+      if (m >= p.M || n >= p.N) continue;
+      if (p.vec_ok && n + 16 <= p.N) {
+        if (bias) {
+          float b[16];
+          ld8<true>(bias, n, *reinterpret_cast<float(*)[8]>(b));
+          ld8<true>(bias, n + 8, *reinterpret_cast<float(*)[8]>(b + 8));
+#pragma unroll
+          for (int e = 0; e < 16; ++e) v[e] += b[e];
+        }
+        if constexpr (EPI == EPI_GELU) {
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            if (n + e >= p.gelu_from) v[e] = gelu_tanh_f(v[e]);
+        } else if constexpr (EPI == EPI_GATED) {
+          const uint64_t smp = static_cast<uint64_t>(m) / static_cast<uint64_t>(p.rows_per_sample);
+          const float* g = p.gate + smp * p.gate_ld + n;
+          float rs[16];
+          ld8<true>(p.resid, m * p.ldr + n, *reinterpret_cast<float(*)[8]>(rs));
+          ld8<true>(p.resid, m * p.ldr + n + 8, *reinterpret_cast<float(*)[8]>(rs + 8));
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float4 t = *reinterpret_cast<const float4*>(g + 4 * q);
+            v[4 * q] = fmaf(t.x, v[4 * q], rs[4 * q]);
+            v[4 * q + 1] = fmaf(t.y, v[4 * q + 1], rs[4 * q + 1]);
+            v[4 * q + 2] = fmaf(t.z, v[4 * q + 2], rs[4 * q + 2]);
+            v[4 * q + 3] = fmaf(t.w, v[4 * q + 3], rs[4 * q + 3]);
+          }
+        }
+        st8<true>(out, m * p.ldo + n, *reinterpret_cast<const float(*)[8]>(v));
+        st8<true>(out, m * p.ldo + n + 8, *reinterpret_cast<const float(*)[8]>(v + 8));
+      } else {
+        for (int e = 0; e < 16 && n + e < p.N; ++e) epi_store<true, EPI>(p, m, n + e, v[e]);
+      }
+    }
+}
+
+
+template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI, bool DIRECT, bool SCHED>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_bf16_kernel(GemmParams p) {
   constexpr int THREADS = WAVES_M * WAVES_N * 64;
   constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
@@ -89,48 +162,213 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_bf16_kernel(Gem
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
 
-  // Global source rows/chunks of this thread (fixed across K).
-  const bf16_t* A1 = static_cast<const bf16_t*>(p.A1);
-  const bf16_t* A2 = static_cast<const bf16_t*>(p.A2);
-  const bf16_t* Wp = static_cast<const bf16_t*>(p.W);
-  int a_row[A_LOADS], b_row[B_LOADS];
-  int64_t a_grow[A_LOADS], b_grow[B_LOADS];
-  const int chunk = tid & 7;
+  // Global source pointers of this thread.
+  //  staged (DIRECT = false): row (tid + i*THREADS)/8, 16-byte chunk tid%8, written to LDS by
+  //    the thread at chunk ^ (row & 7);
+  //  direct (DIRECT = true): one wave instruction fills a contiguous 1 KB of LDS (8 rows),
+  //    lane l landing at byte 16 l, i.e. row l/8, stored chunk l%8, so the lane fetches the
+  //    logical chunk (l%8) ^ (row & 7) from global memory.
+  // Rows past the matrix edge are clamped.
+  constexpr int WAVES = WAVES_M * WAVES_N;
+  auto a_row_of = [&](int i) { return DIRECT ? (i * WAVES + wave) * 8 + (lane >> 3) : (tid + i * THREADS) >> 3; };
+  auto b_row_of = a_row_of;
+  const int chunk_st = tid & 7;
+  const bf16_t* a_src[A_LOADS];
+  const bf16_t* b_src[B_LOADS];
+  int a_lds[A_LOADS], b_lds[B_LOADS], a_ck[A_LOADS];
 #pragma unroll
   for (int i = 0; i < A_LOADS; ++i) {
-    a_row[i] = (tid + i * THREADS) >> 3;
-    int64_t g = m0 + a_row[i];
-    a_grow[i] = g < p.M ? g : p.M - 1;
+    const int row = a_row_of(i);
+    const int64_t g = m0 + row < p.M ? m0 + row : p.M - 1;
+    a_ck[i] = DIRECT ? ((lane & 7) ^ ((row >> 1) & 7)) : chunk_st;
+    a_src[i] = static_cast<const bf16_t*>(p.A1) + g * p.lda1 + a_ck[i] * 8;
+    a_lds[i] = DIRECT ? (i * WAVES + wave) * 1024 : row * 128 + ((chunk_st ^ ((row >> 1) & 7)) << 4);
   }
 #pragma unroll
   for (int i = 0; i < B_LOADS; ++i) {
-    b_row[i] = (tid + i * THREADS) >> 3;
-    int64_t g = n0 + b_row[i];
-    b_grow[i] = g < p.N ? g : p.N - 1;
+    const int row = b_row_of(i);
+    const int64_t g = n0 + row < p.N ? n0 + row : p.N - 1;
+    const int ck = DIRECT ? ((lane & 7) ^ ((row >> 1) & 7)) : chunk_st;
+    b_src[i] = static_cast<const bf16_t*>(p.W) + g * p.ldw + ck * 8;
+    b_lds[i] = BM * BK * 2 + (DIRECT ? (i * WAVES + wave) * 1024 : row * 128 + ((chunk_st ^ ((row >> 1) & 7)) << 4));
   }
 
-  uint4 ra[A_LOADS], rb[B_LOADS];
-  auto load_slab = [&](int64_t k0) {
-    const bf16_t* src;
-    int64_t ld, kc;
-    if (k0 < p.K1) { src = A1; ld = p.lda1; kc = k0; }
-    else { src = A2; ld = p.lda2; kc = k0 - p.K1; }
+  f32x16_t acc[FM][FN];
 #pragma unroll
-    for (int i = 0; i < A_LOADS; ++i)
-      ra[i] = *reinterpret_cast<const uint4*>(src + a_grow[i] * ld + kc + chunk * 8);
+  for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int i = 0; i < B_LOADS; ++i)
-      rb[i] = *reinterpret_cast<const uint4*>(Wp + b_grow[i] * p.ldw + k0 + chunk * 8);
-  };
-  auto store_slab = [&](int buf) {
-    char* As = smem + buf * STAGE;
-    char* Bs = As + BM * BK * 2;
+    for (int j = 0; j < FN; ++j)
 #pragma unroll
-    for (int i = 0; i < A_LOADS; ++i)
-      *reinterpret_cast<uint4*>(As + a_row[i] * 128 + ((chunk ^ (a_row[i] & 7)) << 4)) = ra[i];
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int frow = lane & 31, fhalf = lane >> 5;
+  // LDS byte offsets of this lane's fragment rows (chunk 0), and the row's swizzle key.
+  int a_frag[FM], b_frag[FN];
 #pragma unroll
-    for (int i = 0; i < B_LOADS; ++i)
-      *reinterpret_cast<uint4*>(Bs + b_row[i] * 128 + ((chunk ^ (b_row[i] & 7)) << 4)) = rb[i];
+  for (int i = 0; i < FM; ++i) a_frag[i] = (wm * TM + i * 32 + frow) * 128;
+#pragma unroll
+  for (int j = 0; j < FN; ++j) b_frag[j] = BM * BK * 2 + (wn * TN + j * 32 + frow) * 128;
+  const int key = (frow >> 1) & 7;   // the same for every fragment row of this lane
+
+  const int64_t KT = p.K / BK;
+  const int64_t KT1 = p.K1 / BK;   // slab at which A switches to the second source
+  u32x4_t ra[DIRECT ? 1 : A_LOADS], rb[DIRECT ? 1 : B_LOADS];
+
+  // Issue the global loads of the current source pointers into stage `buf`
+  // (direct) or into registers (staged).
+#define FF_GEMM_ISSUE(buf)                                                                          \
+  if constexpr (DIRECT) {                                                                          \
+    _Pragma("unroll") for (int i = 0; i < A_LOADS; ++i)                                            \
+      __builtin_amdgcn_global_load_lds((const glb_t*)a_src[i], (lds_t*)(smem + (buf) * STAGE + a_lds[i]), 16, 0, 0); \
+    _Pragma("unroll") for (int i = 0; i < B_LOADS; ++i)                                            \
+      __builtin_amdgcn_global_load_lds((const glb_t*)b_src[i], (lds_t*)(smem + (buf) * STAGE + b_lds[i]), 16, 0, 0); \
+  } else {                                                                                         \
+    _Pragma("unroll") for (int i = 0; i < A_LOADS; ++i) ra[DIRECT ? 0 : i] = *reinterpret_cast<const u32x4_t*>(a_src[i]); \
+    _Pragma("unroll") for (int i = 0; i < B_LOADS; ++i) rb[DIRECT ? 0 : i] = *reinterpret_cast<const u32x4_t*>(b_src[i]); \
+  }
+#define FF_GEMM_COMMIT(buf)                                                                        \
+  if constexpr (DIRECT) {                                                                          \
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");                                               \
+  } else {                                                                                         \
+    char* D_ = smem + (buf) * STAGE;                                                               \
+    _Pragma("unroll") for (int i = 0; i < A_LOADS; ++i) *reinterpret_cast<u32x4_t*>(D_ + a_lds[i]) = ra[DIRECT ? 0 : i]; \
+    _Pragma("unroll") for (int i = 0; i < B_LOADS; ++i) *reinterpret_cast<u32x4_t*>(D_ + b_lds[i]) = rb[DIRECT ? 0 : i]; \
+  }
+
+  FF_GEMM_ISSUE(0)
+  FF_GEMM_COMMIT(0)
+  __syncthreads();
+
+  for (int64_t kt = 0; kt < KT; ++kt) {
+    const int buf = static_cast<int>(kt & 1);
+    const bool more = kt + 1 < KT;
+    if (more) {
+      if (kt + 1 == KT1) {
+        // continue K in the second A source
+#pragma unroll
+        for (int i = 0; i < A_LOADS; ++i) {
+          const int row = a_row_of(i);
+          const int64_t g = m0 + row < p.M ? m0 + row : p.M - 1;
+          a_src[i] = static_cast<const bf16_t*>(p.A2) + g * p.lda2 + a_ck[i] * 8;
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < A_LOADS; ++i) a_src[i] += BK;
+      }
+#pragma unroll
+      for (int i = 0; i < B_LOADS; ++i) b_src[i] += BK;
+      FF_GEMM_ISSUE(buf ^ 1)
+    }
+    const char* S = smem + buf * STAGE;
+    // Fragments of k16 step ks + 1 are read while the MFMAs of step ks run.
+    bf16x8_t af[2][FM], bfr[2][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) af[0][i] = *reinterpret_cast<const bf16x8_t*>(S + a_frag[i] + ((fhalf ^ key) << 4));
+#pragma unroll
+    for (int j = 0; j < FN; ++j) bfr[0][j] = *reinterpret_cast<const bf16x8_t*>(S + b_frag[j] + ((fhalf ^ key) << 4));
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      const int cur = ks & 1;
+      if (ks + 1 < BK / 16) {
+        const int coff = (((ks + 1) * 2 + fhalf) ^ key) << 4;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) af[cur ^ 1][i] = *reinterpret_cast<const bf16x8_t*>(S + a_frag[i] + coff);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) bfr[cur ^ 1][j] = *reinterpret_cast<const bf16x8_t*>(S + b_frag[j] + coff);
+      }
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
+      if constexpr (SCHED) {
+        // interleave: one MFMA, then one LDS read, while reads remain
+#pragma unroll
+        for (int m = 0; m < FM * FN; ++m) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          if (ks + 1 < BK / 16 && m < FM + FN) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+      }
+    }
+    if (more) {
+      FF_GEMM_COMMIT(buf ^ 1)
+    }
+    __syncthreads();
+  }
+#undef FF_GEMM_ISSUE
+#undef FF_GEMM_COMMIT
+
+  // acc[i][j][r] holds C[row, col] with col = lane % 32 and row = 8 (r / 4) + 4 (lane / 32) + r % 4.
+  __syncthreads();
+  epilogue_blocks<EPI, FM, FN>(p, acc, m0 + wm * TM, n0 + wn * TN,
+                               reinterpret_cast<float*>(smem) + wave * 32 * 36, lane);
+}
+
+// ------------------------------------------------------------------ bf16, multi-stage
+// 256 x 256 tile, 8 waves of 128 x 64, K slabs of 32 in a ring of STAGES LDS
+// buffers filled by direct global->LDS loads issued STAGES-1 slabs ahead, so
+// global latency is covered by several slabs of MFMA work.  A 64-byte LDS row
+// holds 4 chunks of 16 bytes at chunk ^ ((row >> 2) & 3): the fragment reads
+// of 16 consecutive rows then hit 16 distinct bank groups.  Each wave reads all
+// fragments of a slab, then runs its MFMAs at raised priority, so the two
+// waves sharing a SIMD alternate between LDS reads and MFMA.
+template <int EPI, int STAGES>
+__global__ __launch_bounds__(512, 1) void gemm_bf16_ms(GemmParams p) {
+  constexpr int BM = 256, BN = 256, K32 = 32, WAVES = 8, WAVES_N = 4;
+  constexpr int TM = 128, TN = 64, FM = 4, FN = 2;
+  constexpr int A_INS = BM * 64 / 1024 / WAVES;   // 1 KB direct loads per wave per slab (A)
+  constexpr int B_INS = BN * 64 / 1024 / WAVES;
+  constexpr int LPW = A_INS + B_INS;
+  constexpr int STAGE = (BM + BN) * K32 * 2;      // 32 KB
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+
+  const int64_t num_m = (p.M + BM - 1) / BM, num_n = (p.N + BN - 1) / BN;
+  int64_t tm, tn;
+  tile_coords(blockIdx.x, num_m, num_n, tm, tn);
+  const int64_t m0 = tm * BM, n0 = tn * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+
+  // Direct load i of this wave fills rows 16 (i*WAVES + wave) .. +15 of the tile;
+  // lane l lands at row + l/4, stored chunk l%4, so it fetches logical chunk
+  // (l%4) ^ ((row >> 2) & 3) = (l%4) ^ ((l >> 4) & 3).
+  const int ck = (lane & 3) ^ ((lane >> 4) & 3);
+  const bf16_t* a_src[A_INS];
+  const bf16_t* b_src[B_INS];
+  int a_row[A_INS];
+#pragma unroll
+  for (int i = 0; i < A_INS; ++i) {
+    a_row[i] = (i * WAVES + wave) * 16 + (lane >> 2);
+    const int64_t g = m0 + a_row[i] < p.M ? m0 + a_row[i] : p.M - 1;
+    a_src[i] = static_cast<const bf16_t*>(p.A1) + g * p.lda1 + ck * 8;
+  }
+#pragma unroll
+  for (int i = 0; i < B_INS; ++i) {
+    const int row = (i * WAVES + wave) * 16 + (lane >> 2);
+    const int64_t g = n0 + row < p.N ? n0 + row : p.N - 1;
+    b_src[i] = static_cast<const bf16_t*>(p.W) + g * p.ldw + ck * 8;
+  }
+  const int64_t KT = p.K / K32, KT1 = p.K1 / K32;
+
+  auto issue = [&](int64_t slab, int stage) {
+    if (slab == KT1 && slab > 0) {
+#pragma unroll
+      for (int i = 0; i < A_INS; ++i) {
+        const int64_t g = m0 + a_row[i] < p.M ? m0 + a_row[i] : p.M - 1;
+        a_src[i] = static_cast<const bf16_t*>(p.A2) + g * p.lda2 + ck * 8;
+      }
+    }
+    char* base = smem + stage * STAGE;
+#pragma unroll
+    for (int i = 0; i < A_INS; ++i) {
+      __builtin_amdgcn_global_load_lds((const glb_t*)a_src[i], (lds_t*)(base + (i * WAVES + wave) * 1024), 16, 0, 0);
+      a_src[i] += K32;
+    }
+#pragma unroll
+    for (int i = 0; i < B_INS; ++i) {
+      __builtin_amdgcn_global_load_lds((const glb_t*)b_src[i], (lds_t*)(base + BM * 64 + (i * WAVES + wave) * 1024), 16, 0, 0);
+      b_src[i] += K32;
+    }
   };
 
   f32x16_t acc[FM][FN];
@@ -141,54 +379,187 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_bf16_kernel(Gem
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  const int64_t KT = p.K / BK;
-  load_slab(0);
-  store_slab(0);
-  __syncthreads();
-
   const int frow = lane & 31, fhalf = lane >> 5;
+  const int key = (frow >> 2) & 3;
+  int a_frag[FM], b_frag[FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) a_frag[i] = (wm * TM + i * 32 + frow) * 64;
+#pragma unroll
+  for (int j = 0; j < FN; ++j) b_frag[j] = BM * 64 + (wn * TN + j * 32 + frow) * 64;
+
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < KT) issue(s, s);
+
   for (int64_t kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < KT) load_slab((kt + 1) * BK);
-    const char* As = smem + buf * STAGE;
-    const char* Bs = As + BM * BK * 2;
+    // slab kt has landed once at most min(STAGES-2, KT-1-kt) younger slabs are in flight
+    const int64_t younger = KT - 1 - kt;
+    if (younger >= STAGES - 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"((STAGES - 2) * LPW) : "memory");
+    else if (younger == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPW) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    if (kt + STAGES - 1 < KT) issue(kt + STAGES - 1, static_cast<int>((kt + STAGES - 1) % STAGES));
+    const char* S = smem + (kt % STAGES) * STAGE;
+    bf16x8_t af[2][FM], bfr[2][FN];
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int c = ks * 2 + fhalf;
-      bf16x8_t af[FM], bfr[FN];
+    for (int ks = 0; ks < 2; ++ks) {
+      const int coff = ((ks * 2 + fhalf) ^ key) << 4;
 #pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        const int row = wm * TM + i * 32 + frow;
-        af[i] = *reinterpret_cast<const bf16x8_t*>(As + row * 128 + ((c ^ (row & 7)) << 4));
-      }
+      for (int i = 0; i < FM; ++i) af[ks][i] = *reinterpret_cast<const bf16x8_t*>(S + a_frag[i] + coff);
 #pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int row = wn * TN + j * 32 + frow;
-        bfr[j] = *reinterpret_cast<const bf16x8_t*>(Bs + row * 128 + ((c ^ (row & 7)) << 4));
-      }
+      for (int j = 0; j < FN; ++j) bfr[ks][j] = *reinterpret_cast<const bf16x8_t*>(S + b_frag[j] + coff);
+    }
+    __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-    }
-    if (kt + 1 < KT) store_slab(buf ^ 1);
-    __syncthreads();
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks][i], bfr[ks][j], acc[i][j], 0, 0, 0);
+    __builtin_amdgcn_s_setprio(0);
   }
 
-  // acc[i][j][r] holds C[row, col] with col = lane % 32 and row = 8 (r / 4) + 4 (lane / 32) + r % 4.
+  __syncthreads();
+  epilogue_blocks<EPI, FM, FN>(p, acc, m0 + wm * TM, n0 + wn * TN,
+                               reinterpret_cast<float*>(smem) + wave * 32 * 36, lane);
+}
+
+// ------------------------------------------------------------------ bf16, ping-pong
+// Same tile, LDS ring and loads as gemm_bf16_ms, scheduled as two groups of
+// four waves (one wave of each group per SIMD) offset by one barrier: while
+// one group runs its MFMA cluster on slab k, the other reads slab k's
+// fragments from LDS and issues the direct loads of slab k + STAGES - 1.
+// Every phase ends with a workgroup barrier, so on each SIMD the matrix core
+// is fed by one wave while the other wave's memory work is hidden.
+template <int STAGES, int LPW>
+__device__ __forceinline__ void wait_slab_after(int64_t n_after) {
+  // at most n_after younger slabs (LPW loads each) may still be in flight
+  if (n_after >= STAGES - 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"((STAGES - 2) * LPW) : "memory");
+  else if (n_after == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPW) : "memory");
+  else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+// Workgroup barrier that no instruction (memory or not) is scheduled across.
+__device__ __forceinline__ void wg_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_barrier" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+template <int EPI, int STAGES>
+__global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmParams p) {
+  constexpr int BM = 256, BN = 256, K32 = 32, WAVES = 8, WAVES_N = 4;
+  constexpr int TM = 128, TN = 64, FM = 4, FN = 2;
+  constexpr int A_INS = BM * 64 / 1024 / WAVES;
+  constexpr int B_INS = BN * 64 / 1024 / WAVES;
+  constexpr int LPW = A_INS + B_INS;
+  constexpr int STAGE = (BM + BN) * K32 * 2;
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+
+  const int64_t num_m = (p.M + BM - 1) / BM, num_n = (p.N + BN - 1) / BN;
+  int64_t tm, tn;
+  tile_coords(blockIdx.x, num_m, num_n, tm, tn);
+  const int64_t m0 = tm * BM, n0 = tn * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+  const int grp = wave >> 2;
+
+  const int ck = (lane & 3) ^ ((lane >> 4) & 3);
+  const bf16_t* a_src[A_INS];
+  const bf16_t* b_src[B_INS];
+  int a_row[A_INS];
+#pragma unroll
+  for (int i = 0; i < A_INS; ++i) {
+    a_row[i] = (i * WAVES + wave) * 16 + (lane >> 2);
+    const int64_t g = m0 + a_row[i] < p.M ? m0 + a_row[i] : p.M - 1;
+    a_src[i] = static_cast<const bf16_t*>(p.A1) + g * p.lda1 + ck * 8;
+  }
+#pragma unroll
+  for (int i = 0; i < B_INS; ++i) {
+    const int row = (i * WAVES + wave) * 16 + (lane >> 2);
+    const int64_t g = n0 + row < p.N ? n0 + row : p.N - 1;
+    b_src[i] = static_cast<const bf16_t*>(p.W) + g * p.ldw + ck * 8;
+  }
+  const int64_t KT = p.K / K32, KT1 = p.K1 / K32;
+
+  auto issue = [&](int64_t slab, int stage) {
+    if (slab == KT1 && slab > 0) {
+#pragma unroll
+      for (int i = 0; i < A_INS; ++i) {
+        const int64_t g = m0 + a_row[i] < p.M ? m0 + a_row[i] : p.M - 1;
+        a_src[i] = static_cast<const bf16_t*>(p.A2) + g * p.lda2 + ck * 8;
+      }
+    }
+    char* base = smem + stage * STAGE;
+#pragma unroll
+    for (int i = 0; i < A_INS; ++i) {
+      __builtin_amdgcn_global_load_lds((const glb_t*)a_src[i], (lds_t*)(base + (i * WAVES + wave) * 1024), 16, 0, 0);
+      a_src[i] += K32;
+    }
+#pragma unroll
+    for (int i = 0; i < B_INS; ++i) {
+      __builtin_amdgcn_global_load_lds((const glb_t*)b_src[i], (lds_t*)(base + BM * 64 + (i * WAVES + wave) * 1024), 16, 0, 0);
+      b_src[i] += K32;
+    }
+  };
+
+  f32x16_t acc[FM][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      const int64_t n = n0 + wn * TN + j * 32 + frow;
-      if (n >= p.N) continue;
+    for (int j = 0; j < FN; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t m = m0 + wm * TM + i * 32 + 8 * (r >> 2) + 4 * fhalf + (r & 3);
-        if (m < p.M) epi_store<true, EPI>(p, m, n, acc[i][j][r]);
-      }
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int frow = lane & 31, fhalf = lane >> 5;
+  const int key = (frow >> 2) & 3;
+  int a_frag[FM], b_frag[FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) a_frag[i] = (wm * TM + i * 32 + frow) * 64;
+#pragma unroll
+  for (int j = 0; j < FN; ++j) b_frag[j] = BM * 64 + (wn * TN + j * 32 + frow) * 64;
+
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < KT) issue(s, s);
+  wait_slab_after<STAGES, LPW>(KT - 1 < STAGES - 2 ? KT - 1 : STAGES - 2);
+  wg_barrier();
+  if (grp == 1) wg_barrier();
+
+  for (int64_t kt = 0; kt < KT; ++kt) {
+    // memory phase: fragments of slab kt, loads of slab kt + STAGES - 1
+    const char* S = smem + (kt % STAGES) * STAGE;
+    bf16x8_t af[2][FM], bfr[2][FN];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const int coff = ((ks * 2 + fhalf) ^ key) << 4;
+#pragma unroll
+      for (int i = 0; i < FM; ++i) af[ks][i] = *reinterpret_cast<const bf16x8_t*>(S + a_frag[i] + coff);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) bfr[ks][j] = *reinterpret_cast<const bf16x8_t*>(S + b_frag[j] + coff);
     }
+    if (kt + STAGES - 1 < KT) issue(kt + STAGES - 1, static_cast<int>((kt + STAGES - 1) % STAGES));
+    const int64_t n_after = KT - 2 - kt;   // slabs younger than kt + 1 that may stay in flight
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    if (grp == 1 && n_after >= 0) wait_slab_after<STAGES, LPW>(n_after);
+    wg_barrier();
+    // compute phase
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks][i], bfr[ks][j], acc[i][j], 0, 0, 0);
+    if (grp == 0 && n_after >= 0) wait_slab_after<STAGES, LPW>(n_after);
+    wg_barrier();
+  }
+  if (grp == 0) wg_barrier();
+
+  __syncthreads();
+  epilogue_blocks<EPI, FM, FN>(p, acc, m0 + wm * TM, n0 + wn * TN,
+                               reinterpret_cast<float*>(smem) + wave * 32 * 36, lane);
 }
 
 // ------------------------------------------------------------------ float32
@@ -240,27 +611,79 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
     }
 }
 
-template <int BM, int BN, int WM, int WN, int EPI>
+template <int BM, int BN, int WM, int WN, int EPI, bool DIRECT, bool SCHED = false>
 int launch_bf16(const GemmParams& p, hipStream_t s, const char* name, double flops, double bytes) {
   constexpr int smem = 2 * (BM + BN) * BK * 2;
   static bool attr_set = false;
   if (!attr_set) {
-    FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<BM, BN, WM, WN, EPI>),
+    FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<BM, BN, WM, WN, EPI, DIRECT, SCHED>),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, smem),
                  "gemm smem attribute");
     attr_set = true;
   }
   const int64_t tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
   LaunchScope ls(name, s, flops, bytes);
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, EPI>), dim3(static_cast<unsigned>(tiles)),
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, EPI, DIRECT, SCHED>), dim3(static_cast<unsigned>(tiles)),
                      dim3(WM * WN * 64), smem, s, p);
+  return ls.status();
+}
+
+// Tile configurations (BM x BN, waves; LDS fill): 0 = 256x256, 8 waves of 128x64, staged
+// through registers; 1 = same with direct global->LDS loads; 2 = 256x256, 4 waves of
+// 128x128, direct; 3 = 128x128, 4 waves of 64x64, staged.  FF_GEMM_TILE overrides the choice.
+int pick_tile(const GemmParams& p) {
+  static const char* env = getenv("FF_GEMM_TILE");
+  if (env && env[0] >= '0' && env[0] <= '7') return env[0] - '0';
+  const int64_t tiles256 = ((p.M + 255) / 256) * ((p.N + 255) / 256);
+  if (tiles256 >= 256) return 7;   // at least one 256 x 256 tile per CU
+  return 3;
+}
+
+template <int EPI, int STAGES>
+int launch_ms(const GemmParams& p, hipStream_t s, const char* name, double flops, double bytes) {
+  constexpr int smem = STAGES * 512 * 32 * 2;
+  static bool attr_set = false;
+  if (!attr_set) {
+    FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_ms<EPI, STAGES>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, smem),
+                 "gemm smem attribute");
+    attr_set = true;
+  }
+  const int64_t tiles = ((p.M + 255) / 256) * ((p.N + 255) / 256);
+  LaunchScope ls(name, s, flops, bytes);
+  hipLaunchKernelGGL((gemm_bf16_ms<EPI, STAGES>), dim3(static_cast<unsigned>(tiles)), dim3(512), smem, s, p);
+  return ls.status();
+}
+
+template <int EPI, int STAGES>
+int launch_pp(const GemmParams& p, hipStream_t s, const char* name, double flops, double bytes) {
+  constexpr int smem = STAGES * 512 * 32 * 2;
+  static bool attr_set = false;
+  if (!attr_set) {
+    FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_pp<EPI, STAGES>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, smem),
+                 "gemm smem attribute");
+    attr_set = true;
+  }
+  const int64_t tiles = ((p.M + 255) / 256) * ((p.N + 255) / 256);
+  LaunchScope ls(name, s, flops, bytes);
+  hipLaunchKernelGGL((gemm_bf16_pp<EPI, STAGES>), dim3(static_cast<unsigned>(tiles)), dim3(512), smem, s, p);
   return ls.status();
 }
 
 template <int EPI>
 int dispatch_bf16(const GemmParams& p, hipStream_t s, double flops, double bytes) {
   static const char* names[3] = {"gemm_bf16", "gemm_bf16_gelu", "gemm_bf16_gated"};
-  return launch_bf16<256, 256, 2, 4, EPI>(p, s, names[EPI], flops, bytes);
+  switch (pick_tile(p)) {
+    case 1: return launch_bf16<256, 256, 2, 4, EPI, true>(p, s, names[EPI], flops, bytes);
+    case 2: return launch_bf16<256, 256, 2, 4, EPI, true, true>(p, s, names[EPI], flops, bytes);
+    case 3: return launch_bf16<128, 128, 2, 2, EPI, false>(p, s, names[EPI], flops, bytes);
+    case 4: return launch_ms<EPI, 4>(p, s, names[EPI], flops, bytes);
+    case 5: return launch_ms<EPI, 3>(p, s, names[EPI], flops, bytes);
+    case 6: return launch_pp<EPI, 4>(p, s, names[EPI], flops, bytes);
+    case 7: return launch_pp<EPI, 3>(p, s, names[EPI], flops, bytes);
+    default: return launch_bf16<256, 256, 2, 4, EPI, false>(p, s, names[EPI], flops, bytes);
+  }
 }
 
 template <int EPI>
@@ -278,7 +701,9 @@ int gemm(const GemmArgs& a, hipStream_t s) {
   if (a.M == 0 || a.N == 0) return FF_OK;
   GemmParams p{a.M, a.N, a.K, a.A1, a.lda1, a.K1, a.A2 ? a.A2 : a.A1, a.A2 ? a.lda2 : a.lda1,
                a.W, a.ldw, a.bias, a.out, a.ldo, a.gelu_from, a.gate, a.gate_ld, a.resid, a.ldr,
-               a.rows_per_sample > 0 ? a.rows_per_sample : a.M};
+               a.rows_per_sample > 0 ? a.rows_per_sample : a.M, 0};
+  p.vec_ok = a.ldo % 8 == 0 && aligned16(a.out) && (!a.bias || aligned16(a.bias)) &&
+             (a.epi != EPI_GATED || (a.ldr % 8 == 0 && aligned16(a.resid) && a.gate_ld % 4 == 0 && aligned16(a.gate)));
   const double esz = static_cast<double>(dtype_size(a.dtype));
   const double flops = 2.0 * a.M * a.N * a.K;
   const double bytes = esz * (static_cast<double>(a.M) * a.K + static_cast<double>(a.N) * a.K +
