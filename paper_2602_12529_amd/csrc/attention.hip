@@ -18,6 +18,7 @@
 // float32 (any d <= 64): one thread per query with the same online softmax,
 // for the small float32 configuration.
 #include <cmath>
+#include <cstdlib>
 
 #include "dev.h"
 #include "ff_internal.h"
@@ -48,12 +49,66 @@ __device__ __forceinline__ int k_off(int r, int c) { return r * 256 + ((c ^ (r &
 // 16-byte chunk c of V^T row r (8 chunks per 128-byte row).
 __device__ __forceinline__ int v_off(int r, int c) { return r * 128 + ((c ^ ((r >> 1) & 7)) << 4); }
 
-template <int WAVES>
-__global__ __launch_bounds__(WAVES * 64, 2) void attn_bf16_d128(AttnParams p) {
-  constexpr int THREADS = WAVES * 64;
-  constexpr int K_LOADS = KT * 16 / THREADS;   // 16-byte chunks per thread per K tile
-  constexpr int V_LOADS = D * 8 / THREADS;
-  __shared__ __attribute__((aligned(16))) char smem[2 * (K_STAGE + V_STAGE)];
+typedef __attribute__((address_space(3))) void lds_t;
+typedef __attribute__((address_space(1))) void glb_t;
+
+// One 64-key tile: S^T = K Q^T, online softmax (masked when MASK), O^T += V^T P^T.
+#define FF_ATTN_TILE(MASK)                                                                          \
+  {                                                                                                 \
+    const char* Ks = smem + (it % STAGES) * (K_STAGE + V_STAGE);                                     \
+    const char* Vs = Ks + K_STAGE;                                                                  \
+    f32x16_t s[2];                                                                                  \
+    _Pragma("unroll") for (int kb = 0; kb < 2; ++kb)                                                \
+      _Pragma("unroll") for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;                                \
+    _Pragma("unroll") for (int t = 0; t < 8; ++t)                                                   \
+      _Pragma("unroll") for (int kb = 0; kb < 2; ++kb) {                                            \
+        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(Ks + k_off(32 * kb + krow, 2 * t + g)); \
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[t], s[kb], 0, 0, 0);                  \
+      }                                                                                             \
+    if (MASK) {                                                                                     \
+      /* keys come in aligned groups of 8 (n_kv % 8 == 0): one test per group */                    \
+      _Pragma("unroll") for (int kb = 0; kb < 2; ++kb)                                              \
+        _Pragma("unroll") for (int u = 0; u < 2; ++u) {                                             \
+          const bool dead = kv0 + 32 * kb + 16 * u + 8 * g >= p.n_kv;                              \
+          _Pragma("unroll") for (int j = 0; j < 8; ++j)                                             \
+            if (dead) s[kb][8 * u + j] = -INFINITY;                                                 \
+        }                                                                                           \
+    }                                                                                               \
+    float mx = -INFINITY;                                                                           \
+    _Pragma("unroll") for (int kb = 0; kb < 2; ++kb)                                                \
+      _Pragma("unroll") for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);                      \
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.scale_log2;                                          \
+    if (__any(mx > m_run + 8.0f)) {                                                                 \
+      const float m_new = fmaxf(m_run, mx);                                                         \
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);                                    \
+      m_run = m_new;                                                                                \
+      l_run *= alpha;                                                                               \
+      _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                 \
+        _Pragma("unroll") for (int r = 0; r < 16; ++r) o[i][r] *= alpha;                            \
+    }                                                                                               \
+    const float neg_m = -m_run;                                                                     \
+    float lsum = 0.f;                                                                               \
+    bf16x8_t pf[4];                                                                                 \
+    _Pragma("unroll") for (int kb = 0; kb < 2; ++kb)                                                \
+      _Pragma("unroll") for (int u = 0; u < 2; ++u)                                                 \
+        _Pragma("unroll") for (int j = 0; j < 8; ++j) {                                             \
+          const float e = __builtin_amdgcn_exp2f(fmaf(s[kb][8 * u + j], p.scale_log2, neg_m));      \
+          lsum += e;                                                                                \
+          pf[2 * kb + u][j] = static_cast<__bf16>(e);                                               \
+        }                                                                                           \
+    l_run += lsum;                                                                                  \
+    _Pragma("unroll") for (int sl = 0; sl < 4; ++sl)                                                \
+      _Pragma("unroll") for (int db = 0; db < 4; ++db) {                                            \
+        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(Vs + v_off(32 * db + ql, 2 * sl + g)); \
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[sl], o[db], 0, 0, 0);                 \
+      }                                                                                             \
+  }
+
+template <int WAVES, int STAGES>
+__global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_bf16_d128(AttnParams p) {
+  constexpr int K_INS = K_STAGE / 1024 / WAVES;   // 1 KB direct loads per wave per K tile
+  constexpr int V_INS = V_STAGE / 1024 / WAVES;
+  __shared__ __attribute__((aligned(16))) char smem[STAGES * (K_STAGE + V_STAGE)];
 
   // Workgroup -> (query tile, batch*head): ids are regrouped so the query
   // tiles of one (b, h) run on one XCD and share its L2.
@@ -67,6 +122,7 @@ __global__ __launch_bounds__(WAVES * 64, 2) void attn_bf16_d128(AttnParams p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int ql = lane & 31, g = lane >> 5;
   const int64_t q0 = qt * 32 * WAVES + wave * 32;
+  const int n_kv = static_cast<int>(p.n_kv);
 
   const bf16_t* Kb = p.K + bh * p.n_kv * D;
   const bf16_t* Vb = p.Vt + bh * D * p.n_kv;
@@ -81,37 +137,34 @@ __global__ __launch_bounds__(WAVES * 64, 2) void attn_bf16_d128(AttnParams p) {
     for (int t = 0; t < 8; ++t) qf[t] = *reinterpret_cast<const bf16x8_t*>(qp + 16 * t);
   }
 
-  uint4 rk[K_LOADS], rv[V_LOADS];
-  auto load_tile = [&](int64_t kv0) {
+  // Direct loads.  K: instruction i of this wave fills K rows 4(i*WAVES + wave) .. +3; lane l
+  // lands at row + l/16, stored chunk l%16 = logical chunk ^ (row & 15).  V^T: instruction i
+  // fills rows 8(i*WAVES + wave) .. +7; lane l lands at row + l/8, stored chunk l%8 = logical
+  // chunk ^ ((row >> 1) & 7).  Keys past n_kv are clamped to valid memory and masked.
+  int k_row[K_INS], k_ck[K_INS], v_row[V_INS], v_ck[V_INS];
 #pragma unroll
-    for (int i = 0; i < K_LOADS; ++i) {
-      const int e = tid + i * THREADS;
-      const int r = e >> 4, c = e & 15;
-      int64_t key = kv0 + r;
-      if (key >= p.n_kv) key = p.n_kv - 1;
-      rk[i] = *reinterpret_cast<const uint4*>(Kb + key * D + c * 8);
+  for (int i = 0; i < K_INS; ++i) {
+    k_row[i] = 4 * (i * WAVES + wave) + (lane >> 4);
+    k_ck[i] = (lane & 15) ^ (k_row[i] & 15);
+  }
+#pragma unroll
+  for (int i = 0; i < V_INS; ++i) {
+    v_row[i] = 8 * (i * WAVES + wave) + (lane >> 3);
+    v_ck[i] = (lane & 7) ^ ((v_row[i] >> 1) & 7);
+  }
+  auto issue = [&](int kv0, int stage) {
+    char* base = smem + stage * (K_STAGE + V_STAGE);
+#pragma unroll
+    for (int i = 0; i < K_INS; ++i) {
+      const int key = kv0 + k_row[i] < n_kv ? kv0 + k_row[i] : n_kv - 1;
+      __builtin_amdgcn_global_load_lds((const glb_t*)(Kb + key * D + k_ck[i] * 8),
+                                       (lds_t*)(base + (i * WAVES + wave) * 1024), 16, 0, 0);
     }
 #pragma unroll
-    for (int i = 0; i < V_LOADS; ++i) {
-      const int e = tid + i * THREADS;
-      const int r = e >> 3, c = e & 7;
-      const int64_t col = kv0 + c * 8;
-      if (col < p.n_kv) rv[i] = *reinterpret_cast<const uint4*>(Vb + r * p.n_kv + col);
-      else rv[i] = make_uint4(0u, 0u, 0u, 0u);
-    }
-  };
-  auto store_tile = [&](int buf) {
-    char* Ks = smem + buf * (K_STAGE + V_STAGE);
-    char* Vs = Ks + K_STAGE;
-#pragma unroll
-    for (int i = 0; i < K_LOADS; ++i) {
-      const int e = tid + i * THREADS;
-      *reinterpret_cast<uint4*>(Ks + k_off(e >> 4, e & 15)) = rk[i];
-    }
-#pragma unroll
-    for (int i = 0; i < V_LOADS; ++i) {
-      const int e = tid + i * THREADS;
-      *reinterpret_cast<uint4*>(Vs + v_off(e >> 3, e & 7)) = rv[i];
+    for (int i = 0; i < V_INS; ++i) {
+      const int col = kv0 + v_ck[i] * 8 < n_kv ? kv0 + v_ck[i] * 8 : n_kv - 8;
+      __builtin_amdgcn_global_load_lds((const glb_t*)(Vb + v_row[i] * n_kv + col),
+                                       (lds_t*)(base + K_STAGE + (i * WAVES + wave) * 1024), 16, 0, 0);
     }
   };
 
@@ -125,78 +178,25 @@ __global__ __launch_bounds__(WAVES * 64, 2) void attn_bf16_d128(AttnParams p) {
   // Row of K fed to MFMA row rho: bits 2 and 3 swapped.
   const int krow = (ql & ~12) | ((ql & 4) << 1) | ((ql & 8) >> 1);
 
-  const int64_t ntiles = (p.n_kv + KT - 1) / KT;
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
+  const int ntiles = (n_kv + KT - 1) / KT;
+  const int nfull = n_kv / KT;   // tiles without masked keys
+#pragma unroll
+  for (int st = 0; st < STAGES - 1; ++st)
+    if (st < ntiles) issue(st * KT, st);
 
-  for (int64_t it = 0; it < ntiles; ++it) {
-    const int buf = it & 1;
-    const int64_t kv0 = it * KT;
-    if (it + 1 < ntiles) load_tile(kv0 + KT);
-    const char* Ks = smem + buf * (K_STAGE + V_STAGE);
-    const char* Vs = Ks + K_STAGE;
-
-    f32x16_t s[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
-#pragma unroll
-    for (int t = 0; t < 8; ++t)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(Ks + k_off(32 * kb + krow, 2 * t + g));
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[t], s[kb], 0, 0, 0);
-      }
-
-    // s[kb][8u + j] is the score of key kv0 + 32kb + 16u + 8g + j for query q0 + ql.
-    float mx = -INFINITY;
-    const bool tail = kv0 + KT > p.n_kv;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float v = s[kb][r] * p.scale_log2;
-        if (tail) {
-          const int64_t key = kv0 + 32 * kb + 16 * (r >> 3) + 8 * g + (r & 7);
-          if (key >= p.n_kv) v = -INFINITY;
-        }
-        s[kb][r] = v;
-        mx = fmaxf(mx, v);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = exp2f(m_run - m_new);
-    m_run = m_new;
-    float lsum = 0.f;
-    bf16x8_t pf[4];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int u = 0; u < 2; ++u)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const float e = exp2f(s[kb][8 * u + j] - m_new);
-          lsum += e;
-          pf[2 * kb + u][j] = static_cast<__bf16>(e);
-        }
-    l_run = l_run * alpha + lsum;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
-
-#pragma unroll
-    for (int sl = 0; sl < 4; ++sl)
-#pragma unroll
-      for (int db = 0; db < 4; ++db) {
-        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(Vs + v_off(32 * db + ql, 2 * sl + g));
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[sl], o[db], 0, 0, 0);
-      }
-
-    if (it + 1 < ntiles) store_tile(buf ^ 1);
-    __syncthreads();
+  for (int it = 0; it < ntiles; ++it) {
+    const int kv0 = it * KT;
+    // tile it has landed once at most STAGES-2 younger tiles are in flight
+    if (it + STAGES - 2 < ntiles) {
+      if constexpr (STAGES == 3) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(K_INS + V_INS) : "memory");
+      else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    } else {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
+    asm volatile("s_barrier" ::: "memory");
+    if (it + STAGES - 1 < ntiles) issue((it + STAGES - 1) * KT, (it + STAGES - 1) % STAGES);
+    if (it < nfull) FF_ATTN_TILE(false)
+    else FF_ATTN_TILE(true)
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
@@ -219,6 +219,7 @@ __global__ __launch_bounds__(WAVES * 64, 2) void attn_bf16_d128(AttnParams p) {
       *reinterpret_cast<uint2*>(row + 32 * db + 8 * u + 4 * g) = w;
     }
 }
+#undef FF_ATTN_TILE
 
 // ------------------------------------------------------------------ float32
 struct AttnF32Params {
@@ -271,10 +272,19 @@ int attention(const AttnArgs& a, hipStream_t s) {
                  static_cast<const bf16_t*>(a.Q), static_cast<const bf16_t*>(a.K), static_cast<const bf16_t*>(a.Vt),
                  static_cast<bf16_t*>(a.out0), static_cast<bf16_t*>(a.out1), a.split, a.ldo,
                  static_cast<float>(a.scale * 1.4426950408889634)};
-    constexpr int WAVES = 4;
-    const int64_t tiles = (a.n_q + 32 * WAVES - 1) / (32 * WAVES) * a.B * a.heads;
+    static const char* env = getenv("FF_ATTN_WAVES");
+    const int waves = (env && env[0] == '4') ? 4 : 8;
     LaunchScope ls("attn_bf16_d128", s, flops, bytes);
-    hipLaunchKernelGGL(attn_bf16_d128<WAVES>, dim3(static_cast<unsigned>(tiles)), dim3(WAVES * 64), 0, s, p);
+    static const char* envs = getenv("FF_ATTN_STAGES");
+    const int stages = (envs && envs[0] == '2') ? 2 : 3;
+    if (waves == 8) {
+      const int64_t tiles = (a.n_q + 255) / 256 * a.B * a.heads;
+      if (stages == 3) hipLaunchKernelGGL((attn_bf16_d128<8, 3>), dim3(static_cast<unsigned>(tiles)), dim3(512), 0, s, p);
+      else hipLaunchKernelGGL((attn_bf16_d128<8, 2>), dim3(static_cast<unsigned>(tiles)), dim3(512), 0, s, p);
+    } else {
+      const int64_t tiles = (a.n_q + 127) / 128 * a.B * a.heads;
+      hipLaunchKernelGGL((attn_bf16_d128<4, 2>), dim3(static_cast<unsigned>(tiles)), dim3(256), 0, s, p);
+    }
     return ls.status();
   }
   if (a.d > 64) return fail(FF_EUNSUPPORTED, "attention: f32 head_dim %lld > 64", (long long)a.d);

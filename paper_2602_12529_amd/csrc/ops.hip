@@ -89,64 +89,102 @@ int skinny_dispatch(const SkinnyArgs& a, int64_t b0, int bc, hipStream_t s) {
 
 // ------------------------------------------------------------------ norm + modulate
 // One wave per row.  NCH > 0: the row is held in registers as NCH chunks of 8
-// per lane (row width 512 * NCH, 16-byte aligned); NCH == 0: generic scalar path.
+// per lane (row width 512 * NCH, 16-byte aligned) and a wave walks ROWS rows,
+// keeping the sample's (1 + scale) and shift for its columns in registers
+// (reloaded only when the sample changes), so every global access is a
+// 16-byte vector access.  NCH == 0: generic scalar path, one row per wave.
+constexpr int kNormRows = 4;
+
 template <bool BF16, int NCH>
 __global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
   const int lane = threadIdx.x & 63;
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
-  if (row >= a.rows) return;
   const int64_t H = a.H;
-  const int64_t b = row / a.rows_per_sample;
   const float invH = 1.0f / static_cast<float>(H);
-  const float* sh = a.shift ? a.shift + b * a.mod_ld : nullptr;
-  const float* sc = a.scale ? a.scale + b * a.mod_ld : nullptr;
-  auto finish = [&](int64_t j, float xn) {
-    float mul = sc ? 1.0f + sc[j] : 1.0f;
-    if (a.w) mul *= ld1<BF16>(a.w, j);
-    float add = sh ? sh[j] : 0.0f;
-    if (a.bias) add += ld1<BF16>(a.bias, j);
-    return fmaf(xn, mul, add);
-  };
   if constexpr (NCH > 0) {
-    float v[NCH][8];
+    const int64_t row0 = (static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6)) * kNormRows;
+    float mul[NCH][8], add[NCH][8];
+    int64_t cur_b = -1;
+    for (int rr = 0; rr < kNormRows; ++rr) {
+      const int64_t row = row0 + rr;
+      if (row >= a.rows) break;
+      const int64_t b = row / a.rows_per_sample;
+      if (b != cur_b) {
+        cur_b = b;
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) ld8<BF16>(a.x, row * a.ldx + (c * 64 + lane) * 8, v[c]);
-    float mean = 0.f;
-    if (a.norm_kind == FF_NORM_LN) {
-      float s = 0.f;
+        for (int c = 0; c < NCH; ++c) {
+          const int64_t j0 = (c * 64 + lane) * 8;
+#pragma unroll
+          for (int q = 0; q < 2; ++q) {
+            float4 sc = a.scale ? *reinterpret_cast<const float4*>(a.scale + b * a.mod_ld + j0 + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
+            float4 sh = a.shift ? *reinterpret_cast<const float4*>(a.shift + b * a.mod_ld + j0 + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
+            mul[c][4 * q] = 1.f + sc.x; mul[c][4 * q + 1] = 1.f + sc.y; mul[c][4 * q + 2] = 1.f + sc.z; mul[c][4 * q + 3] = 1.f + sc.w;
+            add[c][4 * q] = sh.x; add[c][4 * q + 1] = sh.y; add[c][4 * q + 2] = sh.z; add[c][4 * q + 3] = sh.w;
+          }
+          if (a.w) {
+            float w8[8];
+            ld8<BF16>(a.w, j0, w8);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) mul[c][j] *= w8[j];
+          }
+          if (a.bias) {
+            float b8[8];
+            ld8<BF16>(a.bias, j0, b8);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) add[c][j] += b8[j];
+          }
+        }
+      }
+      float v[NCH][8];
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) ld8<BF16>(a.x, row * a.ldx + (c * 64 + lane) * 8, v[c]);
+      float mean = 0.f;
+      if (a.norm_kind == FF_NORM_LN) {
+        float sum = 0.f;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c)
+#pragma unroll
+          for (int j = 0; j < 8; ++j) sum += v[c][j];
+        mean = wave_sum(sum) * invH;
+      }
+      float ss = 0.f;
 #pragma unroll
       for (int c = 0; c < NCH; ++c)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) s += v[c][j];
-      mean = wave_sum(s) * invH;
-    }
-    float ss = 0.f;
+        for (int j = 0; j < 8; ++j) {
+          const float d = v[c][j] - mean;
+          ss = fmaf(d, d, ss);
+        }
+      const float rstd = rsqrtf(wave_sum(ss) * invH + a.eps);
 #pragma unroll
-    for (int c = 0; c < NCH; ++c)
+      for (int c = 0; c < NCH; ++c) {
+        float o[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        float d = v[c][j] - mean;
-        ss = fmaf(d, d, ss);
+        for (int j = 0; j < 8; ++j) o[j] = fmaf((v[c][j] - mean) * rstd, mul[c][j], add[c][j]);
+        st8<BF16>(a.y, row * a.ldy + (c * 64 + lane) * 8, o);
       }
-    const float rstd = rsqrtf(wave_sum(ss) * invH + a.eps);
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      float o[8];
-      const int64_t j0 = (c * 64 + lane) * 8;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) o[j] = finish(j0 + j, (v[c][j] - mean) * rstd);
-      st8<BF16>(a.y, row * a.ldy + j0, o);
     }
   } else {
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+    if (row >= a.rows) return;
+    const int64_t b = row / a.rows_per_sample;
+    const float* sh = a.shift ? a.shift + b * a.mod_ld : nullptr;
+    const float* sc = a.scale ? a.scale + b * a.mod_ld : nullptr;
+    auto finish = [&](int64_t j, float xn) {
+      float mul = sc ? 1.0f + sc[j] : 1.0f;
+      if (a.w) mul *= ld1<BF16>(a.w, j);
+      float add = sh ? sh[j] : 0.0f;
+      if (a.bias) add += ld1<BF16>(a.bias, j);
+      return fmaf(xn, mul, add);
+    };
     float mean = 0.f;
     if (a.norm_kind == FF_NORM_LN) {
-      float s = 0.f;
-      for (int64_t j = lane; j < H; j += 64) s += ld1<BF16>(a.x, row * a.ldx + j);
-      mean = wave_sum(s) * invH;
+      float sum = 0.f;
+      for (int64_t j = lane; j < H; j += 64) sum += ld1<BF16>(a.x, row * a.ldx + j);
+      mean = wave_sum(sum) * invH;
     }
     float ss = 0.f;
     for (int64_t j = lane; j < H; j += 64) {
-      float d = ld1<BF16>(a.x, row * a.ldx + j) - mean;
+      const float d = ld1<BF16>(a.x, row * a.ldx + j) - mean;
       ss = fmaf(d, d, ss);
     }
     const float rstd = rsqrtf(wave_sum(ss) * invH + a.eps);
@@ -155,17 +193,111 @@ __global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
   }
 }
 
+// bf16 fast path: a block of 4 waves normalises 32 rows of one sample.  The
+// sample's (1 + scale) and shift are staged once in LDS; each wave walks 8
+// rows with the next row's loads issued before the current row is finished.
+constexpr int kNormBlockRows = 32;
+
+template <int NCH>
+__global__ __launch_bounds__(256) void norm_lds_kernel(NormArgs a) {
+  extern __shared__ __attribute__((aligned(16))) float mod_s[];   // [2][H]: mul, add
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t H = a.H;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kNormBlockRows;
+  const int64_t b = r0 / a.rows_per_sample;
+  float* mul_s = mod_s;
+  float* add_s = mod_s + H;
+  for (int64_t j = threadIdx.x * 4; j < H; j += 1024) {
+    float4 sc = a.scale ? *reinterpret_cast<const float4*>(a.scale + b * a.mod_ld + j) : make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 sh = a.shift ? *reinterpret_cast<const float4*>(a.shift + b * a.mod_ld + j) : make_float4(0.f, 0.f, 0.f, 0.f);
+    *reinterpret_cast<float4*>(mul_s + j) = make_float4(1.f + sc.x, 1.f + sc.y, 1.f + sc.z, 1.f + sc.w);
+    *reinterpret_cast<float4*>(add_s + j) = sh;
+  }
+  __syncthreads();
+  const float invH = 1.0f / static_cast<float>(H);
+  const bf16_t* __restrict__ xp = static_cast<const bf16_t*>(a.x);
+  bf16_t* __restrict__ yp = static_cast<bf16_t*>(a.y);
+  constexpr int RPW = kNormBlockRows / 4;
+  const int64_t rw = r0 + wave * RPW;
+  float v[NCH][8], nx[NCH][8];
+  if (rw < a.rows) {
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) ld8<true>(xp, rw * a.ldx + (c * 64 + lane) * 8, v[c]);
+  }
+  for (int rr = 0; rr < RPW; ++rr) {
+    const int64_t row = rw + rr;
+    if (row >= a.rows) break;
+    const bool more = rr + 1 < RPW && row + 1 < a.rows;
+    if (more) {
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) ld8<true>(xp, (row + 1) * a.ldx + (c * 64 + lane) * 8, nx[c]);
+    }
+    float mean = 0.f;
+    if (a.norm_kind == FF_NORM_LN) {
+      float sum = 0.f;
+#pragma unroll
+      for (int c = 0; c < NCH; ++c)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) sum += v[c][j];
+      mean = wave_sum(sum) * invH;
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float d = v[c][j] - mean;
+        ss = fmaf(d, d, ss);
+      }
+    const float rstd = rsqrtf(wave_sum(ss) * invH + a.eps);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int j0 = (c * 64 + lane) * 8;
+      const float4 m0 = *reinterpret_cast<const float4*>(mul_s + j0), m1 = *reinterpret_cast<const float4*>(mul_s + j0 + 4);
+      const float4 a0 = *reinterpret_cast<const float4*>(add_s + j0), a1 = *reinterpret_cast<const float4*>(add_s + j0 + 4);
+      const float mu[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
+      const float ad[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+      float o[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) o[j] = fmaf((v[c][j] - mean) * rstd, mu[j], ad[j]);
+      st8<true>(yp, row * a.ldy + j0, o);
+    }
+    if (more) {
+#pragma unroll
+      for (int c = 0; c < NCH; ++c)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[c][j] = nx[c][j];
+    }
+  }
+}
+
 template <bool BF16>
 int norm_dispatch(const NormArgs& a, hipStream_t s) {
-  dim3 grid(static_cast<unsigned>((a.rows + 3) / 4));
   int nch = 0;
-  const bool fits = a.H % 512 == 0 && a.ldx % 8 == 0 && a.ldy % 8 == 0 && aligned16(a.x) && aligned16(a.y);
+  const bool mod_ok = (!a.shift || (aligned16(a.shift) && a.mod_ld % 4 == 0)) &&
+                      (!a.scale || (aligned16(a.scale) && a.mod_ld % 4 == 0)) &&
+                      (!a.w || aligned16(a.w)) && (!a.bias || aligned16(a.bias));
+  const bool fits = a.H % 512 == 0 && a.ldx % 8 == 0 && a.ldy % 8 == 0 && aligned16(a.x) && aligned16(a.y) && mod_ok;
   if (BF16 && fits) nch = static_cast<int>(a.H / 512);
+  if (nch > 8) nch = 0;
+  const bool one_sample_blocks = a.rows_per_sample % kNormBlockRows == 0 || a.rows <= a.rows_per_sample;
+  if (BF16 && nch > 0 && nch <= 6 && one_sample_blocks && !a.w && !a.bias) {
+    const dim3 grid(static_cast<unsigned>((a.rows + kNormBlockRows - 1) / kNormBlockRows));
+    const size_t shm = 2 * a.H * sizeof(float);
+    switch (nch) {
+#define FF_NL(N) case N: hipLaunchKernelGGL((norm_lds_kernel<N>), grid, dim3(256), shm, s, a); return FF_OK;
+      FF_NL(1) FF_NL(2) FF_NL(3) FF_NL(4) FF_NL(5) FF_NL(6)
+#undef FF_NL
+    }
+  }
+  const dim3 grid_rows(static_cast<unsigned>((a.rows + 4 * kNormRows - 1) / (4 * kNormRows)));
   switch (nch) {
-#define FF_NM(N) case N: hipLaunchKernelGGL((norm_kernel<BF16, N>), grid, dim3(256), 0, s, a); break;
+#define FF_NM(N) case N: hipLaunchKernelGGL((norm_kernel<BF16, N>), grid_rows, dim3(256), 0, s, a); break;
     FF_NM(1) FF_NM(2) FF_NM(3) FF_NM(4) FF_NM(5) FF_NM(6) FF_NM(7) FF_NM(8)
 #undef FF_NM
-    default: hipLaunchKernelGGL((norm_kernel<BF16, 0>), grid, dim3(256), 0, s, a); break;
+    default:
+      hipLaunchKernelGGL((norm_kernel<BF16, 0>), dim3(static_cast<unsigned>((a.rows + 3) / 4)), dim3(256), 0, s, a);
+      break;
   }
   return FF_OK;
 }
@@ -238,6 +370,78 @@ __global__ __launch_bounds__(256) void qk_rope_kernel(QkvArgs a) {
       const int64_t o = ((b * a.heads + h) * d + dd) * a.n_joint + col0 + tt;
       st1<BF16>(a.Vt, o, vs[tt][dd]);
     }
+  }
+}
+
+// bf16, d = 128 fast path: 16 lanes per token, 8 consecutive elements per lane,
+// so every load/store is 16 bytes; the per-head RMS reduction runs over the 16
+// lanes of a token.  A block covers 64 tokens of one head; V^T leaves through
+// an LDS transpose as 16-byte row segments.
+__global__ __launch_bounds__(256) void qk_rope_vec_kernel(QkvArgs a) {
+  __shared__ bf16_t vt[128][72];
+  const int t = threadIdx.x, c = t & 15, tr = t >> 4;
+  const int64_t t0 = static_cast<int64_t>(blockIdx.x) * kRopeTok;
+  const int h = blockIdx.y;
+  const int64_t b = blockIdx.z;
+  float qw[8], kw[8];
+  ld8<true>(a.q_w, c * 8, qw);
+  ld8<true>(a.k_w, c * 8, kw);
+  const int64_t out_head = (b * a.heads + h) * a.n_joint;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int tt = tr + 16 * i;
+    const int64_t tok_raw = t0 + tt;
+    const bool live = tok_raw < a.n_tok;
+    const int64_t tok = live ? tok_raw : a.n_tok - 1;
+    const int64_t src = (b * a.src_rows + tok) * a.ld + static_cast<int64_t>(h) * 128 + c * 8;
+    float cs[8];   // (cos, sin) of pairs 4c .. 4c+3
+    if (a.rope) {
+      const float4* rp = reinterpret_cast<const float4*>(a.rope + tok * 64 + c * 4);
+      const float4 r0 = rp[0], r1 = rp[1];
+      cs[0] = r0.x; cs[1] = r0.y; cs[2] = r0.z; cs[3] = r0.w; cs[4] = r1.x; cs[5] = r1.y; cs[6] = r1.z; cs[7] = r1.w;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) { cs[2 * j] = 1.f; cs[2 * j + 1] = 0.f; }
+    }
+    const int64_t dst = (out_head + a.tok_offset + tok) * 128 + c * 8;
+#pragma unroll
+    for (int which = 0; which < 2; ++which) {
+      float x[8];
+      ld8<true>(which == 0 ? a.q : a.k, src, x);
+      float ss = 0.f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) ss = fmaf(x[j], x[j], ss);
+      ss += __shfl_xor(ss, 8, 64);
+      ss += __shfl_xor(ss, 4, 64);
+      ss += __shfl_xor(ss, 2, 64);
+      ss += __shfl_xor(ss, 1, 64);
+      const float rstd = rsqrtf(ss * (1.0f / 128.0f) + a.eps);
+      const float* w = which == 0 ? qw : kw;
+      float y[8];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float x0 = x[2 * j] * rstd * w[2 * j], x1 = x[2 * j + 1] * rstd * w[2 * j + 1];
+        y[2 * j] = x0 * cs[2 * j] - x1 * cs[2 * j + 1];
+        y[2 * j + 1] = x0 * cs[2 * j + 1] + x1 * cs[2 * j];
+      }
+      if (live) st8<true>(which == 0 ? a.Q : a.Kd, dst, y);
+    }
+    const uint4 vv = *reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(a.v) + src);
+    const uint32_t w4[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      vt[c * 8 + 2 * j][tt] = bf16_t(w4[j] & 0xffffu);
+      vt[c * 8 + 2 * j + 1][tt] = bf16_t(w4[j] >> 16);
+    }
+  }
+  __syncthreads();
+  // V^T rows: thread -> (d row t/2, 32 tokens starting at 32 (t&1)), 16-byte stores.
+  const int dd = t >> 1, th = (t & 1) * 32;
+  bf16_t* vrow = static_cast<bf16_t*>(a.Vt) + ((b * a.heads + h) * 128 + dd) * a.n_joint + a.tok_offset + t0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int tt = th + 8 * q;
+    if (t0 + tt < a.n_tok) *reinterpret_cast<uint4*>(vrow + tt) = *reinterpret_cast<const uint4*>(&vt[dd][tt]);
   }
 }
 
@@ -320,7 +524,12 @@ int qk_norm_rope(const QkvArgs& a, hipStream_t s) {
   if (a.d > 128 || a.d % 2) return fail(FF_EUNSUPPORTED, "qk_norm_rope: head_dim %d", a.d);
   dim3 grid(blocks_for(a.n_tok, kRopeTok), static_cast<unsigned>(a.heads), static_cast<unsigned>(a.B));
   LaunchScope ls("qk_norm_rope", s, 0.0, 6.0 * dtype_size(a.dtype) * a.B * a.n_tok * a.heads * a.d);
-  if (a.dtype == FF_BF16) hipLaunchKernelGGL(qk_rope_kernel<true>, grid, dim3(256), 0, s, a);
+  const bool vec = a.dtype == FF_BF16 && a.d == 128 && a.v_transposed && a.apply_norm && !a.full_width_norm &&
+                   a.ld % 8 == 0 && aligned16(a.q) && aligned16(a.k) && aligned16(a.v) && aligned16(a.Q) &&
+                   aligned16(a.Kd) && aligned16(a.Vt) && aligned16(a.q_w) && aligned16(a.k_w) &&
+                   (!a.rope || aligned16(a.rope)) && a.n_joint % 8 == 0 && a.tok_offset % 8 == 0 && a.n_tok % 8 == 0;
+  if (vec) hipLaunchKernelGGL(qk_rope_vec_kernel, grid, dim3(256), 0, s, a);
+  else if (a.dtype == FF_BF16) hipLaunchKernelGGL(qk_rope_kernel<true>, grid, dim3(256), 0, s, a);
   else hipLaunchKernelGGL(qk_rope_kernel<false>, grid, dim3(256), 0, s, a);
   return ls.status();
 }

@@ -62,25 +62,39 @@ __global__ __launch_bounds__(kSdeThreads) void sde_kernel(
   const int64_t end = start + chunk < D ? start + chunk : D;
   double acc = 0.0;
   if constexpr (VEC) {
-    for (int64_t i = start + threadIdx.x * kSdeVec; i < end; i += kSdeThreads * kSdeVec) {
-      float xv[8], vv[8], tv[8], out[8];
-      ld8<BF16>(x, base + i, xv);
-      ld8<BF16>(v, base + i, vv);
-      ld8<BF16>(third, base + i, tv);
-      float part = 0.f;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        if constexpr (MODE == 0) {
-          float r2 = sde_elem<BF16>(xv[j], vv[j], tv[j], a, b, c, out[j]);
-          part = part + r2;
-        } else {
-          float mean = fmaf(a, xv[j], b * vv[j]);
-          float r = tv[j] - mean;
-          part = part + r * r;
-        }
+    // Two groups of 8 per thread per pass (loads of both issued first); the
+    // chunk is a multiple of 2 * 256 * 8 elements except possibly at the end
+    // of the sample, where the second group is skipped.
+    for (int64_t i = start + threadIdx.x * kSdeVec; i < end; i += 2 * kSdeThreads * kSdeVec) {
+      const int64_t i2 = i + kSdeThreads * kSdeVec;
+      const bool two = i2 < end;
+      float xv[2][8], vv[2][8], tv[2][8], out[8];
+      ld8<BF16>(x, base + i, xv[0]);
+      ld8<BF16>(v, base + i, vv[0]);
+      ld8<BF16>(third, base + i, tv[0]);
+      if (two) {
+        ld8<BF16>(x, base + i2, xv[1]);
+        ld8<BF16>(v, base + i2, vv[1]);
+        ld8<BF16>(third, base + i2, tv[1]);
       }
-      if constexpr (MODE == 0) st8<BF16>(x_next, base + i, out);
-      if constexpr (LOGP) acc += static_cast<double>(part);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        if (h == 1 && !two) break;
+        float part = 0.f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          if constexpr (MODE == 0) {
+            float r2 = sde_elem<BF16>(xv[h][j], vv[h][j], tv[h][j], a, b, c, out[j]);
+            part = part + r2;
+          } else {
+            float mean = fmaf(a, xv[h][j], b * vv[h][j]);
+            float r = tv[h][j] - mean;
+            part = part + r * r;
+          }
+        }
+        if constexpr (MODE == 0) st8<BF16>(x_next, base + (h == 0 ? i : i2), out);
+        if constexpr (LOGP) acc += static_cast<double>(part);
+      }
     }
   } else {
     for (int64_t i = start + threadIdx.x; i < end; i += kSdeThreads) {
