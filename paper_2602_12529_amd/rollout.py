@@ -77,19 +77,25 @@ class Rollout:
         if w.fixed_step is not None:
             t, tn = w.fixed_step
             self.sigmas = [w.eta * math.sqrt(t / (1.0 - t))]
+        # group ids (sample b belongs to prompt b // G), unit reward weights, outputs
+        self.group_id = torch.tensor([b // w.group for b in range(B)], dtype=torch.int32, device=device)
+        self.counts = torch.empty(w.prompts, dtype=torch.int32, device=device)
+        self.adv = torch.empty(B, dtype=torch.float32, device=device)
+        self.unit_weights = torch.ones(w.n_rewards, dtype=torch.float32, device=device)
+        # per-step time vectors t_k for all samples, uploaded once
+        self.t_steps = torch.tensor([[t] * B for t in self.ts[:-1]], dtype=torch.float32, device=device)
 
     def run(self, x0, txt, eps_steps, cond=None, txt_index=None, txt_out=None) -> RolloutResult:
         w, m = self.w, self.w.model
         B = w.batch
         x = x0
         xs, vs, logp = [x0], [], {}
-        t_dev = torch.empty(B, dtype=torch.float32, device=self.device)
         for k in range(len(self.ts) - 1):
             t, tn, sigma = self.ts[k], self.ts[k + 1], self.sigmas[k]
             v = torch.empty(self.shape, dtype=self.dt, device=self.device)
             if m.io_mode == C.IO_LATENT:
-                t_dev.fill_(t)
-                self.dit.forward(x, txt, w.grid, v, t=t_dev, cond=cond, txt_index=txt_index, ws=self.ws_dit)
+                self.dit.forward(x, txt, w.grid, v, t=self.t_steps[k], cond=cond, txt_index=txt_index,
+                                 ws=self.ws_dit)
             else:
                 self.dit.forward(x, txt, w.grid, v, cond=cond, txt_out=txt_out, ws=self.ws_dit)
             x_next = torch.empty_like(x)
@@ -105,11 +111,9 @@ class Rollout:
         return RolloutResult(xs=xs, vs=vs, logp=logp, ts=list(self.ts), sigmas=list(self.sigmas))
 
     def advantages(self, rewards, weights=None, mode: int = 0, eps: float = 1e-4):
-        B = self.w.batch
-        gid = (torch.arange(B, device=self.device, dtype=torch.int32) // self.w.group).contiguous()
-        n_groups = self.w.prompts
         if weights is None:
-            weights = torch.ones(rewards.shape[1], dtype=torch.float32, device=self.device)
-        counts = torch.empty(n_groups, dtype=torch.int32, device=self.device)
-        adv = api.group_advantage(rewards, weights, gid, n_groups, mode, eps, counts=counts)
-        return adv, counts
+            weights = self.unit_weights if rewards.shape[1] == self.unit_weights.numel() else \
+                torch.ones(rewards.shape[1], dtype=torch.float32, device=self.device)
+        api.group_advantage(rewards, weights, self.group_id, self.w.prompts, mode, eps, adv=self.adv,
+                            counts=self.counts)
+        return self.adv, self.counts
