@@ -25,8 +25,9 @@ enum { FF_EPI_BIAS = 0, FF_EPI_GELU = 1, FF_EPI_GATED = 2 };
  *   FF_EPI_GELU:  out = GELU_tanh(A W^T + bias) on columns >= gelu_from
  *                 (earlier columns get A W^T + bias)
  *   FF_EPI_GATED: out = resid + gate[m / rows_per_sample] * (A W^T + bias), the
- *                 adaLN-gated residual; gate float32 [*, gate_ld], resid
- *                 [M, N] (row stride ldr) may alias out.
+ *                 adaLN-gated residual; gate float32 [*, gate_ld] or NULL for a
+ *                 plain residual (gate = 1), resid [M, N] (row stride ldr) may
+ *                 alias out.
  * Accumulation is float32.  bf16 requires K % 64 == 0 and lda, ldo, ldr % 8 == 0. */
 int ff_linear(const void* A, int64_t lda, const void* W, const void* bias, void* out, int64_t ldo,
               int64_t M, int64_t N, int64_t K, int32_t epi, int64_t gelu_from, const float* gate,

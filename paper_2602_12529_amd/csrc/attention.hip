@@ -34,6 +34,7 @@ struct AttnParams {
   const bf16_t* Q; const bf16_t* K; const bf16_t* Vt;
   bf16_t* out0; bf16_t* out1; int64_t split; int64_t ldo;
   float scale_log2;
+  int64_t q_bs, q_hs, q_rs;   // Q element (b, h, q, :) at b*q_bs + h*q_hs + q*q_rs
 };
 
 constexpr int D = 128;
@@ -132,7 +133,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_bf16_d128(AttnPara
   {
     int64_t q = q0 + ql;
     if (q >= p.n_q) q = p.n_q - 1;
-    const bf16_t* qp = p.Q + (bh * p.n_q + q) * D + 8 * g;
+    const bf16_t* qp = p.Q + (bh / p.heads) * p.q_bs + (bh % p.heads) * p.q_hs + q * p.q_rs + 8 * g;
 #pragma unroll
     for (int t = 0; t < 8; ++t) qf[t] = *reinterpret_cast<const bf16x8_t*>(qp + 16 * t);
   }
@@ -227,6 +228,7 @@ struct AttnF32Params {
   const float* Q; const float* K; const float* V;   // V not transposed: [B, h, n_kv, d]
   float* out0; float* out1; int64_t split; int64_t ldo;
   float scale;
+  int64_t q_bs, q_hs, q_rs;
 };
 
 __global__ __launch_bounds__(64) void attn_f32_kernel(AttnF32Params p) {
@@ -236,7 +238,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnF32Params p) {
   constexpr int MAXD = 64;
   float qv[MAXD], acc[MAXD];
   const int d = static_cast<int>(p.d);
-  const float* qp = p.Q + (bh * p.n_q + q) * d;
+  const float* qp = p.Q + (bh / p.heads) * p.q_bs + (bh % p.heads) * p.q_hs + q * p.q_rs;
   for (int i = 0; i < d; ++i) { qv[i] = qp[i]; acc[i] = 0.f; }
   float m = -INFINITY, l = 0.f;
   for (int64_t k = 0; k < p.n_kv; ++k) {
@@ -262,6 +264,10 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnF32Params p) {
 
 int attention(const AttnArgs& a, hipStream_t s) {
   if (a.B == 0 || a.n_q == 0) return FF_OK;
+  const bool default_q = a.q_bs == 0 && a.q_hs == 0 && a.q_rs == 0;
+  const int64_t qbs = default_q ? a.heads * a.n_q * a.d : a.q_bs;
+  const int64_t qhs = default_q ? a.n_q * a.d : a.q_hs;
+  const int64_t qrs = default_q ? a.d : a.q_rs;
   const double flops = 4.0 * a.B * a.heads * static_cast<double>(a.n_q) * a.n_kv * a.d;
   const double esz = static_cast<double>(dtype_size(a.dtype));
   const double bytes = esz * a.B * a.heads * a.d * (2.0 * a.n_q + 2.0 * a.n_kv);
@@ -271,7 +277,7 @@ int attention(const AttnArgs& a, hipStream_t s) {
     AttnParams p{a.B, a.heads, a.n_q, a.n_kv,
                  static_cast<const bf16_t*>(a.Q), static_cast<const bf16_t*>(a.K), static_cast<const bf16_t*>(a.Vt),
                  static_cast<bf16_t*>(a.out0), static_cast<bf16_t*>(a.out1), a.split, a.ldo,
-                 static_cast<float>(a.scale * 1.4426950408889634)};
+                 static_cast<float>(a.scale * 1.4426950408889634), qbs, qhs, qrs};
     static const char* env = getenv("FF_ATTN_WAVES");
     const int waves = (env && env[0] == '4') ? 4 : 8;
     LaunchScope ls("attn_bf16_d128", s, flops, bytes);
@@ -290,7 +296,7 @@ int attention(const AttnArgs& a, hipStream_t s) {
   if (a.d > 64) return fail(FF_EUNSUPPORTED, "attention: f32 head_dim %lld > 64", (long long)a.d);
   AttnF32Params p{a.B, a.heads, a.n_q, a.n_kv, a.d,
                   static_cast<const float*>(a.Q), static_cast<const float*>(a.K), static_cast<const float*>(a.Vt),
-                  static_cast<float*>(a.out0), static_cast<float*>(a.out1), a.split, a.ldo, a.scale};
+                  static_cast<float*>(a.out0), static_cast<float*>(a.out1), a.split, a.ldo, a.scale, qbs, qhs, qrs};
   LaunchScope ls("attn_f32", s, flops, bytes);
   hipLaunchKernelGGL(attn_f32_kernel, dim3(static_cast<unsigned>((a.n_q + 63) / 64), static_cast<unsigned>(a.B * a.heads)),
                      dim3(64), 0, s, p);

@@ -144,6 +144,16 @@ struct Single {
   const void* qn = nullptr;
   const void* kn = nullptr;
 };
+struct Wan {
+  const void* mod = nullptr;            // E_block [6, H]
+  Lin qkv, o, cq, ckv, co, ffn1, ffn2;
+  const void* qn = nullptr;             // self-attention Q/K RMSNorm weights [H]
+  const void* kn = nullptr;
+  const void* can_w = nullptr;          // cross-attention query LayerNorm affine [H]
+  const void* can_b = nullptr;
+  const void* cqn = nullptr;            // cross-attention Q/K RMSNorm weights [H]
+  const void* ckn = nullptr;
+};
 
 }  // namespace
 
@@ -151,8 +161,10 @@ struct ff_dit {
   ff_dit_config cfg;
   std::vector<const void*> ptr;
   Lin temb1, temb2, pooled1, pooled2, x_in, txt_in, final_mod, final_proj;
+  Lin temb_proj, txt1, txt2;            // WAN: e(t) projection, text MLP
   std::vector<Stream> dual_img, dual_txt;
   std::vector<Single> single;
+  std::vector<Wan> wan;
 };
 
 namespace {
@@ -160,7 +172,8 @@ namespace {
 // Workspace plan: byte offsets of every buffer of one forward.
 struct Plan {
   int64_t B, Ni, Nt, N, P;
-  size_t rope, temb_in, c, tmp, condB, cond32, mods, ximg, xtxt, joint, y, qkv, q, k, vt, o, u, txth, total;
+  size_t rope, temb_in, c, tmp, condB, cond32, mods, ximg, xtxt, joint, y, qkv, q, k, vt, o, u, txth;
+  size_t e6, ctx1, ctxp, kvc, kc, vct, qd, total;
 };
 
 Plan plan(const ff_dit& m, int64_t B, const int32_t grid[3], int64_t n_txt, int64_t n_prompts) {
@@ -194,6 +207,14 @@ Plan plan(const ff_dit& m, int64_t B, const int32_t grid[3], int64_t n_txt, int6
   p.o = take(static_cast<size_t>(B) * p.N * H * es);
   p.u = take(static_cast<size_t>(B) * (p.Ni > p.Nt ? p.Ni : p.Nt) * F * es);
   p.txth = take(latent ? static_cast<size_t>(p.P) * p.Nt * H * es : 0);
+  const bool wan = c.model == FF_MODEL_WAN;
+  p.e6 = take(wan ? static_cast<size_t>(B) * 6 * H * 4 : 0);
+  p.ctx1 = take(wan ? static_cast<size_t>(p.P) * p.Nt * H * es : 0);
+  p.ctxp = take(wan ? static_cast<size_t>(p.P) * p.Nt * H * es : 0);
+  p.kvc = take(wan ? static_cast<size_t>(B) * p.Nt * 2 * H * es : 0);
+  p.kc = take(wan ? static_cast<size_t>(B) * p.Nt * H * es : 0);
+  p.vct = take(wan ? static_cast<size_t>(B) * p.Nt * H * es : 0);
+  p.qd = take(wan ? static_cast<size_t>(B) * p.Nt * H * es : 0);
   p.total = round_up(cv.off, 256);
   return p;
 }
@@ -355,6 +376,135 @@ int single_block(const ff_dit& m, const Plan& p, void* ws, int j, const float* c
   return gemm(g2, s);
 }
 
+// In-place RMSNorm * w over rows of width H with row stride ld (full-width QK norm).
+int rms_rows(const ff_dit_config& c, void* x, int64_t rows, int64_t ld, const void* w, hipStream_t s) {
+  NormArgs a{};
+  a.dtype = c.dtype;
+  a.rows = rows; a.H = c.hidden;
+  a.x = x; a.ldx = ld; a.y = x; a.ldy = ld;
+  a.norm_kind = FF_NORM_RMS;
+  a.eps = static_cast<float>(c.norm_eps);
+  a.shift = nullptr; a.scale = nullptr; a.mod_ld = 0;
+  a.w = w; a.bias = nullptr;
+  a.rows_per_sample = rows;
+  return norm_modulate(a, s);
+}
+
+// Relayout (no norm, optional RoPE) of packed Q|K|V rows into the attention layout.
+int relayout(const ff_dit_config& c, const Plan& p, const void* q, const void* k, const void* v, int64_t ld,
+             int64_t n_tok, const float2* rope, void* Q, void* K, void* Vt, hipStream_t s) {
+  QkvArgs a{};
+  a.dtype = c.dtype;
+  a.B = p.B; a.n_tok = n_tok; a.tok_offset = 0; a.n_joint = n_tok; a.src_rows = n_tok;
+  a.heads = c.heads; a.d = c.head_dim;
+  a.q = q; a.k = k; a.v = v; a.ld = ld;
+  a.q_w = nullptr; a.k_w = nullptr;
+  a.full_width_norm = 0; a.apply_norm = 0;
+  a.eps = static_cast<float>(c.norm_eps);
+  a.rope = rope;
+  a.Q = Q; a.Kd = K; a.Vt = Vt;
+  a.v_transposed = c.dtype == FF_BF16;
+  return qk_norm_rope(a, s);
+}
+
+// One WAN block on X [B*N_img, H] in place; ctx [B*N_txt, H]; mods [B, 6H].
+int wan_block(const ff_dit& m, const Plan& p, void* ws, int i, const void* ctx, void* X, hipStream_t s) {
+  const ff_dit_config& c = m.cfg;
+  const int64_t H = c.hidden, F = c.mlp_hidden;
+  const size_t es = dtype_size(c.dtype);
+  const Wan& wb = m.wan[i];
+  const int64_t rows = p.B * p.Ni, crow = p.B * p.Nt;
+  float* mods = reinterpret_cast<float*>(at(ws, p.mods));
+  const float* e6 = reinterpret_cast<const float*>(at(ws, p.e6));
+  char* Y = at(ws, p.y);
+  char* QKV = at(ws, p.qkv);
+  char* O = at(ws, p.o);
+  const float scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(c.head_dim)));
+  FF_TRY(add_table(wb.mod, c.dtype, e6, mods, p.B, 6 * H, s));
+  // self-attention
+  FF_TRY(norm_modulate(norm_args(c, rows, X, Y, mods, mods + H, 6 * H, p.Ni), s));
+  FF_TRY(gemm(gemm_args(c.dtype, rows, 3 * H, H, Y, H, wb.qkv, QKV, 3 * H, EPI_NONE), s));
+  FF_TRY(rms_rows(c, QKV, rows, 3 * H, wb.qn, s));
+  FF_TRY(rms_rows(c, QKV + H * es, rows, 3 * H, wb.kn, s));
+  FF_TRY(relayout(c, p, QKV, QKV + H * es, QKV + 2 * H * es, 3 * H, p.Ni,
+                  reinterpret_cast<const float2*>(at(ws, p.rope)), at(ws, p.q), at(ws, p.k), at(ws, p.vt), s));
+  {
+    AttnArgs a{};
+    a.dtype = c.dtype;
+    a.B = p.B; a.heads = c.heads; a.d = c.head_dim;
+    a.n_q = p.Ni; a.n_kv = p.Ni;
+    a.Q = at(ws, p.q); a.K = at(ws, p.k); a.Vt = at(ws, p.vt);
+    a.out0 = O; a.out1 = O; a.split = p.Ni; a.ldo = H;
+    a.scale = scale;
+    FF_TRY(attention(a, s));
+  }
+  GemmArgs go = gemm_args(c.dtype, rows, H, H, O, H, wb.o, X, H, EPI_GATED);
+  go.gate = mods + 2 * H; go.gate_ld = 6 * H; go.resid = X; go.ldr = H; go.rows_per_sample = p.Ni;
+  FF_TRY(gemm(go, s));
+  // cross-attention to the text context (K/V from ctx; Q read token-major)
+  {
+    NormArgs na = norm_args(c, rows, X, Y, nullptr, nullptr, 0, p.Ni);
+    na.norm_kind = FF_NORM_LN;
+    na.w = wb.can_w; na.bias = wb.can_b;
+    FF_TRY(norm_modulate(na, s));
+  }
+  FF_TRY(gemm(gemm_args(c.dtype, rows, H, H, Y, H, wb.cq, QKV, H, EPI_NONE), s));
+  FF_TRY(rms_rows(c, QKV, rows, H, wb.cqn, s));
+  char* KV = at(ws, p.kvc);
+  FF_TRY(gemm(gemm_args(c.dtype, crow, 2 * H, H, ctx, H, wb.ckv, KV, 2 * H, EPI_NONE), s));
+  FF_TRY(rms_rows(c, KV, crow, 2 * H, wb.ckn, s));
+  FF_TRY(relayout(c, p, KV, KV, KV + H * es, 2 * H, p.Nt, nullptr, at(ws, p.qd), at(ws, p.kc), at(ws, p.vct), s));
+  {
+    AttnArgs a{};
+    a.dtype = c.dtype;
+    a.B = p.B; a.heads = c.heads; a.d = c.head_dim;
+    a.n_q = p.Ni; a.n_kv = p.Nt;
+    a.Q = QKV; a.K = at(ws, p.kc); a.Vt = at(ws, p.vct);
+    a.q_bs = p.Ni * H; a.q_hs = c.head_dim; a.q_rs = H;
+    a.out0 = O; a.out1 = O; a.split = p.Ni; a.ldo = H;
+    a.scale = scale;
+    FF_TRY(attention(a, s));
+  }
+  GemmArgs gc = gemm_args(c.dtype, rows, H, H, O, H, wb.co, X, H, EPI_GATED);
+  gc.gate = nullptr; gc.resid = X; gc.ldr = H; gc.rows_per_sample = p.Ni;
+  FF_TRY(gemm(gc, s));
+  // FFN
+  FF_TRY(norm_modulate(norm_args(c, rows, X, Y, mods + 3 * H, mods + 4 * H, 6 * H, p.Ni), s));
+  char* U = at(ws, p.u);
+  FF_TRY(gemm(gemm_args(c.dtype, rows, F, H, Y, H, wb.ffn1, U, F, EPI_GELU), s));
+  GemmArgs g2 = gemm_args(c.dtype, rows, H, F, U, F, wb.ffn2, X, H, EPI_GATED);
+  g2.gate = mods + 5 * H; g2.gate_ld = 6 * H; g2.resid = X; g2.ldr = H; g2.rows_per_sample = p.Ni;
+  return gemm(g2, s);
+}
+
+int forward_wan(const ff_dit& m, const Plan& p, const void* x, const void* txt, const int32_t* txt_index,
+                const float* t, const int32_t grid[3], void* v_out, void* ws, hipStream_t s) {
+  const ff_dit_config& c = m.cfg;
+  const int64_t H = c.hidden;
+  float* temb = reinterpret_cast<float*>(at(ws, p.c));
+  float* tmp = reinterpret_cast<float*>(at(ws, p.tmp));
+  float* te = reinterpret_cast<float*>(at(ws, p.temb_in));
+  FF_TRY(rope_table(reinterpret_cast<float2*>(at(ws, p.rope)), grid, c.head_dim, c.rope_axes, c.rope_theta, s));
+  FF_TRY(timestep_sinusoid(t, te, p.B, s));
+  FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, H, 256, te, ACT_NONE, m.temb1, tmp), s));
+  FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, H, H, tmp, ACT_SILU, m.temb2, temb), s));
+  FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 6 * H, H, temb, ACT_SILU, m.temb_proj, reinterpret_cast<float*>(at(ws, p.e6))), s));
+  char* c1 = at(ws, p.ctx1);
+  char* cp = at(ws, p.ctxp);
+  FF_TRY(gemm(gemm_args(c.dtype, p.P * p.Nt, H, c.txt_dim, txt, c.txt_dim, m.txt1, c1, H, EPI_GELU), s));
+  FF_TRY(gemm(gemm_args(c.dtype, p.P * p.Nt, H, H, c1, H, m.txt2, cp, H, EPI_NONE), s));
+  char* ctx = at(ws, p.xtxt);
+  FF_TRY(gather_rows(c.dtype, cp, txt_index, p.P, ctx, p.B, p.Nt, H, s));
+  char* X = at(ws, p.ximg);
+  FF_TRY(gemm(gemm_args(c.dtype, p.B * p.Ni, H, c.in_channels, x, c.in_channels, m.x_in, X, H, EPI_NONE), s));
+  for (int i = 0; i < c.n_wan; ++i) FF_TRY(wan_block(m, p, ws, i, ctx, X, s));
+  float* mods = reinterpret_cast<float*>(at(ws, p.mods));
+  FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 2 * H, H, temb, ACT_SILU, m.final_mod, mods), s));
+  char* Y = at(ws, p.y);
+  FF_TRY(norm_modulate(norm_args(c, p.B * p.Ni, X, Y, mods, mods + H, 2 * H, p.Ni), s));
+  return gemm(gemm_args(c.dtype, p.B * p.Ni, c.in_channels, H, Y, H, m.final_proj, v_out, c.in_channels, EPI_NONE), s);
+}
+
 int forward_mmdit(const ff_dit& m, const Plan& p, const void* x, const void* txt, const int32_t* txt_index,
                   const void* cond, const float* t, const int32_t grid[3], void* v_out, void* txt_out, void* ws,
                   hipStream_t s) {
@@ -457,7 +607,8 @@ int ff_dit_tensor_info(const ff_dit_config* cfg, int64_t i, char* name, size_t n
 
 int ff_dit_create(const ff_dit_config* cfg, const void* const* tensors, int64_t n_tensors, ff_dit** out) {
   FF_TRY(check_config(cfg));
-  if (cfg->model == FF_MODEL_WAN) return fail(FF_EUNSUPPORTED, "ff_dit_create: the WAN block is not implemented in this build");
+  if (cfg->model == FF_MODEL_WAN && cfg->io_mode != FF_IO_LATENT)
+    return fail(FF_EUNSUPPORTED, "ff_dit_create: the WAN model runs in latent mode only");
   if (!out) return fail(FF_EINVAL, "ff_dit_create: null output");
   *out = nullptr;
   std::vector<TensorSpec> t = tensor_table(*cfg);
@@ -477,13 +628,31 @@ int ff_dit_create(const ff_dit_config* cfg, const void* const* tensors, int64_t 
   if (cfg->io_mode == FF_IO_LATENT) {
     m->temb1 = L("temb.fc1");
     m->temb2 = L("temb.fc2");
-    if (cfg->pooled_dim) { m->pooled1 = L("pooled.fc1"); m->pooled2 = L("pooled.fc2"); }
+    if (cfg->model == FF_MODEL_MMDIT) {
+      if (cfg->pooled_dim) { m->pooled1 = L("pooled.fc1"); m->pooled2 = L("pooled.fc2"); }
+      m->txt_in = L("txt_in");
+    } else {
+      m->temb_proj = L("temb.proj");
+      m->txt1 = L("txt_in.fc1");
+      m->txt2 = L("txt_in.fc2");
+    }
     m->x_in = L("x_in");
-    m->txt_in = L("txt_in");
     m->final_mod = L("final.mod");
     m->final_proj = L("final.proj");
   }
-  for (int i = 0; i < cfg->n_dual; ++i)
+  for (int i = 0; i < (cfg->model == FF_MODEL_WAN ? cfg->n_wan : 0); ++i) {
+    std::string p = "wan." + std::to_string(i) + ".";
+    Wan wb;
+    wb.mod = by[p + "mod"];
+    wb.qkv = L(p + "sa.qkv"); wb.o = L(p + "sa.o");
+    wb.qn = by[p + "sa.q_norm.w"]; wb.kn = by[p + "sa.k_norm.w"];
+    wb.can_w = by[p + "ca.norm.w"]; wb.can_b = by[p + "ca.norm.b"];
+    wb.cq = L(p + "ca.q"); wb.ckv = L(p + "ca.kv"); wb.co = L(p + "ca.o");
+    wb.cqn = by[p + "ca.q_norm.w"]; wb.ckn = by[p + "ca.k_norm.w"];
+    wb.ffn1 = L(p + "ffn1"); wb.ffn2 = L(p + "ffn2");
+    m->wan.push_back(wb);
+  }
+  for (int i = 0; i < (cfg->model == FF_MODEL_MMDIT ? cfg->n_dual : 0); ++i)
     for (int k = 0; k < 2; ++k) {
       std::string p = "dual." + std::to_string(i) + (k == 0 ? ".img." : ".txt.");
       Stream st;
@@ -492,7 +661,7 @@ int ff_dit_create(const ff_dit_config* cfg, const void* const* tensors, int64_t 
       st.qn = by[p + "q_norm.w"]; st.kn = by[p + "k_norm.w"];
       (k == 0 ? m->dual_img : m->dual_txt).push_back(st);
     }
-  for (int j = 0; j < cfg->n_single; ++j) {
+  for (int j = 0; j < (cfg->model == FF_MODEL_MMDIT ? cfg->n_single : 0); ++j) {
     std::string p = "single." + std::to_string(j) + ".";
     Single sb;
     sb.mod = L(p + "mod"); sb.lin1 = L(p + "lin1"); sb.lin2 = L(p + "lin2");
@@ -553,6 +722,8 @@ int ff_dit_forward(const ff_dit* m, const void* x, const void* txt, const int32_
   if (!workspace || ws_bytes < p.total)
     return fail(FF_EWORKSPACE, "ff_dit_forward: workspace of %zu bytes needed, %zu given", p.total, workspace ? ws_bytes : 0);
   if (!aligned16(workspace)) return fail(FF_EINVAL, "ff_dit_forward: workspace must be 16-byte aligned");
+  if (c.model == FF_MODEL_WAN)
+    return forward_wan(*m, p, x, txt, txt_index, t, grid, v_out, workspace, static_cast<hipStream_t>(stream));
   return forward_mmdit(*m, p, x, txt, txt_index, cond, t, grid, v_out, txt_out, workspace, static_cast<hipStream_t>(stream));
 }
 

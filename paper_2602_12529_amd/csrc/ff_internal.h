@@ -67,7 +67,7 @@ struct Carver {
 enum Epi : int {
   EPI_NONE = 0,       // out = acc + bias
   EPI_GELU = 1,       // out = gelu_tanh(acc + bias) for columns >= gelu_from, else acc + bias
-  EPI_GATED = 2,      // out = resid + gate[b] * (acc + bias)
+  EPI_GATED = 2,      // out = resid + gate[b] * (acc + bias); gate null: out = resid + acc + bias
 };
 
 struct GemmArgs {
@@ -147,6 +147,8 @@ struct AttnArgs {
   // output split by query index: q < split -> out0 rows, else out1 rows (token-major, ld = H)
   void* out0; void* out1; int64_t split; int64_t ldo;
   float scale;
+  // optional Q layout: element (b, h, q, :) at b*q_bs + h*q_hs + q*q_rs (all 0: [B, h, n_q, d])
+  int64_t q_bs, q_hs, q_rs;
 };
 int attention(const AttnArgs& a, hipStream_t s);
 

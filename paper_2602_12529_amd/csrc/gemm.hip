@@ -53,7 +53,7 @@ __device__ __forceinline__ void epi_store(const GemmParams& p, int64_t m, int64_
   if constexpr (EPI == EPI_GELU) {
     if (n >= p.gelu_from) v = gelu_tanh_f(v);
   } else if constexpr (EPI == EPI_GATED) {
-    const float g = p.gate[(m / p.rows_per_sample) * p.gate_ld + n];
+    const float g = p.gate ? p.gate[(m / p.rows_per_sample) * p.gate_ld + n] : 1.0f;
     v = ld1<BF16>(p.resid, m * p.ldr + n) + g * v;
   }
   st1<BF16>(p.out, m * p.ldo + n, v);
@@ -121,18 +121,23 @@ __device__ __forceinline__ void epilogue_blocks(const GemmParams& p, const f32x1
           for (int e = 0; e < 16; ++e)
             if (n + e >= p.gelu_from) v[e] = gelu_tanh_f(v[e]);
         } else if constexpr (EPI == EPI_GATED) {
-          const uint64_t smp = static_cast<uint64_t>(m) / static_cast<uint64_t>(p.rows_per_sample);
-          const float* g = p.gate + smp * p.gate_ld + n;
           float rs[16];
           ld8<true>(p.resid, m * p.ldr + n, *reinterpret_cast<float(*)[8]>(rs));
           ld8<true>(p.resid, m * p.ldr + n + 8, *reinterpret_cast<float(*)[8]>(rs + 8));
+          if (p.gate) {
+            const uint64_t smp = static_cast<uint64_t>(m) / static_cast<uint64_t>(p.rows_per_sample);
+            const float* g = p.gate + smp * p.gate_ld + n;
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const float4 t = *reinterpret_cast<const float4*>(g + 4 * q);
-            v[4 * q] = fmaf(t.x, v[4 * q], rs[4 * q]);
-            v[4 * q + 1] = fmaf(t.y, v[4 * q + 1], rs[4 * q + 1]);
-            v[4 * q + 2] = fmaf(t.z, v[4 * q + 2], rs[4 * q + 2]);
-            v[4 * q + 3] = fmaf(t.w, v[4 * q + 3], rs[4 * q + 3]);
+            for (int q = 0; q < 4; ++q) {
+              const float4 t = *reinterpret_cast<const float4*>(g + 4 * q);
+              v[4 * q] = fmaf(t.x, v[4 * q], rs[4 * q]);
+              v[4 * q + 1] = fmaf(t.y, v[4 * q + 1], rs[4 * q + 1]);
+              v[4 * q + 2] = fmaf(t.z, v[4 * q + 2], rs[4 * q + 2]);
+              v[4 * q + 3] = fmaf(t.w, v[4 * q + 3], rs[4 * q + 3]);
+            }
+          } else {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) v[e] += rs[e];
           }
         }
         st8<true>(out, m * p.ldo + n, *reinterpret_cast<const float(*)[8]>(v));
@@ -703,7 +708,7 @@ int gemm(const GemmArgs& a, hipStream_t s) {
                a.W, a.ldw, a.bias, a.out, a.ldo, a.gelu_from, a.gate, a.gate_ld, a.resid, a.ldr,
                a.rows_per_sample > 0 ? a.rows_per_sample : a.M, 0};
   p.vec_ok = a.ldo % 8 == 0 && aligned16(a.out) && (!a.bias || aligned16(a.bias)) &&
-             (a.epi != EPI_GATED || (a.ldr % 8 == 0 && aligned16(a.resid) && a.gate_ld % 4 == 0 && aligned16(a.gate)));
+             (a.epi != EPI_GATED || (a.ldr % 8 == 0 && aligned16(a.resid) && (!a.gate || (a.gate_ld % 4 == 0 && aligned16(a.gate)))));
   const double esz = static_cast<double>(dtype_size(a.dtype));
   const double flops = 2.0 * a.M * a.N * a.K;
   const double bytes = esz * (static_cast<double>(a.M) * a.K + static_cast<double>(a.N) * a.K +

@@ -384,8 +384,13 @@ __global__ __launch_bounds__(256) void qk_rope_vec_kernel(QkvArgs a) {
   const int h = blockIdx.y;
   const int64_t b = blockIdx.z;
   float qw[8], kw[8];
-  ld8<true>(a.q_w, c * 8, qw);
-  ld8<true>(a.k_w, c * 8, kw);
+  if (a.apply_norm) {
+    ld8<true>(a.q_w, c * 8, qw);
+    ld8<true>(a.k_w, c * 8, kw);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) qw[j] = kw[j] = 1.0f;
+  }
   const int64_t out_head = (b * a.heads + h) * a.n_joint;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -415,7 +420,7 @@ __global__ __launch_bounds__(256) void qk_rope_vec_kernel(QkvArgs a) {
       ss += __shfl_xor(ss, 4, 64);
       ss += __shfl_xor(ss, 2, 64);
       ss += __shfl_xor(ss, 1, 64);
-      const float rstd = rsqrtf(ss * (1.0f / 128.0f) + a.eps);
+      const float rstd = a.apply_norm ? rsqrtf(ss * (1.0f / 128.0f) + a.eps) : 1.0f;
       const float* w = which == 0 ? qw : kw;
       float y[8];
 #pragma unroll
@@ -524,9 +529,9 @@ int qk_norm_rope(const QkvArgs& a, hipStream_t s) {
   if (a.d > 128 || a.d % 2) return fail(FF_EUNSUPPORTED, "qk_norm_rope: head_dim %d", a.d);
   dim3 grid(blocks_for(a.n_tok, kRopeTok), static_cast<unsigned>(a.heads), static_cast<unsigned>(a.B));
   LaunchScope ls("qk_norm_rope", s, 0.0, 6.0 * dtype_size(a.dtype) * a.B * a.n_tok * a.heads * a.d);
-  const bool vec = a.dtype == FF_BF16 && a.d == 128 && a.v_transposed && a.apply_norm && !a.full_width_norm &&
+  const bool vec = a.dtype == FF_BF16 && a.d == 128 && a.v_transposed && !a.full_width_norm &&
                    a.ld % 8 == 0 && aligned16(a.q) && aligned16(a.k) && aligned16(a.v) && aligned16(a.Q) &&
-                   aligned16(a.Kd) && aligned16(a.Vt) && aligned16(a.q_w) && aligned16(a.k_w) &&
+                   aligned16(a.Kd) && aligned16(a.Vt) && (!a.apply_norm || (aligned16(a.q_w) && aligned16(a.k_w))) &&
                    (!a.rope || aligned16(a.rope)) && a.n_joint % 8 == 0 && a.tok_offset % 8 == 0 && a.n_tok % 8 == 0;
   if (vec) hipLaunchKernelGGL(qk_rope_vec_kernel, grid, dim3(256), 0, s, a);
   else if (a.dtype == FF_BF16) hipLaunchKernelGGL(qk_rope_kernel<true>, grid, dim3(256), 0, s, a);

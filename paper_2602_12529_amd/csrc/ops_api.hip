@@ -26,8 +26,8 @@ int ff_linear(const void* A, int64_t lda, const void* W, const void* bias, void*
   if (lda < K || ldo < N) return fail(FF_EINVAL, "%s: lda < K or ldo < N", fn);
   if (epi < FF_EPI_BIAS || epi > FF_EPI_GATED) return fail(FF_EINVAL, "%s: bad epilogue %d", fn, epi);
   if (epi == FF_EPI_GATED) {
-    if (!gate || !resid) return fail(FF_EINVAL, "%s: gated epilogue needs gate and resid", fn);
-    if (rows_per_sample < 1 || gate_ld < N || ldr < N) return fail(FF_EINVAL, "%s: bad gate/resid layout", fn);
+    if (!resid) return fail(FF_EINVAL, "%s: gated epilogue needs resid", fn);
+    if (ldr < N || (gate && (rows_per_sample < 1 || gate_ld < N))) return fail(FF_EINVAL, "%s: bad gate/resid layout", fn);
   }
   if (!aligned16(A) || !aligned16(W) || !aligned16(out)) return fail(FF_EINVAL, "%s: pointers must be 16-byte aligned", fn);
   if (dtype == FF_BF16) {

@@ -155,3 +155,90 @@ def test_flux_dual_block_full_size(gpu_lib):
         assert rel(xn[b:b + 1], xr) <= TOL[C.BF16]
         lr = osde.step_log_prob(x0[b:b + 1], v[b:b + 1], xn[b:b + 1], t, tn, sigma)
         assert abs(lp[b] - lr[0]) <= LOGP_ABS
+
+
+def _small_wan(dtype):
+    if dtype == C.BF16:
+        m = C.ModelConfig(model=C.MODEL_WAN, io_mode=C.IO_LATENT, dtype=C.BF16, n_wan=2, hidden=256, heads=2,
+                          head_dim=128, mlp_hidden=512, in_channels=64, txt_dim=128, norm_kind=C.NORM_LN,
+                          rope_axes=(44, 42, 42))
+        return C.Workload(name="small-wan-bf16", index=13, model=m, prompts=1, group=2, grid=(3, 4, 4), n_txt=16,
+                          steps=2)
+    m = C.ModelConfig(model=C.MODEL_WAN, io_mode=C.IO_LATENT, dtype=C.F32, n_wan=2, hidden=64, heads=4,
+                      head_dim=16, mlp_hidden=128, in_channels=16, txt_dim=32, norm_kind=C.NORM_LN,
+                      rope_axes=(4, 6, 6))
+    return C.Workload(name="small-wan-f32", index=14, model=m, prompts=2, group=1, grid=(2, 3, 4), n_txt=8, steps=2)
+
+
+@pytest.mark.parametrize("dt", [C.F32, C.BF16], ids=["f32", "bf16"])
+def test_wan_rollout_teacher_forced(gpu_lib, dt):
+    """WAN blocks (3D RoPE, full-width QK norm, cross-attention, LN modulation) in a 2-step rollout."""
+    w = _small_wan(dt)
+    m = w.model
+    W, txt, cond, x0, eps = _inputs(w)
+    Wd, T, Cd, X0, E = _device(w, W, txt, cond, x0, eps)
+    dit = api.Dit(m, Wd)
+    ro = R.Rollout(w, dit)
+    tidx = torch.from_numpy(synth.txt_index(w)).cuda()
+    res = ro.run(X0, T, E, txt_index=tidx)
+    torch.cuda.synchronize()
+    for k in range(w.steps):
+        xk = host(res.xs[k])
+        v_ref = odit.forward(m, W, xk, txt, t=np.full(w.batch, res.ts[k]), txt_index=synth.txt_index(w), grid=w.grid)
+        say("wan step", k, rel(host(res.vs[k]), v_ref))
+        assert rel(host(res.vs[k]), v_ref) <= TOL[dt]
+        lp_ref = osde.step_log_prob(xk, host(res.vs[k]), host(res.xs[k + 1]), res.ts[k], res.ts[k + 1], res.sigmas[k])
+        assert np.max(np.abs(host(res.logp[k]) - lp_ref)) <= LOGP_ABS
+
+
+@pytest.mark.timeout(900)
+def test_wan_block_full_size_sampled_rows(gpu_lib):
+    """One WAN block at full size (B=1, 21x30x52 = 32760 video tokens, 512 text tokens, H=1536, bf16):
+    the oracle recomputes K/V for all tokens and everything else for 48 sampled query tokens."""
+    base = C.WAN_STACK
+    m = base.model.replace(n_wan=1)
+    w = C.Workload(**{**base.__dict__, "model": m, "steps": 1})
+    say("full wan block: generating inputs")
+    W, txt, cond, x0, eps = _inputs(w)
+    Wd, T, Cd, X0, E = _device(w, W, txt, cond, x0, eps)
+    dit = api.Dit(m, Wd)
+    v = torch.empty_like(X0)
+    t = torch.full((1,), 0.6, dtype=torch.float32, device="cuda")
+    tidx = torch.zeros(1, dtype=torch.int32, device="cuda")
+    dit.forward(X0, T, w.grid, v, t=t, txt_index=tidx)
+    torch.cuda.synchronize()
+    vg = host(v)[0]
+    # oracle, sampled rows
+    f = odit.f64
+    eps_n, H, h = m.norm_eps, m.hidden, m.heads
+    rows = np.linspace(0, w.n_img - 1, 48).astype(int)
+    temb = odit.mlp2(odit.timestep_sinusoid(np.array([0.6])), W, "temb.fc1", "temb.fc2", odit.silu)
+    e6 = odit.linear(odit.silu(temb), W, "temb.proj").reshape(1, 6, H)
+    ctx = odit.mlp2(txt, W, "txt_in.fc1", "txt_in.fc2", odit.gelu_tanh)[0]
+    xh = odit.linear(x0[0], W, "x_in")
+    mod = f(W["wan.0.mod"]) + e6[0]
+    sh1, sc1, g1, sh2, sc2, g2 = (mod[n] for n in range(6))
+    y = odit.layer_norm(xh, eps_n) * (1 + sc1) + sh1
+    qkv = odit.linear(y, W, "wan.0.sa.qkv")
+    ang = odit.rope_angles(odit.grid_positions(w.grid), m.rope_axes, m.rope_theta)
+    k = odit.rms_norm(qkv[:, H:2 * H], eps_n) * f(W["wan.0.sa.k_norm.w"])
+    vv = qkv[:, 2 * H:]
+    k = odit.apply_rope(k.reshape(-1, h, 128).transpose(1, 0, 2), ang)
+    q = odit.rms_norm(qkv[rows, :H], eps_n) * f(W["wan.0.sa.q_norm.w"])
+    q = odit.apply_rope(q.reshape(-1, h, 128).transpose(1, 0, 2), ang[rows])
+    o = odit.attention(q, k, vv.reshape(-1, h, 128).transpose(1, 0, 2)).transpose(1, 0, 2).reshape(len(rows), H)
+    xr = xh[rows] + g1 * odit.linear(o, W, "wan.0.sa.o")
+    yc = odit.layer_norm(xr, eps_n) * f(W["wan.0.ca.norm.w"]) + f(W["wan.0.ca.norm.b"])
+    qc = odit.rms_norm(odit.linear(yc, W, "wan.0.ca.q"), eps_n) * f(W["wan.0.ca.q_norm.w"])
+    kv = odit.linear(ctx, W, "wan.0.ca.kv")
+    kc = odit.rms_norm(kv[:, :H], eps_n) * f(W["wan.0.ca.k_norm.w"])
+    oc = odit.attention(qc.reshape(-1, h, 128).transpose(1, 0, 2), kc.reshape(-1, h, 128).transpose(1, 0, 2),
+                        kv[:, H:].reshape(-1, h, 128).transpose(1, 0, 2)).transpose(1, 0, 2).reshape(len(rows), H)
+    xr = xr + odit.linear(oc, W, "wan.0.ca.o")
+    y2 = odit.layer_norm(xr, eps_n) * (1 + sc2) + sh2
+    xr = xr + g2 * odit.mlp2(y2, W, "wan.0.ffn1", "wan.0.ffn2", odit.gelu_tanh)
+    fm = odit.linear(odit.silu(temb), W, "final.mod")[0]
+    v_ref = odit.linear(odit.layer_norm(xr, eps_n) * (1 + fm[H:]) + fm[:H], W, "final.proj")
+    err = rel(vg[rows], v_ref)
+    say("  rel v (sampled rows)", err)
+    assert err <= TOL[C.BF16]
