@@ -55,6 +55,7 @@ def main() -> int:
 
     from paper_2602_12529_amd import api
     from paper_2602_12529_amd import configs as C
+    from paper_2602_12529_amd import profiling
     from paper_2602_12529_amd import rollout as R
     from paper_2602_12529_amd import synth
 
@@ -120,18 +121,24 @@ def main() -> int:
     block_flops = sum(p["flops"] for n, p in prof.items() if n.startswith(("gemm", "attn"))) / args.steps
     dominant = max(prof, key=lambda n: prof[n]["ms"])
     dp = prof[dominant]
+    per_launch = {"flops": dp["flops"] / dp["launches"], "algorithmic_bytes": dp["bytes"] / dp["launches"],
+                  "avg_us": 1e3 * dp["ms"] / dp["launches"]}
+    # HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE summary of this kernel,
+    # null when there is none or the kernel's sources have changed since it was taken.
+    rec = profiling.lookup_traffic(dominant)
+    traffic = rec["traffic_bytes_per_launch"] if rec else None
+    if rec:
+        per_launch["traffic_source"] = rec["summary"]
     compute_bound = dp["flops"] > 0 and dominant.startswith(("gemm", "attn"))
     if compute_bound:
         peak = PEAK_BF16_TFLOPS if m.dtype == C.BF16 else PEAK_FP32_TFLOPS
         achieved = dp["flops"] / (dp["ms"] * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
-                "traffic": None, "kernel": dominant,
-                "per_launch": {"flops": dp["flops"] / dp["launches"], "avg_us": 1e3 * dp["ms"] / dp["launches"]}}
+                "traffic": traffic, "kernel": dominant, "per_launch": per_launch}
     else:
         achieved = dp["bytes"] / (dp["ms"] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": achieved / PEAK_HBM_GBS, "traffic": None, "kernel": dominant,
-                "per_launch": {"bytes": dp["bytes"] / dp["launches"], "avg_us": 1e3 * dp["ms"] / dp["launches"]}}
+                "frac": achieved / PEAK_HBM_GBS, "traffic": traffic, "kernel": dominant, "per_launch": per_launch}
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -205,7 +205,7 @@ Plan plan(const ff_dit& m, int64_t B, const int32_t grid[3], int64_t n_txt, int6
   p.k = take(static_cast<size_t>(B) * p.N * H * es);
   p.vt = take(static_cast<size_t>(B) * p.N * H * es);
   p.o = take(static_cast<size_t>(B) * p.N * H * es);
-  p.u = take(static_cast<size_t>(B) * (p.Ni > p.Nt ? p.Ni : p.Nt) * F * es);
+  p.u = take(static_cast<size_t>(B) * (p.Ni + p.Nt) * F * es);
   p.txth = take(latent ? static_cast<size_t>(p.P) * p.Nt * H * es : 0);
   const bool wan = c.model == FF_MODEL_WAN;
   p.e6 = take(wan ? static_cast<size_t>(B) * 6 * H * 4 : 0);
@@ -315,29 +315,35 @@ int dual_block(const ff_dit& m, const Plan& p, void* ws, int i, const float* c32
   char* Y = at(ws, p.y);
   char* O = at(ws, p.o);
   char* QKV = at(ws, p.qkv);
+  char* qkv_k[2] = {QKV, QKV + p.B * p.Nt * 3 * H * es};
+  char* U[2] = {at(ws, p.u), at(ws, p.u) + p.B * p.Nt * F * es};
   for (int k = 0; k < 2; ++k) {
     FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 6 * H, H, c32, ACT_SILU, st[k]->mod, mods[k]), s));
     FF_TRY(norm_modulate(norm_args(c, rows[k], cur[k], Y + y_off[k] * es, mods[k], mods[k] + H, 6 * H, ntok[k]), s));
-    char* qkv_k = QKV + (k == 0 ? 0 : p.B * p.Nt * 3 * H * es);
-    FF_TRY(gemm(gemm_args(c.dtype, rows[k], 3 * H, H, Y + y_off[k] * es, H, st[k]->qkv, qkv_k, 3 * H, EPI_NONE), s));
-    FF_TRY(qkv_stream(c, p, ws, qkv_k, 3 * H, ntok[k], 0, ntok[k], k == 0 ? 0 : p.Nt, st[k]->qn, st[k]->kn, k == 1, s));
   }
+  FF_TRY(gemm2(gemm_args(c.dtype, rows[0], 3 * H, H, Y + y_off[0] * es, H, st[0]->qkv, qkv_k[0], 3 * H, EPI_NONE),
+               gemm_args(c.dtype, rows[1], 3 * H, H, Y + y_off[1] * es, H, st[1]->qkv, qkv_k[1], 3 * H, EPI_NONE), s));
+  for (int k = 0; k < 2; ++k)
+    FF_TRY(qkv_stream(c, p, ws, qkv_k[k], 3 * H, ntok[k], 0, ntok[k], k == 0 ? 0 : p.Nt, st[k]->qn, st[k]->kn, k == 1, s));
   FF_TRY(attention_joint(c, p, ws, O, O + p.B * p.Nt * H * es, s));
+  GemmArgs go[2], g1[2], g2[2];
   for (int k = 0; k < 2; ++k) {
-    GemmArgs g = gemm_args(c.dtype, rows[k], H, H, O + y_off[k] * es, H, st[k]->o, dst[k], H, EPI_GATED);
-    g.gate = mods[k] + 2 * H; g.gate_ld = 6 * H;
-    g.resid = cur[k]; g.ldr = H;
-    g.rows_per_sample = ntok[k];
-    FF_TRY(gemm(g, s));
-    FF_TRY(norm_modulate(norm_args(c, rows[k], dst[k], Y + y_off[k] * es, mods[k] + 3 * H, mods[k] + 4 * H, 6 * H, ntok[k]), s));
-    char* U = at(ws, p.u);
-    FF_TRY(gemm(gemm_args(c.dtype, rows[k], F, H, Y + y_off[k] * es, H, st[k]->mlp1, U, F, EPI_GELU), s));
-    GemmArgs g2 = gemm_args(c.dtype, rows[k], H, F, U, F, st[k]->mlp2, dst[k], H, EPI_GATED);
-    g2.gate = mods[k] + 5 * H; g2.gate_ld = 6 * H;
-    g2.resid = dst[k]; g2.ldr = H;
-    g2.rows_per_sample = ntok[k];
-    FF_TRY(gemm(g2, s));
+    go[k] = gemm_args(c.dtype, rows[k], H, H, O + y_off[k] * es, H, st[k]->o, dst[k], H, EPI_GATED);
+    go[k].gate = mods[k] + 2 * H; go[k].gate_ld = 6 * H;
+    go[k].resid = cur[k]; go[k].ldr = H;
+    go[k].rows_per_sample = ntok[k];
   }
+  FF_TRY(gemm2(go[0], go[1], s));
+  for (int k = 0; k < 2; ++k) {
+    FF_TRY(norm_modulate(norm_args(c, rows[k], dst[k], Y + y_off[k] * es, mods[k] + 3 * H, mods[k] + 4 * H, 6 * H, ntok[k]), s));
+    g1[k] = gemm_args(c.dtype, rows[k], F, H, Y + y_off[k] * es, H, st[k]->mlp1, U[k], F, EPI_GELU);
+    g2[k] = gemm_args(c.dtype, rows[k], H, F, U[k], F, st[k]->mlp2, dst[k], H, EPI_GATED);
+    g2[k].gate = mods[k] + 5 * H; g2[k].gate_ld = 6 * H;
+    g2[k].resid = dst[k]; g2[k].ldr = H;
+    g2[k].rows_per_sample = ntok[k];
+  }
+  FF_TRY(gemm2(g1[0], g1[1], s));
+  FF_TRY(gemm2(g2[0], g2[1], s));
   return FF_OK;
 }
 

@@ -86,6 +86,8 @@ struct GemmArgs {
   int64_t rows_per_sample;
 };
 int gemm(const GemmArgs& a, hipStream_t s);
+// Two GEMMs with the same epilogue kind, launched together when both are large bf16 problems.
+int gemm2(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s);
 
 // out[b, n] (+)= sum_k W[n, k] * act(in[b, k]) + bias[n]; in/out float32, W of dtype.
 enum Act : int { ACT_NONE = 0, ACT_SILU = 1, ACT_GELU = 2 };

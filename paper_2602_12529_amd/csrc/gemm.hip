@@ -2,24 +2,21 @@
 //
 // bf16: MFMA 32x32x16 (gfx950) tiles, fp32 accumulation.  A [M, K] and W [N, K]
 // are both K-contiguous (nn.Linear layout).  A workgroup computes a BM x BN
-// tile; its waves split it into wave tiles of (BM/WAVES_M) x (BN/WAVES_N),
-// each a grid of 32x32 MFMA blocks.  K advances in slabs of 64 that are
-// staged into LDS with two buffers (the next slab's global loads are in
-// flight while the current slab is multiplied), either through registers or
-// with direct global->LDS loads.  gfx950's LDS serves a 16-byte-per-lane read
-// for 16 lanes per clock across 64 banks (256 bytes): each 128-byte LDS row
-// holds 8 chunks of 16 bytes stored at chunk ^ ((row >> 1) & 7), so the
-// fragment reads of 16 consecutive rows land on 16 distinct bank groups.
-// Tiles are ordered so that consecutive tiles of one XCD (workgroups are
-// dealt round-robin over the 8 XCDs) share A rows in that XCD's L2.
+// tile; its waves split it into wave tiles, each a grid of 32x32 MFMA blocks.
+// Large problems use a 256 x 256 ping-pong kernel fed by direct global->LDS
+// loads (gemm_bf16_pp); small ones a 128 x 128 kernel staged through registers
+// with two LDS buffers (gemm_bf16_kernel).  gfx950's LDS serves a
+// 16-byte-per-lane read for 16 lanes per clock across 64 banks (256 bytes), so
+// LDS rows are stored with their 16-byte chunks permuted by a row-dependent
+// XOR: the fragment reads of 16 consecutive rows land on 16 distinct bank
+// groups.  Tiles are ordered so that consecutive tiles of one XCD (workgroups
+// are dealt round-robin over the 8 XCDs) share A rows in that XCD's L2.
 //
 // Epilogues fuse the bias, GELU-tanh (from a column on, for the fused
 // single-stream projection) and the adaLN-gated residual X + g * (.).
 //
 // f32: a plain LDS-tiled FMA kernel with the same epilogues, for the float32
 // configurations.
-#include <cstdlib>
-
 #include "dev.h"
 #include "ff_internal.h"
 
@@ -61,12 +58,11 @@ __device__ __forceinline__ void epi_store(const GemmParams& p, int64_t m, int64_
 
 // Maps the linear workgroup id to a (tile_m, tile_n) pair: first regroup ids
 // so each XCD owns a contiguous range, then walk GROUP_M tile rows at a time.
-__device__ __forceinline__ void tile_coords(int64_t pid, int64_t num_m, int64_t num_n, int64_t& tm,
-                                            int64_t& tn) {
-  const int64_t total = num_m * num_n;
+__device__ __forceinline__ int64_t xcd_remap(int64_t pid, int64_t total) {
   const int64_t full = total / 8 * 8;
-  int64_t lid = pid;
-  if (pid < full) lid = (pid % 8) * (full / 8) + pid / 8;
+  return pid < full ? (pid % 8) * (full / 8) + pid / 8 : pid;
+}
+__device__ __forceinline__ void group_order(int64_t lid, int64_t num_m, int64_t num_n, int64_t& tm, int64_t& tn) {
   constexpr int64_t GROUP_M = 8;
   const int64_t in_group = GROUP_M * num_n;
   const int64_t gidx = lid / in_group;
@@ -76,6 +72,17 @@ __device__ __forceinline__ void tile_coords(int64_t pid, int64_t num_m, int64_t 
   tm = first_m + r % gsize;
   tn = r / gsize;
 }
+__device__ __forceinline__ void tile_coords(int64_t pid, int64_t num_m, int64_t num_n, int64_t& tm,
+                                            int64_t& tn) {
+  group_order(xcd_remap(pid, num_m * num_n), num_m, num_n, tm, tn);
+}
+
+// Up to two GEMM problems with the same tile kernel in one launch (the text and
+// image streams of a dual-stream block): tiles [0, tiles0) belong to p[0].
+struct GemmBatch {
+  GemmParams p[2];
+  int64_t tiles0, tiles;
+};
 
 constexpr int BK = 64;
 
@@ -149,7 +156,7 @@ __device__ __forceinline__ void epilogue_blocks(const GemmParams& p, const f32x1
 }
 
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI, bool DIRECT, bool SCHED>
+template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_bf16_kernel(GemmParams p) {
   constexpr int THREADS = WAVES_M * WAVES_N * 64;
   constexpr int TM = BM / WAVES_M, TN = BN / WAVES_N;
@@ -167,35 +174,26 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_bf16_kernel(Gem
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
 
-  // Global source pointers of this thread.
-  //  staged (DIRECT = false): row (tid + i*THREADS)/8, 16-byte chunk tid%8, written to LDS by
-  //    the thread at chunk ^ (row & 7);
-  //  direct (DIRECT = true): one wave instruction fills a contiguous 1 KB of LDS (8 rows),
-  //    lane l landing at byte 16 l, i.e. row l/8, stored chunk l%8, so the lane fetches the
-  //    logical chunk (l%8) ^ (row & 7) from global memory.
-  // Rows past the matrix edge are clamped.
-  constexpr int WAVES = WAVES_M * WAVES_N;
-  auto a_row_of = [&](int i) { return DIRECT ? (i * WAVES + wave) * 8 + (lane >> 3) : (tid + i * THREADS) >> 3; };
-  auto b_row_of = a_row_of;
-  const int chunk_st = tid & 7;
+  // Global loads of this thread: row (tid + i*THREADS)/8, 16-byte chunk tid%8, staged
+  // through registers and written to LDS at chunk ^ ((row >> 1) & 7).  Rows past the
+  // matrix edge are clamped.
+  const int chunk = tid & 7;
   const bf16_t* a_src[A_LOADS];
   const bf16_t* b_src[B_LOADS];
-  int a_lds[A_LOADS], b_lds[B_LOADS], a_ck[A_LOADS];
+  int a_lds[A_LOADS], b_lds[B_LOADS];
 #pragma unroll
   for (int i = 0; i < A_LOADS; ++i) {
-    const int row = a_row_of(i);
+    const int row = (tid + i * THREADS) >> 3;
     const int64_t g = m0 + row < p.M ? m0 + row : p.M - 1;
-    a_ck[i] = DIRECT ? ((lane & 7) ^ ((row >> 1) & 7)) : chunk_st;
-    a_src[i] = static_cast<const bf16_t*>(p.A1) + g * p.lda1 + a_ck[i] * 8;
-    a_lds[i] = DIRECT ? (i * WAVES + wave) * 1024 : row * 128 + ((chunk_st ^ ((row >> 1) & 7)) << 4);
+    a_src[i] = static_cast<const bf16_t*>(p.A1) + g * p.lda1 + chunk * 8;
+    a_lds[i] = row * 128 + ((chunk ^ ((row >> 1) & 7)) << 4);
   }
 #pragma unroll
   for (int i = 0; i < B_LOADS; ++i) {
-    const int row = b_row_of(i);
+    const int row = (tid + i * THREADS) >> 3;
     const int64_t g = n0 + row < p.N ? n0 + row : p.N - 1;
-    const int ck = DIRECT ? ((lane & 7) ^ ((row >> 1) & 7)) : chunk_st;
-    b_src[i] = static_cast<const bf16_t*>(p.W) + g * p.ldw + ck * 8;
-    b_lds[i] = BM * BK * 2 + (DIRECT ? (i * WAVES + wave) * 1024 : row * 128 + ((chunk_st ^ ((row >> 1) & 7)) << 4));
+    b_src[i] = static_cast<const bf16_t*>(p.W) + g * p.ldw + chunk * 8;
+    b_lds[i] = BM * BK * 2 + row * 128 + ((chunk ^ ((row >> 1) & 7)) << 4);
   }
 
   f32x16_t acc[FM][FN];
@@ -217,30 +215,21 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_bf16_kernel(Gem
 
   const int64_t KT = p.K / BK;
   const int64_t KT1 = p.K1 / BK;   // slab at which A switches to the second source
-  u32x4_t ra[DIRECT ? 1 : A_LOADS], rb[DIRECT ? 1 : B_LOADS];
+  u32x4_t ra[A_LOADS], rb[B_LOADS];
 
-  // Issue the global loads of the current source pointers into stage `buf`
-  // (direct) or into registers (staged).
-#define FF_GEMM_ISSUE(buf)                                                                          \
-  if constexpr (DIRECT) {                                                                          \
-    _Pragma("unroll") for (int i = 0; i < A_LOADS; ++i)                                            \
-      __builtin_amdgcn_global_load_lds((const glb_t*)a_src[i], (lds_t*)(smem + (buf) * STAGE + a_lds[i]), 16, 0, 0); \
-    _Pragma("unroll") for (int i = 0; i < B_LOADS; ++i)                                            \
-      __builtin_amdgcn_global_load_lds((const glb_t*)b_src[i], (lds_t*)(smem + (buf) * STAGE + b_lds[i]), 16, 0, 0); \
-  } else {                                                                                         \
-    _Pragma("unroll") for (int i = 0; i < A_LOADS; ++i) ra[DIRECT ? 0 : i] = *reinterpret_cast<const u32x4_t*>(a_src[i]); \
-    _Pragma("unroll") for (int i = 0; i < B_LOADS; ++i) rb[DIRECT ? 0 : i] = *reinterpret_cast<const u32x4_t*>(b_src[i]); \
-  }
+  // Issue the global loads of the current source pointers into registers, then
+  // (after the current slab's MFMAs) write them to stage `buf`.
+#define FF_GEMM_ISSUE()                                                                            \
+  _Pragma("unroll") for (int i = 0; i < A_LOADS; ++i) ra[i] = *reinterpret_cast<const u32x4_t*>(a_src[i]); \
+  _Pragma("unroll") for (int i = 0; i < B_LOADS; ++i) rb[i] = *reinterpret_cast<const u32x4_t*>(b_src[i]);
 #define FF_GEMM_COMMIT(buf)                                                                        \
-  if constexpr (DIRECT) {                                                                          \
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");                                               \
-  } else {                                                                                         \
+  {                                                                                                \
     char* D_ = smem + (buf) * STAGE;                                                               \
-    _Pragma("unroll") for (int i = 0; i < A_LOADS; ++i) *reinterpret_cast<u32x4_t*>(D_ + a_lds[i]) = ra[DIRECT ? 0 : i]; \
-    _Pragma("unroll") for (int i = 0; i < B_LOADS; ++i) *reinterpret_cast<u32x4_t*>(D_ + b_lds[i]) = rb[DIRECT ? 0 : i]; \
+    _Pragma("unroll") for (int i = 0; i < A_LOADS; ++i) *reinterpret_cast<u32x4_t*>(D_ + a_lds[i]) = ra[i]; \
+    _Pragma("unroll") for (int i = 0; i < B_LOADS; ++i) *reinterpret_cast<u32x4_t*>(D_ + b_lds[i]) = rb[i]; \
   }
 
-  FF_GEMM_ISSUE(0)
+  FF_GEMM_ISSUE()
   FF_GEMM_COMMIT(0)
   __syncthreads();
 
@@ -252,9 +241,9 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_bf16_kernel(Gem
         // continue K in the second A source
 #pragma unroll
         for (int i = 0; i < A_LOADS; ++i) {
-          const int row = a_row_of(i);
+          const int row = (tid + i * THREADS) >> 3;
           const int64_t g = m0 + row < p.M ? m0 + row : p.M - 1;
-          a_src[i] = static_cast<const bf16_t*>(p.A2) + g * p.lda2 + a_ck[i] * 8;
+          a_src[i] = static_cast<const bf16_t*>(p.A2) + g * p.lda2 + chunk * 8;
         }
       } else {
 #pragma unroll
@@ -262,7 +251,7 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_bf16_kernel(Gem
       }
 #pragma unroll
       for (int i = 0; i < B_LOADS; ++i) b_src[i] += BK;
-      FF_GEMM_ISSUE(buf ^ 1)
+      FF_GEMM_ISSUE()
     }
     const char* S = smem + buf * STAGE;
     // Fragments of k16 step ks + 1 are read while the MFMAs of step ks run.
@@ -286,14 +275,6 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_bf16_kernel(Gem
 #pragma unroll
         for (int j = 0; j < FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
-      if constexpr (SCHED) {
-        // interleave: one MFMA, then one LDS read, while reads remain
-#pragma unroll
-        for (int m = 0; m < FM * FN; ++m) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          if (ks + 1 < BK / 16 && m < FM + FN) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        }
-      }
     }
     if (more) {
       FF_GEMM_COMMIT(buf ^ 1)
@@ -309,140 +290,26 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_bf16_kernel(Gem
                                reinterpret_cast<float*>(smem) + wave * 32 * 36, lane);
 }
 
-// ------------------------------------------------------------------ bf16, multi-stage
-// 256 x 256 tile, 8 waves of 128 x 64, K slabs of 32 in a ring of STAGES LDS
-// buffers filled by direct global->LDS loads issued STAGES-1 slabs ahead, so
-// global latency is covered by several slabs of MFMA work.  A 64-byte LDS row
-// holds 4 chunks of 16 bytes at chunk ^ ((row >> 2) & 3): the fragment reads
-// of 16 consecutive rows then hit 16 distinct bank groups.  Each wave reads all
-// fragments of a slab, then runs its MFMAs at raised priority, so the two
-// waves sharing a SIMD alternate between LDS reads and MFMA.
-template <int EPI, int STAGES>
-__global__ __launch_bounds__(512, 1) void gemm_bf16_ms(GemmParams p) {
-  constexpr int BM = 256, BN = 256, K32 = 32, WAVES = 8, WAVES_N = 4;
-  constexpr int TM = 128, TN = 64, FM = 4, FN = 2;
-  constexpr int A_INS = BM * 64 / 1024 / WAVES;   // 1 KB direct loads per wave per slab (A)
-  constexpr int B_INS = BN * 64 / 1024 / WAVES;
-  constexpr int LPW = A_INS + B_INS;
-  constexpr int STAGE = (BM + BN) * K32 * 2;      // 32 KB
-  extern __shared__ __attribute__((aligned(16))) char smem[];
-
-  const int64_t num_m = (p.M + BM - 1) / BM, num_n = (p.N + BN - 1) / BN;
-  int64_t tm, tn;
-  tile_coords(blockIdx.x, num_m, num_n, tm, tn);
-  const int64_t m0 = tm * BM, n0 = tn * BN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
-
-  // Direct load i of this wave fills rows 16 (i*WAVES + wave) .. +15 of the tile;
-  // lane l lands at row + l/4, stored chunk l%4, so it fetches logical chunk
-  // (l%4) ^ ((row >> 2) & 3) = (l%4) ^ ((l >> 4) & 3).
-  const int ck = (lane & 3) ^ ((lane >> 4) & 3);
-  const bf16_t* a_src[A_INS];
-  const bf16_t* b_src[B_INS];
-  int a_row[A_INS];
-#pragma unroll
-  for (int i = 0; i < A_INS; ++i) {
-    a_row[i] = (i * WAVES + wave) * 16 + (lane >> 2);
-    const int64_t g = m0 + a_row[i] < p.M ? m0 + a_row[i] : p.M - 1;
-    a_src[i] = static_cast<const bf16_t*>(p.A1) + g * p.lda1 + ck * 8;
-  }
-#pragma unroll
-  for (int i = 0; i < B_INS; ++i) {
-    const int row = (i * WAVES + wave) * 16 + (lane >> 2);
-    const int64_t g = n0 + row < p.N ? n0 + row : p.N - 1;
-    b_src[i] = static_cast<const bf16_t*>(p.W) + g * p.ldw + ck * 8;
-  }
-  const int64_t KT = p.K / K32, KT1 = p.K1 / K32;
-
-  auto issue = [&](int64_t slab, int stage) {
-    if (slab == KT1 && slab > 0) {
-#pragma unroll
-      for (int i = 0; i < A_INS; ++i) {
-        const int64_t g = m0 + a_row[i] < p.M ? m0 + a_row[i] : p.M - 1;
-        a_src[i] = static_cast<const bf16_t*>(p.A2) + g * p.lda2 + ck * 8;
-      }
-    }
-    char* base = smem + stage * STAGE;
-#pragma unroll
-    for (int i = 0; i < A_INS; ++i) {
-      __builtin_amdgcn_global_load_lds((const glb_t*)a_src[i], (lds_t*)(base + (i * WAVES + wave) * 1024), 16, 0, 0);
-      a_src[i] += K32;
-    }
-#pragma unroll
-    for (int i = 0; i < B_INS; ++i) {
-      __builtin_amdgcn_global_load_lds((const glb_t*)b_src[i], (lds_t*)(base + BM * 64 + (i * WAVES + wave) * 1024), 16, 0, 0);
-      b_src[i] += K32;
-    }
-  };
-
-  f32x16_t acc[FM][FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-  const int frow = lane & 31, fhalf = lane >> 5;
-  const int key = (frow >> 2) & 3;
-  int a_frag[FM], b_frag[FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i) a_frag[i] = (wm * TM + i * 32 + frow) * 64;
-#pragma unroll
-  for (int j = 0; j < FN; ++j) b_frag[j] = BM * 64 + (wn * TN + j * 32 + frow) * 64;
-
-#pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s)
-    if (s < KT) issue(s, s);
-
-  for (int64_t kt = 0; kt < KT; ++kt) {
-    // slab kt has landed once at most min(STAGES-2, KT-1-kt) younger slabs are in flight
-    const int64_t younger = KT - 1 - kt;
-    if (younger >= STAGES - 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"((STAGES - 2) * LPW) : "memory");
-    else if (younger == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPW) : "memory");
-    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    if (kt + STAGES - 1 < KT) issue(kt + STAGES - 1, static_cast<int>((kt + STAGES - 1) % STAGES));
-    const char* S = smem + (kt % STAGES) * STAGE;
-    bf16x8_t af[2][FM], bfr[2][FN];
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const int coff = ((ks * 2 + fhalf) ^ key) << 4;
-#pragma unroll
-      for (int i = 0; i < FM; ++i) af[ks][i] = *reinterpret_cast<const bf16x8_t*>(S + a_frag[i] + coff);
-#pragma unroll
-      for (int j = 0; j < FN; ++j) bfr[ks][j] = *reinterpret_cast<const bf16x8_t*>(S + b_frag[j] + coff);
-    }
-    __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks][i], bfr[ks][j], acc[i][j], 0, 0, 0);
-    __builtin_amdgcn_s_setprio(0);
-  }
-
-  __syncthreads();
-  epilogue_blocks<EPI, FM, FN>(p, acc, m0 + wm * TM, n0 + wn * TN,
-                               reinterpret_cast<float*>(smem) + wave * 32 * 36, lane);
-}
-
 // ------------------------------------------------------------------ bf16, ping-pong
-// Same tile, LDS ring and loads as gemm_bf16_ms, scheduled as two groups of
-// four waves (one wave of each group per SIMD) offset by one barrier: while
-// one group runs its MFMA cluster on slab k, the other reads slab k's
-// fragments from LDS and issues the direct loads of slab k + STAGES - 1.
-// Every phase ends with a workgroup barrier, so on each SIMD the matrix core
-// is fed by one wave while the other wave's memory work is hidden.
+// 256 x 256 tile, 8 waves of 128 x 64, K slabs of 32 in a ring of STAGES LDS
+// buffers filled by direct global->LDS loads issued STAGES - 1 slabs ahead.  A
+// 64-byte LDS row holds 4 chunks of 16 bytes at chunk ^ ((row >> 2) & 3): the
+// fragment reads of 16 consecutive rows then hit 16 distinct bank groups.  The
+// waves form two groups of four (one wave of each group per SIMD) offset by
+// one barrier: while one group runs its MFMA cluster on slab k, the other
+// reads slab k's fragments from LDS and issues the direct loads of a later
+// slab.  Every phase ends with a workgroup barrier, so on each SIMD the matrix
+// core is fed by one wave while the other wave's memory work is hidden.
 template <int STAGES, int LPW>
 __device__ __forceinline__ void wait_slab_after(int64_t n_after) {
   // at most n_after younger slabs (LPW loads each) may still be in flight
-  if (n_after >= STAGES - 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"((STAGES - 2) * LPW) : "memory");
-  else if (n_after == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPW) : "memory");
-  else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  if constexpr (STAGES <= 2) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  } else {
+    if (n_after >= STAGES - 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"((STAGES - 2) * LPW) : "memory");
+    else if (n_after == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPW) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
 }
 
 // Workgroup barrier that no instruction (memory or not) is scheduled across.
@@ -453,59 +320,73 @@ __device__ __forceinline__ void wg_barrier() {
 }
 
 template <int EPI, int STAGES>
-__global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmParams p) {
-  constexpr int BM = 256, BN = 256, K32 = 32, WAVES = 8, WAVES_N = 4;
+__global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
+  constexpr int BM = 256, BN = 256, WAVES = 8, WAVES_N = 4;
   constexpr int TM = 128, TN = 64, FM = 4, FN = 2;
-  constexpr int A_INS = BM * 64 / 1024 / WAVES;
-  constexpr int B_INS = BN * 64 / 1024 / WAVES;
+  constexpr int KS = 32;                           // slab width (k)
+  constexpr int ROWB = KS * 2;                     // bytes per LDS row
+  constexpr int CPR = ROWB / 16;                   // 16-byte chunks per row
+  constexpr int RPI = 1024 / ROWB;                 // rows per 1 KB direct load
+  constexpr int A_INS = BM / RPI / WAVES;
+  constexpr int B_INS = BN / RPI / WAVES;
   constexpr int LPW = A_INS + B_INS;
-  constexpr int STAGE = (BM + BN) * K32 * 2;
+  constexpr int STAGE = (BM + BN) * ROWB;
+  constexpr int KSTEPS = KS / 16;
   extern __shared__ __attribute__((aligned(16))) char smem[];
 
+  const int64_t lid = xcd_remap(blockIdx.x, batch.tiles);
+  const int which = lid >= batch.tiles0 ? 1 : 0;
+  const GemmParams& p = batch.p[which];
   const int64_t num_m = (p.M + BM - 1) / BM, num_n = (p.N + BN - 1) / BN;
   int64_t tm, tn;
-  tile_coords(blockIdx.x, num_m, num_n, tm, tn);
+  group_order(lid - (which ? batch.tiles0 : 0), num_m, num_n, tm, tn);
   const int64_t m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
   const int grp = wave >> 2;
 
-  const int ck = (lane & 3) ^ ((lane >> 4) & 3);
+  // Swizzle of a row's chunks: 16 consecutive rows read by 16 lanes land on 16 bank groups.
+  auto swz = [](int row) { return (row >> 2) & 3; };
+  // Direct load i of this wave fills RPI rows starting at RPI (i*WAVES + wave); lane l lands
+  // at row + l/CPR, stored chunk l%CPR, so it fetches logical chunk (l%CPR) ^ swz(row).
   const bf16_t* a_src[A_INS];
   const bf16_t* b_src[B_INS];
-  int a_row[A_INS];
+  int a_row[A_INS], a_ck[A_INS];
 #pragma unroll
   for (int i = 0; i < A_INS; ++i) {
-    a_row[i] = (i * WAVES + wave) * 16 + (lane >> 2);
+    a_row[i] = (i * WAVES + wave) * RPI + lane / CPR;
+    a_ck[i] = (lane % CPR) ^ swz(a_row[i]);
     const int64_t g = m0 + a_row[i] < p.M ? m0 + a_row[i] : p.M - 1;
-    a_src[i] = static_cast<const bf16_t*>(p.A1) + g * p.lda1 + ck * 8;
+    a_src[i] = static_cast<const bf16_t*>(p.A1) + g * p.lda1 + a_ck[i] * 8;
   }
 #pragma unroll
   for (int i = 0; i < B_INS; ++i) {
-    const int row = (i * WAVES + wave) * 16 + (lane >> 2);
+    const int row = (i * WAVES + wave) * RPI + lane / CPR;
+    const int ck = (lane % CPR) ^ swz(row);
     const int64_t g = n0 + row < p.N ? n0 + row : p.N - 1;
     b_src[i] = static_cast<const bf16_t*>(p.W) + g * p.ldw + ck * 8;
   }
-  const int64_t KT = p.K / K32, KT1 = p.K1 / K32;
+  const int64_t KT = p.K / KS, KT1 = p.K1 / KS;
 
-  auto issue = [&](int64_t slab, int stage) {
+  auto issue = [&](int64_t slab) {
+    if (slab >= KT) return;
     if (slab == KT1 && slab > 0) {
 #pragma unroll
       for (int i = 0; i < A_INS; ++i) {
         const int64_t g = m0 + a_row[i] < p.M ? m0 + a_row[i] : p.M - 1;
-        a_src[i] = static_cast<const bf16_t*>(p.A2) + g * p.lda2 + ck * 8;
+        a_src[i] = static_cast<const bf16_t*>(p.A2) + g * p.lda2 + a_ck[i] * 8;
       }
     }
-    char* base = smem + stage * STAGE;
+    char* base = smem + static_cast<int>(slab % STAGES) * STAGE;
 #pragma unroll
     for (int i = 0; i < A_INS; ++i) {
       __builtin_amdgcn_global_load_lds((const glb_t*)a_src[i], (lds_t*)(base + (i * WAVES + wave) * 1024), 16, 0, 0);
-      a_src[i] += K32;
+      a_src[i] += KS;
     }
 #pragma unroll
     for (int i = 0; i < B_INS; ++i) {
-      __builtin_amdgcn_global_load_lds((const glb_t*)b_src[i], (lds_t*)(base + BM * 64 + (i * WAVES + wave) * 1024), 16, 0, 0);
-      b_src[i] += K32;
+      __builtin_amdgcn_global_load_lds((const glb_t*)b_src[i], (lds_t*)(base + BM * ROWB + (i * WAVES + wave) * 1024), 16, 0, 0);
+      b_src[i] += KS;
     }
   };
 
@@ -518,45 +399,54 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmParams p) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int frow = lane & 31, fhalf = lane >> 5;
-  const int key = (frow >> 2) & 3;
+  const int key = swz(frow);   // the same for every fragment row of this lane
   int a_frag[FM], b_frag[FN];
 #pragma unroll
-  for (int i = 0; i < FM; ++i) a_frag[i] = (wm * TM + i * 32 + frow) * 64;
+  for (int i = 0; i < FM; ++i) a_frag[i] = (wm * TM + i * 32 + frow) * ROWB;
 #pragma unroll
-  for (int j = 0; j < FN; ++j) b_frag[j] = BM * 64 + (wn * TN + j * 32 + frow) * 64;
+  for (int j = 0; j < FN; ++j) b_frag[j] = BM * ROWB + (wn * TN + j * 32 + frow) * ROWB;
 
+  // Phases: group 0 runs M(k) C(k) M(k+1) ..., group 1 one barrier behind, so at any
+  // time one group multiplies while the other reads LDS.  Slab k + STAGES - 1 is
+  // issued in the first phase after slab k - 1's last read (group 0: its M(k); group 1:
+  // its C(k - 1)), and slab k + 1 must have landed before the phase of group 0's M(k + 1).
 #pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s)
-    if (s < KT) issue(s, s);
+  for (int st = 0; st < STAGES - 1; ++st) issue(st);
   wait_slab_after<STAGES, LPW>(KT - 1 < STAGES - 2 ? KT - 1 : STAGES - 2);
   wg_barrier();
-  if (grp == 1) wg_barrier();
+  if (grp == 1) {
+    issue(STAGES - 1);
+    wg_barrier();
+  }
 
   for (int64_t kt = 0; kt < KT; ++kt) {
-    // memory phase: fragments of slab kt, loads of slab kt + STAGES - 1
-    const char* S = smem + (kt % STAGES) * STAGE;
-    bf16x8_t af[2][FM], bfr[2][FN];
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
+    if (grp == 0) issue(kt + STAGES - 1);
+    const char* S = smem + static_cast<int>(kt % STAGES) * STAGE;
+    // The memory phase reads all fragments of the slab: the other group may overwrite
+    // this stage once the phase's closing barrier has passed.
+    bf16x8_t af[KSTEPS][FM], bfr[KSTEPS][FN];
+    auto read_step = [&](int ks) {
       const int coff = ((ks * 2 + fhalf) ^ key) << 4;
 #pragma unroll
       for (int i = 0; i < FM; ++i) af[ks][i] = *reinterpret_cast<const bf16x8_t*>(S + a_frag[i] + coff);
 #pragma unroll
       for (int j = 0; j < FN; ++j) bfr[ks][j] = *reinterpret_cast<const bf16x8_t*>(S + b_frag[j] + coff);
-    }
-    if (kt + STAGES - 1 < KT) issue(kt + STAGES - 1, static_cast<int>((kt + STAGES - 1) % STAGES));
+    };
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) read_step(ks);
     const int64_t n_after = KT - 2 - kt;   // slabs younger than kt + 1 that may stay in flight
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     if (grp == 1 && n_after >= 0) wait_slab_after<STAGES, LPW>(n_after);
     wg_barrier();
-    // compute phase
+    if (grp == 1) issue(kt + STAGES);
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
+    for (int ks = 0; ks < KSTEPS; ++ks) {
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks][i], bfr[ks][j], acc[i][j], 0, 0, 0);
+    }
     if (grp == 0 && n_after >= 0) wait_slab_after<STAGES, LPW>(n_after);
     wg_barrier();
   }
@@ -616,52 +506,25 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
     }
 }
 
-template <int BM, int BN, int WM, int WN, int EPI, bool DIRECT, bool SCHED = false>
+template <int BM, int BN, int WM, int WN, int EPI>
 int launch_bf16(const GemmParams& p, hipStream_t s, const char* name, double flops, double bytes) {
   constexpr int smem = 2 * (BM + BN) * BK * 2;
   static bool attr_set = false;
   if (!attr_set) {
-    FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<BM, BN, WM, WN, EPI, DIRECT, SCHED>),
+    FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<BM, BN, WM, WN, EPI>),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, smem),
                  "gemm smem attribute");
     attr_set = true;
   }
   const int64_t tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
   LaunchScope ls(name, s, flops, bytes);
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, EPI, DIRECT, SCHED>), dim3(static_cast<unsigned>(tiles)),
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, EPI>), dim3(static_cast<unsigned>(tiles)),
                      dim3(WM * WN * 64), smem, s, p);
   return ls.status();
 }
 
-// Tile configurations (BM x BN, waves; LDS fill): 0 = 256x256, 8 waves of 128x64, staged
-// through registers; 1 = same with direct global->LDS loads; 2 = 256x256, 4 waves of
-// 128x128, direct; 3 = 128x128, 4 waves of 64x64, staged.  FF_GEMM_TILE overrides the choice.
-int pick_tile(const GemmParams& p) {
-  static const char* env = getenv("FF_GEMM_TILE");
-  if (env && env[0] >= '0' && env[0] <= '7') return env[0] - '0';
-  const int64_t tiles256 = ((p.M + 255) / 256) * ((p.N + 255) / 256);
-  if (tiles256 >= 256) return 7;   // at least one 256 x 256 tile per CU
-  return 3;
-}
-
 template <int EPI, int STAGES>
-int launch_ms(const GemmParams& p, hipStream_t s, const char* name, double flops, double bytes) {
-  constexpr int smem = STAGES * 512 * 32 * 2;
-  static bool attr_set = false;
-  if (!attr_set) {
-    FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_ms<EPI, STAGES>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, smem),
-                 "gemm smem attribute");
-    attr_set = true;
-  }
-  const int64_t tiles = ((p.M + 255) / 256) * ((p.N + 255) / 256);
-  LaunchScope ls(name, s, flops, bytes);
-  hipLaunchKernelGGL((gemm_bf16_ms<EPI, STAGES>), dim3(static_cast<unsigned>(tiles)), dim3(512), smem, s, p);
-  return ls.status();
-}
-
-template <int EPI, int STAGES>
-int launch_pp(const GemmParams& p, hipStream_t s, const char* name, double flops, double bytes) {
+int launch_pp_batch(const GemmBatch& b, hipStream_t s, const char* name, double flops, double bytes) {
   constexpr int smem = STAGES * 512 * 32 * 2;
   static bool attr_set = false;
   if (!attr_set) {
@@ -670,25 +533,30 @@ int launch_pp(const GemmParams& p, hipStream_t s, const char* name, double flops
                  "gemm smem attribute");
     attr_set = true;
   }
-  const int64_t tiles = ((p.M + 255) / 256) * ((p.N + 255) / 256);
   LaunchScope ls(name, s, flops, bytes);
-  hipLaunchKernelGGL((gemm_bf16_pp<EPI, STAGES>), dim3(static_cast<unsigned>(tiles)), dim3(512), smem, s, p);
+  hipLaunchKernelGGL((gemm_bf16_pp<EPI, STAGES>), dim3(static_cast<unsigned>(b.tiles)), dim3(512), smem, s, b);
   return ls.status();
 }
 
+int64_t tiles256(const GemmParams& p) { return ((p.M + 255) / 256) * ((p.N + 255) / 256); }
+
+template <int EPI, int STAGES>
+int launch_pp(const GemmParams& p, hipStream_t s, const char* name, double flops, double bytes) {
+  GemmBatch b{};
+  b.p[0] = p;
+  b.p[1] = p;
+  b.tiles0 = tiles256(p);
+  b.tiles = b.tiles0;
+  return launch_pp_batch<EPI, STAGES>(b, s, name, flops, bytes);
+}
+
+// Problems with at least one 256 x 256 tile per CU take the ping-pong kernel with
+// a three-slab ring; smaller ones the 128 x 128 tile, which fills more CUs.
 template <int EPI>
 int dispatch_bf16(const GemmParams& p, hipStream_t s, double flops, double bytes) {
   static const char* names[3] = {"gemm_bf16", "gemm_bf16_gelu", "gemm_bf16_gated"};
-  switch (pick_tile(p)) {
-    case 1: return launch_bf16<256, 256, 2, 4, EPI, true>(p, s, names[EPI], flops, bytes);
-    case 2: return launch_bf16<256, 256, 2, 4, EPI, true, true>(p, s, names[EPI], flops, bytes);
-    case 3: return launch_bf16<128, 128, 2, 2, EPI, false>(p, s, names[EPI], flops, bytes);
-    case 4: return launch_ms<EPI, 4>(p, s, names[EPI], flops, bytes);
-    case 5: return launch_ms<EPI, 3>(p, s, names[EPI], flops, bytes);
-    case 6: return launch_pp<EPI, 4>(p, s, names[EPI], flops, bytes);
-    case 7: return launch_pp<EPI, 3>(p, s, names[EPI], flops, bytes);
-    default: return launch_bf16<256, 256, 2, 4, EPI, false>(p, s, names[EPI], flops, bytes);
-  }
+  if (tiles256(p) >= 256) return launch_pp<EPI, 3>(p, s, names[EPI], flops, bytes);
+  return launch_bf16<128, 128, 2, 2, EPI>(p, s, names[EPI], flops, bytes);
 }
 
 template <int EPI>
@@ -702,17 +570,27 @@ int dispatch_f32(const GemmParams& p, hipStream_t s, double flops, double bytes)
 
 }  // namespace
 
-int gemm(const GemmArgs& a, hipStream_t s) {
-  if (a.M == 0 || a.N == 0) return FF_OK;
+namespace {
+GemmParams make_params(const GemmArgs& a) {
   GemmParams p{a.M, a.N, a.K, a.A1, a.lda1, a.K1, a.A2 ? a.A2 : a.A1, a.A2 ? a.lda2 : a.lda1,
                a.W, a.ldw, a.bias, a.out, a.ldo, a.gelu_from, a.gate, a.gate_ld, a.resid, a.ldr,
                a.rows_per_sample > 0 ? a.rows_per_sample : a.M, 0};
   p.vec_ok = a.ldo % 8 == 0 && aligned16(a.out) && (!a.bias || aligned16(a.bias)) &&
              (a.epi != EPI_GATED || (a.ldr % 8 == 0 && aligned16(a.resid) && (!a.gate || (a.gate_ld % 4 == 0 && aligned16(a.gate)))));
+  return p;
+}
+double gemm_flops(const GemmArgs& a) { return 2.0 * a.M * a.N * a.K; }
+double gemm_bytes(const GemmArgs& a) {
   const double esz = static_cast<double>(dtype_size(a.dtype));
-  const double flops = 2.0 * a.M * a.N * a.K;
-  const double bytes = esz * (static_cast<double>(a.M) * a.K + static_cast<double>(a.N) * a.K +
-                              static_cast<double>(a.M) * a.N * (a.epi == EPI_GATED ? 2.0 : 1.0));
+  return esz * (static_cast<double>(a.M) * a.K + static_cast<double>(a.N) * a.K +
+                static_cast<double>(a.M) * a.N * (a.epi == EPI_GATED ? 2.0 : 1.0));
+}
+}  // namespace
+
+int gemm(const GemmArgs& a, hipStream_t s) {
+  if (a.M == 0 || a.N == 0) return FF_OK;
+  GemmParams p = make_params(a);
+  const double flops = gemm_flops(a), bytes = gemm_bytes(a);
   if (a.dtype == FF_BF16) {
     if (a.K % BK != 0 || a.K1 % BK != 0)
       return fail(FF_EUNSUPPORTED, "gemm: bf16 K=%lld (K1=%lld) must be a multiple of %d", (long long)a.K,
@@ -727,6 +605,32 @@ int gemm(const GemmArgs& a, hipStream_t s) {
     case EPI_NONE: return dispatch_f32<EPI_NONE>(p, s, flops, bytes);
     case EPI_GELU: return dispatch_f32<EPI_GELU>(p, s, flops, bytes);
     default: return dispatch_f32<EPI_GATED>(p, s, flops, bytes);
+  }
+}
+
+int gemm2(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
+  const bool grouped = a0.dtype == FF_BF16 && a1.dtype == FF_BF16 && a0.epi == a1.epi && a0.M > 0 && a1.M > 0 &&
+                       a0.N > 0 && a1.N > 0 && a0.K % BK == 0 && a1.K % BK == 0 && a0.K1 % BK == 0 &&
+                       a1.K1 % BK == 0;
+  if (!grouped) {
+    FF_TRY(gemm(a0, s));
+    return gemm(a1, s);
+  }
+  GemmBatch b{};
+  b.p[0] = make_params(a0);
+  b.p[1] = make_params(a1);
+  b.tiles0 = tiles256(b.p[0]);
+  b.tiles = b.tiles0 + tiles256(b.p[1]);
+  if (b.tiles < 256) {
+    FF_TRY(gemm(a0, s));
+    return gemm(a1, s);
+  }
+  const double flops = gemm_flops(a0) + gemm_flops(a1), bytes = gemm_bytes(a0) + gemm_bytes(a1);
+  static const char* names[3] = {"gemm_bf16", "gemm_bf16_gelu", "gemm_bf16_gated"};
+  switch (a0.epi) {
+    case EPI_NONE: return launch_pp_batch<EPI_NONE, 3>(b, s, names[0], flops, bytes);
+    case EPI_GELU: return launch_pp_batch<EPI_GELU, 3>(b, s, names[1], flops, bytes);
+    default: return launch_pp_batch<EPI_GATED, 3>(b, s, names[2], flops, bytes);
   }
 }
 

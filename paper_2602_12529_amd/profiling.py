@@ -1,0 +1,225 @@
+"""rocprofv3 summaries for the rollout's kernels, and the HBM traffic lookup of bench.py.
+
+Subcommands (python -m paper_2602_12529_amd.profiling ...):
+
+  copy --bytes N --reps R
+      A plain device-to-device copy of N bytes, R times: the calibration kernel
+      whose FETCH_SIZE / WRITE_SIZE counters are compared with the known N.
+  stats CSV OUT --title T --cmd C
+      kernel_stats.csv of `rocprofv3 --kernel-trace --stats` -> markdown table.
+  traffic --fetch CSV --write CSV --copy-fetch CSV --copy-write CSV --copy-bytes N
+          --key NAME=PATTERN OUT --title T --cmd C [--cmd C ...]
+      counter_collection.csv files of four `rocprofv3 --pmc` runs (FETCH_SIZE,
+      then WRITE_SIZE, over the workload and over the copy) -> per-kernel HBM
+      bytes per launch.  Each counter is scaled by N / (its value for the copy),
+      so the numbers are in the copy's units: bytes that crossed the HBM
+      interface.  NAME is the library's profiler name of the kernel the bench
+      reports (gemm_bf16_gated, attn_bf16, ...), PATTERN a substring of
+      rocprofv3's kernel name; the summary stores NAME's traffic per launch
+      with the hash of the sources the kernel is built from, and bench.py
+      reports it only while that hash still matches.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import hashlib
+import json
+import os
+import re
+import sys
+from collections import defaultdict
+from typing import Dict, List, Optional
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2602_12529_amd", "csrc")
+PROFILES = os.path.join(ROOT, "profiles")
+
+# Source files each kernel family is compiled from (beside the shared headers).
+_FAMILY_SOURCES = {
+    "gemm": ["gemm.hip"],
+    "attn": ["attention.hip"],
+    "sde": ["sde.hip"],
+    "logp": ["sde.hip"],
+    "group_adv": ["sde.hip"],
+}
+_SHARED = ["dev.h", "ff_internal.h"]
+
+
+def sources_of(kernel: str) -> List[str]:
+    fam = next((v for k, v in _FAMILY_SOURCES.items() if kernel.startswith(k)), ["ops.hip", "dit.hip"])
+    return [os.path.join(CSRC, f) for f in fam + _SHARED]
+
+
+def sources_sha256(kernel: str) -> str:
+    h = hashlib.sha256()
+    for path in sources_of(kernel):
+        with open(path, "rb") as f:
+            h.update(os.path.basename(path).encode() + b"\0" + f.read())
+    return h.hexdigest()
+
+
+def short_name(name: str) -> str:
+    s = name.replace("void ", "").replace("ff::(anonymous namespace)::", "")
+    s = s.replace("(anonymous namespace)::", "")
+    depth, out = 0, []
+    for ch in s:                     # drop the argument list
+        if ch == "(" and depth == 0:
+            break
+        depth += ch == "<"
+        depth -= ch == ">"
+        out.append(ch)
+    s = "".join(out)
+    return s if len(s) <= 70 else s[:67] + "..."
+
+
+# ---------------------------------------------------------------------------- copy calibration
+def run_copy(nbytes: int, reps: int) -> None:
+    import torch
+
+    if not torch.cuda.is_available():
+        raise SystemExit("copy calibration needs a GPU")
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    src.random_(0, 255)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": nbytes, "reps": reps}), flush=True)
+
+
+# ---------------------------------------------------------------------------- summaries
+def _header(title: str, cmds: List[str]) -> List[str]:
+    out = [f"# {title}", "", "Commands (run from the repository root on one MI355X):", "", "```"]
+    out += cmds
+    out += ["```", ""]
+    return out
+
+
+def stats_md(csv_path: str, out_md: str, title: str, cmds: List[str]) -> None:
+    rows = list(csv.DictReader(open(csv_path)))
+    out = _header(title, cmds)
+    out += ["rocprofv3 kernel statistics (all launches of the run, warmup included):", "",
+            "| kernel | calls | total ms | avg us | min us | max us | % |", "|---|---|---|---|---|---|---|"]
+    for r in rows:
+        out.append(f"| `{short_name(r['Name'])}` | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.3f} | "
+                   f"{float(r['AverageNs']) / 1e3:.1f} | {float(r['MinNs']) / 1e3:.1f} | "
+                   f"{float(r['MaxNs']) / 1e3:.1f} | {float(r['Percentage']):.2f} |")
+    with open(out_md, "w") as f:
+        f.write("\n".join(out) + "\n")
+
+
+def _counter_per_kernel(path: str, counter: str) -> Dict[str, List[float]]:
+    """Kernel name -> per-dispatch values (KiB) of `counter`, summed over a dispatch's rows."""
+    per_dispatch: Dict[tuple, float] = defaultdict(float)
+    for r in csv.DictReader(open(path)):
+        if r["Counter_Name"] != counter:
+            continue
+        per_dispatch[(r["Kernel_Name"], int(r["Dispatch_Id"]))] += float(r["Counter_Value"])
+    out: Dict[str, List[float]] = defaultdict(list)
+    for (name, _), v in sorted(per_dispatch.items(), key=lambda kv: kv[0][1]):
+        out[name].append(v)
+    return out
+
+
+def _copy_factor(path: str, counter: str, nbytes: int) -> float:
+    """Bytes per counter unit: nbytes / the median counter of the copy kernel's dispatches."""
+    vals = sorted(v for name, vs in _counter_per_kernel(path, counter).items() if "copy" in name.lower() for v in vs)
+    if not vals:
+        raise SystemExit(f"{path}: no {counter} values of a copy kernel")
+    return nbytes / vals[len(vals) // 2]
+
+
+def traffic_md(fetch_csv: str, write_csv: str, copy_fetch_csv: str, copy_write_csv: str, copy_bytes: int,
+               keys: Dict[str, str], out_md: str, title: str, cmds: List[str]) -> dict:
+    ff_ = _copy_factor(copy_fetch_csv, "FETCH_SIZE", copy_bytes)
+    fw_ = _copy_factor(copy_write_csv, "WRITE_SIZE", copy_bytes)
+    fetch = _counter_per_kernel(fetch_csv, "FETCH_SIZE")
+    write = _counter_per_kernel(write_csv, "WRITE_SIZE")
+    out = _header(title, cmds)
+    out += [f"Copy calibration: a {copy_bytes} B device copy reads FETCH_SIZE = {copy_bytes / ff_ / 1024:.1f} KiB "
+            f"and WRITE_SIZE = {copy_bytes / fw_ / 1024:.1f} KiB, so one counter KiB is {ff_:.1f} B fetched and "
+            f"{fw_:.1f} B written.", "",
+            "Per kernel, averaged over its launches (warmup included), scaled by those factors:", "",
+            "| kernel | launches | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM read MB | HBM write MB | total MB / launch |",
+            "|---|---|---|---|---|---|---|"]
+    rows = []
+    for name in sorted(set(fetch) | set(write), key=lambda n: -sum(fetch.get(n, [0.0]))):
+        fv, wv = fetch.get(name, []), write.get(name, [])
+        if not fv or not wv:
+            continue
+        af, aw = sum(fv) / len(fv), sum(wv) / len(wv)
+        rb, wb = af * ff_, aw * fw_
+        rows.append((name, len(fv), af, aw, rb, wb))
+        out.append(f"| `{short_name(name)}` | {len(fv)} | {af:.0f} | {aw:.0f} | {rb / 1e6:.1f} | {wb / 1e6:.1f} | "
+                   f"{(rb + wb) / 1e6:.1f} |")
+    records = []
+    for lib_name, pattern in keys.items():
+        match = [r for r in rows if pattern in r[0]]
+        if len(match) != 1:
+            raise SystemExit(f"pattern {pattern!r} matches {len(match)} kernels")
+        name, n, af, aw, rb, wb = match[0]
+        records.append({"kernel": lib_name, "rocprof_kernel": short_name(name), "launches": n,
+                        "fetch_bytes_per_launch": rb, "write_bytes_per_launch": wb,
+                        "traffic_bytes_per_launch": rb + wb, "copy_factor_fetch": ff_, "copy_factor_write": fw_,
+                        "sources_sha256": sources_sha256(lib_name)})
+    out += ["", "Traffic records read by bench.py (valid while the kernel's sources hash the same):", "",
+            "```json", json.dumps(records, indent=1), "```"]
+    with open(out_md, "w") as f:
+        f.write("\n".join(out) + "\n")
+    return {"records": records}
+
+
+def lookup_traffic(kernel: str) -> Optional[dict]:
+    """The committed traffic record of `kernel` whose sources still hash the same, else None."""
+    if not os.path.isdir(PROFILES):
+        return None
+    want = sources_sha256(kernel)
+    for fn in sorted(os.listdir(PROFILES)):
+        if not fn.endswith(".md"):
+            continue
+        text = open(os.path.join(PROFILES, fn)).read()
+        for block in re.findall(r"```json\n(.*?)```", text, flags=re.S):
+            try:
+                recs = json.loads(block)
+            except ValueError:
+                continue
+            for r in recs if isinstance(recs, list) else []:
+                if r.get("kernel") == kernel and r.get("sources_sha256") == want:
+                    return dict(r, summary=os.path.join("profiles", fn))
+    return None
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(prog="python -m paper_2602_12529_amd.profiling")
+    sub = ap.add_subparsers(dest="action", required=True)
+    c = sub.add_parser("copy")
+    c.add_argument("--bytes", type=int, default=1 << 30)
+    c.add_argument("--reps", type=int, default=4)
+    s = sub.add_parser("stats")
+    s.add_argument("csv")
+    s.add_argument("out")
+    s.add_argument("--title", required=True)
+    s.add_argument("--cmd", action="append", required=True)
+    t = sub.add_parser("traffic")
+    for k in ("fetch", "write", "copy_fetch", "copy_write"):
+        t.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
+    t.add_argument("--copy-bytes", type=int, required=True)
+    t.add_argument("--key", action="append", default=[], help="NAME=PATTERN")
+    t.add_argument("out")
+    t.add_argument("--title", required=True)
+    t.add_argument("--cmd", action="append", required=True)
+    a = ap.parse_args(argv)
+    if a.action == "copy":
+        run_copy(a.bytes, a.reps)
+    elif a.action == "stats":
+        stats_md(a.csv, a.out, a.title, a.cmd)
+    else:
+        keys = dict(kv.split("=", 1) for kv in a.key)
+        traffic_md(a.fetch, a.write, a.copy_fetch, a.copy_write, a.copy_bytes, keys, a.out, a.title, a.cmd)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
