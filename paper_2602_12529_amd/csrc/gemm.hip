@@ -3,9 +3,9 @@
 // bf16: MFMA 32x32x16 (gfx950) tiles, fp32 accumulation.  A [M, K] and W [N, K]
 // are both K-contiguous (nn.Linear layout).  A workgroup computes a BM x BN
 // tile; its waves split it into wave tiles, each a grid of 32x32 MFMA blocks.
-// Large problems use a 256 x 256 ping-pong kernel fed by direct global->LDS
-// loads (gemm_bf16_pp); small ones a 128 x 128 kernel staged through registers
-// with two LDS buffers (gemm_bf16_kernel).  gfx950's LDS serves a
+// Large problems use a 256 x 256 tile with one wave per SIMD fed by direct
+// global->LDS loads of 64-wide K slabs (gemm_bf16_256); small ones a 128 x 128
+// tile staged through registers with two LDS buffers (gemm_bf16_kernel).  gfx950's LDS serves a
 // 16-byte-per-lane read for 16 lanes per clock across 64 banks (256 bytes), so
 // LDS rows are stored with their 16-byte chunks permuted by a row-dependent
 // XOR: the fragment reads of 16 consecutive rows land on 16 distinct bank
@@ -91,68 +91,77 @@ constexpr int BK = 64;
 // LDS is free) and comes back row-major: lane l owns row l/2, 16 consecutive
 // columns, so bias, gate and residual are read and the output written with
 // 16-byte vector accesses, one sample-index division per row.
-template <int EPI, int FM, int FN>
-__device__ __forceinline__ void epilogue_blocks(const GemmParams& p, const f32x16_t (&acc)[FM][FN], int64_t mw,
-                                                int64_t nw, float* scratch, int lane) {
+template <int EPI>
+__device__ __forceinline__ void epilogue_block(const GemmParams& p, const f32x16_t& a, int64_t mb, int64_t nb,
+                                               float* scratch, int lane) {
   const int frow = lane & 31, fhalf = lane >> 5;
   const int rr = lane >> 1, cc = (lane & 1) * 16;
   const bf16_t* bias = static_cast<const bf16_t*>(p.bias);
   bf16_t* out = static_cast<bf16_t*>(p.out);
 #pragma unroll
-  for (int i = 0; i < FM; ++i)
+  for (int r = 0; r < 16; ++r) scratch[(8 * (r >> 2) + 4 * fhalf + (r & 3)) * 36 + frow] = a[r];
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  float v[16];
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
+  for (int q = 0; q < 4; ++q) {
+    const float4 t = *reinterpret_cast<const float4*>(scratch + rr * 36 + cc + 4 * q);
+    v[4 * q] = t.x; v[4 * q + 1] = t.y; v[4 * q + 2] = t.z; v[4 * q + 3] = t.w;
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  const int64_t m = mb + rr;
+  const int64_t n = nb + cc;
+  if (m >= p.M || n >= p.N) return;
+  if (p.vec_ok && n + 16 <= p.N) {
+    if (bias) {
+      float b[16];
+      ld8<true>(bias, n, *reinterpret_cast<float(*)[8]>(b));
+      ld8<true>(bias, n + 8, *reinterpret_cast<float(*)[8]>(b + 8));
 #pragma unroll
-      for (int r = 0; r < 16; ++r) scratch[(8 * (r >> 2) + 4 * fhalf + (r & 3)) * 36 + frow] = acc[i][j][r];
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      float v[16];
+      for (int e = 0; e < 16; ++e) v[e] += b[e];
+    }
+    if constexpr (EPI == EPI_GELU) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float4 t = *reinterpret_cast<const float4*>(scratch + rr * 36 + cc + 4 * q);
-        v[4 * q] = t.x; v[4 * q + 1] = t.y; v[4 * q + 2] = t.z; v[4 * q + 3] = t.w;
-      }
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      const int64_t m = mw + i * 32 + rr;
-      const int64_t n = nw + j * 32 + cc;
-      if (m >= p.M || n >= p.N) continue;
-      if (p.vec_ok && n + 16 <= p.N) {
-        if (bias) {
-          float b[16];
-          ld8<true>(bias, n, *reinterpret_cast<float(*)[8]>(b));
-          ld8<true>(bias, n + 8, *reinterpret_cast<float(*)[8]>(b + 8));
+      for (int e = 0; e < 16; ++e)
+        if (n + e >= p.gelu_from) v[e] = gelu_tanh_f(v[e]);
+    } else if constexpr (EPI == EPI_GATED) {
+      float rs[16];
+      ld8<true>(p.resid, m * p.ldr + n, *reinterpret_cast<float(*)[8]>(rs));
+      ld8<true>(p.resid, m * p.ldr + n + 8, *reinterpret_cast<float(*)[8]>(rs + 8));
+      if (p.gate) {
+        const uint64_t smp = static_cast<uint64_t>(m) / static_cast<uint64_t>(p.rows_per_sample);
+        const float* g = p.gate + smp * p.gate_ld + n;
 #pragma unroll
-          for (int e = 0; e < 16; ++e) v[e] += b[e];
+        for (int q = 0; q < 4; ++q) {
+          const float4 t = *reinterpret_cast<const float4*>(g + 4 * q);
+          v[4 * q] = fmaf(t.x, v[4 * q], rs[4 * q]);
+          v[4 * q + 1] = fmaf(t.y, v[4 * q + 1], rs[4 * q + 1]);
+          v[4 * q + 2] = fmaf(t.z, v[4 * q + 2], rs[4 * q + 2]);
+          v[4 * q + 3] = fmaf(t.w, v[4 * q + 3], rs[4 * q + 3]);
         }
-        if constexpr (EPI == EPI_GELU) {
-#pragma unroll
-          for (int e = 0; e < 16; ++e)
-            if (n + e >= p.gelu_from) v[e] = gelu_tanh_f(v[e]);
-        } else if constexpr (EPI == EPI_GATED) {
-          float rs[16];
-          ld8<true>(p.resid, m * p.ldr + n, *reinterpret_cast<float(*)[8]>(rs));
-          ld8<true>(p.resid, m * p.ldr + n + 8, *reinterpret_cast<float(*)[8]>(rs + 8));
-          if (p.gate) {
-            const uint64_t smp = static_cast<uint64_t>(m) / static_cast<uint64_t>(p.rows_per_sample);
-            const float* g = p.gate + smp * p.gate_ld + n;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const float4 t = *reinterpret_cast<const float4*>(g + 4 * q);
-              v[4 * q] = fmaf(t.x, v[4 * q], rs[4 * q]);
-              v[4 * q + 1] = fmaf(t.y, v[4 * q + 1], rs[4 * q + 1]);
-              v[4 * q + 2] = fmaf(t.z, v[4 * q + 2], rs[4 * q + 2]);
-              v[4 * q + 3] = fmaf(t.w, v[4 * q + 3], rs[4 * q + 3]);
-            }
-          } else {
-#pragma unroll
-            for (int e = 0; e < 16; ++e) v[e] += rs[e];
-          }
-        }
-        st8<true>(out, m * p.ldo + n, *reinterpret_cast<const float(*)[8]>(v));
-        st8<true>(out, m * p.ldo + n + 8, *reinterpret_cast<const float(*)[8]>(v + 8));
       } else {
-        for (int e = 0; e < 16 && n + e < p.N; ++e) epi_store<true, EPI>(p, m, n + e, v[e]);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) v[e] += rs[e];
       }
     }
+    st8<true>(out, m * p.ldo + n, *reinterpret_cast<const float(*)[8]>(v));
+    st8<true>(out, m * p.ldo + n + 8, *reinterpret_cast<const float(*)[8]>(v + 8));
+  } else {
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      if (n + e < p.N) epi_store<true, EPI>(p, m, n + e, v[e]);
+  }
+}
+
+// All FM x FN blocks of a wave, block (i, j) at rows mw + 32 i, columns nw + 32 j.  The
+// recursion keeps every accumulator index a compile-time constant (a dynamic index would
+// send the whole accumulator array to scratch memory).
+template <int EPI, int FM, int FN, int B = 0>
+__device__ __forceinline__ void epilogue_blocks(const GemmParams& p, const f32x16_t (&acc)[FM][FN], int64_t mw,
+                                                int64_t nw, float* scratch, int lane) {
+  if constexpr (B < FM * FN) {
+    epilogue_block<EPI>(p, acc[B / FN][B % FN], mw + (B / FN) * 32, nw + (B % FN) * 32, scratch, lane);
+    epilogue_blocks<EPI, FM, FN, B + 1>(p, acc, mw, nw, scratch, lane);
+  }
 }
 
 
@@ -290,28 +299,6 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_bf16_kernel(Gem
                                reinterpret_cast<float*>(smem) + wave * 32 * 36, lane);
 }
 
-// ------------------------------------------------------------------ bf16, ping-pong
-// 256 x 256 tile, 8 waves of 128 x 64, K slabs of 32 in a ring of STAGES LDS
-// buffers filled by direct global->LDS loads issued STAGES - 1 slabs ahead.  A
-// 64-byte LDS row holds 4 chunks of 16 bytes at chunk ^ ((row >> 2) & 3): the
-// fragment reads of 16 consecutive rows then hit 16 distinct bank groups.  The
-// waves form two groups of four (one wave of each group per SIMD) offset by
-// one barrier: while one group runs its MFMA cluster on slab k, the other
-// reads slab k's fragments from LDS and issues the direct loads of a later
-// slab.  Every phase ends with a workgroup barrier, so on each SIMD the matrix
-// core is fed by one wave while the other wave's memory work is hidden.
-template <int STAGES, int LPW>
-__device__ __forceinline__ void wait_slab_after(int64_t n_after) {
-  // at most n_after younger slabs (LPW loads each) may still be in flight
-  if constexpr (STAGES <= 2) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  } else {
-    if (n_after >= STAGES - 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"((STAGES - 2) * LPW) : "memory");
-    else if (n_after == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPW) : "memory");
-    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  }
-}
-
 // Workgroup barrier that no instruction (memory or not) is scheduled across.
 __device__ __forceinline__ void wg_barrier() {
   __builtin_amdgcn_sched_barrier(0);
@@ -319,19 +306,25 @@ __device__ __forceinline__ void wg_barrier() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int EPI, int STAGES>
-__global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
-  constexpr int BM = 256, BN = 256, WAVES = 8, WAVES_N = 4;
-  constexpr int TM = 128, TN = 64, FM = 4, FN = 2;
-  constexpr int KS = 32;                           // slab width (k)
-  constexpr int ROWB = KS * 2;                     // bytes per LDS row
-  constexpr int CPR = ROWB / 16;                   // 16-byte chunks per row
-  constexpr int RPI = 1024 / ROWB;                 // rows per 1 KB direct load
-  constexpr int A_INS = BM / RPI / WAVES;
-  constexpr int B_INS = BN / RPI / WAVES;
-  constexpr int LPW = A_INS + B_INS;
-  constexpr int STAGE = (BM + BN) * ROWB;
-  constexpr int KSTEPS = KS / 16;
+// ------------------------------------------------------------------ bf16, 256 x 256 tiles
+// 256 x 256 tile, one wave per SIMD, each wave a 128 x 128 grid of 4 x 4 MFMA
+// blocks.  K advances in slabs of 64, so every row segment a direct load
+// fetches is a whole 128-byte cache line (32-wide slabs fetch half lines, which
+// halves the L2 -> LDS rate); two 64 KB LDS buffers.  Half a slab (two k16
+// steps) of fragments sits in each of two register sets: the second half of
+// slab s is read from LDS while the first half's MFMAs run, and the first half
+// of slab s + 1 while the second half's run.  Per slab: barrier X (everyone has
+// read slab s) lets slab s + 2's loads go into slab s's buffer between the
+// MFMAs of the third k16 step; barrier Y (each wave has waited for its own
+// loads of slab s + 1) publishes slab s + 1.  Loads past the end of K replay
+// the last slab, so the number in flight is the same on every step.
+template <int EPI>
+__global__ __launch_bounds__(256, 1) void gemm_bf16_256(GemmBatch batch) {
+  constexpr int BM = 256, BN = 256, WAVES = 4;
+  constexpr int KS = 64, ROWB = KS * 2, CPR = ROWB / 16, RPI = 1024 / ROWB;   // 128-byte rows, 8 rows per load
+  constexpr int TM = 128, TN = 128, FM = 4, FN = 4;
+  constexpr int A_INS = BM / RPI / WAVES, B_INS = BN / RPI / WAVES, LPW = A_INS + B_INS;   // 8 + 8
+  constexpr int STAGE = (BM + BN) * ROWB;   // 64 KB
   extern __shared__ __attribute__((aligned(16))) char smem[];
 
   const int64_t lid = xcd_remap(blockIdx.x, batch.tiles);
@@ -342,53 +335,57 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
   group_order(lid - (which ? batch.tiles0 : 0), num_m, num_n, tm, tn);
   const int64_t m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
-  const int grp = wave >> 2;
+  const int wm = wave >> 1, wn = wave & 1;
 
-  // Swizzle of a row's chunks: 16 consecutive rows read by 16 lanes land on 16 bank groups.
-  auto swz = [](int row) { return (row >> 2) & 3; };
-  // Direct load i of this wave fills RPI rows starting at RPI (i*WAVES + wave); lane l lands
-  // at row + l/CPR, stored chunk l%CPR, so it fetches logical chunk (l%CPR) ^ swz(row).
-  const bf16_t* a_src[A_INS];
-  const bf16_t* b_src[B_INS];
-  int a_row[A_INS], a_ck[A_INS];
+  // Load i of this wave fills rows RPI (i*WAVES + wave) .. +RPI-1 (1 KB of LDS); lane l lands at
+  // row + l/CPR, stored chunk l%CPR, so it fetches logical chunk (l%CPR) ^ ((row >> 1) & 7).
+  // Sources: a uniform base (the tile's first row) plus 32-bit per-lane byte offsets.
+  const char* a_base = reinterpret_cast<const char*>(static_cast<const bf16_t*>(p.A1) + m0 * p.lda1);
+  const char* b_base = reinterpret_cast<const char*>(static_cast<const bf16_t*>(p.W) + n0 * p.ldw);
+  uint32_t a_off[A_INS], b_off[B_INS];
+  auto a_offsets = [&](int64_t lda) {
 #pragma unroll
-  for (int i = 0; i < A_INS; ++i) {
-    a_row[i] = (i * WAVES + wave) * RPI + lane / CPR;
-    a_ck[i] = (lane % CPR) ^ swz(a_row[i]);
-    const int64_t g = m0 + a_row[i] < p.M ? m0 + a_row[i] : p.M - 1;
-    a_src[i] = static_cast<const bf16_t*>(p.A1) + g * p.lda1 + a_ck[i] * 8;
-  }
+    for (int i = 0; i < A_INS; ++i) {
+      const int row = (i * WAVES + wave) * RPI + lane / CPR;
+      const int ck = (lane % CPR) ^ ((row >> 1) & 7);
+      const int64_t r = m0 + row < p.M ? row : p.M - 1 - m0;
+      a_off[i] = static_cast<uint32_t>((r * lda + ck * 8) * 2);
+    }
+  };
+  a_offsets(p.lda1);
 #pragma unroll
   for (int i = 0; i < B_INS; ++i) {
     const int row = (i * WAVES + wave) * RPI + lane / CPR;
-    const int ck = (lane % CPR) ^ swz(row);
-    const int64_t g = n0 + row < p.N ? n0 + row : p.N - 1;
-    b_src[i] = static_cast<const bf16_t*>(p.W) + g * p.ldw + ck * 8;
+    const int ck = (lane % CPR) ^ ((row >> 1) & 7);
+    const int64_t r = n0 + row < p.N ? row : p.N - 1 - n0;
+    b_off[i] = static_cast<uint32_t>((r * p.ldw + ck * 8) * 2);
   }
-  const int64_t KT = p.K / KS, KT1 = p.K1 / KS;
+  const int KT = static_cast<int>(p.K / KS), KT1 = static_cast<int>(p.K1 / KS);
 
-  auto issue = [&](int64_t slab) {
-    if (slab >= KT) return;
-    if (slab == KT1 && slab > 0) {
-#pragma unroll
-      for (int i = 0; i < A_INS; ++i) {
-        const int64_t g = m0 + a_row[i] < p.M ? m0 + a_row[i] : p.M - 1;
-        a_src[i] = static_cast<const bf16_t*>(p.A2) + g * p.lda2 + a_ck[i] * 8;
-      }
-    }
-    char* base = smem + static_cast<int>(slab % STAGES) * STAGE;
-#pragma unroll
-    for (int i = 0; i < A_INS; ++i) {
-      __builtin_amdgcn_global_load_lds((const glb_t*)a_src[i], (lds_t*)(base + (i * WAVES + wave) * 1024), 16, 0, 0);
-      a_src[i] += KS;
-    }
-#pragma unroll
-    for (int i = 0; i < B_INS; ++i) {
-      __builtin_amdgcn_global_load_lds((const glb_t*)b_src[i], (lds_t*)(base + BM * ROWB + (i * WAVES + wave) * 1024), 16, 0, 0);
-      b_src[i] += KS;
+  auto switch_a = [&](int slab) {
+    if (slab == KT1 && slab > 0 && slab < KT) {
+      // continue K in the second A source (the two-source single-stream projection)
+      a_base = reinterpret_cast<const char*>(static_cast<const bf16_t*>(p.A2) + m0 * p.lda2);
+      a_offsets(p.lda2);
     }
   };
+  // Loads [first, first + count) of slab `slab` (A loads, then B loads).
+  auto issue_part = [&](int slab, int first, int count) {
+    const uint32_t back = slab < KT ? 0u : static_cast<uint32_t>(KS * 2);
+    char* base = smem + (slab & 1) * STAGE + wave * 1024;
+#pragma unroll
+    for (int q = first; q < first + count; ++q) {
+      if (q < A_INS) {
+        __builtin_amdgcn_global_load_lds((const glb_t*)(a_base + (a_off[q] - back)), (lds_t*)(base + q * WAVES * 1024), 16, 0, 0);
+        a_off[q] += KS * 2 - back;
+      } else {
+        const int i = q - A_INS;
+        __builtin_amdgcn_global_load_lds((const glb_t*)(b_base + (b_off[i] - back)), (lds_t*)(base + BM * ROWB + i * WAVES * 1024), 16, 0, 0);
+        b_off[i] += KS * 2 - back;
+      }
+    }
+  };
+  auto issue = [&](int slab) { issue_part(slab, 0, LPW); };
 
   f32x16_t acc[FM][FN];
 #pragma unroll
@@ -399,59 +396,80 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int frow = lane & 31, fhalf = lane >> 5;
-  const int key = swz(frow);   // the same for every fragment row of this lane
-  int a_frag[FM], b_frag[FN];
+  const int key = (frow >> 1) & 7;
+  const int a_frag0 = (wm * TM + frow) * ROWB, b_frag0 = BM * ROWB + (wn * TN + frow) * ROWB;
+  // Register sets: r0 = k16 steps 0, 1 of a slab; r1 = steps 2, 3.  [step][block]
+  bf16x8_t ra0[2][FM], rb0[2][FN], ra1[2][FM], rb1[2][FN];
+  auto read_half = [&](int slab, int half, bf16x8_t (&ra)[2][FM], bf16x8_t (&rb)[2][FN]) {
+    const char* S = smem + (slab & 1) * STAGE;
 #pragma unroll
-  for (int i = 0; i < FM; ++i) a_frag[i] = (wm * TM + i * 32 + frow) * ROWB;
+    for (int ks = 0; ks < 2; ++ks) {
+      const int coff = (((half * 2 + ks) * 2 + fhalf) ^ key) << 4;
 #pragma unroll
-  for (int j = 0; j < FN; ++j) b_frag[j] = BM * ROWB + (wn * TN + j * 32 + frow) * ROWB;
-
-  // Phases: group 0 runs M(k) C(k) M(k+1) ..., group 1 one barrier behind, so at any
-  // time one group multiplies while the other reads LDS.  Slab k + STAGES - 1 is
-  // issued in the first phase after slab k - 1's last read (group 0: its M(k); group 1:
-  // its C(k - 1)), and slab k + 1 must have landed before the phase of group 0's M(k + 1).
+      for (int i = 0; i < FM; ++i) ra[ks][i] = *reinterpret_cast<const bf16x8_t*>(S + a_frag0 + i * 32 * ROWB + coff);
 #pragma unroll
-  for (int st = 0; st < STAGES - 1; ++st) issue(st);
-  wait_slab_after<STAGES, LPW>(KT - 1 < STAGES - 2 ? KT - 1 : STAGES - 2);
-  wg_barrier();
-  if (grp == 1) {
-    issue(STAGES - 1);
-    wg_barrier();
-  }
-
-  for (int64_t kt = 0; kt < KT; ++kt) {
-    if (grp == 0) issue(kt + STAGES - 1);
-    const char* S = smem + static_cast<int>(kt % STAGES) * STAGE;
-    // The memory phase reads all fragments of the slab: the other group may overwrite
-    // this stage once the phase's closing barrier has passed.
-    bf16x8_t af[KSTEPS][FM], bfr[KSTEPS][FN];
-    auto read_step = [&](int ks) {
-      const int coff = ((ks * 2 + fhalf) ^ key) << 4;
-#pragma unroll
-      for (int i = 0; i < FM; ++i) af[ks][i] = *reinterpret_cast<const bf16x8_t*>(S + a_frag[i] + coff);
-#pragma unroll
-      for (int j = 0; j < FN; ++j) bfr[ks][j] = *reinterpret_cast<const bf16x8_t*>(S + b_frag[j] + coff);
-    };
-#pragma unroll
-    for (int ks = 0; ks < KSTEPS; ++ks) read_step(ks);
-    const int64_t n_after = KT - 2 - kt;   // slabs younger than kt + 1 that may stay in flight
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    if (grp == 1 && n_after >= 0) wait_slab_after<STAGES, LPW>(n_after);
-    wg_barrier();
-    if (grp == 1) issue(kt + STAGES);
-#pragma unroll
-    for (int ks = 0; ks < KSTEPS; ++ks) {
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks][i], bfr[ks][j], acc[i][j], 0, 0, 0);
+      for (int j = 0; j < FN; ++j) rb[ks][j] = *reinterpret_cast<const bf16x8_t*>(S + b_frag0 + j * 32 * ROWB + coff);
     }
-    if (grp == 0 && n_after >= 0) wait_slab_after<STAGES, LPW>(n_after);
-    wg_barrier();
-  }
-  if (grp == 0) wg_barrier();
+  };
+  auto mfma_step = [&](const bf16x8_t (&ra)[FM], const bf16x8_t (&rb)[FN]) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ra[i], rb[j], acc[i][j], 0, 0, 0);
+  };
 
+  switch_a(0);
+  issue(0);
+  switch_a(1);
+  issue(1);
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPW) : "memory");   // slab 0 has landed
+  wg_barrier();
+  read_half(0, 0, ra0, rb0);
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  // Loads of slab s + 2 per k16 step 1, 2, 3 (the address unit takes a 1 KB load every
+  // 16 clocks, so the 64 loads of a slab are spread over three steps of MFMAs).
+  constexpr int G1 = 6, G2 = 5, G3 = LPW - G1 - G2;
+  for (int s = 0; s < KT; ++s) {
+    // step 0: read steps 2, 3 of slab s between the MFMAs
+    read_half(s, 1, ra1, rb1);
+    mfma_step(ra0[0], rb0[0]);
+#pragma unroll
+    for (int m = 0; m < FM * FN; ++m) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    switch_a(s + 2);
+    wg_barrier();                                     // X: every wave has read slab s
+    // steps 1, 2: slab s + 2's first loads into slab s's buffer
+    issue_part(s + 2, 0, G1 + G2);
+    mfma_step(ra0[1], rb0[1]);
+    mfma_step(ra1[0], rb1[0]);
+#pragma unroll
+    for (int m = 0; m < 2 * FM * FN; ++m) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (m < FM * FN ? m < G1 : m - FM * FN < G2) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(G1 + G2) : "memory");   // slab s + 1 has landed
+    wg_barrier();                                     // Y: publish slab s + 1
+    // step 3: the rest of the loads; read steps 0, 1 of slab s + 1 (past the end: replayed data)
+    issue_part(s + 2, G1 + G2, G3);
+    read_half(s + 1, 0, ra0, rb0);
+    mfma_step(ra1[1], rb1[1]);
+#pragma unroll
+    for (int m = 0; m < FM * FN; ++m) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      if (m < G3) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  }
+
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // replayed loads may still target LDS
   __syncthreads();
   epilogue_blocks<EPI, FM, FN>(p, acc, m0 + wm * TM, n0 + wn * TN,
                                reinterpret_cast<float*>(smem) + wave * 32 * 36, lane);
@@ -523,39 +541,35 @@ int launch_bf16(const GemmParams& p, hipStream_t s, const char* name, double flo
   return ls.status();
 }
 
-template <int EPI, int STAGES>
-int launch_pp_batch(const GemmBatch& b, hipStream_t s, const char* name, double flops, double bytes) {
-  constexpr int smem = STAGES * 512 * 32 * 2;
+template <int EPI>
+int launch_256_batch(const GemmBatch& b, hipStream_t s, const char* name, double flops, double bytes) {
+  constexpr int smem = 2 * 512 * 64 * 2;
   static bool attr_set = false;
   if (!attr_set) {
-    FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_pp<EPI, STAGES>),
+    FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_256<EPI>),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, smem),
                  "gemm smem attribute");
     attr_set = true;
   }
   LaunchScope ls(name, s, flops, bytes);
-  hipLaunchKernelGGL((gemm_bf16_pp<EPI, STAGES>), dim3(static_cast<unsigned>(b.tiles)), dim3(512), smem, s, b);
+  hipLaunchKernelGGL((gemm_bf16_256<EPI>), dim3(static_cast<unsigned>(b.tiles)), dim3(256), smem, s, b);
   return ls.status();
 }
 
 int64_t tiles256(const GemmParams& p) { return ((p.M + 255) / 256) * ((p.N + 255) / 256); }
 
-template <int EPI, int STAGES>
-int launch_pp(const GemmParams& p, hipStream_t s, const char* name, double flops, double bytes) {
-  GemmBatch b{};
-  b.p[0] = p;
-  b.p[1] = p;
-  b.tiles0 = tiles256(p);
-  b.tiles = b.tiles0;
-  return launch_pp_batch<EPI, STAGES>(b, s, name, flops, bytes);
-}
-
-// Problems with at least one 256 x 256 tile per CU take the ping-pong kernel with
-// a three-slab ring; smaller ones the 128 x 128 tile, which fills more CUs.
+// Problems with at least one 256 x 256 tile per CU take the 256 x 256 kernel;
+// smaller ones the 128 x 128 tile, which fills more CUs.
 template <int EPI>
 int dispatch_bf16(const GemmParams& p, hipStream_t s, double flops, double bytes) {
   static const char* names[3] = {"gemm_bf16", "gemm_bf16_gelu", "gemm_bf16_gated"};
-  if (tiles256(p) >= 256) return launch_pp<EPI, 3>(p, s, names[EPI], flops, bytes);
+  if (tiles256(p) >= 256) {
+    GemmBatch b{};
+    b.p[0] = p;
+    b.p[1] = p;
+    b.tiles0 = b.tiles = tiles256(p);
+    return launch_256_batch<EPI>(b, s, names[EPI], flops, bytes);
+  }
   return launch_bf16<128, 128, 2, 2, EPI>(p, s, names[EPI], flops, bytes);
 }
 
@@ -628,9 +642,9 @@ int gemm2(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
   const double flops = gemm_flops(a0) + gemm_flops(a1), bytes = gemm_bytes(a0) + gemm_bytes(a1);
   static const char* names[3] = {"gemm_bf16", "gemm_bf16_gelu", "gemm_bf16_gated"};
   switch (a0.epi) {
-    case EPI_NONE: return launch_pp_batch<EPI_NONE, 3>(b, s, names[0], flops, bytes);
-    case EPI_GELU: return launch_pp_batch<EPI_GELU, 3>(b, s, names[1], flops, bytes);
-    default: return launch_pp_batch<EPI_GATED, 3>(b, s, names[2], flops, bytes);
+    case EPI_NONE: return launch_256_batch<EPI_NONE>(b, s, names[0], flops, bytes);
+    case EPI_GELU: return launch_256_batch<EPI_GELU>(b, s, names[1], flops, bytes);
+    default: return launch_256_batch<EPI_GATED>(b, s, names[2], flops, bytes);
   }
 }
 

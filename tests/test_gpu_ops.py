@@ -23,7 +23,11 @@ LIN = [
 ]
 
 
-@pytest.mark.parametrize("M,N,K,dt", LIN)
+# Shapes with at least one 256 x 256 tile per CU: these take the large-tile kernel.
+LIN_LARGE = [(4133, 4133, 192, C.BF16), (8197, 2088, 128, C.BF16)]
+
+
+@pytest.mark.parametrize("M,N,K,dt", LIN + LIN_LARGE)
 @pytest.mark.parametrize("epi", ["bias", "gelu", "gelu_from", "gated"])
 def test_linear_parity(gpu_lib, M, N, K, dt, epi):
     say("linear", M, N, K, dt, epi)
