@@ -11,7 +11,17 @@ Prints one JSON line: steps/s (and latent tokens/s), the roofline of the
 dominant kernel measured with HIP events on its launch stream over the timed
 region, and the plain CPU oracle timed on a bounded sample of the same work.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload flux-block|tiny]
+The other workloads (--workload flux-stack | qwen-stack | wan) run whole
+rollouts of the full model: 19 dual + 38 single Flux blocks (B = 16, 1024 +
+512 tokens, 10 SDE steps), 60 Qwen-Image-shaped dual blocks (B = 8, 4096 +
+256 tokens, 10 steps with SDE on steps 2-4) or 30 WAN blocks (B = 1, 32760 +
+512 tokens, 8 steps).  Their weights are drawn on the device (N(0, 0.02),
+norm weights 1 + N(0, 0.02)); a step is one denoising step of the batch, and
+--steps / --warmup count whole rollouts.  The oracle is timed on the default
+workload only.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+                       [--workload flux-block|flux-stack|qwen-stack|wan|tiny]
 """
 from __future__ import annotations
 
@@ -30,13 +40,18 @@ PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3       # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 
+# workload name -> (configs attribute, default timed units, default warmup units); the one-block
+# and tiny workloads time single steps, the stacks whole rollouts.
+WORKLOADS = {"flux-block": ("FLUX_BLOCK", 20, 3), "tiny": ("TINY", 20, 3), "flux-stack": ("FLUX_STACK", 2, 1),
+             "qwen-stack": ("QWEN_STACK", 1, 1), "wan": ("WAN_STACK", 2, 1)}
+
 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="flux-block", choices=["flux-block", "tiny"])
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=None)
+    ap.add_argument("--workload", default="flux-block", choices=list(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-samples", type=int, default=3, help="samples of the batch the oracle times")
     return ap.parse_args()
@@ -63,13 +78,21 @@ def main() -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
     api.load()
-    w = C.FLUX_BLOCK if args.workload == "flux-block" else C.TINY
+    attr, def_steps, def_warmup = WORKLOADS[args.workload]
+    w = getattr(C, attr)
+    args.steps = def_steps if args.steps is None else args.steps
+    args.warmup = def_warmup if args.warmup is None else args.warmup
     m = w.model
     dt = api.torch_dtype(m.dtype)
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda().to(dt)
     print(f"[bench] workload {w.name}: generating inputs", file=sys.stderr, flush=True)
-    W = synth.weights(w)
-    Wd = {k: dev(v) for k, v in W.items()}
+    device_drawn = args.workload in ("flux-stack", "qwen-stack", "wan")
+    if device_drawn:
+        W = None
+        Wd = device_weights(m, 1000 + w.index, dt)
+    else:
+        W = synth.weights(w)
+        Wd = {k: dev(v) for k, v in W.items()}
     txt, cond, x0 = synth.text_input(w), synth.cond_input(w), synth.x0(w)
     eps = [synth.sde_noise(w, k) for k in range(len(R.time_grid(w.steps)) - 1)]
     T, Cd, X0 = dev(txt), (dev(cond) if cond is not None else None), dev(x0)
@@ -79,6 +102,7 @@ def main() -> int:
     dit = api.Dit(m, Wd)
     ro = R.Rollout(w, dit, keep_velocities=False)
     txt_out = torch.empty_like(T) if m.io_mode == C.IO_HIDDEN else None
+    steps_per_unit = len(ro.sigmas)     # denoising steps in one timed unit (a rollout, or the one step)
 
     def step():
         res = ro.run(X0, T, E, cond=Cd, txt_index=tidx, txt_out=txt_out)
@@ -93,24 +117,27 @@ def main() -> int:
     api.profile_enable(True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for i in range(args.steps):
         step()
+        if steps_per_unit > 1:
+            print(f"[bench] rollout {i + 1}/{args.steps} issued", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     api.profile_enable(False)
     prof = api.profile_read()
     print(f"[bench] timed {args.steps} steps in {elapsed:.3f} s", file=sys.stderr, flush=True)
 
-    ms_per_step = 1e3 * elapsed / args.steps
-    steps_per_s = args.steps / elapsed
+    n_steps = args.steps * steps_per_unit
+    ms_per_step = 1e3 * elapsed / n_steps
+    steps_per_s = n_steps / elapsed
     latent_tok_s = steps_per_s * w.batch * w.n_img
 
     # Per-kernel achieved rates from HIP events over the timed region.
     kernels = {}
     for name, p in prof.items():
         avg_ms = p["ms"] / max(p["launches"], 1)
-        k = {"launches_per_step": p["launches"] / args.steps, "avg_us": 1e3 * avg_ms,
-             "ms_per_step": p["ms"] / args.steps}
+        k = {"launches_per_step": p["launches"] / n_steps, "avg_us": 1e3 * avg_ms,
+             "ms_per_step": p["ms"] / n_steps}
         if p["flops"] > 0 and name.startswith(("gemm", "attn")):
             k["tflops"] = p["flops"] / (p["ms"] * 1e-3) / 1e12
             k["mfma_frac"] = k["tflops"] / (PEAK_BF16_TFLOPS if m.dtype == C.BF16 else PEAK_FP32_TFLOPS)
@@ -118,7 +145,7 @@ def main() -> int:
             k["gbs"] = p["bytes"] / (p["ms"] * 1e-3) / 1e9
             k["hbm_frac"] = k["gbs"] / PEAK_HBM_GBS
         kernels[name] = k
-    block_flops = sum(p["flops"] for n, p in prof.items() if n.startswith(("gemm", "attn"))) / args.steps
+    block_flops = sum(p["flops"] for n, p in prof.items() if n.startswith(("gemm", "attn"))) / n_steps
     dominant = max(prof, key=lambda n: prof[n]["ms"])
     dp = prof[dominant]
     per_launch = {"flops": dp["flops"] / dp["launches"], "algorithmic_bytes": dp["bytes"] / dp["launches"],
@@ -141,7 +168,7 @@ def main() -> int:
                 "frac": achieved / PEAK_HBM_GBS, "traffic": traffic, "kernel": dominant, "per_launch": per_launch}
 
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and W is not None:
         cpu = cpu_baseline(w, W, txt, cond, x0, eps, args.cpu_samples)
 
     out = {
@@ -149,8 +176,8 @@ def main() -> int:
         "value": steps_per_s,
         "unit": "steps/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": n_steps,
+        "warmup": args.warmup * steps_per_unit,
         "ms_per_step": ms_per_step,
         "higher_is_better": True,
         "scaling": "weak",
@@ -159,12 +186,15 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": w.name, "batch": w.batch, "img_tokens": w.n_img, "txt_tokens": w.n_txt,
                    "hidden": m.hidden, "heads": m.heads, "head_dim": m.head_dim, "mlp_hidden": m.mlp_hidden,
-                   "dual_blocks": m.n_dual, "single_blocks": m.n_single, "sde_steps_per_step": len(ro.sigmas),
+                   "dual_blocks": m.n_dual, "single_blocks": m.n_single, "wan_blocks": m.n_wan,
+                   "denoising_steps": len(ro.sigmas), "sde_steps": sum(1 for s in ro.sigmas if s > 0),
+                   "timed_unit": "rollout" if steps_per_unit > 1 else "step",
+                   "weights": "device-drawn N(0,0.02)" if device_drawn else "host-drawn N(0,0.02), seeded",
                    "t": ro.ts[0], "t_next": ro.ts[1], "sigma": ro.sigmas[0]},
         "latent_tokens_per_s": latent_tok_s,
         "sample_steps_per_s": steps_per_s * w.batch,
-        "block_tflops": block_flops / (ms_per_step * 1e-3) / 1e12,
-        "block_mfma_frac": block_flops / (ms_per_step * 1e-3) / 1e12 /
+        "model_tflops": block_flops / (ms_per_step * 1e-3) / 1e12,
+        "model_mfma_frac": block_flops / (ms_per_step * 1e-3) / 1e12 /
                            (PEAK_BF16_TFLOPS if m.dtype == C.BF16 else PEAK_FP32_TFLOPS),
         "roofline": roof,
         "kernels": kernels,
@@ -172,6 +202,23 @@ def main() -> int:
     }
     print(json.dumps(out), flush=True)
     return 0
+
+
+def device_weights(m, seed: int, dt):
+    """Random weights of the model drawn on the device: N(0, 0.02^2), norm weights 1 + N(0, 0.02^2)."""
+    import torch
+
+    from paper_2602_12529_amd import synth
+
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    out = {}
+    for name, shape, kind in synth.tensor_table(m):
+        t = torch.randn(shape, device="cuda", generator=g, dtype=torch.float32).mul_(0.02)
+        if kind == "norm":
+            t.add_(1.0)
+        out[name] = t.to(dt)
+    return out
 
 
 def cpu_baseline(w, W, txt, cond, x0, eps, n_samples: int):

@@ -87,14 +87,18 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
-__device__ __forceinline__ float silu_f(float x) { return x / (1.0f + __expf(-x)); }
+// x * sigmoid(x), with the sigmoid from the hardware exp2 and reciprocal (about 1 ulp each;
+// an IEEE divide is a ten-instruction sequence).
+__device__ __forceinline__ float silu_f(float x) {
+  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * x));
+}
 
-// GELU, tanh approximation, with tanh(u) = 1 - 2 / (exp(2u) + 1).
+// GELU, tanh approximation: 0.5 x (1 + tanh(u)) with u = sqrt(2/pi) (x + 0.044715 x^3), written
+// as x * sigmoid(2u) and evaluated like silu_f.
 __device__ __forceinline__ float gelu_tanh_f(float x) {
-  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
-  float u = k0 * fmaf(0.044715f * x, x * x, x);
-  float t = 1.0f - 2.0f / (__expf(2.0f * u) + 1.0f);
-  return 0.5f * x * (1.0f + t);
+  const float k = -2.0f * 0.7978845608028654f * 1.4426950408889634f;   // -2 sqrt(2/pi) log2(e)
+  const float e = __builtin_amdgcn_exp2f(k * fmaf(0.044715f * x, x * x, x));
+  return x * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
 }  // namespace ff
