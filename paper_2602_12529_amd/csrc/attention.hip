@@ -2,8 +2,8 @@
 //
 // bf16, d = 128: a flash-style kernel with online softmax in float32.  Each
 // wave owns 32 queries; a workgroup of WAVES waves shares 64-key tiles of K
-// and V^T staged through LDS (double-buffered, the next tile's global loads in
-// flight during the current tile's math).  Both products are computed
+// and V^T staged through a ring of LDS buffers by direct global->LDS loads.
+// Both products are computed
 // transposed on MFMA 32x32x16:
 //   S^T (keys x queries) = K Q^T        A = K rows (LDS), B = Q (registers)
 //   O^T (d x queries)   += V^T P^T      A = V^T rows (LDS), B = P (registers)
@@ -18,7 +18,6 @@
 // float32 (any d <= 64): one thread per query with the same online softmax,
 // for the small float32 configuration.
 #include <cmath>
-#include <cstdlib>
 
 #include "dev.h"
 #include "ff_internal.h"
@@ -53,66 +52,23 @@ __device__ __forceinline__ int v_off(int r, int c) { return r * 128 + ((c ^ ((r 
 typedef __attribute__((address_space(3))) void lds_t;
 typedef __attribute__((address_space(1))) void glb_t;
 
-// One 64-key tile: S^T = K Q^T, online softmax (masked when MASK), O^T += V^T P^T.
-#define FF_ATTN_TILE(MASK)                                                                          \
-  {                                                                                                 \
-    const char* Ks = smem + (it % STAGES) * (K_STAGE + V_STAGE);                                     \
-    const char* Vs = Ks + K_STAGE;                                                                  \
-    f32x16_t s[2];                                                                                  \
-    _Pragma("unroll") for (int kb = 0; kb < 2; ++kb)                                                \
-      _Pragma("unroll") for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;                                \
-    _Pragma("unroll") for (int t = 0; t < 8; ++t)                                                   \
-      _Pragma("unroll") for (int kb = 0; kb < 2; ++kb) {                                            \
-        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(Ks + k_off(32 * kb + krow, 2 * t + g)); \
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[t], s[kb], 0, 0, 0);                  \
-      }                                                                                             \
-    if (MASK) {                                                                                     \
-      /* keys come in aligned groups of 8 (n_kv % 8 == 0): one test per group */                    \
-      _Pragma("unroll") for (int kb = 0; kb < 2; ++kb)                                              \
-        _Pragma("unroll") for (int u = 0; u < 2; ++u) {                                             \
-          const bool dead = kv0 + 32 * kb + 16 * u + 8 * g >= p.n_kv;                              \
-          _Pragma("unroll") for (int j = 0; j < 8; ++j)                                             \
-            if (dead) s[kb][8 * u + j] = -INFINITY;                                                 \
-        }                                                                                           \
-    }                                                                                               \
-    float mx = -INFINITY;                                                                           \
-    _Pragma("unroll") for (int kb = 0; kb < 2; ++kb)                                                \
-      _Pragma("unroll") for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);                      \
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.scale_log2;                                          \
-    if (__any(mx > m_run + 8.0f)) {                                                                 \
-      const float m_new = fmaxf(m_run, mx);                                                         \
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);                                    \
-      m_run = m_new;                                                                                \
-      l_run *= alpha;                                                                               \
-      _Pragma("unroll") for (int i = 0; i < 4; ++i)                                                 \
-        _Pragma("unroll") for (int r = 0; r < 16; ++r) o[i][r] *= alpha;                            \
-    }                                                                                               \
-    const float neg_m = -m_run;                                                                     \
-    float lsum = 0.f;                                                                               \
-    bf16x8_t pf[4];                                                                                 \
-    _Pragma("unroll") for (int kb = 0; kb < 2; ++kb)                                                \
-      _Pragma("unroll") for (int u = 0; u < 2; ++u)                                                 \
-        _Pragma("unroll") for (int j = 0; j < 8; ++j) {                                             \
-          const float e = __builtin_amdgcn_exp2f(fmaf(s[kb][8 * u + j], p.scale_log2, neg_m));      \
-          lsum += e;                                                                                \
-          pf[2 * kb + u][j] = static_cast<__bf16>(e);                                               \
-        }                                                                                           \
-    l_run += lsum;                                                                                  \
-    _Pragma("unroll") for (int sl = 0; sl < 4; ++sl)                                                \
-      _Pragma("unroll") for (int db = 0; db < 4; ++db) {                                            \
-        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(Vs + v_off(32 * db + ql, 2 * sl + g)); \
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[sl], o[db], 0, 0, 0);                 \
-      }                                                                                             \
-  }
-
+// ------------------------------------------------------------------ bf16
+// Each wave's work is ordered so the matrix core and the vector ALUs overlap
+// inside one wave: while the MFMAs of S = K Q^T for tile i + 1 run, the softmax of tile i
+// (exp2, row sums, bf16 packing) is issued between them; while the MFMAs of
+// O += V P^T for tile i - 1 run, the row max of tile i is taken.  K / V^T tiles
+// come through a ring of STAGES LDS buffers filled STAGES - 1 tiles ahead by
+// direct loads; loads past the last tile replay it into a buffer that is never
+// read again, so the number of loads in flight is the same on every tile.
 template <int WAVES, int STAGES>
-__global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_bf16_d128(AttnParams p) {
+__global__ __launch_bounds__(WAVES * 64, 1) void attn_bf16_d128(AttnParams p) {
   constexpr int K_INS = K_STAGE / 1024 / WAVES;   // 1 KB direct loads per wave per K tile
   constexpr int V_INS = V_STAGE / 1024 / WAVES;
-  __shared__ __attribute__((aligned(16))) char smem[STAGES * (K_STAGE + V_STAGE)];
+  constexpr int LPW = K_INS + V_INS;
+  constexpr int STAGE = K_STAGE + V_STAGE;
+  static_assert(STAGES >= 3, "ring depth");
+  extern __shared__ __attribute__((aligned(16))) char smem[];
 
-  // Workgroup -> (query tile, batch*head): ids are regrouped so the query
-  // tiles of one (b, h) run on one XCD and share its L2.
   const int64_t nqt = (p.n_q + 32 * WAVES - 1) / (32 * WAVES);
   const int64_t total = nqt * p.B * p.heads;
   const int64_t pid = blockIdx.x;
@@ -124,11 +80,9 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_bf16_d128(AttnPara
   const int ql = lane & 31, g = lane >> 5;
   const int64_t q0 = qt * 32 * WAVES + wave * 32;
   const int n_kv = static_cast<int>(p.n_kv);
-
   const bf16_t* Kb = p.K + bh * p.n_kv * D;
   const bf16_t* Vb = p.Vt + bh * D * p.n_kv;
 
-  // Q fragments: query q0 + ql, d slots 16t + 8g .. +7.
   bf16x8_t qf[8];
   {
     int64_t q = q0 + ql;
@@ -138,10 +92,6 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_bf16_d128(AttnPara
     for (int t = 0; t < 8; ++t) qf[t] = *reinterpret_cast<const bf16x8_t*>(qp + 16 * t);
   }
 
-  // Direct loads.  K: instruction i of this wave fills K rows 4(i*WAVES + wave) .. +3; lane l
-  // lands at row + l/16, stored chunk l%16 = logical chunk ^ (row & 15).  V^T: instruction i
-  // fills rows 8(i*WAVES + wave) .. +7; lane l lands at row + l/8, stored chunk l%8 = logical
-  // chunk ^ ((row >> 1) & 7).  Keys past n_kv are clamped to valid memory and masked.
   int k_row[K_INS], k_ck[K_INS], v_row[V_INS], v_ck[V_INS];
 #pragma unroll
   for (int i = 0; i < K_INS; ++i) {
@@ -153,8 +103,11 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_bf16_d128(AttnPara
     v_row[i] = 8 * (i * WAVES + wave) + (lane >> 3);
     v_ck[i] = (lane & 7) ^ ((v_row[i] >> 1) & 7);
   }
-  auto issue = [&](int kv0, int stage) {
-    char* base = smem + stage * (K_STAGE + V_STAGE);
+  const int ntiles = (n_kv + KT - 1) / KT;
+  const int nfull = n_kv / KT;   // tiles without masked keys
+  auto issue = [&](int tile) {
+    const int kv0 = (tile < ntiles ? tile : ntiles - 1) * KT;
+    char* base = smem + (tile % STAGES) * STAGE;
 #pragma unroll
     for (int i = 0; i < K_INS; ++i) {
       const int key = kv0 + k_row[i] < n_kv ? kv0 + k_row[i] : n_kv - 1;
@@ -175,30 +128,142 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_bf16_d128(AttnPara
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[i][r] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
+  const int krow = (ql & ~12) | ((ql & 4) << 1) | ((ql & 8) >> 1);   // K row fed to MFMA row ql
 
-  // Row of K fed to MFMA row rho: bits 2 and 3 swapped.
-  const int krow = (ql & ~12) | ((ql & 4) << 1) | ((ql & 8) >> 1);
-
-  const int ntiles = (n_kv + KT - 1) / KT;
-  const int nfull = n_kv / KT;   // tiles without masked keys
+  // The two halves of a tile step are written out as 16 fused steps, fenced so the
+  // compiler keeps the order: each issues one MFMA, the LDS read of the fragment six
+  // steps ahead, and the vector work of two scores.
+  constexpr int AHEAD = 6;
+  // K fragment f = (t, kb) of S^T = K Q^T: K rows 32 kb + krow, d slots 16 t + 8 g.
+  auto k_frag = [&](const char* Ks, int f) {
+    return *reinterpret_cast<const bf16x8_t*>(Ks + k_off(32 * (f & 1) + krow, 2 * (f >> 1) + g));
+  };
+  // V^T fragment f = (sl, db) of O^T += V^T P^T: V^T rows 32 db + ql, keys 16 sl + 8 g.
+  auto v_frag = [&](const char* Vs, int f) {
+    return *reinterpret_cast<const bf16x8_t*>(Vs + v_off(32 * (f & 3) + ql, 2 * (f >> 2) + g));
+  };
+  // Score i (0..31) of a tile: s[i / 16][i % 16]; its P slot is pf[i / 8][i % 8].
+  // O += V P^T of tile `tile` with the row max of `s` (log2 units, both lane halves).
+  auto pv_max = [&](int tile, const bf16x8_t (&pf)[4], const f32x16_t (&s)[2]) {
+    const char* Vs = smem + (tile % STAGES) * STAGE + K_STAGE;
+    bf16x8_t vf[16];
+    float mx0 = -INFINITY, mx1 = -INFINITY;
 #pragma unroll
-  for (int st = 0; st < STAGES - 1; ++st)
-    if (st < ntiles) issue(st * KT, st);
-
-  for (int it = 0; it < ntiles; ++it) {
-    const int kv0 = it * KT;
-    // tile it has landed once at most STAGES-2 younger tiles are in flight
-    if (it + STAGES - 2 < ntiles) {
-      if constexpr (STAGES == 3) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(K_INS + V_INS) : "memory");
-      else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    } else {
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    for (int f = 0; f < AHEAD; ++f) vf[f] = v_frag(Vs, f);
+#pragma unroll
+    for (int f = 0; f < 16; ++f) {
+      o[f & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[f], pf[f >> 2], o[f & 3], 0, 0, 0);
+      if (f + AHEAD < 16) vf[f + AHEAD] = v_frag(Vs, f + AHEAD);
+      mx0 = fmaxf(mx0, s[f >> 3][(2 * f) & 15]);
+      mx1 = fmaxf(mx1, s[f >> 3][(2 * f + 1) & 15]);
+      __builtin_amdgcn_sched_barrier(0);
     }
+    const float mx = fmaxf(mx0, mx1);
+    return fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.scale_log2;
+  };
+  auto rowmax = [&](const f32x16_t (&s)[2]) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
+    return fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.scale_log2;
+  };
+  // Lazy rescale: O and l move to a new max only when some lane's max grew by more than 8.
+  auto rescale = [&](float mx) {
+    if (__any(mx > m_run + 8.0f)) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
+    }
+  };
+  // S of tile `next` with P = exp2(S_cur scale - m) of tile `tile` into bf16 operand slots and
+  // l += row sums.  A group of 8 keys past n_kv gets the offset -inf, so its P is 0.
+  auto qk_softmax = [&](int next, f32x16_t (&s_nxt)[2], int tile, const f32x16_t (&s)[2], bf16x8_t (&pf)[4]) {
+    const char* Ks = smem + (next % STAGES) * STAGE;
+    const int kv0 = tile * KT;
+    float nm[4];
+#pragma unroll
+    for (int gi = 0; gi < 4; ++gi) nm[gi] = kv0 + 8 * (2 * gi + g) < n_kv ? -m_run : -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s_nxt[kb][r] = 0.f;
+    bf16x8_t kf[16];
+    float lsum0 = 0.f, lsum1 = 0.f;
+#pragma unroll
+    for (int f = 0; f < AHEAD; ++f) kf[f] = k_frag(Ks, f);
+#pragma unroll
+    for (int f = 0; f < 16; ++f) {
+      s_nxt[f & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[f], qf[f >> 1], s_nxt[f & 1], 0, 0, 0);
+      if (f + AHEAD < 16) kf[f + AHEAD] = k_frag(Ks, f + AHEAD);
+      const int i0 = 2 * f, i1 = 2 * f + 1;   // scores i0, i1: same 8-key group i0 / 8
+      const float e0 = __builtin_amdgcn_exp2f(fmaf(s[i0 >> 4][i0 & 15], p.scale_log2, nm[i0 >> 3]));
+      const float e1 = __builtin_amdgcn_exp2f(fmaf(s[i1 >> 4][i1 & 15], p.scale_log2, nm[i1 >> 3]));
+      lsum0 += e0;
+      lsum1 += e1;
+      pf[i0 >> 3][i0 & 7] = static_cast<__bf16>(e0);
+      pf[i1 >> 3][i1 & 7] = static_cast<__bf16>(e1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    l_run += lsum0 + lsum1;
+  };
+  auto qk = [&](int tile, f32x16_t (&s)[2]) {
+    const char* Ks = smem + (tile % STAGES) * STAGE;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
+#pragma unroll
+    for (int f = 0; f < 16; ++f) s[f & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k_frag(Ks, f), qf[f >> 1], s[f & 1], 0, 0, 0);
+  };
+  auto wait_next = [&]() {   // tile it + 1 has landed in every wave's view
+    if constexpr (STAGES == 3) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(%0)" ::"n"((STAGES - 3) * LPW) : "memory");
+    __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_barrier" ::: "memory");
-    if (it + STAGES - 1 < ntiles) issue((it + STAGES - 1) * KT, (it + STAGES - 1) % STAGES);
-    if (it < nfull) FF_ATTN_TILE(false)
-    else FF_ATTN_TILE(true)
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // Tile it: [O += V P^T of tile it - 1 | row max of tile it], rescale, wait for tile it + 1,
+  // issue tile it + STAGES - 1, [S of tile it + 1 | softmax of tile it].
+  auto iter = [&](int it, f32x16_t (&s_cur)[2], f32x16_t (&s_nxt)[2], const bf16x8_t (&p_prev)[4],
+                  bf16x8_t (&p_cur)[4], bool first) {
+    const float mx = first ? rowmax(s_cur) : pv_max(it - 1, p_prev, s_cur);
+    __builtin_amdgcn_sched_barrier(0);
+    rescale(mx);
+    wait_next();
+    issue(it + STAGES - 1);
+    __builtin_amdgcn_sched_barrier(0);
+    qk_softmax(it + 1, s_nxt, it, s_cur, p_cur);   // past the last tile: replayed data, unused
+  };
+
+#pragma unroll
+  for (int st = 0; st < STAGES - 1; ++st) issue(st);
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"((STAGES - 2) * LPW) : "memory");   // tile 0 has landed
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_barrier" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+  f32x16_t sA[2], sB[2];
+  bf16x8_t pA[4], pB[4];
+  qk(0, sA);
+  iter(0, sA, sB, pB, pA, true);
+  int it = 1;
+  for (; it + 1 < ntiles; it += 2) {
+    iter(it, sB, sA, pA, pB, false);
+    iter(it + 1, sA, sB, pB, pA, false);
   }
+  if (it < ntiles) {
+    iter(it, sB, sA, pA, pB, false);
+    pv_max(it, pB, sA);
+  } else {
+    pv_max(ntiles - 1, pA, sA);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // replayed loads may still target LDS
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   const float inv = 1.0f / l_tot;
@@ -209,7 +274,6 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_bf16_d128(AttnPara
   if (q < p.split) row = p.out0 + (b * p.split + q) * p.ldo;
   else row = p.out1 + (b * (p.n_q - p.split) + (q - p.split)) * p.ldo;
   row += h * D;
-  // o[db][4u + j] is O[q, 32db + 8u + 4g + j].
 #pragma unroll
   for (int db = 0; db < 4; ++db)
 #pragma unroll
@@ -220,7 +284,6 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attn_bf16_d128(AttnPara
       *reinterpret_cast<uint2*>(row + 32 * db + 8 * u + 4 * g) = w;
     }
 }
-#undef FF_ATTN_TILE
 
 // ------------------------------------------------------------------ float32
 struct AttnF32Params {
@@ -278,19 +341,17 @@ int attention(const AttnArgs& a, hipStream_t s) {
                  static_cast<const bf16_t*>(a.Q), static_cast<const bf16_t*>(a.K), static_cast<const bf16_t*>(a.Vt),
                  static_cast<bf16_t*>(a.out0), static_cast<bf16_t*>(a.out1), a.split, a.ldo,
                  static_cast<float>(a.scale * 1.4426950408889634), qbs, qhs, qrs};
-    static const char* env = getenv("FF_ATTN_WAVES");
-    const int waves = (env && env[0] == '4') ? 4 : 8;
-    LaunchScope ls("attn_bf16_d128", s, flops, bytes);
-    static const char* envs = getenv("FF_ATTN_STAGES");
-    const int stages = (envs && envs[0] == '2') ? 2 : 3;
-    if (waves == 8) {
-      const int64_t tiles = (a.n_q + 255) / 256 * a.B * a.heads;
-      if (stages == 3) hipLaunchKernelGGL((attn_bf16_d128<8, 3>), dim3(static_cast<unsigned>(tiles)), dim3(512), 0, s, p);
-      else hipLaunchKernelGGL((attn_bf16_d128<8, 2>), dim3(static_cast<unsigned>(tiles)), dim3(512), 0, s, p);
-    } else {
-      const int64_t tiles = (a.n_q + 127) / 128 * a.B * a.heads;
-      hipLaunchKernelGGL((attn_bf16_d128<4, 2>), dim3(static_cast<unsigned>(tiles)), dim3(256), 0, s, p);
+    constexpr int WAVES = 8, STAGES = 4, smem = STAGES * (K_STAGE + V_STAGE);
+    static bool attr_set = false;
+    if (!attr_set) {
+      FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_bf16_d128<WAVES, STAGES>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, smem),
+                   "attention smem attribute");
+      attr_set = true;
     }
+    const int64_t tiles = (a.n_q + 32 * WAVES - 1) / (32 * WAVES) * a.B * a.heads;
+    LaunchScope ls("attn_bf16_d128", s, flops, bytes);
+    hipLaunchKernelGGL((attn_bf16_d128<WAVES, STAGES>), dim3(static_cast<unsigned>(tiles)), dim3(64 * WAVES), smem, s, p);
     return ls.status();
   }
   if (a.d > 64) return fail(FF_EUNSUPPORTED, "attention: f32 head_dim %lld > 64", (long long)a.d);
