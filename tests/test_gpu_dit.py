@@ -157,6 +157,32 @@ def test_flux_dual_block_full_size(gpu_lib):
         assert abs(lp[b] - lr[0]) <= LOGP_ABS
 
 
+@pytest.mark.timeout(900)
+def test_flux_single_block_full_width(gpu_lib):
+    """One Flux-shaped single-stream block at full width (H=3072, fused H -> 3H + F projection,
+    two-source [attention | MLP] -> H projection with 15360 inputs) on B=4 samples of 1024 image
+    + 512 text tokens: both projections run on the 256 x 256 GEMM tile, the second one switching
+    its A source mid-K.  The oracle recomputes two whole samples."""
+    base = C.FLUX_BLOCK
+    m = base.model.replace(n_dual=0, n_single=1)
+    w = C.Workload(**{**base.__dict__, "name": "flux-single-block-B4", "index": 15, "model": m, "group": 4,
+                      "grid": (1, 32, 32)})
+    say("full-width single block: generating inputs")
+    W, txt, cond, x0, eps = _inputs(w)
+    Wd, T, Cd, X0, E = _device(w, W, txt, cond, x0, eps)
+    dit = api.Dit(m, Wd)
+    ro = R.Rollout(w, dit)
+    res = ro.run(X0, T, E, cond=Cd, txt_out=torch.empty_like(T))
+    torch.cuda.synchronize()
+    v = host(res.vs[0])
+    for b in (0, 3):
+        say("oracle sample", b)
+        img, _ = odit.forward(m, W, x0[b:b + 1], txt[b:b + 1], cond=cond[b:b + 1], grid=w.grid)
+        e_v = rel(v[b:b + 1], img)
+        say("  rel v", e_v)
+        assert e_v <= TOL[C.BF16]
+
+
 def _small_wan(dtype):
     if dtype == C.BF16:
         m = C.ModelConfig(model=C.MODEL_WAN, io_mode=C.IO_LATENT, dtype=C.BF16, n_wan=2, hidden=256, heads=2,
