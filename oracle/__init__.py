@@ -17,5 +17,8 @@ Modules:
                 WAN blocks, embedders, final layer
   rollout    -- the K-step rollout loop with mixed ODE/SDE steps (Sec. 3.1,
                 MixGRPO), per-step log-probs and final advantages
+  losses     -- the objectives that consume the rollout: forward noising and
+                the AWM (Eq. 3) and DiffusionNFT (Eq. 2) losses, the clipped
+                GRPO ratio surrogate on stored trajectories
 """
-from . import advantage, dit, rollout, sde  # noqa: F401
+from . import advantage, dit, losses, rollout, sde  # noqa: F401
