@@ -17,7 +17,12 @@ rollouts of the full model: 19 dual + 38 single Flux blocks (B = 16, 1024 +
 256 tokens, 10 steps with SDE on steps 2-4) or 30 WAN blocks (B = 1, 32760 +
 512 tokens, 8 steps).  Their weights are drawn on the device (N(0, 0.02),
 norm weights 1 + N(0, 0.02)); a step is one denoising step of the batch, and
---steps / --warmup count whole rollouts.  The oracle is timed on the default
+--steps / --warmup count whole rollouts.  Two training-side workloads run on
+the Flux stack: grpo-flux-stack times the GRPO policy-update forward over a
+stored rollout (a DiT forward and a log-prob recompute per SDE step, then the
+clipped-ratio objective; a step is one recomputed SDE step), awm-flux-stack
+the AWM training forward (noising at per-sample t, DiT forward, Eq. 3 loss; a
+step is one forward of the batch).  The oracle is timed on the default
 workload only.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
@@ -43,7 +48,8 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 # workload name -> (configs attribute, default timed units, default warmup units); the one-block
 # and tiny workloads time single steps, the stacks whole rollouts.
 WORKLOADS = {"flux-block": ("FLUX_BLOCK", 20, 3), "tiny": ("TINY", 20, 3), "flux-stack": ("FLUX_STACK", 2, 1),
-             "qwen-stack": ("QWEN_STACK", 1, 1), "wan": ("WAN_STACK", 2, 1)}
+             "qwen-stack": ("QWEN_STACK", 1, 1), "wan": ("WAN_STACK", 2, 1),
+             "grpo-flux-stack": ("FLUX_STACK", 2, 1), "awm-flux-stack": ("FLUX_STACK", 10, 2)}
 
 
 def parse():
@@ -86,7 +92,7 @@ def main() -> int:
     dt = api.torch_dtype(m.dtype)
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda().to(dt)
     print(f"[bench] workload {w.name}: generating inputs", file=sys.stderr, flush=True)
-    device_drawn = args.workload in ("flux-stack", "qwen-stack", "wan")
+    device_drawn = args.workload in ("flux-stack", "qwen-stack", "wan", "grpo-flux-stack", "awm-flux-stack")
     if device_drawn:
         W = None
         Wd = device_weights(m, 1000 + w.index, dt)
@@ -108,6 +114,26 @@ def main() -> int:
         res = ro.run(X0, T, E, cond=Cd, txt_index=tidx, txt_out=txt_out)
         ro.advantages(rewards)
         return res
+
+    if args.workload == "grpo-flux-stack":
+        print("[bench] storing one rollout for the policy update", file=sys.stderr, flush=True)
+        stored = step()
+        adv_stored = ro.adv.clone()
+        steps_per_unit = len(ro.sde_step_ids())
+        step_w = torch.ones(steps_per_unit, dtype=torch.float32, device="cuda")
+
+        def step():  # noqa: F811 -- the timed unit of this workload
+            return ro.grpo_objective(stored, adv_stored, T, cond=Cd, txt_index=tidx, step_w=step_w)
+    elif args.workload == "awm-flux-stack":
+        g = torch.Generator(device="cuda")
+        g.manual_seed(2000 + w.index)
+        t_awm = torch.rand(w.batch, generator=g, device="cuda", dtype=torch.float32)
+        eps_awm = torch.randn(X0.shape, generator=g, device="cuda", dtype=torch.float32).to(dt)
+        adv_awm = torch.randn(w.batch, generator=g, device="cuda", dtype=torch.float32)
+        steps_per_unit = 1
+
+        def step():  # noqa: F811 -- the timed unit of this workload
+            return ro.awm_objective(X0, eps_awm, t_awm, T, adv_awm, cond=Cd, txt_index=tidx)
 
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
@@ -188,7 +214,9 @@ def main() -> int:
                    "hidden": m.hidden, "heads": m.heads, "head_dim": m.head_dim, "mlp_hidden": m.mlp_hidden,
                    "dual_blocks": m.n_dual, "single_blocks": m.n_single, "wan_blocks": m.n_wan,
                    "denoising_steps": len(ro.sigmas), "sde_steps": sum(1 for s in ro.sigmas if s > 0),
-                   "timed_unit": "rollout" if steps_per_unit > 1 else "step",
+                   "timed_unit": {"grpo-flux-stack": "GRPO update forward over a stored rollout",
+                                  "awm-flux-stack": "AWM training forward of the batch"}.get(
+                       args.workload, "rollout" if steps_per_unit > 1 else "step"),
                    "weights": "device-drawn N(0,0.02)" if device_drawn else "host-drawn N(0,0.02), seeded",
                    "t": ro.ts[0], "t_next": ro.ts[1], "sigma": ro.sigmas[0]},
         "latent_tokens_per_s": latent_tok_s,

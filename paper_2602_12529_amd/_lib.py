@@ -1,4 +1,4 @@
-"""ctypes declarations of libff.so (include/ff.h, include/ff_ops.h).
+"""ctypes declarations of libff.so (include/ff.h, include/ff_ops.h, include/ff_loss.h).
 
 Loading fails loudly when the library has not been built: there is no other
 implementation to fall back to.
@@ -64,6 +64,14 @@ _SIGS = {
     "ff_rope_table": (c_int32, [c_void_p, POINTER(c_int32), c_int32, POINTER(c_int32), c_double, c_void_p]),
     "ff_skinny_linear": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_int64, c_int32,
                                    c_int32, c_int32, c_void_p]),
+    "ff_flow_noise": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_int32, c_void_p]),
+    "ff_loss_workspace_size": (c_int32, [c_int64, c_int64, POINTER(c_size_t)]),
+    "ff_awm_loss": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_int32, c_void_p, c_void_p,
+                              c_void_p, c_size_t, c_void_p]),
+    "ff_nft_loss": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_int32, c_void_p,
+                              c_void_p, c_void_p, c_size_t, c_void_p]),
+    "ff_grpo_loss": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_int64, c_int32, c_double, c_void_p,
+                               c_void_p, c_void_p]),
 }
 
 _lib = None

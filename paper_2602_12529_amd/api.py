@@ -88,6 +88,54 @@ def group_advantage(rewards, weights, group_id, n_groups: int, mode: int = 0, ep
     return adv
 
 
+# ------------------------------------------------------------------ objectives that consume the rollout
+def flow_noise(x0, eps, t, xt=None):
+    """x_t = (1 - t) x0 + t eps per sample; t: float32 [B] on the device."""
+    B, D = x0.shape[0], x0[0].numel()
+    if xt is None:
+        xt = torch.empty_like(x0)
+    check(load().ff_flow_noise(_p(x0), _p(eps), _p(t), _p(xt), B, D, dtype_code(x0), _stream()), "ff_flow_noise")
+    return xt
+
+
+def loss_workspace_size(B: int, D: int) -> int:
+    n = c_size_t()
+    check(load().ff_loss_workspace_size(B, D, byref(n)), "ff_loss_workspace_size")
+    return n.value
+
+
+def awm_loss(v, eps, x0, adv, per_sample=None, loss=None, ws=None):
+    """Eq. 3; returns (per_sample float64 [B], loss float64 [1]) on the device."""
+    B, D = v.shape[0], v[0].numel()
+    per_sample = torch.empty(B, dtype=torch.float64, device=v.device) if per_sample is None else per_sample
+    loss = torch.empty(1, dtype=torch.float64, device=v.device) if loss is None else loss
+    ws = workspace(loss_workspace_size(B, D), v.device) if ws is None else ws
+    check(load().ff_awm_loss(_p(v), _p(eps), _p(x0), _p(adv), B, D, dtype_code(v), _p(per_sample), _p(loss), _p(ws),
+                             ws.numel(), _stream()), "ff_awm_loss")
+    return per_sample, loss
+
+
+def nft_loss(v_pos, v_neg, eps, x0, r, per_sample=None, loss=None, ws=None):
+    """Eq. 2; returns (per_sample float64 [B], loss float64 [1]) on the device."""
+    B, D = v_pos.shape[0], v_pos[0].numel()
+    per_sample = torch.empty(B, dtype=torch.float64, device=v_pos.device) if per_sample is None else per_sample
+    loss = torch.empty(1, dtype=torch.float64, device=v_pos.device) if loss is None else loss
+    ws = workspace(loss_workspace_size(B, D), v_pos.device) if ws is None else ws
+    check(load().ff_nft_loss(_p(v_pos), _p(v_neg), _p(eps), _p(x0), _p(r), B, D, dtype_code(v_pos), _p(per_sample),
+                             _p(loss), _p(ws), ws.numel(), _stream()), "ff_nft_loss")
+    return per_sample, loss
+
+
+def grpo_loss(logp_new, logp_old, adv, step_w=None, clip_eps: float = 0.2, loss=None, n_clipped=None):
+    """Clipped ratio objective over float64 [S, B] log-probs; returns (loss float64 [1], n_clipped int32 [1])."""
+    S, B = logp_new.shape
+    loss = torch.empty(1, dtype=torch.float64, device=logp_new.device) if loss is None else loss
+    n_clipped = torch.empty(1, dtype=torch.int32, device=logp_new.device) if n_clipped is None else n_clipped
+    check(load().ff_grpo_loss(_p(logp_new), _p(logp_old), _p(adv), _p(step_w), B, S, clip_eps, _p(loss),
+                              _p(n_clipped), _stream()), "ff_grpo_loss")
+    return loss, n_clipped
+
+
 # ------------------------------------------------------------------ kernel-level ops
 def linear(A, W, bias, out, epi=EPI_BIAS, gelu_from=0, gate=None, gate_ld=0, resid=None, rows_per_sample=0):
     M, K = A.shape

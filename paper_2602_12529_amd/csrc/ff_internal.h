@@ -62,6 +62,15 @@ struct Carver {
 };
 
 // ----------------------------------------------------------------- kernels (launchers)
+// Per-sample streaming passes over [B, D] (SDE step, log-prob, losses): each sample's D
+// elements are cut into `bps` chunks of `chunk` elements (a multiple of 2048), one block
+// each, about 2048 blocks in all; per-block float64 partials are summed in a fixed order.
+struct RowPlan {
+  int64_t bps;     // blocks per sample
+  int64_t chunk;   // elements per block
+};
+RowPlan row_plan(int64_t B, int64_t D);
+
 // All launchers return FF_OK or FF_EHIP and expect validated arguments.
 
 enum Epi : int {

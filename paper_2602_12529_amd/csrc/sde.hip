@@ -20,14 +20,11 @@ namespace {
 
 constexpr int kSdeThreads = 256;
 constexpr int64_t kSdeVec = 8;
-constexpr int64_t kTargetBlocks = 2048;
 
-struct SdePlan {
-  int64_t bps;     // blocks per sample
-  int64_t chunk;   // elements per block (multiple of 8)
-};
+}  // namespace
 
-SdePlan sde_plan(int64_t B, int64_t D) {
+RowPlan row_plan(int64_t B, int64_t D) {
+  constexpr int64_t kTargetBlocks = 2048;
   const int64_t per_pass = kSdeThreads * kSdeVec;
   int64_t want = (kTargetBlocks + B - 1) / B;
   int64_t max_blocks = (D + per_pass - 1) / per_pass;
@@ -38,6 +35,8 @@ SdePlan sde_plan(int64_t B, int64_t D) {
   bps = (D + chunk - 1) / chunk;
   return {bps, chunk};
 }
+
+namespace {
 
 // One element: mean, stored next value, squared residual of the stored value.
 template <bool BF16>
@@ -148,7 +147,7 @@ template <int MODE>
 int launch_sde(int dtype, const void* x, const void* v, const void* third, void* x_next, double* logp,
                int64_t B, int64_t D, float a, float b, float c, double inv_2var, double cst,
                void* ws, hipStream_t s) {
-  SdePlan p = sde_plan(B, D);
+  RowPlan p = row_plan(B, D);
   dim3 grid(static_cast<unsigned>(p.bps), static_cast<unsigned>(B));
   double* partial = static_cast<double*>(ws);
   const bool vec = (D % kSdeVec) == 0;
@@ -200,7 +199,7 @@ int check_sde_args(const char* fn, const void* x, const void* v, const void* thi
 
 int check_ws(const char* fn, int64_t B, int64_t D, bool need, const void* ws, size_t ws_bytes) {
   if (!need) return FF_OK;
-  size_t want = static_cast<size_t>(B) * sde_plan(B, D).bps * sizeof(double);
+  size_t want = static_cast<size_t>(B) * row_plan(B, D).bps * sizeof(double);
   if (!ws || ws_bytes < want)
     return fail(FF_EWORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, want, ws ? ws_bytes : 0);
   if (!aligned16(ws)) return fail(FF_EINVAL, "%s: workspace must be 16-byte aligned", fn);
@@ -241,7 +240,7 @@ extern "C" {
 int ff_sde_workspace_size(int64_t B, int64_t D, size_t* bytes) {
   if (!bytes) return fail(FF_EINVAL, "ff_sde_workspace_size: null output");
   if (B < 0 || D < 0) return fail(FF_EINVAL, "ff_sde_workspace_size: negative shape");
-  *bytes = (B == 0 || D == 0) ? 0 : static_cast<size_t>(B) * sde_plan(B, D).bps * sizeof(double);
+  *bytes = (B == 0 || D == 0) ? 0 : static_cast<size_t>(B) * row_plan(B, D).bps * sizeof(double);
   return FF_OK;
 }
 

@@ -1,10 +1,13 @@
-"""The K-step Flow-GRPO rollout driven through the C ABI (Sec. 3.1).
+"""The K-step Flow-GRPO rollout driven through the C ABI (Sec. 3.1), and the
+objectives that consume it (Sec. 3.1, 3.2).
 
 Host side: the uniform time grid t_k = 1 - k/K, the sigma schedule of Table 1
 (Flow-SDE with its t = 1 singularity evaluated with 1 - t_1, Dance-SDE, or
 ODE) and the MixGRPO step mask.  Device side (all in libff.so): the DiT
 velocity, the SDE step with its per-sample log-probability, the group
-advantages.
+advantages; for training, the log-probabilities of a stored trajectory under
+the current weights with the clipped-ratio GRPO objective, and the noised
+forward pass with the AWM loss (Eq. 3).
 """
 from __future__ import annotations
 
@@ -109,6 +112,45 @@ class Rollout:
             xs.append(x_next)
             x = x_next
         return RolloutResult(xs=xs, vs=vs, logp=logp, ts=list(self.ts), sigmas=list(self.sigmas))
+
+    def sde_step_ids(self) -> List[int]:
+        return [k for k, s in enumerate(self.sigmas) if s > 0.0]
+
+    def policy_logprobs(self, res: RolloutResult, txt, cond=None, txt_index=None, txt_out=None, out=None):
+        """Log-probabilities of the stored SDE transitions x_k -> x_{k+1} under the current weights:
+        a DiT forward at each stored x_k, then ff_logprob of the stored x_{k+1}.  Returns float64
+        [S, B] in SDE-step order."""
+        w, m = self.w, self.w.model
+        steps = self.sde_step_ids()
+        if out is None:
+            out = torch.empty((len(steps), w.batch), dtype=torch.float64, device=self.device)
+        for i, k in enumerate(steps):
+            x = res.xs[k]
+            v = torch.empty(self.shape, dtype=self.dt, device=self.device)
+            if m.io_mode == C.IO_LATENT:
+                self.dit.forward(x, txt, w.grid, v, t=self.t_steps[k], cond=cond, txt_index=txt_index, ws=self.ws_dit)
+            else:
+                self.dit.forward(x, txt, w.grid, v, cond=cond, txt_out=txt_out, ws=self.ws_dit)
+            api.logprob(x, v, res.xs[k + 1], out[i], self.ts[k], self.ts[k + 1], self.sigmas[k], ws=self.ws_sde)
+        return out
+
+    def grpo_objective(self, res: RolloutResult, adv, txt, cond=None, txt_index=None, txt_out=None, step_w=None,
+                       clip_eps: float = 0.2):
+        """Clipped-ratio GRPO objective of a stored rollout: (loss float64 [1], clipped count int32 [1])."""
+        new = self.policy_logprobs(res, txt, cond=cond, txt_index=txt_index, txt_out=txt_out)
+        old = torch.stack([res.logp[k] for k in self.sde_step_ids()])
+        return api.grpo_loss(new, old, adv, step_w, clip_eps)
+
+    def awm_objective(self, x0, eps, t, txt, adv, cond=None, txt_index=None):
+        """AWM (Eq. 3) on clean latents x0 noised to x_t = (1 - t) x0 + t eps at per-sample times t
+        (float32 [B] on the device): (per-sample float64 [B], loss float64 [1])."""
+        w, m = self.w, self.w.model
+        if m.io_mode != C.IO_LATENT:
+            raise ValueError("the AWM objective needs a latent-space model")
+        xt = api.flow_noise(x0, eps, t)
+        v = torch.empty(self.shape, dtype=self.dt, device=self.device)
+        self.dit.forward(xt, txt, w.grid, v, t=t, cond=cond, txt_index=txt_index, ws=self.ws_dit)
+        return api.awm_loss(v, eps, x0, adv)
 
     def advantages(self, rewards, weights=None, mode: int = 0, eps: float = 1e-4):
         if weights is None:

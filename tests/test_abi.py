@@ -17,7 +17,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 def declared_symbols():
     names = set()
-    for h in ("ff.h", "ff_ops.h"):
+    for h in ("ff.h", "ff_ops.h", "ff_loss.h"):
         text = open(os.path.join(ROOT, "include", h)).read()
         names |= set(re.findall(r"^\s*(?:int|const char\*)\s+(ff_\w+)\s*\(", text, re.M))
     return names
@@ -66,6 +66,35 @@ def test_sde_argument_validation():
     n = c_size_t()
     assert lib.ff_sde_workspace_size(8, 12582912, byref(n)) == 0 and n.value >= 8 * 8
     assert lib.ff_sde_workspace_size(0, 5, byref(n)) == 0 and n.value == 0
+
+
+def test_loss_argument_validation():
+    """Host-side checks of the objectives: every rejected call returns before any launch."""
+    lib = _lib.load()
+    f = c_void_p(8192)
+    ws = c_void_p(1 << 20)
+    n = c_size_t()
+    assert lib.ff_loss_workspace_size(4, 1000, byref(n)) == 0 and n.value >= 4 * 8
+    _err(lib.ff_loss_workspace_size(-1, 8, byref(n)), _lib.FF_EINVAL)
+    # noising: bad dtype, null, aliasing output, misaligned
+    _err(lib.ff_flow_noise(f, f, f, c_void_p(16384), 2, 8, 5, None), _lib.FF_EINVAL)
+    _err(lib.ff_flow_noise(None, f, f, c_void_p(16384), 2, 8, 1, None), _lib.FF_EINVAL)
+    _err(lib.ff_flow_noise(f, c_void_p(16384), f, c_void_p(16384), 2, 8, 1, None), _lib.FF_EINVAL)
+    _err(lib.ff_flow_noise(c_void_p(8194), f, f, c_void_p(16384), 2, 8, 1, None), _lib.FF_EINVAL)
+    _err(lib.ff_flow_noise(f, f, f, c_void_p(16384), 70000, 8, 1, None), _lib.FF_EUNSUPPORTED)
+    # matching losses: workspace, null loss, null v_neg
+    _err(lib.ff_awm_loss(f, f, f, f, 4, 1000, 1, None, f, None, 0, None), _lib.FF_EWORKSPACE)
+    _err(lib.ff_awm_loss(f, f, f, f, 4, 1000, 1, None, f, ws, 8, None), _lib.FF_EWORKSPACE)
+    _err(lib.ff_awm_loss(f, f, f, f, 4, 1000, 1, None, None, ws, 1 << 20, None), _lib.FF_EINVAL)
+    _err(lib.ff_nft_loss(f, None, f, f, f, 4, 1000, 1, None, f, ws, 1 << 20, None), _lib.FF_EINVAL)
+    _err(lib.ff_nft_loss(f, f, f, f, f, 4, 1000, 9, None, f, ws, 1 << 20, None), _lib.FF_EINVAL)
+    assert lib.ff_awm_loss(f, f, f, f, 0, 1000, 1, None, f, None, 0, None) == 0   # empty batch: no-op
+    # GRPO objective: clip range, sizes, nulls
+    _err(lib.ff_grpo_loss(f, f, f, None, 8, 3, 0.0, f, None, None), _lib.FF_EDOMAIN)
+    _err(lib.ff_grpo_loss(f, f, f, None, 8, 3, float("nan"), f, None, None), _lib.FF_EDOMAIN)
+    _err(lib.ff_grpo_loss(f, f, f, None, 0, 3, 0.2, f, None, None), _lib.FF_EINVAL)
+    _err(lib.ff_grpo_loss(f, f, f, None, 40000, 3, 0.2, f, None, None), _lib.FF_EUNSUPPORTED)
+    _err(lib.ff_grpo_loss(None, f, f, None, 8, 3, 0.2, f, None, None), _lib.FF_EINVAL)
 
 
 def test_advantage_argument_validation():

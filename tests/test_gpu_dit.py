@@ -14,6 +14,7 @@ import pytest
 import torch
 
 from oracle import dit as odit
+from oracle import losses as olosses
 from oracle import rollout as orollout
 from oracle import sde as osde
 from paper_2602_12529_amd import api
@@ -124,6 +125,96 @@ def test_bf16_latent_with_single_blocks_and_pooled(gpu_lib):
         assert rel(host(res.xs[k + 1]), xn_ref) <= TOL[C.BF16]
         lp_ref = osde.step_log_prob(xk, host(res.vs[k]), host(res.xs[k + 1]), res.ts[k], res.ts[k + 1], res.sigmas[k])
         assert np.max(np.abs(host(res.logp[k]) - lp_ref)) <= LOGP_ABS
+
+
+def _small_latent_stack():
+    m = C.ModelConfig(model=C.MODEL_MMDIT, io_mode=C.IO_LATENT, dtype=C.BF16, n_dual=1, n_single=1, hidden=256,
+                      heads=2, head_dim=128, mlp_hidden=512, in_channels=64, txt_dim=128, pooled_dim=64,
+                      rope_axes=(16, 56, 56))
+    return C.Workload(name="small-latent-grpo", index=16, model=m, prompts=2, group=2, grid=(1, 4, 8), n_txt=16,
+                      steps=3, sde_steps=(0, 2))
+
+
+def test_grpo_policy_update_forward(gpu_lib):
+    """The GRPO update forward on a stored rollout (MixGRPO steps {0, 2}): recomputed with the
+    rollout's own weights every log-prob is bitwise the stored one (ratio 1, nothing clipped,
+    loss = -mean A).  With perturbed weights, per SDE step the recomputed velocity matches the
+    oracle's at the stored latent, the log-prob matches the oracle's density of the stored next
+    latent given that velocity (teacher-forced, as in the rollout tests), the driver's output is
+    bitwise the explicit forward + ff_logprob, and the objective matches the oracle's on those
+    log-probs."""
+    w = _small_latent_stack()
+    m = w.model
+    W, txt, cond, x0, eps = _inputs(w)
+    Wd, T, Cd, X0, E = _device(w, W, txt, cond, x0, eps)
+    tidx = torch.from_numpy(synth.txt_index(w)).cuda()
+    ro = R.Rollout(w, api.Dit(m, Wd))
+    res = ro.run(X0, T, E, cond=Cd, txt_index=tidx)
+    adv = torch.from_numpy(np.array([0.5, -1.5, 1.0, 0.25], dtype=np.float32)).cuda()
+    loss, n = ro.grpo_objective(res, adv, T, cond=Cd, txt_index=tidx)
+    torch.cuda.synchronize()
+    assert int(n.cpu()[0]) == 0
+    assert host(loss)[0] == pytest.approx(-float(np.mean(host(adv))), rel=1e-12)
+    # a slightly different policy
+    W2 = {k: synth.bf16_round((v + synth.normal(500 + i, v.shape, C.F32, 0.002)).astype(np.float32))
+          for i, (k, v) in enumerate(W.items())}
+    ro2 = R.Rollout(w, api.Dit(m, {k: dev(v, C.BF16) for k, v in W2.items()}))
+    step_w = torch.from_numpy(np.array([1.5, 0.5], dtype=np.float32)).cuda()
+    new = ro2.policy_logprobs(res, T, cond=Cd, txt_index=tidx)
+    loss2, n2 = gpu_lib.grpo_loss(new, torch.stack([res.logp[k] for k in ro2.sde_step_ids()]), adv, step_w, 0.2)
+    torch.cuda.synchronize()
+    lp_new = host(new)
+    for i, k in enumerate(ro2.sde_step_ids()):
+        v = torch.empty_like(res.xs[k])
+        ro2.dit.forward(res.xs[k], T, w.grid, v, t=ro2.t_steps[k], cond=Cd, txt_index=tidx)
+        lp = torch.empty(w.batch, dtype=torch.float64, device="cuda")
+        gpu_lib.logprob(res.xs[k], v, res.xs[k + 1], lp, res.ts[k], res.ts[k + 1], res.sigmas[k])
+        torch.cuda.synchronize()
+        assert torch.equal(lp, new[i])
+        xk, xk1 = host(res.xs[k]), host(res.xs[k + 1])
+        v_ref = odit.forward(m, W2, xk, txt, t=np.full(w.batch, res.ts[k]), cond=cond,
+                             txt_index=synth.txt_index(w), grid=w.grid)
+        say("step", k, "rel v", rel(host(v), v_ref))
+        assert rel(host(v), v_ref) <= TOL[C.BF16]
+        lp_ref = osde.step_log_prob(xk, host(v), xk1, res.ts[k], res.ts[k + 1], res.sigmas[k])
+        assert np.max(np.abs(lp_new[i] - lp_ref)) <= LOGP_ABS
+    old = np.stack([host(res.logp[k]) for k in ro2.sde_step_ids()])
+    ref_loss, ref_n = olosses.grpo_loss(lp_new, old, host(adv), host(step_w), 0.2)
+    assert host(loss2)[0] == pytest.approx(ref_loss, rel=1e-12, abs=1e-15)
+    assert int(n2.cpu()[0]) == ref_n
+
+
+def test_awm_training_forward(gpu_lib):
+    """AWM (Eq. 3) through the model: noising, the DiT forward at per-sample t, the loss; each
+    stage against the oracle on the GPU's stored inputs, and the fused driver bit-equal to the
+    staged calls."""
+    w = _small_latent_stack()
+    m = w.model
+    W, txt, cond, x0, eps = _inputs(w)
+    Wd, T, Cd, X0, E = _device(w, W, txt, cond, x0, eps)
+    tidx = torch.from_numpy(synth.txt_index(w)).cuda()
+    ro = R.Rollout(w, api.Dit(m, Wd))
+    e = synth.normal(600, x0.shape, C.BF16)
+    Ed = dev(e, C.BF16)
+    t = np.array([0.1, 0.4, 0.7, 0.95], dtype=np.float32)
+    Td = torch.from_numpy(t).cuda()
+    adv = np.array([1.0, -0.5, 2.0, 0.0], dtype=np.float32)
+    Ad = torch.from_numpy(adv).cuda()
+    per, loss = ro.awm_objective(X0, Ed, Td, T, Ad, cond=Cd, txt_index=tidx)
+    xt = gpu_lib.flow_noise(X0, Ed, Td)
+    v = torch.empty_like(X0)
+    ro.dit.forward(xt, T, w.grid, v, t=Td, cond=Cd, txt_index=tidx)
+    per2, loss2 = gpu_lib.awm_loss(v, Ed, X0, Ad)
+    torch.cuda.synchronize()
+    assert torch.equal(per, per2) and torch.equal(loss, loss2)
+    assert rel(host(xt), olosses.flow_noise(x0, e, t.astype(np.float64))) <= TOL[C.BF16]
+    v_ref = odit.forward(m, W, host(xt), txt, t=t.astype(np.float64), cond=cond, txt_index=synth.txt_index(w),
+                         grid=w.grid)
+    say("awm v rel", rel(host(v), v_ref))
+    assert rel(host(v), v_ref) <= TOL[C.BF16]
+    ref_per, ref_loss = olosses.awm_loss(host(v), e, x0, adv)
+    np.testing.assert_allclose(host(per), ref_per, rtol=1e-5, atol=1e-9)
+    assert host(loss)[0] == pytest.approx(ref_loss, rel=1e-5)
 
 
 @pytest.mark.timeout(900)
