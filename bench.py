@@ -275,7 +275,7 @@ def cpu_baseline(w, W, txt, cond, x0, eps, n_samples: int):
     tidx = synth.txt_index(w)[:n]
     for k in range(len(ts) - 1):
         t, tn = ts[k], ts[k + 1]
-        sigma = (w.eta * math.sqrt(t / (1 - t))) if w.fixed_step else R.sigma_schedule(ts, w.eta, "flow", w.sde_steps)[k]
+        sigma = (w.eta * math.sqrt(t / (1 - t))) if w.fixed_step else R.sigma_schedule(ts, w.eta, w.dynamics, w.sde_steps)[k]
         if m.io_mode == C.IO_HIDDEN:
             v, _ = odit.forward(m, W, x, txt[:n], cond=cond[:n], grid=w.grid)
         else:

@@ -69,6 +69,7 @@ class Workload:
     steps: int                      # K
     eta: float = 0.7
     sde_steps: Optional[Tuple[int, ...]] = None   # 0-indexed SDE steps; None = all
+    dynamics: str = "flow"          # sigma schedule of Table 1: "flow" (Flow-SDE), "dance" (Dance-SDE), "ode"
     reward_kind: str = "uniform"    # "uniform" U(0,1) or "normal" N(0,1)
     n_rewards: int = 1
     # A single fixed step (t, t_next) instead of the uniform grid (one-block workloads).

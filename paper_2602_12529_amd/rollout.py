@@ -76,7 +76,7 @@ class Rollout:
             self.ts = [w.fixed_step[0], w.fixed_step[1]]
         else:
             self.ts = time_grid(w.steps)
-        self.sigmas = sigma_schedule(self.ts, w.eta, "flow", w.sde_steps)
+        self.sigmas = sigma_schedule(self.ts, w.eta, w.dynamics, w.sde_steps)
         if w.fixed_step is not None:
             t, tn = w.fixed_step
             self.sigmas = [w.eta * math.sqrt(t / (1.0 - t))]

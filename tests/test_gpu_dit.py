@@ -74,6 +74,28 @@ def test_tiny_rollout_end_to_end(gpu_lib):
     assert counts.cpu().tolist() == ref_cnt.tolist()
 
 
+def test_tiny_rollout_dance_sde_and_mixgrpo(gpu_lib):
+    """The tiny workload with Dance-SDE (sigma = eta on every SDE step, Table 1) on steps {1, 3} and ODE
+    steps elsewhere (MixGRPO): the whole rollout against the oracle, log-probs only on SDE steps."""
+    w = C.Workload(**{**C.TINY.__dict__, "name": "tiny-dance-mix", "dynamics": "dance", "sde_steps": (1, 3)})
+    m = w.model
+    W, txt, cond, x0, eps = _inputs(w)
+    Wd, T, Cd, X0, E = _device(w, W, txt, cond, x0, eps)
+    ro = R.Rollout(w, api.Dit(m, Wd))
+    tidx = torch.from_numpy(synth.txt_index(w)).cuda()
+    res = ro.run(X0, T, E, cond=Cd, txt_index=tidx)
+    torch.cuda.synchronize()
+    ref = orollout.rollout(m, W, x0, txt, eps, w.steps, w.eta, sde_steps=w.sde_steps, txt_index=synth.txt_index(w),
+                           grid=w.grid, sigma_kind="dance")
+    assert res.sigmas == pytest.approx(list(ref["sigmas"]), rel=1e-15)
+    assert res.sigmas == [0.0, w.eta, 0.0, w.eta]
+    assert sorted(res.logp) == sorted(ref["logp"]) == [1, 3]
+    for k in range(w.steps):
+        assert rel(host(res.xs[k + 1]), ref["xs"][k + 1]) <= TOL[C.F32]
+    for k in (1, 3):
+        assert np.max(np.abs(host(res.logp[k]) - ref["logp"][k])) <= LOGP_ABS
+
+
 def _small_hidden():
     m = C.ModelConfig(model=C.MODEL_MMDIT, io_mode=C.IO_HIDDEN, dtype=C.BF16, n_dual=1, hidden=256, heads=2,
                       head_dim=128, mlp_hidden=1024, in_channels=64, txt_dim=256, rope_axes=(16, 56, 56))
