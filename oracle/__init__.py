@@ -20,5 +20,7 @@ Modules:
   losses     -- the objectives that consume the rollout: forward noising and
                 the AWM (Eq. 3) and DiffusionNFT (Eq. 2) losses, the clipped
                 GRPO ratio surrogate on stored trajectories
+  noise      -- counter-based Gaussian noise for the SDE step (Philox4x32-10
+                with Box-Muller)
 """
-from . import advantage, dit, losses, rollout, sde  # noqa: F401
+from . import advantage, dit, losses, noise, rollout, sde  # noqa: F401
