@@ -59,6 +59,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--workload", default="flux-block", choices=list(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--noise", default="stored", choices=["stored", "philox"],
+                    help="read each step's noise from HBM (default) or draw it in the SDE kernel")
     ap.add_argument("--cpu-samples", type=int, default=3, help="samples of the batch the oracle times")
     return ap.parse_args()
 
@@ -106,7 +108,7 @@ def main() -> int:
     rewards = torch.from_numpy(synth.rewards(w)).cuda()
     tidx = torch.from_numpy(synth.txt_index(w)).cuda() if m.io_mode == C.IO_LATENT else None
     dit = api.Dit(m, Wd)
-    ro = R.Rollout(w, dit, keep_velocities=False)
+    ro = R.Rollout(w, dit, keep_velocities=False, noise_seed=(3000 + w.index) if args.noise == "philox" else None)
     txt_out = torch.empty_like(T) if m.io_mode == C.IO_HIDDEN else None
     steps_per_unit = len(ro.sigmas)     # denoising steps in one timed unit (a rollout, or the one step)
 
@@ -218,6 +220,7 @@ def main() -> int:
                                   "awm-flux-stack": "AWM training forward of the batch"}.get(
                        args.workload, "rollout" if steps_per_unit > 1 else "step"),
                    "weights": "device-drawn N(0,0.02)" if device_drawn else "host-drawn N(0,0.02), seeded",
+                   "noise": "Philox4x32-10 in the SDE kernel" if args.noise == "philox" else "stored eps tensors",
                    "t": ro.ts[0], "t_next": ro.ts[1], "sigma": ro.sigmas[0]},
         "latent_tokens_per_s": latent_tok_s,
         "sample_steps_per_s": steps_per_s * w.batch,

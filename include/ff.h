@@ -90,6 +90,28 @@ int ff_logprob(const void* x, const void* v, const void* x_next, double* logp,
                int64_t B, int64_t D, double t, double t_next, double sigma, int32_t dtype,
                void* workspace, size_t ws_bytes, void* stream);
 
+/* The SDE step with the noise drawn on the device instead of read from memory
+ * (Sec. 3.1: eps ~ N(0, I)), from the counter-based generator Philox4x32-10
+ * (Salmon et al., SC 2011): element d of sample b takes word d % 4 of the block
+ * with counter (d / 4 low word, d / 4 high word, b, step) under the key
+ * (seed low, seed high), and each pair of words gives two normals by the
+ * Box-Muller transform with u = (w + 1/2) 2^-32 (float32).  Same arguments,
+ * domain, logp semantics and workspace as ff_sde_step; x_next may not alias
+ * x or v.  The step reads 2 tensors and writes 1 instead of reading 3. */
+int ff_sde_step_philox(const void* x, const void* v, void* x_next, double* logp, int64_t B, int64_t D,
+                       double t, double t_next, double sigma, uint64_t seed, uint32_t step, int32_t dtype,
+                       void* workspace, size_t ws_bytes, void* stream);
+
+/* The noise ff_sde_step_philox uses, materialised: eps device [B, D] of dtype. */
+int ff_philox_normal(void* eps, int64_t B, int64_t D, uint64_t seed, uint32_t step, int32_t dtype,
+                     void* stream);
+
+/* Raw Philox4x32-10 words: out device uint32 [n, 4], block i with counter
+ * ((ctr_base + i) low word, (ctr_base + i) high word, c2, c3) and key (key low,
+ * key high).  For checking the generator against its known-answer vectors. */
+int ff_philox4x32(uint32_t* out, int64_t n, uint64_t ctr_base, uint32_t c2, uint32_t c3, uint64_t key,
+                  void* stream);
+
 /* ------------------------------------------------------------------------
  * Group-normalised advantages with multi-reward aggregation (Sec. 2.3)
  *

@@ -8,7 +8,7 @@ from __future__ import annotations
 import ctypes
 import os
 import threading
-from ctypes import POINTER, c_char_p, c_double, c_float, c_int32, c_int64, c_size_t, c_void_p
+from ctypes import POINTER, c_char_p, c_double, c_float, c_int32, c_int64, c_size_t, c_uint32, c_uint64, c_void_p
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libff.so")
@@ -37,6 +37,10 @@ _SIGS = {
                               c_double, c_double, c_int32, c_void_p, c_size_t, c_void_p]),
     "ff_logprob": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_double, c_double,
                              c_double, c_int32, c_void_p, c_size_t, c_void_p]),
+    "ff_sde_step_philox": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_double, c_double,
+                                     c_double, c_uint64, c_uint32, c_int32, c_void_p, c_size_t, c_void_p]),
+    "ff_philox_normal": (c_int32, [c_void_p, c_int64, c_int64, c_uint64, c_uint32, c_int32, c_void_p]),
+    "ff_philox4x32": (c_int32, [c_void_p, c_int64, c_uint64, c_uint32, c_uint32, c_uint64, c_void_p]),
     "ff_group_advantage": (c_int32, [c_void_p, c_void_p, c_void_p, c_int64, c_int32, c_int32, c_int32, c_float,
                                      c_void_p, c_void_p, c_void_p]),
     "ff_dit_num_tensors": (c_int32, [POINTER(DitConfig), POINTER(c_int64)]),

@@ -77,6 +77,31 @@ def logprob(x, v, x_next, logp, t: float, t_next: float, sigma: float, ws=None):
                             ws.numel(), _stream()), "ff_logprob")
 
 
+def sde_step_philox(x, v, x_next, t: float, t_next: float, sigma: float, seed: int, step: int, logp=None, ws=None):
+    """The SDE step with its noise drawn on the device (Philox4x32-10, Box-Muller)."""
+    B, D = x.shape[0], x[0].numel()
+    if ws is None and logp is not None:
+        ws = workspace(sde_workspace_size(B, D), x.device)
+    check(load().ff_sde_step_philox(_p(x), _p(v), _p(x_next), _p(logp), B, D, t, t_next, sigma, seed, step,
+                                    dtype_code(x), _p(ws), ws.numel() if ws is not None else 0, _stream()),
+          "ff_sde_step_philox")
+
+
+def philox_normal(shape, seed: int, step: int, dtype=torch.float32, device="cuda"):
+    """The noise of ff_sde_step_philox for a [B, ...] latent, materialised."""
+    out = torch.empty(shape, dtype=dtype, device=device)
+    B, D = out.shape[0], out[0].numel()
+    check(load().ff_philox_normal(_p(out), B, D, seed, step, dtype_code(out), _stream()), "ff_philox_normal")
+    return out
+
+
+def philox4x32(n: int, ctr_base: int, c2: int, c3: int, key: int, device="cuda"):
+    """Raw Philox4x32-10 words, int32 tensor [n, 4] holding the uint32 bit patterns."""
+    out = torch.empty((n, 4), dtype=torch.int32, device=device)
+    check(load().ff_philox4x32(_p(out), n, ctr_base, c2, c3, key, _stream()), "ff_philox4x32")
+    return out
+
+
 def group_advantage(rewards, weights, group_id, n_groups: int, mode: int = 0, eps: float = 1e-4, adv=None,
                     counts=None):
     N = rewards.shape[0]

@@ -38,6 +38,76 @@ RowPlan row_plan(int64_t B, int64_t D) {
 
 namespace {
 
+// Counter-based noise: Philox4x32-10 (Salmon et al., SC 2011) from its definition -- ten
+// rounds of two 32x32 -> 64-bit products by 0xD2511F53 and 0xCD9E8D57 recombined with the
+// other words and the round key, the key advancing by (0x9E3779B9, 0xBB67AE85) -- and the
+// Box-Muller transform with u = (w + 1/2) 2^-32 in float32.  Element d of sample b in SDE
+// step `step` is word d % 4 of the block with counter (d / 4 low, d / 4 high, b, step).
+struct Ctr4 {
+  uint32_t x, y, z, w;
+};
+__device__ __forceinline__ Ctr4 philox4x32_10(Ctr4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c.x), lo0 = 0xD2511F53u * c.x;
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c.z), lo1 = 0xCD9E8D57u * c.z;
+    c = {hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0};
+  }
+  return c;
+}
+// Box-Muller with the hardware transcendentals: v_log_f32 (log2) and v_sin_f32 / v_cos_f32,
+// which take their angle in revolutions, so sin(2 pi u) is one instruction for u in (0, 1].
+__device__ __forceinline__ void box_muller4(Ctr4 w, float* z) {
+  constexpr float kInv32 = 2.3283064365386963e-10f;    // 2^-32
+  constexpr float kM2Ln2 = -1.3862943611198906f;       // -2 ln 2: -2 ln u = kM2Ln2 log2 u
+  const float u0 = (static_cast<float>(w.x) + 0.5f) * kInv32, u1 = (static_cast<float>(w.y) + 0.5f) * kInv32;
+  const float u2 = (static_cast<float>(w.z) + 0.5f) * kInv32, u3 = (static_cast<float>(w.w) + 0.5f) * kInv32;
+  const float r0 = __builtin_amdgcn_sqrtf(kM2Ln2 * __builtin_amdgcn_logf(u0));
+  const float r1 = __builtin_amdgcn_sqrtf(kM2Ln2 * __builtin_amdgcn_logf(u2));
+  z[0] = r0 * __builtin_amdgcn_cosf(u1);
+  z[1] = r0 * __builtin_amdgcn_sinf(u1);
+  z[2] = r1 * __builtin_amdgcn_cosf(u3);
+  z[3] = r1 * __builtin_amdgcn_sinf(u3);
+}
+struct NoiseKey {
+  uint32_t k0, k1, step;
+};
+// The four normals of Philox block n of sample b.
+__device__ __forceinline__ void noise4(const NoiseKey& nk, uint32_t b, int64_t n, float* z) {
+  const Ctr4 c{static_cast<uint32_t>(n), static_cast<uint32_t>(static_cast<uint64_t>(n) >> 32), b, nk.step};
+  box_muller4(philox4x32_10(c, nk.k0, nk.k1), z);
+}
+
+// eps[b, d] of one SDE step, stored in the tensor's dtype.
+template <bool BF16>
+__global__ __launch_bounds__(256) void philox_normal_kernel(void* __restrict__ out, int64_t D, NoiseKey nk) {
+  const int64_t b = blockIdx.y, nb = (D + 3) / 4;
+  for (int64_t n = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; n < nb; n += static_cast<int64_t>(gridDim.x) * 256) {
+    float z[4];
+    noise4(nk, static_cast<uint32_t>(b), n, z);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (4 * n + j < D) st1<BF16>(out, b * D + 4 * n + j, z[j]);
+  }
+}
+
+// Raw Philox words: block i has counter (base + i low, base + i high, c2, c3).
+__global__ __launch_bounds__(256) void philox_words_kernel(uint32_t* __restrict__ out, int64_t n, uint64_t base,
+                                                           uint32_t c2, uint32_t c3, uint32_t k0, uint32_t k1) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n; i += static_cast<int64_t>(gridDim.x) * 256) {
+    const uint64_t ctr = base + static_cast<uint64_t>(i);
+    const Ctr4 w = philox4x32_10({static_cast<uint32_t>(ctr), static_cast<uint32_t>(ctr >> 32), c2, c3}, k0, k1);
+    out[4 * i] = w.x;
+    out[4 * i + 1] = w.y;
+    out[4 * i + 2] = w.z;
+    out[4 * i + 3] = w.w;
+  }
+}
+
 // One element: mean, stored next value, squared residual of the stored value.
 template <bool BF16>
 __device__ __forceinline__ float sde_elem(float x, float v, float e, float a, float b, float c,
@@ -49,12 +119,13 @@ __device__ __forceinline__ float sde_elem(float x, float v, float e, float a, fl
   return r * r;
 }
 
-// MODE 0: SDE step (third = eps, writes x_next); MODE 1: log-prob only (third = x_next).
+// MODE 0: SDE step (third = eps, writes x_next); MODE 1: log-prob only (third = x_next);
+// MODE 2: SDE step with the noise generated from `nk` (third unused).
 template <bool BF16, int MODE, bool LOGP, bool VEC>
 __global__ __launch_bounds__(kSdeThreads) void sde_kernel(
     const void* __restrict__ x, const void* __restrict__ v, const void* __restrict__ third,
     void* __restrict__ x_next, double* __restrict__ partial, int64_t D, int64_t chunk, float a,
-    float b, float c) {
+    float b, float c, NoiseKey nk) {
 #pragma clang fp contract(off)
   const int64_t base = static_cast<int64_t>(blockIdx.y) * D;
   const int64_t start = static_cast<int64_t>(blockIdx.x) * chunk;
@@ -70,11 +141,20 @@ __global__ __launch_bounds__(kSdeThreads) void sde_kernel(
       float xv[2][8], vv[2][8], tv[2][8], out[8];
       ld8<BF16>(x, base + i, xv[0]);
       ld8<BF16>(v, base + i, vv[0]);
-      ld8<BF16>(third, base + i, tv[0]);
+      if constexpr (MODE != 2) ld8<BF16>(third, base + i, tv[0]);
       if (two) {
         ld8<BF16>(x, base + i2, xv[1]);
         ld8<BF16>(v, base + i2, vv[1]);
-        ld8<BF16>(third, base + i2, tv[1]);
+        if constexpr (MODE != 2) ld8<BF16>(third, base + i2, tv[1]);
+      }
+      if constexpr (MODE == 2) {
+        // i and i2 are multiples of 8 within the sample: two whole Philox blocks each
+        noise4(nk, blockIdx.y, i >> 2, tv[0]);
+        noise4(nk, blockIdx.y, (i >> 2) + 1, tv[0] + 4);
+        if (two) {
+          noise4(nk, blockIdx.y, i2 >> 2, tv[1]);
+          noise4(nk, blockIdx.y, (i2 >> 2) + 1, tv[1] + 4);
+        }
       }
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
@@ -82,7 +162,7 @@ __global__ __launch_bounds__(kSdeThreads) void sde_kernel(
         float part = 0.f;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          if constexpr (MODE == 0) {
+          if constexpr (MODE != 1) {
             float r2 = sde_elem<BF16>(xv[h][j], vv[h][j], tv[h][j], a, b, c, out[j]);
             part = part + r2;
           } else {
@@ -91,15 +171,22 @@ __global__ __launch_bounds__(kSdeThreads) void sde_kernel(
             part = part + r * r;
           }
         }
-        if constexpr (MODE == 0) st8<BF16>(x_next, base + (h == 0 ? i : i2), out);
+        if constexpr (MODE != 1) st8<BF16>(x_next, base + (h == 0 ? i : i2), out);
         if constexpr (LOGP) acc += static_cast<double>(part);
       }
     }
   } else {
     for (int64_t i = start + threadIdx.x; i < end; i += kSdeThreads) {
-      float xv = ld1<BF16>(x, base + i), vv = ld1<BF16>(v, base + i), tv = ld1<BF16>(third, base + i);
+      float xv = ld1<BF16>(x, base + i), vv = ld1<BF16>(v, base + i), tv;
+      if constexpr (MODE == 2) {
+        float z[4];
+        noise4(nk, blockIdx.y, i >> 2, z);
+        tv = z[i & 3];
+      } else {
+        tv = ld1<BF16>(third, base + i);
+      }
       float r2;
-      if constexpr (MODE == 0) {
+      if constexpr (MODE != 1) {
         float out;
         r2 = sde_elem<BF16>(xv, vv, tv, a, b, c, out);
         st1<BF16>(x_next, base + i, out);
@@ -146,7 +233,7 @@ __global__ __launch_bounds__(256) void logp_finalize(const double* __restrict__ 
 template <int MODE>
 int launch_sde(int dtype, const void* x, const void* v, const void* third, void* x_next, double* logp,
                int64_t B, int64_t D, float a, float b, float c, double inv_2var, double cst,
-               void* ws, hipStream_t s) {
+               void* ws, hipStream_t s, NoiseKey nk = {0, 0, 0}) {
   RowPlan p = row_plan(B, D);
   dim3 grid(static_cast<unsigned>(p.bps), static_cast<unsigned>(B));
   double* partial = static_cast<double*>(ws);
@@ -155,10 +242,10 @@ int launch_sde(int dtype, const void* x, const void* v, const void* third, void*
   const double esz = static_cast<double>(dtype_size(dtype));
   const double bytes = static_cast<double>(B) * D * esz * (MODE == 0 ? 4.0 : 3.0);
   {
-    LaunchScope ls(MODE == 0 ? "sde_step" : "logprob", s, 0.0, bytes);
+    LaunchScope ls(MODE == 0 ? "sde_step" : (MODE == 2 ? "sde_step_philox" : "logprob"), s, 0.0, bytes);
 #define FF_SDE_LAUNCH(BF, LP, VC)                                                                 \
   hipLaunchKernelGGL((sde_kernel<BF, MODE, LP, VC>), grid, dim3(kSdeThreads), 0, s, x, v, third, \
-                     x_next, partial, D, p.chunk, a, b, c)
+                     x_next, partial, D, p.chunk, a, b, c, nk)
     if (dtype == FF_BF16) {
       if (lp) { if (vec) FF_SDE_LAUNCH(true, true, true); else FF_SDE_LAUNCH(true, true, false); }
       else    { if (vec) FF_SDE_LAUNCH(true, false, true); else FF_SDE_LAUNCH(true, false, false); }
@@ -273,6 +360,58 @@ int ff_logprob(const void* x, const void* v, const void* x_next, double* logp, i
   Coef k = coefficients(t, t_next, sigma, D);
   return launch_sde<1>(dtype, x, v, x_next, nullptr, logp, B, D, k.a, k.b, k.c, k.inv_2var, k.cst,
                        workspace, static_cast<hipStream_t>(stream));
+}
+
+int ff_sde_step_philox(const void* x, const void* v, void* x_next, double* logp, int64_t B, int64_t D, double t,
+                       double t_next, double sigma, uint64_t seed, uint32_t step, int32_t dtype, void* workspace,
+                       size_t ws_bytes, void* stream) {
+  const char* fn = "ff_sde_step_philox";
+  FF_TRY(check_sde_args(fn, x, v, x, x_next, B, D, t, t_next, sigma, dtype));
+  if (sigma == 0.0 && logp) return fail(FF_EDOMAIN, "%s: an ODE step (sigma=0) has no log-probability", fn);
+  if (B == 0 || D == 0) return FF_OK;
+  if (!x_next) return fail(FF_EINVAL, "%s: null x_next", fn);
+  if (x_next == x || x_next == v) return fail(FF_EINVAL, "%s: x_next aliases an input", fn);
+  if (logp && (reinterpret_cast<uintptr_t>(logp) & 7u) != 0) return fail(FF_EINVAL, "%s: logp misaligned", fn);
+  FF_TRY(check_ws(fn, B, D, logp != nullptr, workspace, ws_bytes));
+  Coef k = coefficients(t, t_next, sigma, D);
+  const NoiseKey nk{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32), step};
+  return launch_sde<2>(dtype, x, v, nullptr, x_next, logp, B, D, k.a, k.b, k.c, k.inv_2var, k.cst, workspace,
+                       static_cast<hipStream_t>(stream), nk);
+}
+
+int ff_philox_normal(void* eps, int64_t B, int64_t D, uint64_t seed, uint32_t step, int32_t dtype, void* stream) {
+  const char* fn = "ff_philox_normal";
+  if (dtype != FF_F32 && dtype != FF_BF16) return fail(FF_EINVAL, "%s: bad dtype %d", fn, dtype);
+  if (B < 0 || D < 0) return fail(FF_EINVAL, "%s: negative shape", fn);
+  if (B > 65535) return fail(FF_EUNSUPPORTED, "%s: B=%lld exceeds 65535", fn, (long long)B);
+  if (B == 0 || D == 0) return FF_OK;
+  if (!eps) return fail(FF_EINVAL, "%s: null eps", fn);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const NoiseKey nk{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32), step};
+  const int64_t nb = (D + 3) / 4;
+  int64_t bx = (nb + 255) / 256;
+  const int64_t cap = (2048 + B - 1) / B;
+  if (bx > cap) bx = cap;
+  dim3 grid(static_cast<unsigned>(bx), static_cast<unsigned>(B));
+  LaunchScope ls("philox_normal", s, 0.0, static_cast<double>(B) * D * dtype_size(dtype));
+  if (dtype == FF_BF16) hipLaunchKernelGGL(philox_normal_kernel<true>, grid, dim3(256), 0, s, eps, D, nk);
+  else hipLaunchKernelGGL(philox_normal_kernel<false>, grid, dim3(256), 0, s, eps, D, nk);
+  return ls.status();
+}
+
+int ff_philox4x32(uint32_t* out, int64_t n, uint64_t ctr_base, uint32_t c2, uint32_t c3, uint64_t key,
+                  void* stream) {
+  const char* fn = "ff_philox4x32";
+  if (n < 0) return fail(FF_EINVAL, "%s: negative count", fn);
+  if (n == 0) return FF_OK;
+  if (!out) return fail(FF_EINVAL, "%s: null out", fn);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int64_t bx = (n + 255) / 256;
+  if (bx > 4096) bx = 4096;
+  LaunchScope ls("philox4x32", s, 0.0, static_cast<double>(n) * 16.0);
+  hipLaunchKernelGGL(philox_words_kernel, dim3(static_cast<unsigned>(bx)), dim3(256), 0, s, out, n, ctr_base, c2, c3,
+                     static_cast<uint32_t>(key), static_cast<uint32_t>(key >> 32));
+  return ls.status();
 }
 
 }  // extern "C"

@@ -59,8 +59,12 @@ class RolloutResult:
 class Rollout:
     """Holds the model handle and the per-step buffers of one workload."""
 
-    def __init__(self, w: C.Workload, dit: api.Dit, device="cuda", keep_velocities: bool = True):
+    def __init__(self, w: C.Workload, dit: api.Dit, device="cuda", keep_velocities: bool = True,
+                 noise_seed: Optional[int] = None):
+        """noise_seed: draw each step's noise on the device (Philox4x32-10, counter = (element, sample,
+        step)) instead of reading the eps tensors passed to run()."""
         self.w = w
+        self.noise_seed = noise_seed
         self.dit = dit
         self.device = device
         self.keep_v = keep_velocities
@@ -106,7 +110,10 @@ class Rollout:
             if sigma > 0.0:
                 lp = torch.empty(B, dtype=torch.float64, device=self.device)
                 logp[k] = lp
-            api.sde_step(x, v, eps_steps[k], x_next, t, tn, sigma, logp=lp, ws=self.ws_sde)
+            if self.noise_seed is None:
+                api.sde_step(x, v, eps_steps[k], x_next, t, tn, sigma, logp=lp, ws=self.ws_sde)
+            else:
+                api.sde_step_philox(x, v, x_next, t, tn, sigma, self.noise_seed, k, logp=lp, ws=self.ws_sde)
             if self.keep_v:
                 vs.append(v)
             xs.append(x_next)

@@ -68,6 +68,21 @@ def test_sde_argument_validation():
     assert lib.ff_sde_workspace_size(0, 5, byref(n)) == 0 and n.value == 0
 
 
+def test_philox_argument_validation():
+    lib = _lib.load()
+    f = c_void_p(8192)
+    _err(lib.ff_sde_step_philox(f, f, c_void_p(16384), None, 2, 8, 0.5, 0.6, 1.0, 1, 0, 1, None, 0, None), _lib.FF_EDOMAIN)
+    _err(lib.ff_sde_step_philox(f, f, f, None, 2, 8, 0.5, 0.4, 1.0, 1, 0, 1, None, 0, None), _lib.FF_EINVAL)
+    _err(lib.ff_sde_step_philox(f, f, c_void_p(16384), c_void_p(24576), 2, 8, 0.5, 0.4, 0.0, 1, 0, 1, None, 0, None),
+         _lib.FF_EDOMAIN)
+    _err(lib.ff_sde_step_philox(f, f, c_void_p(16384), c_void_p(24576), 2, 8, 0.5, 0.4, 1.0, 1, 0, 1, None, 0, None),
+         _lib.FF_EWORKSPACE)
+    _err(lib.ff_philox_normal(f, 2, 8, 1, 0, 4, None), _lib.FF_EINVAL)
+    _err(lib.ff_philox_normal(None, 2, 8, 1, 0, 1, None), _lib.FF_EINVAL)
+    _err(lib.ff_philox4x32(None, 4, 0, 0, 0, 0, None), _lib.FF_EINVAL)
+    _err(lib.ff_philox4x32(f, -1, 0, 0, 0, 0, None), _lib.FF_EINVAL)
+
+
 def test_loss_argument_validation():
     """Host-side checks of the objectives: every rejected call returns before any launch."""
     lib = _lib.load()

@@ -120,3 +120,74 @@ def test_group_advantage_edge_cases(gpu_lib):
     a = adv.cpu().numpy()
     assert cnt.cpu().tolist() == [3, 1, 0, 1]
     assert np.all(a[:5] == 0.0) and np.isnan(a[5])
+
+
+# ------------------------------------------------------------------ counter-based noise
+from oracle import noise as onoise  # noqa: E402
+
+
+def _u32(t):
+    return t.cpu().numpy().view(np.uint32)
+
+
+def test_philox_known_answers_on_device(gpu_lib):
+    import json
+    import os
+    gold = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "hand_examples.json")))
+    for case in gold["philox4x32_10_kat"]["cases"]:
+        c = [int(x, 16) for x in case["ctr"]]
+        k = [int(x, 16) for x in case["key"]]
+        w = gpu_lib.philox4x32(1, c[0] | (c[1] << 32), c[2], c[3], k[0] | (k[1] << 32))
+        torch.cuda.synchronize()
+        assert [f"{int(x):08x}" for x in _u32(w)[0]] == case["out"]
+
+
+def test_philox_words_match_oracle_bit_exact(gpu_lib):
+    n, base, c2, c3, key = 100003, (1 << 32) - 17, 5, 9, 0x0123456789ABCDEF
+    w = _u32(gpu_lib.philox4x32(n, base, c2, c3, key))
+    i = np.arange(n, dtype=np.uint64) + np.uint64(base)
+    ctr = np.stack([i & np.uint64(0xFFFFFFFF), i >> np.uint64(32), np.full(n, c2, np.uint64),
+                    np.full(n, c3, np.uint64)], axis=-1)
+    ref = onoise.philox4x32_10(ctr, (key & 0xFFFFFFFF, key >> 32))
+    assert np.array_equal(w, ref)
+
+
+@pytest.mark.parametrize("dt", [C.F32, C.BF16], ids=["f32", "bf16"])
+@pytest.mark.parametrize("B,D", [(3, 1000), (2, 7), (4, 65536), (1, 8 * 2048 + 8)])
+def test_philox_normal_matches_oracle(gpu_lib, dt, B, D):
+    seed, step = 0x5EED0000ABCD, 4
+    z = gpu_lib.philox_normal((B, D), seed, step, dtype=torch.bfloat16 if dt == C.BF16 else torch.float32)
+    torch.cuda.synchronize()
+    ref = onoise.sde_noise(B, D, seed, step)
+    got = host(z)
+    # float32 Box-Muller: log, sqrt, sin/cos to a few ulp of |z| <= ~6.7; bf16 adds half an ulp
+    bound = (2.0 ** -8 * np.abs(ref) if dt == C.BF16 else 0.0) + 2e-5
+    assert np.all(np.abs(got - ref) <= bound)
+
+
+@pytest.mark.parametrize("dt", [C.F32, C.BF16], ids=["f32", "bf16"])
+@pytest.mark.parametrize("B,D", [(8, 256), (3, 1000), (2, 7), (4, 65536)])
+def test_sde_step_philox_parity(gpu_lib, dt, B, D):
+    t, tn, sigma, seed, step = 0.6, 0.5, 0.7 * math.sqrt(1.5), 987654321, 2
+    x, v = normal(200, (B, D), dt), normal(201, (B, D), dt)
+    X, V = dev(x, dt), dev(v, dt)
+    Xn = torch.empty_like(X)
+    lp = torch.empty(B, dtype=torch.float64, device="cuda")
+    gpu_lib.sde_step_philox(X, V, Xn, t, tn, sigma, seed, step, logp=lp)
+    lp2 = torch.empty_like(lp)
+    gpu_lib.logprob(X, V, Xn, lp2, t, tn, sigma)
+    torch.cuda.synchronize()
+    eps = onoise.sde_noise(B, D, seed, step)
+    ref = osde.sde_step(x, v, eps, t, tn, sigma)
+    got = host(Xn)
+    assert rel(got, ref) <= TOL[dt]
+    assert np.max(np.abs(host(lp) - osde.step_log_prob(x, v, got, t, tn, sigma))) <= LOGP_ABS
+    assert torch.equal(lp, lp2)   # the recompute of the fused step's log-prob is bitwise identical
+    if dt == C.F32:
+        # the fused step equals the step on the materialised noise, bit for bit
+        E = gpu_lib.philox_normal((B, D), seed, step)
+        Xn2 = torch.empty_like(X)
+        lp3 = torch.empty_like(lp)
+        gpu_lib.sde_step(X, V, E, Xn2, t, tn, sigma, logp=lp3)
+        torch.cuda.synchronize()
+        assert torch.equal(Xn, Xn2) and torch.equal(lp, lp3)
