@@ -105,20 +105,28 @@ __global__ __launch_bounds__(WAVES * 64, 1) void attn_bf16_d128(AttnParams p) {
   }
   const int ntiles = (n_kv + KT - 1) / KT;
   const int nfull = n_kv / KT;   // tiles without masked keys
+  // The direct loads are written as inline assembly: the compiler's wait-count pass cannot
+  // tell an LDS-DMA load's destination from the fragment reads, and with one in flight it
+  // turns every LDS wait into lgkmcnt(0) (and adds a vmcnt(0) before the reads), which
+  // defeats the read prefetch.  Their completion is ordered explicitly instead (vmcnt wait
+  // and barrier before a tile is read; its buffer is refilled only after the next barrier).
+  auto dma16 = [](const void* src, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :: "s"(lds_addr), "v"(src) : "memory", "m0");
+  };
+  const uint32_t smem_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
   auto issue = [&](int tile) {
     const int kv0 = (tile < ntiles ? tile : ntiles - 1) * KT;
-    char* base = smem + (tile % STAGES) * STAGE;
+    const uint32_t base = smem_base + static_cast<uint32_t>((tile % STAGES) * STAGE);
 #pragma unroll
     for (int i = 0; i < K_INS; ++i) {
       const int key = kv0 + k_row[i] < n_kv ? kv0 + k_row[i] : n_kv - 1;
-      __builtin_amdgcn_global_load_lds((const glb_t*)(Kb + key * D + k_ck[i] * 8),
-                                       (lds_t*)(base + (i * WAVES + wave) * 1024), 16, 0, 0);
+      dma16(Kb + key * D + k_ck[i] * 8, __builtin_amdgcn_readfirstlane(base + (i * WAVES + wave) * 1024));
     }
 #pragma unroll
     for (int i = 0; i < V_INS; ++i) {
       const int col = kv0 + v_ck[i] * 8 < n_kv ? kv0 + v_ck[i] * 8 : n_kv - 8;
-      __builtin_amdgcn_global_load_lds((const glb_t*)(Vb + v_row[i] * n_kv + col),
-                                       (lds_t*)(base + K_STAGE + (i * WAVES + wave) * 1024), 16, 0, 0);
+      dma16(Vb + v_row[i] * n_kv + col, __builtin_amdgcn_readfirstlane(base + K_STAGE + (i * WAVES + wave) * 1024));
     }
   };
 
