@@ -3,14 +3,15 @@
 // bf16: MFMA 32x32x16 (gfx950) tiles, fp32 accumulation.  A [M, K] and W [N, K]
 // are both K-contiguous (nn.Linear layout).  A workgroup computes a BM x BN
 // tile; its waves split it into wave tiles, each a grid of 32x32 MFMA blocks.
-// Large problems use a 256 x 256 tile with one wave per SIMD fed by direct
-// global->LDS loads of 64-wide K slabs (gemm_bf16_256); small ones a 128 x 128
-// tile staged through registers with two LDS buffers (gemm_bf16_kernel).  gfx950's LDS serves a
-// 16-byte-per-lane read for 16 lanes per clock across 64 banks (256 bytes), so
-// LDS rows are stored with their 16-byte chunks permuted by a row-dependent
-// XOR: the fragment reads of 16 consecutive rows land on 16 distinct bank
-// groups.  Tiles are ordered so that consecutive tiles of one XCD (workgroups
-// are dealt round-robin over the 8 XCDs) share A rows in that XCD's L2.
+// Large problems use a 256 x 256 tile computed by eight waves in a compute /
+// memory ping-pong and fed by direct buffer->LDS loads of 64-wide K slabs
+// (gemm_bf16_pp); small ones a 128 x 128 tile staged through registers with two
+// LDS buffers (gemm_bf16_kernel).  gfx950's LDS serves a 16-byte-per-lane read
+// for 16 lanes per clock across 64 banks (256 bytes), so LDS rows are stored
+// with their 16-byte chunks permuted by a row-dependent XOR: the fragment reads
+// of 16 consecutive rows land on 16 distinct bank groups.  Tiles are walked a
+// few tile rows at a time so that tiles running together share A rows and W
+// rows in L2.
 //
 // Epilogues fuse the bias, GELU-tanh (from a column on, for the fused
 // single-stream projection) and the adaLN-gated residual X + g * (.).
@@ -62,8 +63,8 @@ __device__ __forceinline__ int64_t xcd_remap(int64_t pid, int64_t total) {
   const int64_t full = total / 8 * 8;
   return pid < full ? (pid % 8) * (full / 8) + pid / 8 : pid;
 }
+template <int64_t GROUP_M = 8>
 __device__ __forceinline__ void group_order(int64_t lid, int64_t num_m, int64_t num_n, int64_t& tm, int64_t& tn) {
-  constexpr int64_t GROUP_M = 8;
   const int64_t in_group = GROUP_M * num_n;
   const int64_t gidx = lid / in_group;
   const int64_t first_m = gidx * GROUP_M;
@@ -306,86 +307,99 @@ __device__ __forceinline__ void wg_barrier() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-// ------------------------------------------------------------------ bf16, 256 x 256 tiles
-// 256 x 256 tile, one wave per SIMD, each wave a 128 x 128 grid of 4 x 4 MFMA
-// blocks.  K advances in slabs of 64, so every row segment a direct load
-// fetches is a whole 128-byte cache line (32-wide slabs fetch half lines, which
-// halves the L2 -> LDS rate); two 64 KB LDS buffers.  Half a slab (two k16
-// steps) of fragments sits in each of two register sets: the second half of
-// slab s is read from LDS while the first half's MFMAs run, and the first half
-// of slab s + 1 while the second half's run.  Per slab: barrier X (everyone has
-// read slab s) lets slab s + 2's loads go into slab s's buffer between the
-// MFMAs of the third k16 step; barrier Y (each wave has waited for its own
-// loads of slab s + 1) publishes slab s + 1.  Loads past the end of K replay
-// the last slab, so the number in flight is the same on every step.
+// ------------------------------------------------------------------ bf16, 256 x 256, ping-pong
+// Eight waves, two per SIMD, in two groups of four (wave w and wave w + 4 share a SIMD).
+// Each wave owns a 128 x 64 block of the 256 x 256 tile (4 x 2 MFMA blocks) and alternates
+// between a compute phase (the 32 MFMAs of one 64-wide K slab) and a memory phase (the LDS
+// reads of the fragments it needs next); the groups are one phase apart, so one wave of a
+// SIMD keeps the matrix core busy while the other feeds itself.  A barrier separates
+// phases: slab s is computed by group 0 in phase 2s and by group 1 in phase 2s + 1, so it
+// is read from LDS in phases 2s - 1 and 2s only and two 64 KB buffers suffice.  Slab
+// s + 2's direct loads go into slab s's buffer during phase 2s + 1 (both groups are done
+// with it): group 0 issues the A rows in its memory phase, group 1 the W rows between the
+// MFMAs of its compute phase, and each waits for its own loads one phase later, before the
+// barrier that publishes the slab.  Loads go through buffer resources whose record count
+// ends at the matrix's last row, so rows past M (or N) read as zero without a per-row
+// clamp; K rows are 128-byte lines (a 64-wide slab), stored with the chunk swizzle
+// chunk ^ ((row >> 1) & 7).
+
+__device__ __forceinline__ u32x4_t buffer_rsrc(const void* base, uint64_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  u32x4_t r;
+  r.x = static_cast<uint32_t>(a);
+  r.y = static_cast<uint32_t>(a >> 32);   // stride 0: raw buffer, range check on the offset
+  r.z = static_cast<uint32_t>(bytes < 0xffffffffull ? bytes : 0xffffffffull);
+  r.w = 0x00020000u;                      // 32-bit data format
+  return r;
+}
+// One 16-byte-per-lane direct load from a buffer into LDS at the wave-uniform `lds` address.
+// Written as inline assembly: the compiler's wait-count pass cannot tell an LDS-DMA
+// destination from the fragment reads and would wait for every load before any LDS read;
+// the kernel orders them itself (vmcnt wait + barrier before a slab is read).
+__device__ __forceinline__ void dma_buf16(const u32x4_t& rsrc, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :: "s"(lds), "v"(voff), "s"(rsrc) : "memory", "m0");
+}
+
 template <int EPI>
-__global__ __launch_bounds__(256, 1) void gemm_bf16_256(GemmBatch batch) {
-  constexpr int BM = 256, BN = 256, WAVES = 4;
-  constexpr int KS = 64, ROWB = KS * 2, CPR = ROWB / 16, RPI = 1024 / ROWB;   // 128-byte rows, 8 rows per load
-  constexpr int TM = 128, TN = 128, FM = 4, FN = 4;
-  constexpr int A_INS = BM / RPI / WAVES, B_INS = BN / RPI / WAVES, LPW = A_INS + B_INS;   // 8 + 8
-  constexpr int STAGE = (BM + BN) * ROWB;   // 64 KB
+__global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
+  constexpr int BM = 256, BN = 256, KS = 64, ROWB = KS * 2;   // 128-byte LDS rows
+  constexpr int STAGE = (BM + BN) * ROWB;                     // 64 KB
+  constexpr int TM = 128, TN = 64, FM = 4, FN = 2;
+  constexpr int A_INS = BM / 8 / 4, B_INS = BN / 8 / 4;       // 1 KB loads per wave per slab
   extern __shared__ __attribute__((aligned(16))) char smem[];
 
-  const int64_t lid = xcd_remap(blockIdx.x, batch.tiles);
+  // Plain launch order (consecutive tiles on different XCDs) walking 4 tile rows at a time:
+  // measured faster than giving each XCD a contiguous range on the DiT's shapes.
+  const int64_t lid = blockIdx.x;
   const int which = lid >= batch.tiles0 ? 1 : 0;
   const GemmParams& p = batch.p[which];
   const int64_t num_m = (p.M + BM - 1) / BM, num_n = (p.N + BN - 1) / BN;
   int64_t tm, tn;
-  group_order(lid - (which ? batch.tiles0 : 0), num_m, num_n, tm, tn);
+  group_order<4>(lid - (which ? batch.tiles0 : 0), num_m, num_n, tm, tn);
   const int64_t m0 = tm * BM, n0 = tn * BN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-
-  // Load i of this wave fills rows RPI (i*WAVES + wave) .. +RPI-1 (1 KB of LDS); lane l lands at
-  // row + l/CPR, stored chunk l%CPR, so it fetches logical chunk (l%CPR) ^ ((row >> 1) & 7).
-  // Sources: a uniform base (the tile's first row) plus 32-bit per-lane byte offsets.
-  const char* a_base = reinterpret_cast<const char*>(static_cast<const bf16_t*>(p.A1) + m0 * p.lda1);
-  const char* b_base = reinterpret_cast<const char*>(static_cast<const bf16_t*>(p.W) + n0 * p.ldw);
-  uint32_t a_off[A_INS], b_off[B_INS];
-  auto a_offsets = [&](int64_t lda) {
-#pragma unroll
-    for (int i = 0; i < A_INS; ++i) {
-      const int row = (i * WAVES + wave) * RPI + lane / CPR;
-      const int ck = (lane % CPR) ^ ((row >> 1) & 7);
-      const int64_t r = m0 + row < p.M ? row : p.M - 1 - m0;
-      a_off[i] = static_cast<uint32_t>((r * lda + ck * 8) * 2);
-    }
-  };
-  a_offsets(p.lda1);
-#pragma unroll
-  for (int i = 0; i < B_INS; ++i) {
-    const int row = (i * WAVES + wave) * RPI + lane / CPR;
-    const int ck = (lane % CPR) ^ ((row >> 1) & 7);
-    const int64_t r = n0 + row < p.N ? row : p.N - 1 - n0;
-    b_off[i] = static_cast<uint32_t>((r * p.ldw + ck * 8) * 2);
-  }
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave >> 2, w4 = wave & 3;
+  const int wm = w4 >> 1, wn = grp * 2 + (w4 & 1);
   const int KT = static_cast<int>(p.K / KS), KT1 = static_cast<int>(p.K1 / KS);
 
-  auto switch_a = [&](int slab) {
-    if (slab == KT1 && slab > 0 && slab < KT) {
-      // continue K in the second A source (the two-source single-stream projection)
-      a_base = reinterpret_cast<const char*>(static_cast<const bf16_t*>(p.A2) + m0 * p.lda2);
-      a_offsets(p.lda2);
-    }
+  // Load q of a wave fills LDS rows 32 q + 8 w4 .. + 7 of its matrix; lane l lands at
+  // row + l / 8, stored chunk l % 8, so it fetches logical chunk (l % 8) ^ ((row >> 1) & 7),
+  // which does not depend on q.
+  const int lrow = 8 * w4 + (lane >> 3);
+  const int lck = (lane & 7) ^ ((lrow >> 1) & 7);
+  const int64_t rows_a = p.M - m0, rows_b = p.N - n0;
+  // A may come from two sources (the two-part K of the fused single-stream projection):
+  // slabs [0, KT1) from A1, the rest from A2.
+  const bool two = KT1 > 0 && KT1 < KT;
+  const char* a1_tile = reinterpret_cast<const char*>(static_cast<const bf16_t*>(p.A1) + m0 * p.lda1);
+  const char* a2_tile = reinterpret_cast<const char*>(static_cast<const bf16_t*>(p.A2) + m0 * p.lda2);
+  const int64_t a1_bytes = rows_a * p.lda1 * 2, a2_bytes = rows_a * p.lda2 * 2;
+  const uint32_t a1_off = static_cast<uint32_t>((lrow * p.lda1 + lck * 8) * 2);
+  const uint32_t a2_off = static_cast<uint32_t>((lrow * p.lda2 + lck * 8) * 2);
+  const uint32_t a1_step = static_cast<uint32_t>(32 * p.lda1 * 2), a2_step = static_cast<uint32_t>(32 * p.lda2 * 2);
+  const char* b_tile = reinterpret_cast<const char*>(static_cast<const bf16_t*>(p.W) + n0 * p.ldw);
+  const int64_t b_bytes = rows_b * p.ldw * 2;
+  const uint32_t b_off = static_cast<uint32_t>((lrow * p.ldw + lck * 8) * 2);
+  const uint32_t b_step = static_cast<uint32_t>(32 * p.ldw * 2);
+  const uint32_t smem_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
+  // A slab index past the end replays the last slab into a buffer that is never read again,
+  // so every phase has the same shape.
+  auto rsrc_b = [&](int s) {
+    const int64_t db = static_cast<int64_t>(s < KT ? s : KT - 1) * ROWB;
+    return buffer_rsrc(b_tile + db, static_cast<uint64_t>(b_bytes - db));
   };
-  // Loads [first, first + count) of slab `slab` (A loads, then B loads).
-  auto issue_part = [&](int slab, int first, int count) {
-    const uint32_t back = slab < KT ? 0u : static_cast<uint32_t>(KS * 2);
-    char* base = smem + (slab & 1) * STAGE + wave * 1024;
+  auto issue_a = [&](int s, int dst) {   // slab s's A rows into the buffer of slab dst
+    if (s >= KT) s = KT - 1;
+    const bool second = two && s >= KT1;
+    const int64_t da = static_cast<int64_t>(second ? s - KT1 : s) * ROWB;
+    const u32x4_t r = buffer_rsrc((second ? a2_tile : a1_tile) + da, static_cast<uint64_t>((second ? a2_bytes : a1_bytes) - da));
+    const uint32_t off = second ? a2_off : a1_off, step = second ? a2_step : a1_step;
+    const uint32_t lds = smem_base + (dst & 1) * STAGE + w4 * 1024;
 #pragma unroll
-    for (int q = first; q < first + count; ++q) {
-      if (q < A_INS) {
-        __builtin_amdgcn_global_load_lds((const glb_t*)(a_base + (a_off[q] - back)), (lds_t*)(base + q * WAVES * 1024), 16, 0, 0);
-        a_off[q] += KS * 2 - back;
-      } else {
-        const int i = q - A_INS;
-        __builtin_amdgcn_global_load_lds((const glb_t*)(b_base + (b_off[i] - back)), (lds_t*)(base + BM * ROWB + i * WAVES * 1024), 16, 0, 0);
-        b_off[i] += KS * 2 - back;
-      }
-    }
+    for (int q = 0; q < A_INS; ++q) dma_buf16(r, off + q * step, lds + q * 4096);
   };
-  auto issue = [&](int slab) { issue_part(slab, 0, LPW); };
 
   f32x16_t acc[FM][FN];
 #pragma unroll
@@ -398,79 +412,84 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_256(GemmBatch batch) {
   const int frow = lane & 31, fhalf = lane >> 5;
   const int key = (frow >> 1) & 7;
   const int a_frag0 = (wm * TM + frow) * ROWB, b_frag0 = BM * ROWB + (wn * TN + frow) * ROWB;
-  // Register sets: r0 = k16 steps 0, 1 of a slab; r1 = steps 2, 3.  [step][block]
-  bf16x8_t ra0[2][FM], rb0[2][FN], ra1[2][FM], rb1[2][FN];
-  auto read_half = [&](int slab, int half, bf16x8_t (&ra)[2][FM], bf16x8_t (&rb)[2][FN]) {
-    const char* S = smem + (slab & 1) * STAGE;
+  bf16x8_t fa[4][FM], fb[4][FN];   // one slab of fragments: [k16 step][block]
+  auto read_frags = [&](int s) {
+    const char* S = smem + (s & 1) * STAGE;
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const int coff = (((half * 2 + ks) * 2 + fhalf) ^ key) << 4;
+    for (int ks = 0; ks < 4; ++ks) {
+      const int coff = ((ks * 2 + fhalf) ^ key) << 4;
 #pragma unroll
-      for (int i = 0; i < FM; ++i) ra[ks][i] = *reinterpret_cast<const bf16x8_t*>(S + a_frag0 + i * 32 * ROWB + coff);
+      for (int i = 0; i < FM; ++i) fa[ks][i] = *reinterpret_cast<const bf16x8_t*>(S + a_frag0 + i * 32 * ROWB + coff);
 #pragma unroll
-      for (int j = 0; j < FN; ++j) rb[ks][j] = *reinterpret_cast<const bf16x8_t*>(S + b_frag0 + j * 32 * ROWB + coff);
+      for (int j = 0; j < FN; ++j) fb[ks][j] = *reinterpret_cast<const bf16x8_t*>(S + b_frag0 + j * 32 * ROWB + coff);
     }
   };
-  auto mfma_step = [&](const bf16x8_t (&ra)[FM], const bf16x8_t (&rb)[FN]) {
+  // The 32 MFMAs of a slab; with `rb` set, the W rows of a later slab are loaded between them.
+  auto compute = [&](const u32x4_t* rb, uint32_t lds_b) {
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+    for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ra[i], rb[j], acc[i][j], 0, 0, 0);
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks][i], fb[ks][j], acc[i][j], 0, 0, 0);
+          if (rb != nullptr && j == 1 && (i & 1) == 1) {
+            const int q = ks * 2 + (i >> 1);
+            dma_buf16(*rb, b_off + q * b_step, lds_b + q * 4096);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
   };
 
-  switch_a(0);
-  issue(0);
-  switch_a(1);
-  issue(1);
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPW) : "memory");   // slab 0 has landed
-  wg_barrier();
-  read_half(0, 0, ra0, rb0);
-  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-  // Loads of slab s + 2 per k16 step 1, 2, 3 (the address unit takes a 1 KB load every
-  // 16 clocks, so the 64 loads of a slab are spread over three steps of MFMAs).
-  constexpr int G1 = 6, G2 = 5, G3 = LPW - G1 - G2;
-  for (int s = 0; s < KT; ++s) {
-    // step 0: read steps 2, 3 of slab s between the MFMAs
-    read_half(s, 1, ra1, rb1);
-    mfma_step(ra0[0], rb0[0]);
-#pragma unroll
-    for (int m = 0; m < FM * FN; ++m) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
+  // Two code paths, one per group (the group is wave-uniform), with the same sequence of
+  // barriers; a single loop branching on the group would keep both groups' fragments live
+  // at once.  Neither loop branches: past the last slab the loads replay and the reads
+  // fetch unused data.
+  if (grp == 0) {
+    issue_a(0, 0);
+    issue_a(1, 1);
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(A_INS) : "memory");   // A of slab 0 has landed
+    wg_barrier();
+    read_frags(0);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    switch_a(s + 2);
-    wg_barrier();                                     // X: every wave has read slab s
-    // steps 1, 2: slab s + 2's first loads into slab s's buffer
-    issue_part(s + 2, 0, G1 + G2);
-    mfma_step(ra0[1], rb0[1]);
-    mfma_step(ra1[0], rb1[0]);
-#pragma unroll
-    for (int m = 0; m < 2 * FM * FN; ++m) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      if (m < FM * FN ? m < G1 : m - FM * FN < G2) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    wg_barrier();
+    for (int s = 0; s < KT; ++s) {
+      compute(nullptr, 0);                                 // phase 2s
+      __builtin_amdgcn_sched_barrier(0);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");    // A of slab s + 1 has landed
+      wg_barrier();
+      read_frags(s + 1);                                   // phase 2s + 1
+      issue_a(s + 2, s);
+      __builtin_amdgcn_sched_barrier(0);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      wg_barrier();
     }
-    __builtin_amdgcn_sched_barrier(0);
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(G1 + G2) : "memory");   // slab s + 1 has landed
-    wg_barrier();                                     // Y: publish slab s + 1
-    // step 3: the rest of the loads; read steps 0, 1 of slab s + 1 (past the end: replayed data)
-    issue_part(s + 2, G1 + G2, G3);
-    read_half(s + 1, 0, ra0, rb0);
-    mfma_step(ra1[1], rb1[1]);
+  } else {
+    {
+      const uint32_t lds = smem_base + w4 * 1024 + BM * ROWB;
+      const u32x4_t r0 = rsrc_b(0), r1 = rsrc_b(1);
 #pragma unroll
-    for (int m = 0; m < FM * FN; ++m) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      if (m < G3) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      for (int q = 0; q < B_INS; ++q) dma_buf16(r0, b_off + q * b_step, lds + q * 4096);
+#pragma unroll
+      for (int q = 0; q < B_INS; ++q) dma_buf16(r1, b_off + q * b_step, lds + STAGE + q * 4096);
     }
-    __builtin_amdgcn_sched_barrier(0);
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(B_INS) : "memory");   // W of slab 0 has landed
+    wg_barrier();
+    wg_barrier();
+    for (int s = 0; s < KT; ++s) {
+      read_frags(s);                                       // phase 2s
+      __builtin_amdgcn_sched_barrier(0);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");    // W of slab s + 1 has landed
+      wg_barrier();
+      const u32x4_t rb = rsrc_b(s + 2);                   // phase 2s + 1
+      compute(&rb, smem_base + (s & 1) * STAGE + w4 * 1024 + BM * ROWB);
+      __builtin_amdgcn_sched_barrier(0);
+      wg_barrier();
+    }
   }
-
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // replayed loads may still target LDS
-  __syncthreads();
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // replayed loads still target LDS
+  wg_barrier();
   epilogue_blocks<EPI, FM, FN>(p, acc, m0 + wm * TM, n0 + wn * TN,
                                reinterpret_cast<float*>(smem) + wave * 32 * 36, lane);
 }
@@ -542,17 +561,17 @@ int launch_bf16(const GemmParams& p, hipStream_t s, const char* name, double flo
 }
 
 template <int EPI>
-int launch_256_batch(const GemmBatch& b, hipStream_t s, const char* name, double flops, double bytes) {
+int launch_pp_batch(const GemmBatch& b, hipStream_t s, const char* name, double flops, double bytes) {
   constexpr int smem = 2 * 512 * 64 * 2;
   static bool attr_set = false;
   if (!attr_set) {
-    FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_256<EPI>),
+    FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_pp<EPI>),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, smem),
                  "gemm smem attribute");
     attr_set = true;
   }
   LaunchScope ls(name, s, flops, bytes);
-  hipLaunchKernelGGL((gemm_bf16_256<EPI>), dim3(static_cast<unsigned>(b.tiles)), dim3(256), smem, s, b);
+  hipLaunchKernelGGL((gemm_bf16_pp<EPI>), dim3(static_cast<unsigned>(b.tiles)), dim3(512), smem, s, b);
   return ls.status();
 }
 
@@ -568,7 +587,7 @@ int dispatch_bf16(const GemmParams& p, hipStream_t s, double flops, double bytes
     b.p[0] = p;
     b.p[1] = p;
     b.tiles0 = b.tiles = tiles256(p);
-    return launch_256_batch<EPI>(b, s, names[EPI], flops, bytes);
+    return launch_pp_batch<EPI>(b, s, names[EPI], flops, bytes);
   }
   return launch_bf16<128, 128, 2, 2, EPI>(p, s, names[EPI], flops, bytes);
 }
@@ -642,9 +661,9 @@ int gemm2(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
   const double flops = gemm_flops(a0) + gemm_flops(a1), bytes = gemm_bytes(a0) + gemm_bytes(a1);
   static const char* names[3] = {"gemm_bf16", "gemm_bf16_gelu", "gemm_bf16_gated"};
   switch (a0.epi) {
-    case EPI_NONE: return launch_256_batch<EPI_NONE>(b, s, names[0], flops, bytes);
-    case EPI_GELU: return launch_256_batch<EPI_GELU>(b, s, names[1], flops, bytes);
-    default: return launch_256_batch<EPI_GATED>(b, s, names[2], flops, bytes);
+    case EPI_NONE: return launch_pp_batch<EPI_NONE>(b, s, names[0], flops, bytes);
+    case EPI_GELU: return launch_pp_batch<EPI_GELU>(b, s, names[1], flops, bytes);
+    default: return launch_pp_batch<EPI_GATED>(b, s, names[2], flops, bytes);
   }
 }
 
