@@ -11,8 +11,12 @@ namespace {
 
 // ------------------------------------------------------------------ skinny linear
 // out[b, n] = act_out(sum_k W[n,k] act_in(in[b,k]) + bias[n]) (+ out[b, n] when accumulating).
-// A wave owns 8 output rows; lanes stride over K in 8-element chunks.  Bc <= 8 samples per launch.
-constexpr int kSkRows = 8;
+// Weight-bandwidth bound (B <= 16 samples per pass).  A block of four waves owns 4 R output
+// rows, R per wave; lanes stride over K in 8-element chunks.  K is walked in 512-wide slices:
+// the block stages act_in(in[b, slice]) for all its samples in LDS (the activation is evaluated
+// once per block, not once per wave), and each wave holds the raw weights of the next slice in
+// flight while it multiplies the current one against the staged inputs.
+constexpr int kSkSlice = 512, kSkMaxB = 16;
 
 __device__ __forceinline__ float act_apply(int act, float x) {
   if (act == ACT_SILU) return silu_f(x);
@@ -20,67 +24,121 @@ __device__ __forceinline__ float act_apply(int act, float x) {
   return x;
 }
 
-template <bool BF16, int BC>
+template <bool BF16, int BC, int R>
 __global__ __launch_bounds__(256) void skinny_kernel(const float* __restrict__ in, int64_t ldi, int act_in,
                                                      const void* __restrict__ W, const void* __restrict__ bias,
                                                      float* __restrict__ out, int64_t ldo, int64_t N, int64_t K,
                                                      int accumulate, int act_out) {
+  constexpr int WORDS = BF16 ? 4 : 8;           // 32-bit words of an 8-element chunk of a weight row
+  constexpr int XPT = BC * kSkSlice / 256;      // staged inputs per thread per slice (2 per sample)
+  static_assert(kSkSlice == 512, "two staged inputs per sample and thread");
+  __shared__ __attribute__((aligned(16))) float xs[BC][kSkSlice];
   const int lane = threadIdx.x & 63;
-  const int64_t n0 = (static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6)) * kSkRows;
-  if (n0 >= N) return;
-  float acc[kSkRows][BC];
+  const int64_t n0 = (static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6)) * R;
+  const bool active = n0 < N;   // wave-uniform
+  float acc[R][BC];
 #pragma unroll
-  for (int r = 0; r < kSkRows; ++r)
+  for (int r = 0; r < R; ++r)
 #pragma unroll
     for (int b = 0; b < BC; ++b) acc[r][b] = 0.f;
-  for (int64_t k = static_cast<int64_t>(lane) * 8; k < K; k += 512) {
-    float xin[BC][8];
+  // Everything a slice needs from memory is loaded one slice ahead: this lane's chunk of the
+  // R weight rows and this thread's share of the inputs to stage.
+  uint32_t raw[R][WORDS];
+  float xin[XPT];
+  auto fetch = [&](int64_t k0) {
+    const int len = K - k0 < kSkSlice ? static_cast<int>(K - k0) : kSkSlice;
+    if (len <= 0) return;
+    const float* src_x = in + k0 + threadIdx.x;
 #pragma unroll
-    for (int b = 0; b < BC; ++b) {
-      const float4* q = reinterpret_cast<const float4*>(in + b * ldi + k);
-      float4 u = q[0], v = q[1];
-      float t[8] = {u.x, u.y, u.z, u.w, v.x, v.y, v.z, v.w};
-#pragma unroll
-      for (int j = 0; j < 8; ++j) xin[b][j] = act_apply(act_in, t[j]);
+    for (int q = 0; q < XPT; ++q) {   // sample q / 2, column threadIdx.x + 256 (q % 2) of the slice
+      const int b = q >> 1, j = static_cast<int>(threadIdx.x) + ((q & 1) << 8);
+      xin[q] = j < len ? src_x[b * ldi + ((q & 1) << 8)] : 0.f;
     }
+    if (!active || lane * 8 >= len) return;
 #pragma unroll
-    for (int r = 0; r < kSkRows; ++r) {
+    for (int r = 0; r < R; ++r) {
       const int64_t n = n0 + r < N ? n0 + r : N - 1;
-      float w[8];
-      ld8<BF16>(W, n * K + k, w);
+      const uint4* src = reinterpret_cast<const uint4*>(static_cast<const char*>(W) + (n * K + k0 + lane * 8) * (BF16 ? 2 : 4));
 #pragma unroll
-      for (int b = 0; b < BC; ++b)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc[r][b] = fmaf(w[j], xin[b][j], acc[r][b]);
-    }
-  }
-#pragma unroll
-  for (int r = 0; r < kSkRows; ++r)
-#pragma unroll
-    for (int b = 0; b < BC; ++b) {
-      float s = wave_sum(acc[r][b]);
-      const int64_t n = n0 + r;
-      if (lane == 0 && n < N) {
-        float v = s + (bias ? ld1<BF16>(bias, n) : 0.f);
-        v = act_apply(act_out, v);
-        if (accumulate) v += out[b * ldo + n];
-        out[b * ldo + n] = v;
+      for (int h = 0; h < WORDS / 4; ++h) {
+        const uint4 u = src[h];
+        raw[r][4 * h] = u.x; raw[r][4 * h + 1] = u.y; raw[r][4 * h + 2] = u.z; raw[r][4 * h + 3] = u.w;
       }
     }
+  };
+  fetch(0);
+  for (int64_t k0 = 0; k0 < K; k0 += kSkSlice) {
+    const int len = K - k0 < kSkSlice ? static_cast<int>(K - k0) : kSkSlice;
+    __syncthreads();   // the previous slice has been consumed
+#pragma unroll
+    for (int q = 0; q < XPT; ++q) xs[q >> 1][threadIdx.x + ((q & 1) << 8)] = act_apply(act_in, xin[q]);
+    float w[R][8];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if constexpr (BF16) w[r][j] = __uint_as_float(j & 1 ? raw[r][j >> 1] & 0xffff0000u : raw[r][j >> 1] << 16);
+        else w[r][j] = __uint_as_float(raw[r][j]);
+      }
+    fetch(k0 + kSkSlice);
+    __syncthreads();
+    if (active && lane * 8 < len) {
+#pragma unroll
+      for (int b = 0; b < BC; ++b) {
+        const float4 u = *reinterpret_cast<const float4*>(&xs[b][lane * 8]);
+        const float4 v = *reinterpret_cast<const float4*>(&xs[b][lane * 8 + 4]);
+        const float x[8] = {u.x, u.y, u.z, u.w, v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+          for (int j = 0; j < 8; ++j) acc[r][b] = fmaf(w[r][j], x[j], acc[r][b]);
+      }
+    }
+  }
+  if (!active) return;
+  // Lane b finishes sample b: the bias and accumulate loads of all R rows are issued together,
+  // one round trip per wave rather than one per (row, sample).
+  float mine[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    mine[r] = 0.f;
+#pragma unroll
+    for (int b = 0; b < BC; ++b) {
+      const float s = wave_sum(acc[r][b]);
+      mine[r] = lane == b ? s : mine[r];
+    }
+  }
+  if (lane < BC) {
+    float bv[R], ov[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int64_t n = n0 + r < N ? n0 + r : N - 1;
+      bv[r] = bias ? ld1<BF16>(bias, n) : 0.f;
+      ov[r] = accumulate ? out[lane * ldo + n] : 0.f;
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+      if (n0 + r < N) {
+        float v = act_apply(act_out, mine[r] + bv[r]);
+        if (accumulate) v += ov[r];
+        out[lane * ldo + n0 + r] = v;
+      }
+  }
 }
 
 template <bool BF16>
 int skinny_dispatch(const SkinnyArgs& a, int64_t b0, int bc, hipStream_t s) {
-  dim3 grid(static_cast<unsigned>((a.N + 4 * kSkRows - 1) / (4 * kSkRows)));
   const float* in = a.in + b0 * a.ldi;
   float* out = a.out + b0 * a.ldo;
-#define FF_SK(BCV)                                                                                   \
-  case BCV:                                                                                         \
-    hipLaunchKernelGGL((skinny_kernel<BF16, BCV>), grid, dim3(256), 0, s, in, a.ldi, a.act_in, a.W, \
-                       a.bias, out, a.ldo, a.N, a.K, a.accumulate, a.act_out);                      \
+#define FF_SK(BCV, R)                                                                                      \
+  case BCV:                                                                                               \
+    hipLaunchKernelGGL((skinny_kernel<BF16, BCV, R>), dim3(static_cast<unsigned>((a.N + 4 * R - 1) / (4 * R))), \
+                       dim3(256), 0, s, in, a.ldi, a.act_in, a.W, a.bias, out, a.ldo, a.N, a.K, a.accumulate,   \
+                       a.act_out);                                                                        \
     break;
   switch (bc) {
-    FF_SK(1) FF_SK(2) FF_SK(3) FF_SK(4) FF_SK(5) FF_SK(6) FF_SK(7) FF_SK(8)
+    FF_SK(1, 4) FF_SK(2, 4) FF_SK(3, 4) FF_SK(4, 4) FF_SK(5, 4) FF_SK(6, 4) FF_SK(7, 4) FF_SK(8, 4)
+    FF_SK(9, 4) FF_SK(10, 4) FF_SK(11, 4) FF_SK(12, 4) FF_SK(13, 4) FF_SK(14, 4) FF_SK(15, 4) FF_SK(16, 4)
     default: return fail(FF_EUNSUPPORTED, "skinny_linear: chunk %d", bc);
   }
 #undef FF_SK
@@ -510,8 +568,8 @@ int skinny_linear(const SkinnyArgs& a, hipStream_t s) {
   if (a.K % 8 != 0 || a.ldi % 4 != 0) return fail(FF_EUNSUPPORTED, "skinny_linear: K=%lld must be a multiple of 8", (long long)a.K);
   LaunchScope ls("skinny_linear", s, 2.0 * a.B * a.N * a.K,
                  static_cast<double>(dtype_size(a.dtype)) * a.N * a.K + 4.0 * a.B * (a.K + a.N));
-  for (int64_t b0 = 0; b0 < a.B; b0 += 8) {
-    const int bc = static_cast<int>(a.B - b0 < 8 ? a.B - b0 : 8);
+  for (int64_t b0 = 0; b0 < a.B; b0 += kSkMaxB) {
+    const int bc = static_cast<int>(a.B - b0 < kSkMaxB ? a.B - b0 : kSkMaxB);
     FF_TRY(a.dtype == FF_BF16 ? skinny_dispatch<true>(a, b0, bc, s) : skinny_dispatch<false>(a, b0, bc, s));
   }
   return ls.status();

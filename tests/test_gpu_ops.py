@@ -176,7 +176,8 @@ def test_rope_table_parity(gpu_lib):
 
 
 @pytest.mark.parametrize("B,N,K,dt,act", [(8, 200, 3072, C.BF16, 1), (3, 64, 256, C.F32, 0), (16, 100, 64, C.F32, 1),
-                                          (11, 520, 768, C.BF16, 2)])
+                                          (11, 520, 768, C.BF16, 2), (16, 9216, 3072, C.BF16, 1),
+                                          (20, 300, 1000, C.F32, 1), (1, 33, 8, C.BF16, 0)])
 def test_skinny_linear_parity(gpu_lib, B, N, K, dt, act):
     x = normal(60, (B, K), C.F32)
     w, b = normal(61, (N, K), dt, 0.02), normal(62, (N,), dt, 0.02)
