@@ -166,6 +166,92 @@ __device__ __forceinline__ void epilogue_blocks(const GemmParams& p, const f32x1
 }
 
 
+// Epilogue of a 32 x 64 pair of accumulator blocks (the two column blocks of one block row).
+// The pair goes through a per-wave 32 x 68 float scratch in LDS and comes back with lane l
+// holding rows l / 8 + 8 q (q = 0..3), columns 8 (l % 8) .. + 7: each output row of the pair is
+// one 128-byte line, written by 8 lanes with 16-byte stores.  (A row stride of 68 floats keeps
+// both the column writes and the 16-byte row reads free of bank conflicts.)  All global loads of
+// the pair (bias, gate, residual) are issued before its stores.
+constexpr int PAIR_LD = 68;
+template <int EPI>
+__device__ __forceinline__ void epilogue_pair(const GemmParams& p, const f32x16_t& a0, const f32x16_t& a1, int64_t mb,
+                                              int64_t nb, float* scratch, int lane) {
+  const int fcol = lane & 31, fhalf = lane >> 5;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int row = 8 * (r >> 2) + 4 * fhalf + (r & 3);
+    scratch[row * PAIR_LD + fcol] = a0[r];
+    scratch[row * PAIR_LD + 32 + fcol] = a1[r];
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  const int rr = lane >> 3, cc = (lane & 7) * 8;
+  float v[4][8];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float4 x = *reinterpret_cast<const float4*>(scratch + (rr + 8 * q) * PAIR_LD + cc);
+    const float4 y = *reinterpret_cast<const float4*>(scratch + (rr + 8 * q) * PAIR_LD + cc + 4);
+    v[q][0] = x.x; v[q][1] = x.y; v[q][2] = x.z; v[q][3] = x.w;
+    v[q][4] = y.x; v[q][5] = y.y; v[q][6] = y.z; v[q][7] = y.w;
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  const int64_t n = nb + cc;
+  bf16_t* out = static_cast<bf16_t*>(p.out);
+  if (p.vec_ok && n + 8 <= p.N) {
+    float bv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (p.bias) ld8<true>(p.bias, n, bv);
+    float rs[4][8], gv[4][8];
+    if constexpr (EPI == EPI_GATED) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        int64_t m = mb + rr + 8 * q;
+        if (m >= p.M) m = p.M - 1;
+        ld8<true>(p.resid, m * p.ldr + n, rs[q]);
+        if (p.gate) {
+          const uint64_t smp = static_cast<uint64_t>(m) / static_cast<uint64_t>(p.rows_per_sample);
+          const float4 g0 = *reinterpret_cast<const float4*>(p.gate + smp * p.gate_ld + n);
+          const float4 g1 = *reinterpret_cast<const float4*>(p.gate + smp * p.gate_ld + n + 4);
+          gv[q][0] = g0.x; gv[q][1] = g0.y; gv[q][2] = g0.z; gv[q][3] = g0.w;
+          gv[q][4] = g1.x; gv[q][5] = g1.y; gv[q][6] = g1.z; gv[q][7] = g1.w;
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float x = v[q][e] + bv[e];
+        if constexpr (EPI == EPI_GELU) {
+          if (n + e >= p.gelu_from) x = gelu_tanh_f(x);
+        } else if constexpr (EPI == EPI_GATED) {
+          x = p.gate ? fmaf(gv[q][e], x, rs[q][e]) : x + rs[q][e];
+        }
+        v[q][e] = x;
+      }
+      const int64_t m = mb + rr + 8 * q;
+      if (m < p.M) st8<true>(out, m * p.ldo + n, v[q]);
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int64_t m = mb + rr + 8 * q;
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (m < p.M && n + e < p.N) epi_store<true, EPI>(p, m, n + e, v[q][e]);
+    }
+  }
+}
+
+// All FM block rows of a wave with two column blocks each (row i at mw + 32 i, columns nw ..
+// nw + 63); the recursion keeps accumulator indices compile-time constants.
+template <int EPI, int FM, int I = 0>
+__device__ __forceinline__ void epilogue_pairs(const GemmParams& p, const f32x16_t (&acc)[FM][2], int64_t mw, int64_t nw,
+                                               float* scratch, int lane) {
+  if constexpr (I < FM) {
+    epilogue_pair<EPI>(p, acc[I][0], acc[I][1], mw + I * 32, nw, scratch, lane);
+    epilogue_pairs<EPI, FM, I + 1>(p, acc, mw, nw, scratch, lane);
+  }
+}
+
 template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64, 1) void gemm_bf16_kernel(GemmParams p) {
   constexpr int THREADS = WAVES_M * WAVES_N * 64;
@@ -490,8 +576,8 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // replayed loads still target LDS
   wg_barrier();
-  epilogue_blocks<EPI, FM, FN>(p, acc, m0 + wm * TM, n0 + wn * TN,
-                               reinterpret_cast<float*>(smem) + wave * 32 * 36, lane);
+  static_assert(FN == 2 && 8 * 32 * PAIR_LD * 4 <= 2 * STAGE, "epilogue scratch fits the LDS ring");
+  epilogue_pairs<EPI, FM>(p, acc, m0 + wm * TM, n0 + wn * TN, reinterpret_cast<float*>(smem) + wave * 32 * PAIR_LD, lane);
 }
 
 // ------------------------------------------------------------------ float32
