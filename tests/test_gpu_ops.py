@@ -24,7 +24,7 @@ LIN = [
 
 
 # Shapes with at least one 256 x 256 tile per CU: these take the large-tile kernel.
-LIN_LARGE = [(4133, 4133, 192, C.BF16), (8197, 2088, 128, C.BF16)]
+LIN_LARGE = [(4133, 4133, 192, C.BF16), (8197, 2088, 128, C.BF16), (8200, 2100, 64, C.BF16)]
 
 
 @pytest.mark.parametrize("M,N,K,dt", LIN + LIN_LARGE)
