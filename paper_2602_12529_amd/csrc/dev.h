@@ -55,6 +55,17 @@ __device__ __forceinline__ void ld8(const void* p, int64_t i, float (&o)[8]) {
     o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
   }
 }
+// Eight values stored as bf16 with one non-temporal 16-byte store: for outputs written once and
+// read by a later kernel, so they stream out without displacing cached inputs.
+__device__ __forceinline__ void st8_bf16_nt(void* p, int64_t i, const float (&v)[8]) {
+  typedef uint32_t u32x4_nt __attribute__((ext_vector_type(4)));
+  u32x4_nt u;
+  u.x = uint32_t(f2bf(v[0])) | (uint32_t(f2bf(v[1])) << 16);
+  u.y = uint32_t(f2bf(v[2])) | (uint32_t(f2bf(v[3])) << 16);
+  u.z = uint32_t(f2bf(v[4])) | (uint32_t(f2bf(v[5])) << 16);
+  u.w = uint32_t(f2bf(v[6])) | (uint32_t(f2bf(v[7])) << 16);
+  __builtin_nontemporal_store(u, reinterpret_cast<u32x4_nt*>(static_cast<bf16_t*>(p) + i));
+}
 template <bool BF16>
 __device__ __forceinline__ void st8(void* p, int64_t i, const float (&v)[8]) {
   if constexpr (BF16) {
