@@ -166,27 +166,27 @@ __device__ __forceinline__ void epilogue_blocks(const GemmParams& p, const f32x1
 }
 
 
-// Epilogue of a 32 x 64 pair of accumulator blocks (the two column blocks of one block row).
-// The pair goes through a per-wave 32 x 68 float scratch in LDS and comes back with lane l
-// holding rows l / 8 + 8 q (q = 0..3), columns 8 (l % 8) .. + 7: each output row of the pair is
-// one 128-byte line, written by 8 lanes with 16-byte non-temporal stores (the output streams to
-// memory rather than through the caches: -5 to -8% on the write-bound epilogue).  (A row stride of 68 floats keeps
-// both the column writes and the 16-byte row reads free of bank conflicts.)  All global loads of
-// the pair (bias, gate, residual) are issued before its stores.
+// Epilogue of a wave's FM pairs of 32 x 64 accumulator blocks (the two column blocks of one
+// block row; pair i at rows mw + 32 i, columns nw .. nw + 63).  Each pair goes through a per-wave
+// 32 x 68 float scratch in LDS and comes back with lane l holding rows l / 8 + 8 q (q = 0..3),
+// columns 8 (l % 8) .. + 7: every output row of a pair is one 128-byte line, written by 8 lanes
+// with 16-byte non-temporal stores (the output streams to memory rather than through the caches:
+// -5 to -8% on the write-bound epilogue).  A row stride of 68 floats keeps both the column writes
+// and the 16-byte row reads free of bank conflicts.  Bias and gate (one row when the wave's rows
+// lie in one sample) are loaded once, and each pair's residual rows are issued two pairs ahead,
+// before the previous pair's stores, so no pair waits on the stores of another.
 constexpr int PAIR_LD = 68;
-template <int EPI>
-__device__ __forceinline__ void epilogue_pair(const GemmParams& p, const f32x16_t& a0, const f32x16_t& a1, int64_t mb,
-                                              int64_t nb, float* scratch, int lane) {
+template <int EPI, int FM, int I = 0>
+__device__ __forceinline__ void transpose_pair(const f32x16_t (&acc)[FM][2], float* scratch, int lane, float (&v)[4][8]) {
   const int fcol = lane & 31, fhalf = lane >> 5;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int row = 8 * (r >> 2) + 4 * fhalf + (r & 3);
-    scratch[row * PAIR_LD + fcol] = a0[r];
-    scratch[row * PAIR_LD + 32 + fcol] = a1[r];
+    scratch[row * PAIR_LD + fcol] = acc[I][0][r];
+    scratch[row * PAIR_LD + 32 + fcol] = acc[I][1][r];
   }
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   const int rr = lane >> 3, cc = (lane & 7) * 8;
-  float v[4][8];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const float4 x = *reinterpret_cast<const float4*>(scratch + (rr + 8 * q) * PAIR_LD + cc);
@@ -195,62 +195,88 @@ __device__ __forceinline__ void epilogue_pair(const GemmParams& p, const f32x16_
     v[q][4] = y.x; v[q][5] = y.y; v[q][6] = y.z; v[q][7] = y.w;
   }
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-  const int64_t n = nb + cc;
-  bf16_t* out = static_cast<bf16_t*>(p.out);
-  if (p.vec_ok && n + 8 <= p.N) {
-    float bv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    if (p.bias) ld8<true>(p.bias, n, bv);
-    float rs[4][8], gv[4][8];
-    if constexpr (EPI == EPI_GATED) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        int64_t m = mb + rr + 8 * q;
-        if (m >= p.M) m = p.M - 1;
-        ld8<true>(p.resid, m * p.ldr + n, rs[q]);
-        if (p.gate) {
-          const uint64_t smp = static_cast<uint64_t>(m) / static_cast<uint64_t>(p.rows_per_sample);
-          const float4 g0 = *reinterpret_cast<const float4*>(p.gate + smp * p.gate_ld + n);
-          const float4 g1 = *reinterpret_cast<const float4*>(p.gate + smp * p.gate_ld + n + 4);
-          gv[q][0] = g0.x; gv[q][1] = g0.y; gv[q][2] = g0.z; gv[q][3] = g0.w;
-          gv[q][4] = g1.x; gv[q][5] = g1.y; gv[q][6] = g1.z; gv[q][7] = g1.w;
-        }
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        float x = v[q][e] + bv[e];
-        if constexpr (EPI == EPI_GELU) {
-          if (n + e >= p.gelu_from) x = gelu_tanh_f(x);
-        } else if constexpr (EPI == EPI_GATED) {
-          x = p.gate ? fmaf(gv[q][e], x, rs[q][e]) : x + rs[q][e];
-        }
-        v[q][e] = x;
-      }
-      const int64_t m = mb + rr + 8 * q;
-      if (m < p.M) st8_bf16_nt(out, m * p.ldo + n, v[q]);
-    }
-  } else {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int64_t m = mb + rr + 8 * q;
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (m < p.M && n + e < p.N) epi_store<true, EPI>(p, m, n + e, v[q][e]);
-    }
-  }
 }
 
-// All FM block rows of a wave with two column blocks each (row i at mw + 32 i, columns nw ..
-// nw + 63); the recursion keeps accumulator indices compile-time constants.
-template <int EPI, int FM, int I = 0>
+template <int EPI, int FM>
 __device__ __forceinline__ void epilogue_pairs(const GemmParams& p, const f32x16_t (&acc)[FM][2], int64_t mw, int64_t nw,
                                                float* scratch, int lane) {
-  if constexpr (I < FM) {
-    epilogue_pair<EPI>(p, acc[I][0], acc[I][1], mw + I * 32, nw, scratch, lane);
-    epilogue_pairs<EPI, FM, I + 1>(p, acc, mw, nw, scratch, lane);
+  static_assert(FM <= 4, "pairs per wave");
+  const int rr = lane >> 3, cc = (lane & 7) * 8;
+  const int64_t n = nw + cc;
+  bf16_t* out = static_cast<bf16_t*>(p.out);
+  // Per lane: 16-byte vector path, or element-wise at a ragged right edge / unaligned operands.
+  // The transposes below involve every lane, so they stay outside any per-lane branch.
+  const bool vec = p.vec_ok && n + 8 <= p.N;
+  float bv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (vec && p.bias) ld8<true>(p.bias, n, bv);
+  uint4 rs[2][4];     // residual rows of two pairs in flight (bf16)
+  auto load_resid = [&](int i, uint4 (&dst)[4]) {
+    if (!vec) return;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      int64_t m = mw + 32 * i + rr + 8 * q;
+      if (m >= p.M) m = p.M - 1;
+      dst[q] = *reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(p.resid) + m * p.ldr + n);
+    }
+  };
+  float gv[8];        // gate row of the wave's sample, when its rows lie in one sample
+  bool one_sample = false;
+  if constexpr (EPI == EPI_GATED) {
+    load_resid(0, rs[0]);
+    if (FM > 1) load_resid(1, rs[1]);
+    const int64_t m_lo = mw < p.M ? mw : p.M - 1, m_hi = mw + 32 * FM - 1 < p.M ? mw + 32 * FM - 1 : p.M - 1;
+    const uint64_t s_lo = static_cast<uint64_t>(m_lo) / static_cast<uint64_t>(p.rows_per_sample);
+    one_sample = s_lo == static_cast<uint64_t>(m_hi) / static_cast<uint64_t>(p.rows_per_sample);
+    if (vec && p.gate && one_sample) {
+      const float4 g0 = *reinterpret_cast<const float4*>(p.gate + s_lo * p.gate_ld + n);
+      const float4 g1 = *reinterpret_cast<const float4*>(p.gate + s_lo * p.gate_ld + n + 4);
+      gv[0] = g0.x; gv[1] = g0.y; gv[2] = g0.z; gv[3] = g0.w;
+      gv[4] = g1.x; gv[5] = g1.y; gv[6] = g1.z; gv[7] = g1.w;
+    }
   }
+  float v[4][8];
+#define FF_PAIR(I)                                                                                   \
+  if constexpr (I < FM) {                                                                            \
+    transpose_pair<EPI, FM, I>(acc, scratch, lane, v);                                               \
+    for (int q = 0; q < 4; ++q) {                                                                    \
+      const int64_t m = mw + 32 * (I) + rr + 8 * q;                                                  \
+      if (!vec) {                                                                                    \
+        for (int e = 0; e < 8; ++e)                                                                  \
+          if (m < p.M && n + e < p.N) epi_store<true, EPI>(p, m, n + e, v[q][e]);                    \
+        continue;                                                                                    \
+      }                                                                                              \
+      float g[8], r8[8];                                                                             \
+      if constexpr (EPI == EPI_GATED) {                                                              \
+        const uint32_t w[4] = {rs[(I) & 1][q].x, rs[(I) & 1][q].y, rs[(I) & 1][q].z, rs[(I) & 1][q].w};  \
+        for (int j = 0; j < 4; ++j) {                                                                \
+          r8[2 * j] = __uint_as_float(w[j] << 16);                                                   \
+          r8[2 * j + 1] = __uint_as_float(w[j] & 0xffff0000u);                                       \
+        }                                                                                            \
+        if (p.gate) {                                                                                \
+          if (one_sample) {                                                                          \
+            for (int e = 0; e < 8; ++e) g[e] = gv[e];                                                \
+          } else {                                                                                   \
+            const int64_t mc = m < p.M ? m : p.M - 1;                                                \
+            const uint64_t smp = static_cast<uint64_t>(mc) / static_cast<uint64_t>(p.rows_per_sample); \
+            for (int e = 0; e < 8; ++e) g[e] = p.gate[smp * p.gate_ld + n + e];                      \
+          }                                                                                          \
+        }                                                                                            \
+      }                                                                                              \
+      for (int e = 0; e < 8; ++e) {                                                                  \
+        float x = v[q][e] + bv[e];                                                                   \
+        if constexpr (EPI == EPI_GELU) {                                                             \
+          if (n + e >= p.gelu_from) x = gelu_tanh_f(x);                                              \
+        } else if constexpr (EPI == EPI_GATED) {                                                     \
+          x = p.gate ? fmaf(g[e], x, r8[e]) : x + r8[e];                                             \
+        }                                                                                            \
+        v[q][e] = x;                                                                                 \
+      }                                                                                              \
+      if (m < p.M) st8_bf16_nt(out, m * p.ldo + n, v[q]);                                            \
+    }                                                                                                \
+    if constexpr (EPI == EPI_GATED && (I) + 2 < FM) load_resid((I) + 2, rs[(I) & 1]);                 \
+  }
+  FF_PAIR(0) FF_PAIR(1) FF_PAIR(2) FF_PAIR(3)
+#undef FF_PAIR
 }
 
 template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI>
