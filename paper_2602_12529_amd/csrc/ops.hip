@@ -251,17 +251,16 @@ __global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
   }
 }
 
-// bf16 fast path: a block of 4 waves normalises 32 rows of one sample.  The
-// sample's (1 + scale) and shift are staged once in LDS; each wave walks 8
-// rows with the next row's loads issued before the current row is finished.
-constexpr int kNormBlockRows = 32;
-
-template <int NCH>
+// bf16 fast path: a block of 4 waves normalises 4 RPW rows of one sample (32, or 8 when
+// there are too few rows to give every CU a block).  The sample's (1 + scale) and shift are
+// staged once in LDS; each wave walks RPW rows with the next row's loads issued before the
+// current row is finished.
+template <int NCH, int RPW>
 __global__ __launch_bounds__(256) void norm_lds_kernel(NormArgs a) {
   extern __shared__ __attribute__((aligned(16))) float mod_s[];   // [2][H]: mul, add
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t H = a.H;
-  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kNormBlockRows;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * 4 * RPW;
   const int64_t b = r0 / a.rows_per_sample;
   float* mul_s = mod_s;
   float* add_s = mod_s + H;
@@ -275,7 +274,6 @@ __global__ __launch_bounds__(256) void norm_lds_kernel(NormArgs a) {
   const float invH = 1.0f / static_cast<float>(H);
   const bf16_t* __restrict__ xp = static_cast<const bf16_t*>(a.x);
   bf16_t* __restrict__ yp = static_cast<bf16_t*>(a.y);
-  constexpr int RPW = kNormBlockRows / 4;
   const int64_t rw = r0 + wave * RPW;
   float v[NCH][8], nx[NCH][8];
   if (rw < a.rows) {
@@ -338,13 +336,15 @@ int norm_dispatch(const NormArgs& a, hipStream_t s) {
   const bool fits = a.H % 512 == 0 && a.ldx % 8 == 0 && a.ldy % 8 == 0 && aligned16(a.x) && aligned16(a.y) && mod_ok;
   if (BF16 && fits) nch = static_cast<int>(a.H / 512);
   if (nch > 8) nch = 0;
-  const bool one_sample_blocks = a.rows_per_sample % kNormBlockRows == 0 || a.rows <= a.rows_per_sample;
+  const int64_t block_rows = a.rows >= 32 * 512 ? 32 : 8;   // at least ~2 blocks per CU
+  const bool one_sample_blocks = a.rows_per_sample % block_rows == 0 || a.rows <= a.rows_per_sample;
   if (BF16 && nch > 0 && nch <= 6 && one_sample_blocks && !a.w && !a.bias) {
-    const dim3 grid(static_cast<unsigned>((a.rows + kNormBlockRows - 1) / kNormBlockRows));
+    const dim3 grid(static_cast<unsigned>((a.rows + block_rows - 1) / block_rows));
     const size_t shm = 2 * a.H * sizeof(float);
-    switch (nch) {
-#define FF_NL(N) case N: hipLaunchKernelGGL((norm_lds_kernel<N>), grid, dim3(256), shm, s, a); return FF_OK;
-      FF_NL(1) FF_NL(2) FF_NL(3) FF_NL(4) FF_NL(5) FF_NL(6)
+    switch (nch * 100 + static_cast<int>(block_rows)) {
+#define FF_NL(N, R) case N * 100 + R: hipLaunchKernelGGL((norm_lds_kernel<N, R / 4>), grid, dim3(256), shm, s, a); return FF_OK;
+      FF_NL(1, 32) FF_NL(2, 32) FF_NL(3, 32) FF_NL(4, 32) FF_NL(5, 32) FF_NL(6, 32)
+      FF_NL(1, 8) FF_NL(2, 8) FF_NL(3, 8) FF_NL(4, 8) FF_NL(5, 8) FF_NL(6, 8)
 #undef FF_NL
     }
   }

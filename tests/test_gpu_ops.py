@@ -133,6 +133,24 @@ def test_norm_modulate_parity(gpu_lib, rows, H, dt, kind):
     assert rel(host(Y), ref) <= (1e-5 if dt == C.F32 else 6e-3)
 
 
+@pytest.mark.parametrize("rows,rps", [(16384, 4096), (4096, 512), (1003, 1003), (40, 8)])
+def test_norm_modulate_staged_path(gpu_lib, rows, rps):
+    """bf16 rows of one sample per block (the LDS-staged path): 32-row blocks for many rows, 8-row
+    blocks for few, a ragged single-sample tail."""
+    H = 3072
+    x = normal(42, (rows, H), C.BF16, 2.0) + 0.3
+    ns = (rows + rps - 1) // rps
+    mod = normal(43, (ns, 6 * H), C.F32, 0.5)
+    X = dev(x, C.BF16)
+    Y = torch.empty_like(X)
+    Mo = dev(mod)
+    gpu_lib.norm_modulate(X, Y, shift=Mo, scale=Mo[:, H:], mod_ld=6 * H, rows_per_sample=rps, norm_kind=C.NORM_RMS)
+    torch.cuda.synchronize()
+    b = np.arange(rows) // rps
+    ref = odit.norm(host(X), C.NORM_RMS, 1e-6) * (1 + mod[b, H:2 * H]) + mod[b, :H]
+    assert rel(host(Y), ref) <= 6e-3
+
+
 @pytest.mark.parametrize("dt", [C.BF16, C.F32], ids=["bf16", "f32"])
 def test_qk_norm_rope_parity(gpu_lib, dt):
     B, heads, d = 2, 3, 128 if dt == C.BF16 else 16
