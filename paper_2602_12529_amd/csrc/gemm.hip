@@ -498,14 +498,11 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
   const uint32_t b_off = static_cast<uint32_t>((lrow * p.ldw + lck * 8) * 2);
   const uint32_t b_step = static_cast<uint32_t>(32 * p.ldw * 2);
   const uint32_t smem_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
-  // A slab index past the end replays the last slab into a buffer that is never read again,
-  // so every phase has the same shape.
   auto rsrc_b = [&](int s) {
-    const int64_t db = static_cast<int64_t>(s < KT ? s : KT - 1) * ROWB;
+    const int64_t db = static_cast<int64_t>(s) * ROWB;
     return buffer_rsrc(b_tile + db, static_cast<uint64_t>(b_bytes - db));
   };
   auto issue_a = [&](int s, int dst) {   // slab s's A rows into the buffer of slab dst
-    if (s >= KT) s = KT - 1;
     const bool second = two && s >= KT1;
     const int64_t da = static_cast<int64_t>(second ? s - KT1 : s) * ROWB;
     const u32x4_t r = buffer_rsrc((second ? a2_tile : a1_tile) + da, static_cast<uint64_t>((second ? a2_bytes : a1_bytes) - da));
@@ -555,19 +552,24 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
         }
   };
 
-  // Two code paths, one per group (the group is wave-uniform), with the same sequence of
-  // barriers; a single loop branching on the group would keep both groups' fragments live
-  // at once.  Neither loop branches: past the last slab the loads replay and the reads
-  // fetch unused data.
+  // Two code paths, one per group (the group is wave-uniform), with the same number of
+  // barriers; a single loop branching on the group would keep both groups' fragments live at
+  // once.  The last two slabs are peeled: no loads are issued past the end of K, and after the
+  // barrier that ends phase 2 KT - 2 nothing reads the LDS ring any more, so group 0 starts its
+  // epilogue while group 1 computes the last slab (each wave's scratch is its own).
   if (grp == 0) {
     issue_a(0, 0);
-    issue_a(1, 1);
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(A_INS) : "memory");   // A of slab 0 has landed
+    if (KT > 1) {
+      issue_a(1, 1);
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(A_INS) : "memory");   // A of slab 0 has landed
+    } else {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
     wg_barrier();
     read_frags(0);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     wg_barrier();
-    for (int s = 0; s < KT; ++s) {
+    for (int s = 0; s + 2 < KT; ++s) {
       compute(nullptr, 0);                                 // phase 2s
       __builtin_amdgcn_sched_barrier(0);
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");    // A of slab s + 1 has landed
@@ -578,19 +580,37 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       wg_barrier();
     }
+    if (KT > 1) {                                          // slab KT - 2
+      compute(nullptr, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      wg_barrier();
+      read_frags(KT - 1);
+      __builtin_amdgcn_sched_barrier(0);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      wg_barrier();
+    }
+    compute(nullptr, 0);                                   // slab KT - 1
+    __builtin_amdgcn_sched_barrier(0);
+    wg_barrier();
   } else {
     {
       const uint32_t lds = smem_base + w4 * 1024 + BM * ROWB;
-      const u32x4_t r0 = rsrc_b(0), r1 = rsrc_b(1);
+      const u32x4_t r0 = rsrc_b(0);
 #pragma unroll
       for (int q = 0; q < B_INS; ++q) dma_buf16(r0, b_off + q * b_step, lds + q * 4096);
+      if (KT > 1) {
+        const u32x4_t r1 = rsrc_b(1);
 #pragma unroll
-      for (int q = 0; q < B_INS; ++q) dma_buf16(r1, b_off + q * b_step, lds + STAGE + q * 4096);
+        for (int q = 0; q < B_INS; ++q) dma_buf16(r1, b_off + q * b_step, lds + STAGE + q * 4096);
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(B_INS) : "memory");   // W of slab 0 has landed
+      } else {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      }
     }
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(B_INS) : "memory");   // W of slab 0 has landed
     wg_barrier();
     wg_barrier();
-    for (int s = 0; s < KT; ++s) {
+    for (int s = 0; s + 2 < KT; ++s) {
       read_frags(s);                                       // phase 2s
       __builtin_amdgcn_sched_barrier(0);
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
@@ -601,9 +621,23 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
       __builtin_amdgcn_sched_barrier(0);
       wg_barrier();
     }
+    if (KT > 1) {                                          // slab KT - 2
+      read_frags(KT - 2);
+      __builtin_amdgcn_sched_barrier(0);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      wg_barrier();
+      compute(nullptr, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      wg_barrier();
+    }
+    read_frags(KT - 1);                                    // slab KT - 1
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    wg_barrier();
+    compute(nullptr, 0);
+    __builtin_amdgcn_sched_barrier(0);
   }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // replayed loads still target LDS
-  wg_barrier();
   static_assert(FN == 2 && 8 * 32 * PAIR_LD * 4 <= 2 * STAGE, "epilogue scratch fits the LDS ring");
   epilogue_pairs<EPI, FM>(p, acc, m0 + wm * TM, n0 + wn * TN, reinterpret_cast<float*>(smem) + wave * 32 * PAIR_LD, lane);
 }
