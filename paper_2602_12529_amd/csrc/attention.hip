@@ -275,13 +275,13 @@ __global__ __launch_bounds__(WAVES * 64, 1) void attn_bf16_d128(AttnParams p) {
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   const float inv = 1.0f / l_tot;
-  const int64_t q = q0 + ql;
-  if (q >= p.n_q) return;
-  const int64_t b = bh / p.heads, h = bh % p.heads;
-  bf16_t* row;
-  if (q < p.split) row = p.out0 + (b * p.split + q) * p.ldo;
-  else row = p.out1 + (b * (p.n_q - p.split) + (q - p.split)) * p.ldo;
-  row += h * D;
+  // O^T blocks to row-major bf16 through LDS (the ring is free once every wave is past its last
+  // tile): a lane holds 4-element pieces of one query's row, so it writes them into a per-wave
+  // 32 x 132 bf16 scratch (the 264-byte stride keeps the 8-byte writes and the 16-byte reads
+  // conflict-free), and each query row then leaves as 256 contiguous bytes from 16 lanes.
+  constexpr int OLD = 132;
+  __syncthreads();
+  bf16_t* os = reinterpret_cast<bf16_t*>(smem) + wave * 32 * OLD;
 #pragma unroll
   for (int db = 0; db < 4; ++db)
 #pragma unroll
@@ -289,8 +289,22 @@ __global__ __launch_bounds__(WAVES * 64, 1) void attn_bf16_d128(AttnParams p) {
       uint2 w;
       w.x = uint32_t(f2bf(o[db][4 * u] * inv)) | (uint32_t(f2bf(o[db][4 * u + 1] * inv)) << 16);
       w.y = uint32_t(f2bf(o[db][4 * u + 2] * inv)) | (uint32_t(f2bf(o[db][4 * u + 3] * inv)) << 16);
-      *reinterpret_cast<uint2*>(row + 32 * db + 8 * u + 4 * g) = w;
+      *reinterpret_cast<uint2*>(os + ql * OLD + 32 * db + 8 * u + 4 * g) = w;
     }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  const int64_t b = bh / p.heads, h = bh % p.heads;
+  const int cl = (lane & 15) * 8;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int r = k * 4 + (lane >> 4);
+    const uint4 w = *reinterpret_cast<const uint4*>(os + r * OLD + cl);
+    const int64_t q = q0 + r;
+    if (q >= p.n_q) continue;
+    bf16_t* row;
+    if (q < p.split) row = p.out0 + (b * p.split + q) * p.ldo;
+    else row = p.out1 + (b * (p.n_q - p.split) + (q - p.split)) * p.ldo;
+    *reinterpret_cast<uint4*>(row + h * D + cl) = w;
+  }
 }
 
 // ------------------------------------------------------------------ float32
