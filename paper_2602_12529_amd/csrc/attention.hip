@@ -110,10 +110,14 @@ __global__ __launch_bounds__(WAVES * 64, 1) void attn_bf16_d128(AttnParams p) {
   // turns every LDS wait into lgkmcnt(0) (and adds a vmcnt(0) before the reads), which
   // defeats the read prefetch.  Their completion is ordered explicitly instead (vmcnt wait
   // and barrier before a tile is read; its buffer is refilled only after the next barrier).
+  // (M0 is written here as in the GEMM's loads: no compiler value lives in M0 in this kernel.)
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
   auto dma16 = [](const void* src, uint32_t lds_addr) {
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
                  :: "s"(lds_addr), "v"(src) : "memory", "m0");
   };
+#pragma clang diagnostic pop
   const uint32_t smem_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
   auto issue = [&](int tile) {
     const int kv0 = (tile < ntiles ? tile : ntiles - 1) * KT;

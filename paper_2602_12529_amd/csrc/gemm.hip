@@ -449,10 +449,17 @@ __device__ __forceinline__ u32x4_t buffer_rsrc(const void* base, uint64_t bytes)
 // Written as inline assembly: the compiler's wait-count pass cannot tell an LDS-DMA
 // destination from the fragment reads and would wait for every load before any LDS read;
 // the kernel orders them itself (vmcnt wait + barrier before a slab is read).
+// The statement writes M0, a register the compiler reserves (hence clang's -Winline-asm note on
+// the clobber).  Nothing in these kernels keeps a compiler value in M0 across it: the compiler
+// uses M0 only for its own LDS-DMA builtins, s_sendmsg, lane reads with an SGPR index and
+// relative moves, and none of them occur here; the clobber keeps the declaration honest.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma_buf16(const u32x4_t& rsrc, uint32_t voff, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                :: "s"(lds), "v"(voff), "s"(rsrc) : "memory", "m0");
 }
+#pragma clang diagnostic pop
 
 template <int EPI>
 __global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
