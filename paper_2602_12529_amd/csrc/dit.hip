@@ -267,9 +267,8 @@ SkinnyArgs skinny_args(int dtype, int64_t B, int64_t N, int64_t K, const float* 
 
 // QK norm + RoPE + relayout for one stream's rows: source row of token i of sample b is
 // b * src_rows + src_off + i.
-int qkv_stream(const ff_dit_config& c, const Plan& p, void* ws, const void* qkv_base, int64_t ld, int64_t src_rows,
-               int64_t src_off, int64_t n_tok, int64_t tok_offset, const void* qn, const void* kn, bool rope,
-               hipStream_t s) {
+QkvArgs qkv_args(const ff_dit_config& c, const Plan& p, void* ws, const void* qkv_base, int64_t ld, int64_t src_rows,
+                 int64_t src_off, int64_t n_tok, int64_t tok_offset, const void* qn, const void* kn, bool rope) {
   const size_t es = dtype_size(c.dtype);
   const char* base = static_cast<const char*>(qkv_base) + src_off * ld * es;
   QkvArgs a{};
@@ -286,7 +285,13 @@ int qkv_stream(const ff_dit_config& c, const Plan& p, void* ws, const void* qkv_
   a.Q = at(ws, p.q); a.Kd = at(ws, p.k); a.Vt = at(ws, p.vt);
   a.v_transposed = c.dtype == FF_BF16;
   a.src_rows = src_rows;
-  return qk_norm_rope(a, s);
+  return a;
+}
+
+int qkv_stream(const ff_dit_config& c, const Plan& p, void* ws, const void* qkv_base, int64_t ld, int64_t src_rows,
+               int64_t src_off, int64_t n_tok, int64_t tok_offset, const void* qn, const void* kn, bool rope,
+               hipStream_t s) {
+  return qk_norm_rope(qkv_args(c, p, ws, qkv_base, ld, src_rows, src_off, n_tok, tok_offset, qn, kn, rope), s);
 }
 
 int attention_joint(const ff_dit_config& c, const Plan& p, void* ws, void* out_txt, void* out_img, hipStream_t s) {
@@ -321,10 +326,16 @@ int dual_block(const ff_dit& m, const Plan& p, void* ws, int i, const float* c32
     FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 6 * H, H, c32, ACT_SILU, st[k]->mod, mods[k]), s));
     FF_TRY(norm_modulate(norm_args(c, rows[k], cur[k], Y + y_off[k] * es, mods[k], mods[k] + H, 6 * H, ntok[k]), s));
   }
-  FF_TRY(gemm2(gemm_args(c.dtype, rows[0], 3 * H, H, Y + y_off[0] * es, H, st[0]->qkv, qkv_k[0], 3 * H, EPI_NONE),
-               gemm_args(c.dtype, rows[1], 3 * H, H, Y + y_off[1] * es, H, st[1]->qkv, qkv_k[1], 3 * H, EPI_NONE), s));
-  for (int k = 0; k < 2; ++k)
-    FF_TRY(qkv_stream(c, p, ws, qkv_k[k], 3 * H, ntok[k], 0, ntok[k], k == 0 ? 0 : p.Nt, st[k]->qn, st[k]->kn, k == 1, s));
+  // QKV projections of both streams; the QK norm, rotation and relayout run in the GEMM epilogue
+  // when the shapes allow (gemm2 falls back to a second pass otherwise).
+  QkvArgs qa[2];
+  GemmArgs gq[2];
+  for (int k = 0; k < 2; ++k) {
+    qa[k] = qkv_args(c, p, ws, qkv_k[k], 3 * H, ntok[k], 0, ntok[k], k == 0 ? 0 : p.Nt, st[k]->qn, st[k]->kn, k == 1);
+    gq[k] = gemm_args(c.dtype, rows[k], 3 * H, H, Y + y_off[k] * es, H, st[k]->qkv, qkv_k[k], 3 * H, EPI_QKV);
+    gq[k].qkv = &qa[k];
+  }
+  FF_TRY(gemm2(gq[0], gq[1], s));
   FF_TRY(attention_joint(c, p, ws, O, O + p.B * p.Nt * H * es, s));
   GemmArgs go[2], g1[2], g2[2];
   for (int k = 0; k < 2; ++k) {

@@ -77,7 +77,10 @@ enum Epi : int {
   EPI_NONE = 0,       // out = acc + bias
   EPI_GELU = 1,       // out = gelu_tanh(acc + bias) for columns >= gelu_from, else acc + bias
   EPI_GATED = 2,      // out = resid + gate[b] * (acc + bias); gate null: out = resid + acc + bias
+  EPI_QKV = 3,        // columns [Q | K | V] of acc + bias go through qk_norm_rope(*qkv) (fused when possible)
 };
+
+struct QkvArgs;
 
 struct GemmArgs {
   int dtype;
@@ -93,6 +96,8 @@ struct GemmArgs {
   const float* gate; int64_t gate_ld;   // EPI_GATED: gate[(m / rows_per_sample) * gate_ld + n]
   const void* resid; int64_t ldr;       // EPI_GATED: residual (may alias out)
   int64_t rows_per_sample;
+  const QkvArgs* qkv = nullptr;         // EPI_QKV: where Q, K and V^T go (out still names the packed
+                                        // [Q | K | V] buffer, used when the fused path does not apply)
 };
 int gemm(const GemmArgs& a, hipStream_t s);
 // Two GEMMs with the same epilogue kind, launched together when both are large bf16 problems.

@@ -40,8 +40,14 @@ struct GemmParams {
   int64_t gelu_from;
   const float* gate; int64_t gate_ld;
   const void* resid; int64_t ldr;
-  int64_t rows_per_sample;
+  int64_t rows_per_sample;   // EPI_QKV: tokens per sample of the stream
   int vec_ok;   // 16-byte vector access of bias, gate, resid and out is aligned
+  // EPI_QKV (fused): Q, K [B, heads, n_joint, 128] and V^T [B, heads, 128, n_joint] outputs, the
+  // per-head RMSNorm weights, the (cos, sin) table [tokens, 64] (null: no rotation).
+  bf16_t* q_out; bf16_t* k_out; bf16_t* vt_out;
+  const bf16_t* q_w; const bf16_t* k_w; const float2* rope;
+  int64_t hidden, n_joint, tok_offset;
+  int heads; float eps;
 };
 
 template <bool BF16, int EPI>
@@ -176,14 +182,14 @@ __device__ __forceinline__ void epilogue_blocks(const GemmParams& p, const f32x1
 // lie in one sample) are loaded once, and each pair's residual rows are issued two pairs ahead,
 // before the previous pair's stores, so no pair waits on the stores of another.
 constexpr int PAIR_LD = 68;
-template <int EPI, int FM, int I = 0>
-__device__ __forceinline__ void transpose_pair(const f32x16_t (&acc)[FM][2], float* scratch, int lane, float (&v)[4][8]) {
+__device__ __forceinline__ void transpose_blocks(const f32x16_t& a0, const f32x16_t& a1, float* scratch, int lane,
+                                                 float (&v)[4][8]) {
   const int fcol = lane & 31, fhalf = lane >> 5;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int row = 8 * (r >> 2) + 4 * fhalf + (r & 3);
-    scratch[row * PAIR_LD + fcol] = acc[I][0][r];
-    scratch[row * PAIR_LD + 32 + fcol] = acc[I][1][r];
+    scratch[row * PAIR_LD + fcol] = a0[r];
+    scratch[row * PAIR_LD + 32 + fcol] = a1[r];
   }
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   const int rr = lane >> 3, cc = (lane & 7) * 8;
@@ -195,6 +201,10 @@ __device__ __forceinline__ void transpose_pair(const f32x16_t (&acc)[FM][2], flo
     v[q][4] = y.x; v[q][5] = y.y; v[q][6] = y.z; v[q][7] = y.w;
   }
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+}
+template <int EPI, int FM, int I = 0>
+__device__ __forceinline__ void transpose_pair(const f32x16_t (&acc)[FM][2], float* scratch, int lane, float (&v)[4][8]) {
+  transpose_blocks(acc[I][0], acc[I][1], scratch, lane, v);
 }
 
 template <int EPI, int FM>
@@ -277,6 +287,133 @@ __device__ __forceinline__ void epilogue_pairs(const GemmParams& p, const f32x16
   }
   FF_PAIR(0) FF_PAIR(1) FF_PAIR(2) FF_PAIR(3)
 #undef FF_PAIR
+}
+
+// Fused QKV epilogue of a 64-token x 128-column wave tile, i.e. one head of Q, K or V for 64
+// tokens of one stream (the QK norm and the rotation of the attention input, done while the
+// projection is still in registers instead of by a second pass over the packed output).
+//   Q, K: x = acc + bias; RMS over the head's 128 columns (a row's columns sit in 8 lanes of the
+//         wave); y = x / rms * w; each column pair (2j, 2j + 1) is rotated by the token's
+//         (cos, sin) of pair j; rows go to [B, heads, n_joint, 128] at tok_offset + token.
+//   V:    x = acc + bias, written transposed to [B, heads, 128, n_joint] through a per-wave
+//         128 x 68 bf16 LDS scratch, so each head row leaves as 128 contiguous bytes.
+// The norm is taken of the float32 projection (the two-pass path reads it back rounded to bf16).
+constexpr int VT_LD = 68;   // bf16 row stride of the V^T scratch: conflict-free 8-byte writes
+constexpr int QKV_SCRATCH = 128 * VT_LD * 2;   // bytes per wave (the Q/K transposes use less)
+template <int FM, int FN>
+__device__ __forceinline__ void epilogue_qkv(const GemmParams& p, const f32x16_t (&acc)[FM][FN], int64_t mw, int64_t nw,
+                                             char* scratch, int lane) {
+  static_assert(FM == 2 && FN == 4, "64 x 128 wave tile");
+  const int part = static_cast<int>(nw / p.hidden);            // 0 Q, 1 K, 2 V (wave-uniform)
+  const int64_t head = (nw % p.hidden) / 128;
+  const int64_t S = p.rows_per_sample;
+  const bf16_t* bias = static_cast<const bf16_t*>(p.bias);
+  // Tokens of this wave: rows mw .. mw + 63 (clipped at M); one sample when they do not straddle.
+  const int64_t m_last = mw + 63 < p.M ? mw + 63 : p.M - 1;
+  const int64_t b_lo = mw / S;
+  const bool one_sample = b_lo == m_last / S;
+  if (part < 2) {
+    const int rr = lane >> 3, cc = (lane & 7) * 8;
+    bf16_t* dst = part == 0 ? p.q_out : p.k_out;
+    const bf16_t* wn = part == 0 ? p.q_w : p.k_w;
+    float bv[2][8], wv[2][8];
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+      if (bias) {
+        ld8<true>(bias, nw + 64 * h2 + cc, bv[h2]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) bv[h2][e] = 0.f;
+      }
+      ld8<true>(wn, 64 * h2 + cc, wv[h2]);
+    }
+    float* fs = reinterpret_cast<float*>(scratch);
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      float v[2][4][8];
+      transpose_blocks(acc[i][0], acc[i][1], fs, lane, v[0]);
+      transpose_blocks(acc[i][2], acc[i][3], fs, lane, v[1]);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t m = mw + 32 * i + rr + 8 * q;
+        float ss = 0.f;
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            v[h2][q][e] += bv[h2][e];
+            ss = fmaf(v[h2][q][e], v[h2][q][e], ss);
+          }
+        ss += __shfl_xor(ss, 1, 64);
+        ss += __shfl_xor(ss, 2, 64);
+        ss += __shfl_xor(ss, 4, 64);
+        const float rstd = rsqrtf(ss * (1.0f / 128.0f) + p.eps);
+        const int64_t mc = m < p.M ? m : p.M - 1;
+        const int64_t b = one_sample ? b_lo : mc / S;
+        const int64_t tok = mc - b * S;
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2) {
+          float cs[8];
+          if (p.rope) {
+            const float4* rp = reinterpret_cast<const float4*>(p.rope + tok * 64 + 32 * h2 + cc / 2);
+            const float4 r0 = rp[0], r1 = rp[1];
+            cs[0] = r0.x; cs[1] = r0.y; cs[2] = r0.z; cs[3] = r0.w; cs[4] = r1.x; cs[5] = r1.y; cs[6] = r1.z; cs[7] = r1.w;
+          } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) { cs[2 * j] = 1.f; cs[2 * j + 1] = 0.f; }
+          }
+          float y[8];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float x0 = v[h2][q][2 * j] * rstd * wv[h2][2 * j], x1 = v[h2][q][2 * j + 1] * rstd * wv[h2][2 * j + 1];
+            y[2 * j] = x0 * cs[2 * j] - x1 * cs[2 * j + 1];
+            y[2 * j + 1] = x0 * cs[2 * j + 1] + x1 * cs[2 * j];
+          }
+          if (m < p.M) st8<true>(dst, ((b * p.heads + head) * p.n_joint + p.tok_offset + tok) * 128 + 64 * h2 + cc, y);
+        }
+      }
+    }
+    return;
+  }
+  // V: [token][d] accumulators -> [d][token] bf16 scratch -> 128-byte rows of V^T.
+  bf16_t* vs = reinterpret_cast<bf16_t*>(scratch);
+  const int fcol = lane & 31, fhalf = lane >> 5;
+#pragma unroll
+  for (int j = 0; j < FN; ++j) {
+    const float bj = bias ? bf2f(bias[nw + 32 * j + fcol]) : 0.f;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        uint2 w;
+        w.x = uint32_t(f2bf(acc[i][j][4 * g4] + bj)) | (uint32_t(f2bf(acc[i][j][4 * g4 + 1] + bj)) << 16);
+        w.y = uint32_t(f2bf(acc[i][j][4 * g4 + 2] + bj)) | (uint32_t(f2bf(acc[i][j][4 * g4 + 3] + bj)) << 16);
+        *reinterpret_cast<uint2*>(vs + (32 * j + fcol) * VT_LD + 32 * i + 8 * g4 + 4 * fhalf) = w;
+      }
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  const int c8 = lane & 7;
+  bf16_t* vt = p.vt_out;
+  const bool whole = one_sample && mw + 64 <= p.M;
+  const int64_t tok0 = mw - b_lo * S;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    const int d = k * 8 + (lane >> 3);
+    const uint4 w = *reinterpret_cast<const uint4*>(vs + d * VT_LD + 8 * c8);
+    if (whole) {
+      *reinterpret_cast<uint4*>(vt + ((b_lo * p.heads + head) * 128 + d) * p.n_joint + p.tok_offset + tok0 + 8 * c8) = w;
+    } else {
+      const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int64_t m = mw + 8 * c8 + e;
+        if (m >= p.M) continue;
+        const int64_t b = m / S, tok = m - b * S;
+        vt[((b * p.heads + head) * 128 + d) * p.n_joint + p.tok_offset + tok] =
+            static_cast<bf16_t>(e & 1 ? ws[e >> 1] >> 16 : ws[e >> 1] & 0xffffu);
+      }
+    }
+  }
 }
 
 template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI>
@@ -461,11 +598,16 @@ __device__ __forceinline__ void dma_buf16(const u32x4_t& rsrc, uint32_t voff, ui
 }
 #pragma clang diagnostic pop
 
-template <int EPI>
+// LAYOUT 0: each wave a 128 x 64 block (wm = w4 / 2, wn = 2 grp + w4 % 2); LAYOUT 1: a 64 x 128
+// block (wm = w4, wn = grp), one whole 128-column head, for the fused QKV epilogue.  The two
+// waves of a SIMD (same w4) always share their A rows.
+template <int EPI, int LAYOUT>
 __global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
   constexpr int BM = 256, BN = 256, KS = 64, ROWB = KS * 2;   // 128-byte LDS rows
   constexpr int STAGE = (BM + BN) * ROWB;                     // 64 KB
-  constexpr int TM = 128, TN = 64, FM = 4, FN = 2;
+  constexpr int TM = LAYOUT == 0 ? 128 : 64, TN = LAYOUT == 0 ? 64 : 128;
+  constexpr int FM = TM / 32, FN = TN / 32;
+  static_assert(EPI != EPI_QKV || LAYOUT == 1, "the fused QKV epilogue needs a head per wave");
   constexpr int A_INS = BM / 8 / 4, B_INS = BN / 8 / 4;       // 1 KB loads per wave per slab
   extern __shared__ __attribute__((aligned(16))) char smem[];
 
@@ -482,7 +624,7 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave >> 2, w4 = wave & 3;
-  const int wm = w4 >> 1, wn = grp * 2 + (w4 & 1);
+  const int wm = LAYOUT == 0 ? w4 >> 1 : w4, wn = LAYOUT == 0 ? grp * 2 + (w4 & 1) : grp;
   const int KT = static_cast<int>(p.K / KS), KT1 = static_cast<int>(p.K1 / KS);
 
   // Load q of a wave fills LDS rows 32 q + 8 w4 .. + 7 of its matrix; lane l lands at
@@ -551,8 +693,10 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks][i], fb[ks][j], acc[i][j], 0, 0, 0);
-          if (rb != nullptr && j == 1 && (i & 1) == 1) {
-            const int q = ks * 2 + (i >> 1);
+          constexpr int PER = FM * FN / 2;   // one W-row load after every fourth MFMA
+          if (rb != nullptr && ((i * FN + j) & 3) == 3) {
+            const int q = ks * 2 + (i * FN + j) / 4;
+            static_assert(PER == 4, "eight loads per compute phase");
             dma_buf16(*rb, b_off + q * b_step, lds_b + q * 4096);
           }
           __builtin_amdgcn_sched_barrier(0);
@@ -645,8 +789,12 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
     compute(nullptr, 0);
     __builtin_amdgcn_sched_barrier(0);
   }
-  static_assert(FN == 2 && 8 * 32 * PAIR_LD * 4 <= 2 * STAGE, "epilogue scratch fits the LDS ring");
-  epilogue_pairs<EPI, FM>(p, acc, m0 + wm * TM, n0 + wn * TN, reinterpret_cast<float*>(smem) + wave * 32 * PAIR_LD, lane);
+  if constexpr (EPI == EPI_QKV) {
+    epilogue_qkv<FM, FN>(p, acc, m0 + wm * TM, n0 + wn * TN, smem + wave * QKV_SCRATCH, lane);
+  } else {
+    static_assert(FN == 2 && 8 * 32 * PAIR_LD * 4 <= 2 * STAGE, "epilogue scratch fits the LDS ring");
+    epilogue_pairs<EPI, FM>(p, acc, m0 + wm * TM, n0 + wn * TN, reinterpret_cast<float*>(smem) + wave * 32 * PAIR_LD, lane);
+  }
 }
 
 // ------------------------------------------------------------------ float32
@@ -717,34 +865,37 @@ int launch_bf16(const GemmParams& p, hipStream_t s, const char* name, double flo
 
 template <int EPI>
 int launch_pp_batch(const GemmBatch& b, hipStream_t s, const char* name, double flops, double bytes) {
-  constexpr int smem = 2 * 512 * 64 * 2;
+  constexpr int LAYOUT = EPI == EPI_QKV ? 1 : 0;
+  constexpr int ring = 2 * 512 * 64 * 2;
+  constexpr int smem = EPI == EPI_QKV && 8 * QKV_SCRATCH > ring ? 8 * QKV_SCRATCH : ring;
   static bool attr_set = false;
   if (!attr_set) {
-    FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_pp<EPI>),
+    FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_pp<EPI, LAYOUT>),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, smem),
                  "gemm smem attribute");
     attr_set = true;
   }
   LaunchScope ls(name, s, flops, bytes);
-  hipLaunchKernelGGL((gemm_bf16_pp<EPI>), dim3(static_cast<unsigned>(b.tiles)), dim3(512), smem, s, b);
+  hipLaunchKernelGGL((gemm_bf16_pp<EPI, LAYOUT>), dim3(static_cast<unsigned>(b.tiles)), dim3(512), smem, s, b);
   return ls.status();
 }
 
 int64_t tiles256(const GemmParams& p) { return ((p.M + 255) / 256) * ((p.N + 255) / 256); }
 
+const char* const kGemmNames[4] = {"gemm_bf16", "gemm_bf16_gelu", "gemm_bf16_gated", "gemm_bf16_qkv"};
+
 // Problems with at least one 256 x 256 tile per CU take the 256 x 256 kernel;
 // smaller ones the 128 x 128 tile, which fills more CUs.
 template <int EPI>
 int dispatch_bf16(const GemmParams& p, hipStream_t s, double flops, double bytes) {
-  static const char* names[3] = {"gemm_bf16", "gemm_bf16_gelu", "gemm_bf16_gated"};
   if (tiles256(p) >= 256) {
     GemmBatch b{};
     b.p[0] = p;
     b.p[1] = p;
     b.tiles0 = b.tiles = tiles256(p);
-    return launch_pp_batch<EPI>(b, s, names[EPI], flops, bytes);
+    return launch_pp_batch<EPI>(b, s, kGemmNames[EPI], flops, bytes);
   }
-  return launch_bf16<128, 128, 2, 2, EPI>(p, s, names[EPI], flops, bytes);
+  return launch_bf16<128, 128, 2, 2, EPI>(p, s, kGemmNames[EPI], flops, bytes);
 }
 
 template <int EPI>
@@ -765,7 +916,28 @@ GemmParams make_params(const GemmArgs& a) {
                a.rows_per_sample > 0 ? a.rows_per_sample : a.M, 0};
   p.vec_ok = a.ldo % 8 == 0 && aligned16(a.out) && (!a.bias || aligned16(a.bias)) &&
              (a.epi != EPI_GATED || (a.ldr % 8 == 0 && aligned16(a.resid) && (!a.gate || (a.gate_ld % 4 == 0 && aligned16(a.gate)))));
+  if (a.qkv) {
+    const QkvArgs& q = *a.qkv;
+    p.q_out = static_cast<bf16_t*>(q.Q); p.k_out = static_cast<bf16_t*>(q.Kd); p.vt_out = static_cast<bf16_t*>(q.Vt);
+    p.q_w = static_cast<const bf16_t*>(q.q_w); p.k_w = static_cast<const bf16_t*>(q.k_w); p.rope = q.rope;
+    p.hidden = static_cast<int64_t>(q.heads) * 128; p.n_joint = q.n_joint; p.tok_offset = q.tok_offset;
+    p.heads = q.heads; p.eps = q.eps;
+    p.rows_per_sample = q.src_rows;
+  }
   return p;
+}
+
+// The QKV projection of one stream can end in the fused norm / rotation / relayout epilogue:
+// bf16, 128-wide heads with a per-head norm, every GEMM row a token (rows = B x tokens), V taken
+// transposed, and the 16-byte alignment and 8-token granularity the vector stores need.
+bool qkv_fusable(const GemmArgs& a) {
+  if (!a.qkv || a.dtype != FF_BF16) return false;
+  const QkvArgs& q = *a.qkv;
+  const int64_t H = static_cast<int64_t>(q.heads) * 128;
+  return q.dtype == FF_BF16 && q.d == 128 && !q.full_width_norm && q.apply_norm && q.v_transposed &&
+         a.N == 3 * H && a.K1 == a.K && q.src_rows == q.n_tok && a.M == q.B * q.n_tok && q.n_tok % 8 == 0 &&
+         q.n_joint % 8 == 0 && q.tok_offset % 8 == 0 && aligned16(q.Q) && aligned16(q.Kd) && aligned16(q.Vt) &&
+         aligned16(q.q_w) && aligned16(q.k_w) && (!q.rope || aligned16(q.rope)) && (!a.bias || aligned16(a.bias));
 }
 double gemm_flops(const GemmArgs& a) { return 2.0 * a.M * a.N * a.K; }
 double gemm_bytes(const GemmArgs& a) {
@@ -777,6 +949,21 @@ double gemm_bytes(const GemmArgs& a) {
 
 int gemm(const GemmArgs& a, hipStream_t s) {
   if (a.M == 0 || a.N == 0) return FF_OK;
+  if (a.epi == EPI_QKV) {
+    GemmParams p = make_params(a);
+    if (qkv_fusable(a) && a.K % BK == 0 && tiles256(p) >= 256) {
+      GemmBatch b{};
+      b.p[0] = p;
+      b.p[1] = p;
+      b.tiles0 = b.tiles = tiles256(p);
+      return launch_pp_batch<EPI_QKV>(b, s, kGemmNames[EPI_QKV], gemm_flops(a), gemm_bytes(a));
+    }
+    GemmArgs plain = a;   // two passes: the packed projection, then the norm / rotation / relayout
+    plain.epi = EPI_NONE;
+    plain.qkv = nullptr;
+    FF_TRY(gemm(plain, s));
+    return a.qkv ? qk_norm_rope(*a.qkv, s) : fail(FF_EINVAL, "gemm: QKV epilogue without its arguments");
+  }
   GemmParams p = make_params(a);
   const double flops = gemm_flops(a), bytes = gemm_bytes(a);
   if (a.dtype == FF_BF16) {
@@ -797,6 +984,24 @@ int gemm(const GemmArgs& a, hipStream_t s) {
 }
 
 int gemm2(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
+  if (a0.epi == EPI_QKV || a1.epi == EPI_QKV) {
+    GemmBatch b{};
+    b.p[0] = make_params(a0);
+    b.p[1] = make_params(a1);
+    b.tiles0 = tiles256(b.p[0]);
+    b.tiles = b.tiles0 + tiles256(b.p[1]);
+    if (a0.epi == EPI_QKV && a1.epi == EPI_QKV && qkv_fusable(a0) && qkv_fusable(a1) && a0.K % BK == 0 &&
+        a1.K % BK == 0 && b.tiles >= 256)
+      return launch_pp_batch<EPI_QKV>(b, s, kGemmNames[EPI_QKV], gemm_flops(a0) + gemm_flops(a1),
+                                      gemm_bytes(a0) + gemm_bytes(a1));
+    GemmArgs p0 = a0, p1 = a1;   // two passes for both streams
+    if (p0.epi == EPI_QKV) { p0.epi = EPI_NONE; p0.qkv = nullptr; }
+    if (p1.epi == EPI_QKV) { p1.epi = EPI_NONE; p1.qkv = nullptr; }
+    FF_TRY(gemm2(p0, p1, s));
+    if (a0.epi == EPI_QKV) FF_TRY(a0.qkv ? qk_norm_rope(*a0.qkv, s) : fail(FF_EINVAL, "gemm2: QKV epilogue without its arguments"));
+    if (a1.epi == EPI_QKV) FF_TRY(a1.qkv ? qk_norm_rope(*a1.qkv, s) : fail(FF_EINVAL, "gemm2: QKV epilogue without its arguments"));
+    return FF_OK;
+  }
   const bool grouped = a0.dtype == FF_BF16 && a1.dtype == FF_BF16 && a0.epi == a1.epi && a0.M > 0 && a1.M > 0 &&
                        a0.N > 0 && a1.N > 0 && a0.K % BK == 0 && a1.K % BK == 0 && a0.K1 % BK == 0 &&
                        a1.K1 % BK == 0;
@@ -814,11 +1019,10 @@ int gemm2(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
     return gemm(a1, s);
   }
   const double flops = gemm_flops(a0) + gemm_flops(a1), bytes = gemm_bytes(a0) + gemm_bytes(a1);
-  static const char* names[3] = {"gemm_bf16", "gemm_bf16_gelu", "gemm_bf16_gated"};
   switch (a0.epi) {
-    case EPI_NONE: return launch_pp_batch<EPI_NONE>(b, s, names[0], flops, bytes);
-    case EPI_GELU: return launch_pp_batch<EPI_GELU>(b, s, names[1], flops, bytes);
-    default: return launch_pp_batch<EPI_GATED>(b, s, names[2], flops, bytes);
+    case EPI_NONE: return launch_pp_batch<EPI_NONE>(b, s, kGemmNames[EPI_NONE], flops, bytes);
+    case EPI_GELU: return launch_pp_batch<EPI_GELU>(b, s, kGemmNames[EPI_GELU], flops, bytes);
+    default: return launch_pp_batch<EPI_GATED>(b, s, kGemmNames[EPI_GATED], flops, bytes);
   }
 }
 

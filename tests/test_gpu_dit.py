@@ -270,6 +270,39 @@ def test_flux_dual_block_full_size(gpu_lib):
         assert abs(lp[b] - lr[0]) <= LOGP_ABS
 
 
+def test_fused_qkv_epilogue_ragged_streams(gpu_lib):
+    """Dual-stream block whose QKV projections (grouped launch of >= 256 tiles) take the fused QK
+    norm / rotation / relayout epilogue: 264 text tokens per sample, so 64-token waves straddle two
+    samples and the last row tile is ragged; checked against the oracle on whole samples."""
+    m = C.ModelConfig(model=C.MODEL_MMDIT, io_mode=C.IO_HIDDEN, dtype=C.BF16, n_dual=1, n_single=0, hidden=1536,
+                      heads=12, head_dim=128, mlp_hidden=3072, in_channels=64, txt_dim=1536, rope_axes=(16, 56, 56))
+    w = C.Workload(name="fused-qkv-ragged", index=17, model=m, prompts=4, group=1, grid=(1, 32, 32), n_txt=264,
+                   steps=1, fixed_step=(0.6, 0.5))
+    say("fused qkv: generating inputs")
+    W, txt, cond, x0, eps = _inputs(w)
+    Wd, T, Cd, X0, E = _device(w, W, txt, cond, x0, eps)
+    dit = api.Dit(m, Wd)
+    ro = R.Rollout(w, dit)
+    api.profile_reset()
+    api.profile_enable(True)
+    try:
+        res = ro.run(X0, T, E, cond=Cd)
+        torch.cuda.synchronize()
+    finally:
+        api.profile_enable(False)
+    prof = api.profile_read()
+    api.profile_reset()
+    assert prof.get("gemm_bf16_qkv", {}).get("launches", 0) == 1, sorted(prof)
+    assert "qk_norm_rope" not in prof
+    v = host(res.vs[0])
+    for b in (0, 3):
+        say("oracle sample", b)
+        img, _ = odit.forward(m, W, x0[b:b + 1], txt[b:b + 1], cond=cond[b:b + 1], grid=w.grid)
+        e_v = rel(v[b:b + 1], img)
+        say("  rel v", e_v)
+        assert e_v <= TOL[C.BF16]
+
+
 @pytest.mark.timeout(900)
 def test_flux_single_block_full_width(gpu_lib):
     """One Flux-shaped single-stream block at full width (H=3072, fused H -> 3H + F projection,
