@@ -371,11 +371,14 @@ int single_block(const ff_dit& m, const Plan& p, void* ws, int j, const float* c
   char* O = at(ws, p.o);
   FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 3 * H, H, c32, ACT_SILU, sb.mod, mods), s));
   FF_TRY(norm_modulate(norm_args(c, rows, X, Y, mods, mods + H, 3 * H, p.N), s));
-  GemmArgs g1 = gemm_args(c.dtype, rows, W1, H, Y, H, sb.lin1, H1, W1, EPI_GELU);
+  // [Q | K | V | MLP input] in one GEMM: Q, K, V of the joint sequence go to the attention layout
+  // (text tokens unrotated, image tokens rotated by their grid position), GELU from column 3H.
+  QkvArgs qa = qkv_args(c, p, ws, H1, W1, p.N, 0, p.N, 0, sb.qn, sb.kn, true);
+  qa.rope_from = p.Nt;
+  GemmArgs g1 = gemm_args(c.dtype, rows, W1, H, Y, H, sb.lin1, H1, W1, EPI_QKV);
   g1.gelu_from = 3 * H;
+  g1.qkv = &qa;
   FF_TRY(gemm(g1, s));
-  FF_TRY(qkv_stream(c, p, ws, H1, W1, p.N, 0, p.Nt, 0, sb.qn, sb.kn, false, s));
-  FF_TRY(qkv_stream(c, p, ws, H1, W1, p.N, p.Nt, p.Ni, p.Nt, sb.qn, sb.kn, true, s));
   AttnArgs a{};
   a.dtype = c.dtype;
   a.B = p.B; a.heads = c.heads; a.d = c.head_dim;

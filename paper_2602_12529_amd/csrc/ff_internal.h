@@ -77,7 +77,9 @@ enum Epi : int {
   EPI_NONE = 0,       // out = acc + bias
   EPI_GELU = 1,       // out = gelu_tanh(acc + bias) for columns >= gelu_from, else acc + bias
   EPI_GATED = 2,      // out = resid + gate[b] * (acc + bias); gate null: out = resid + acc + bias
-  EPI_QKV = 3,        // columns [Q | K | V] of acc + bias go through qk_norm_rope(*qkv) (fused when possible)
+  EPI_QKV = 3,        // columns [Q | K | V] = [0, 3H) of acc + bias go through qk_norm_rope(*qkv) (fused when
+                      // possible); columns from 3H on (N > 3H: a single-stream block's MLP input) take
+                      // EPI_GELU's treatment with gelu_from = 3H and go to out
 };
 
 struct QkvArgs;
@@ -145,7 +147,9 @@ struct QkvArgs {
   int full_width_norm;                      // 1: RMSNorm over all H before RoPE (WAN)
   int apply_norm;                           // 0: no QK norm (cross-attention V/K handled by caller)
   float eps;
-  const float2* rope;                       // [n_tok, d/2] (cos, sin) or null = no rotation
+  const float2* rope;                       // [n_tok - rope_from, d/2] (cos, sin) or null = no rotation
+  int64_t rope_from;                        // tokens below it are not rotated; token i >= rope_from takes
+                                            // table row i - rope_from (a joint text + image sequence)
   void* Q; void* Kd; void* Vt;              // Q, K [B, h, n_joint, d]; V transposed [B, h, d, n_joint]
   int v_transposed;
 };

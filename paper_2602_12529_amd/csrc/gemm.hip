@@ -30,6 +30,10 @@ typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_t;
 typedef __attribute__((address_space(1))) void glb_t;
 
+// EPI_QKV whose columns from 3H on are a single-stream block's MLP input (bias + GELU-tanh, stored
+// to out): a kernel of its own, so the dual-stream QKV kernel carries no GELU code.
+constexpr int EPI_QKV_GELU = 4;
+
 struct GemmParams {
   int64_t M, N, K;
   const void* A1; int64_t lda1; int64_t K1;
@@ -46,7 +50,7 @@ struct GemmParams {
   // per-head RMSNorm weights, the (cos, sin) table [tokens, 64] (null: no rotation).
   bf16_t* q_out; bf16_t* k_out; bf16_t* vt_out;
   const bf16_t* q_w; const bf16_t* k_w; const float2* rope;
-  int64_t hidden, n_joint, tok_offset;
+  int64_t hidden, n_joint, tok_offset, rope_from;
   int heads; float eps;
 };
 
@@ -354,8 +358,8 @@ __device__ __forceinline__ void epilogue_qkv(const GemmParams& p, const f32x16_t
 #pragma unroll
         for (int h2 = 0; h2 < 2; ++h2) {
           float cs[8];
-          if (p.rope) {
-            const float4* rp = reinterpret_cast<const float4*>(p.rope + tok * 64 + 32 * h2 + cc / 2);
+          if (p.rope && tok >= p.rope_from) {
+            const float4* rp = reinterpret_cast<const float4*>(p.rope + (tok - p.rope_from) * 64 + 32 * h2 + cc / 2);
             const float4 r0 = rp[0], r1 = rp[1];
             cs[0] = r0.x; cs[1] = r0.y; cs[2] = r0.z; cs[3] = r0.w; cs[4] = r1.x; cs[5] = r1.y; cs[6] = r1.z; cs[7] = r1.w;
           } else {
@@ -607,7 +611,7 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
   constexpr int STAGE = (BM + BN) * ROWB;                     // 64 KB
   constexpr int TM = LAYOUT == 0 ? 128 : 64, TN = LAYOUT == 0 ? 64 : 128;
   constexpr int FM = TM / 32, FN = TN / 32;
-  static_assert(EPI != EPI_QKV || LAYOUT == 1, "the fused QKV epilogue needs a head per wave");
+  static_assert((EPI != EPI_QKV && EPI != EPI_QKV_GELU) || LAYOUT == 1, "the fused QKV epilogue needs a head per wave");
   constexpr int A_INS = BM / 8 / 4, B_INS = BN / 8 / 4;       // 1 KB loads per wave per slab
   extern __shared__ __attribute__((aligned(16))) char smem[];
 
@@ -791,6 +795,18 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
   }
   if constexpr (EPI == EPI_QKV) {
     epilogue_qkv<FM, FN>(p, acc, m0 + wm * TM, n0 + wn * TN, smem + wave * QKV_SCRATCH, lane);
+  } else if constexpr (EPI == EPI_QKV_GELU) {
+    // A wave's 128 columns are all Q/K/V (below 3H) or all MLP input: 3H is a multiple of 128.
+    const int64_t mw = m0 + wm * TM, nw = n0 + wn * TN;
+    if (nw < 3 * p.hidden) {
+      epilogue_qkv<FM, FN>(p, acc, mw, nw, smem + wave * QKV_SCRATCH, lane);
+    } else {
+      float* fs = reinterpret_cast<float*>(smem + wave * QKV_SCRATCH);
+      const f32x16_t lo[FM][2] = {{acc[0][0], acc[0][1]}, {acc[1][0], acc[1][1]}};
+      epilogue_pairs<EPI_GELU, FM>(p, lo, mw, nw, fs, lane);
+      const f32x16_t hi[FM][2] = {{acc[0][2], acc[0][3]}, {acc[1][2], acc[1][3]}};
+      epilogue_pairs<EPI_GELU, FM>(p, hi, mw, nw + 64, fs, lane);
+    }
   } else {
     static_assert(FN == 2 && 8 * 32 * PAIR_LD * 4 <= 2 * STAGE, "epilogue scratch fits the LDS ring");
     epilogue_pairs<EPI, FM>(p, acc, m0 + wm * TM, n0 + wn * TN, reinterpret_cast<float*>(smem) + wave * 32 * PAIR_LD, lane);
@@ -865,9 +881,10 @@ int launch_bf16(const GemmParams& p, hipStream_t s, const char* name, double flo
 
 template <int EPI>
 int launch_pp_batch(const GemmBatch& b, hipStream_t s, const char* name, double flops, double bytes) {
-  constexpr int LAYOUT = EPI == EPI_QKV ? 1 : 0;
+  constexpr bool qkv = EPI == EPI_QKV || EPI == EPI_QKV_GELU;
+  constexpr int LAYOUT = qkv ? 1 : 0;
   constexpr int ring = 2 * 512 * 64 * 2;
-  constexpr int smem = EPI == EPI_QKV && 8 * QKV_SCRATCH > ring ? 8 * QKV_SCRATCH : ring;
+  constexpr int smem = qkv && 8 * QKV_SCRATCH > ring ? 8 * QKV_SCRATCH : ring;
   static bool attr_set = false;
   if (!attr_set) {
     FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_pp<EPI, LAYOUT>),
@@ -882,7 +899,8 @@ int launch_pp_batch(const GemmBatch& b, hipStream_t s, const char* name, double 
 
 int64_t tiles256(const GemmParams& p) { return ((p.M + 255) / 256) * ((p.N + 255) / 256); }
 
-const char* const kGemmNames[4] = {"gemm_bf16", "gemm_bf16_gelu", "gemm_bf16_gated", "gemm_bf16_qkv"};
+const char* const kGemmNames[5] = {"gemm_bf16", "gemm_bf16_gelu", "gemm_bf16_gated", "gemm_bf16_qkv",
+                                   "gemm_bf16_qkv_gelu"};
 
 // Problems with at least one 256 x 256 tile per CU take the 256 x 256 kernel;
 // smaller ones the 128 x 128 tile, which fills more CUs.
@@ -921,6 +939,7 @@ GemmParams make_params(const GemmArgs& a) {
     p.q_out = static_cast<bf16_t*>(q.Q); p.k_out = static_cast<bf16_t*>(q.Kd); p.vt_out = static_cast<bf16_t*>(q.Vt);
     p.q_w = static_cast<const bf16_t*>(q.q_w); p.k_w = static_cast<const bf16_t*>(q.k_w); p.rope = q.rope;
     p.hidden = static_cast<int64_t>(q.heads) * 128; p.n_joint = q.n_joint; p.tok_offset = q.tok_offset;
+    p.rope_from = q.rope_from;
     p.heads = q.heads; p.eps = q.eps;
     p.rows_per_sample = q.src_rows;
   }
@@ -935,7 +954,7 @@ bool qkv_fusable(const GemmArgs& a) {
   const QkvArgs& q = *a.qkv;
   const int64_t H = static_cast<int64_t>(q.heads) * 128;
   return q.dtype == FF_BF16 && q.d == 128 && !q.full_width_norm && q.apply_norm && q.v_transposed &&
-         a.N == 3 * H && a.K1 == a.K && q.src_rows == q.n_tok && a.M == q.B * q.n_tok && q.n_tok % 8 == 0 &&
+         (a.N == 3 * H || (a.N > 3 * H && a.gelu_from == 3 * H)) && a.K1 == a.K && q.src_rows == q.n_tok && a.M == q.B * q.n_tok && q.n_tok % 8 == 0 &&
          q.n_joint % 8 == 0 && q.tok_offset % 8 == 0 && aligned16(q.Q) && aligned16(q.Kd) && aligned16(q.Vt) &&
          aligned16(q.q_w) && aligned16(q.k_w) && (!q.rope || aligned16(q.rope)) && (!a.bias || aligned16(a.bias));
 }
@@ -951,15 +970,17 @@ int gemm(const GemmArgs& a, hipStream_t s) {
   if (a.M == 0 || a.N == 0) return FF_OK;
   if (a.epi == EPI_QKV) {
     GemmParams p = make_params(a);
+    const bool tail = a.qkv && a.N > 3 * static_cast<int64_t>(a.qkv->heads) * a.qkv->d;   // MLP columns
     if (qkv_fusable(a) && a.K % BK == 0 && tiles256(p) >= 256) {
       GemmBatch b{};
       b.p[0] = p;
       b.p[1] = p;
       b.tiles0 = b.tiles = tiles256(p);
+      if (tail) return launch_pp_batch<EPI_QKV_GELU>(b, s, kGemmNames[EPI_QKV_GELU], gemm_flops(a), gemm_bytes(a));
       return launch_pp_batch<EPI_QKV>(b, s, kGemmNames[EPI_QKV], gemm_flops(a), gemm_bytes(a));
     }
     GemmArgs plain = a;   // two passes: the packed projection, then the norm / rotation / relayout
-    plain.epi = EPI_NONE;
+    plain.epi = tail ? EPI_GELU : EPI_NONE;
     plain.qkv = nullptr;
     FF_TRY(gemm(plain, s));
     return a.qkv ? qk_norm_rope(*a.qkv, s) : fail(FF_EINVAL, "gemm: QKV epilogue without its arguments");
@@ -985,6 +1006,12 @@ int gemm(const GemmArgs& a, hipStream_t s) {
 
 int gemm2(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
   if (a0.epi == EPI_QKV || a1.epi == EPI_QKV) {
+    const bool tail0 = a0.qkv && a0.N > 3 * static_cast<int64_t>(a0.qkv->heads) * a0.qkv->d;
+    const bool tail1 = a1.qkv && a1.N > 3 * static_cast<int64_t>(a1.qkv->heads) * a1.qkv->d;
+    if (tail0 || tail1 || a0.epi != a1.epi) {   // only two plain QKV projections are grouped
+      FF_TRY(gemm(a0, s));
+      return gemm(a1, s);
+    }
     GemmBatch b{};
     b.p[0] = make_params(a0);
     b.p[1] = make_params(a1);

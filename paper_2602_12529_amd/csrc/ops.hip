@@ -584,6 +584,18 @@ int norm_modulate(const NormArgs& a, hipStream_t s) {
 
 int qk_norm_rope(const QkvArgs& a, hipStream_t s) {
   if (a.B == 0 || a.n_tok == 0) return FF_OK;
+  if (a.rope && a.rope_from > 0) {   // unrotated leading tokens, then the rotated rest: two passes
+    const int64_t lead = a.rope_from < a.n_tok ? a.rope_from : a.n_tok;
+    const size_t off = static_cast<size_t>(lead) * a.ld * dtype_size(a.dtype);
+    QkvArgs head = a, tail = a;
+    head.n_tok = lead; head.rope = nullptr; head.rope_from = 0;
+    tail.n_tok = a.n_tok - lead; tail.tok_offset = a.tok_offset + lead; tail.rope_from = 0;
+    tail.q = static_cast<const char*>(a.q) + off;
+    tail.k = static_cast<const char*>(a.k) + off;
+    tail.v = static_cast<const char*>(a.v) + off;
+    FF_TRY(qk_norm_rope(head, s));
+    return qk_norm_rope(tail, s);
+  }
   if (a.d > 128 || a.d % 2) return fail(FF_EUNSUPPORTED, "qk_norm_rope: head_dim %d", a.d);
   dim3 grid(blocks_for(a.n_tok, kRopeTok), static_cast<unsigned>(a.heads), static_cast<unsigned>(a.B));
   LaunchScope ls("qk_norm_rope", s, 0.0, 6.0 * dtype_size(a.dtype) * a.B * a.n_tok * a.heads * a.d);

@@ -270,15 +270,19 @@ def test_flux_dual_block_full_size(gpu_lib):
         assert abs(lp[b] - lr[0]) <= LOGP_ABS
 
 
-def test_fused_qkv_epilogue_ragged_streams(gpu_lib):
-    """Dual-stream block whose QKV projections (grouped launch of >= 256 tiles) take the fused QK
-    norm / rotation / relayout epilogue: 264 text tokens per sample, so 64-token waves straddle two
-    samples and the last row tile is ragged; checked against the oracle on whole samples."""
-    m = C.ModelConfig(model=C.MODEL_MMDIT, io_mode=C.IO_HIDDEN, dtype=C.BF16, n_dual=1, n_single=0, hidden=1536,
-                      heads=12, head_dim=128, mlp_hidden=3072, in_channels=64, txt_dim=1536, rope_axes=(16, 56, 56))
+@pytest.mark.parametrize("n_dual,n_single,kernel", [(1, 0, "gemm_bf16_qkv"), (0, 1, "gemm_bf16_qkv_gelu")])
+def test_fused_qkv_epilogue_ragged_streams(gpu_lib, n_dual, n_single, kernel):
+    """A dual-stream block (text and image QKV projections grouped in one launch) or a single-stream
+    block (Q, K, V and the MLP input from one projection, GELU from column 3H) whose QKV projection
+    takes the fused QK norm / rotation / relayout epilogue.  264 text tokens per sample: 64-token
+    waves straddle two samples, and in the single-stream block also the text / image boundary where
+    the rotation starts; the last row tile is ragged.  Checked against the oracle on whole samples."""
+    m = C.ModelConfig(model=C.MODEL_MMDIT, io_mode=C.IO_HIDDEN, dtype=C.BF16, n_dual=n_dual, n_single=n_single,
+                      hidden=1536, heads=12, head_dim=128, mlp_hidden=3072, in_channels=64, txt_dim=1536,
+                      rope_axes=(16, 56, 56))
     w = C.Workload(name="fused-qkv-ragged", index=17, model=m, prompts=4, group=1, grid=(1, 32, 32), n_txt=264,
                    steps=1, fixed_step=(0.6, 0.5))
-    say("fused qkv: generating inputs")
+    say("fused qkv:", kernel, "generating inputs")
     W, txt, cond, x0, eps = _inputs(w)
     Wd, T, Cd, X0, E = _device(w, W, txt, cond, x0, eps)
     dit = api.Dit(m, Wd)
@@ -286,13 +290,13 @@ def test_fused_qkv_epilogue_ragged_streams(gpu_lib):
     api.profile_reset()
     api.profile_enable(True)
     try:
-        res = ro.run(X0, T, E, cond=Cd)
+        res = ro.run(X0, T, E, cond=Cd, txt_out=torch.empty_like(T))
         torch.cuda.synchronize()
     finally:
         api.profile_enable(False)
     prof = api.profile_read()
     api.profile_reset()
-    assert prof.get("gemm_bf16_qkv", {}).get("launches", 0) == 1, sorted(prof)
+    assert prof.get(kernel, {}).get("launches", 0) == 1, sorted(prof)
     assert "qk_norm_rope" not in prof
     v = host(res.vs[0])
     for b in (0, 3):
