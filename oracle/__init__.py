@@ -22,5 +22,7 @@ Modules:
                 GRPO ratio surrogate on stored trajectories
   noise      -- counter-based Gaussian noise for the SDE step (Philox4x32-10
                 with Box-Muller)
+  fp8        -- OCP E4M3 row quantisation and the scaled FP8 linear layer (a
+                throughput variant of the DiT's linear layers, not the paper's)
 """
-from . import advantage, dit, losses, noise, rollout, sde  # noqa: F401
+from . import advantage, dit, fp8, losses, noise, rollout, sde  # noqa: F401
