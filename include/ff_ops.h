@@ -70,6 +70,27 @@ int ff_rope_table(float* out, const int32_t grid[3], int32_t head_dim, const int
 int ff_skinny_linear(const float* in, const void* W, const void* bias, float* out, int64_t B, int64_t N,
                      int64_t K, int32_t act_in, int32_t act_out, int32_t dtype, void* stream);
 
+/* FP8 row quantisation to OCP E4M3 (sign, 4 exponent bits with bias 7, 3 mantissa bits; largest
+ * magnitude 448, no infinities).  Not from the paper, whose DiT runs its linear layers in bf16:
+ * the FP8 layer below is a throughput variant of ff_linear.
+ * For each row r of x [rows, cols] (dtype, row stride ldx elements): amax = max |x[r, :]|,
+ * q[r, :] = round-to-nearest-even(x[r, :] * fl32(448 / amax)) as codes (uint8, row stride ldq
+ * bytes; a value that rounds to zero keeps its sign bit) and d[r] = fl32(amax / 448) (float32), so
+ * that x[r, k] ~ d[r] * decode(q[r, k]); a row of zeros gets codes 0 and d = 0.  Non-finite
+ * inputs give unspecified codes.  cols, ldx, ldq % 8 == 0; x and q 16-byte aligned. */
+int ff_quantize_fp8(const void* x, int64_t ldx, uint8_t* q, int64_t ldq, float* d, int64_t rows, int64_t cols,
+                    int32_t dtype, void* stream);
+
+/* FP8 linear layer out = epi(d_a[m] * d_w[n] * (A W^T)[m, n] + bias[n]): A [M, K] and W [N, K]
+ * E4M3 codes (row strides lda, ldw in bytes), d_a [M] and d_w [N] their float32 scales (as
+ * ff_quantize_fp8 produces them), bias bf16 [N] or NULL, out bf16 [M, N] (row stride ldo
+ * elements); epi FF_EPI_BIAS or FF_EPI_GELU (GELU_tanh on columns >= gelu_from).  Products of
+ * codes accumulate in float32.  K % 128 == 0; lda, ldw % 16 == 0; ldo % 8 == 0; A, W, out,
+ * bias and d_w 16-byte aligned. */
+int ff_linear_fp8(const uint8_t* A, int64_t lda, const float* d_a, const uint8_t* W, int64_t ldw, const float* d_w,
+                  const void* bias, void* out, int64_t ldo, int64_t M, int64_t N, int64_t K, int32_t epi,
+                  int64_t gelu_from, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -171,6 +171,27 @@ def linear(A, W, bias, out, epi=EPI_BIAS, gelu_from=0, gate=None, gate_ld=0, res
     return out
 
 
+def quantize_fp8(x, q=None, d=None):
+    """Rows of x [R, C] (bf16 or f32) -> (E4M3 codes uint8 [R, C], float32 scales [R])."""
+    R, Cn = x.shape
+    if q is None:
+        q = torch.empty((R, Cn), dtype=torch.uint8, device=x.device)
+    if d is None:
+        d = torch.empty((R,), dtype=torch.float32, device=x.device)
+    check(load().ff_quantize_fp8(_p(x), x.stride(0), _p(q), q.stride(0), _p(d), R, Cn, dtype_code(x), _stream()),
+          "ff_quantize_fp8")
+    return q, d
+
+
+def linear_fp8(A, d_a, W, d_w, bias, out, epi=EPI_BIAS, gelu_from=0):
+    """out [M, N] bf16 = epi(d_a[m] d_w[n] (A W^T)[m, n] + bias) on E4M3 codes A [M, K], W [N, K]."""
+    M, K = A.shape
+    N = W.shape[0]
+    check(load().ff_linear_fp8(_p(A), A.stride(0), _p(d_a), _p(W), W.stride(0), _p(d_w), _p(bias), _p(out),
+                               out.stride(0), M, N, K, epi, gelu_from, _stream()), "ff_linear_fp8")
+    return out
+
+
 def attention(Q, K, V, out):
     B, h, n_q, d = Q.shape
     n_kv = K.shape[2]

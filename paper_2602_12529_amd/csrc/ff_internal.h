@@ -105,6 +105,26 @@ int gemm(const GemmArgs& a, hipStream_t s);
 // Two GEMMs with the same epilogue kind, launched together when both are large bf16 problems.
 int gemm2(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s);
 
+// out = epi(d_a[m] d_w[n] (A W^T)[m, n] + bias[n]): A [M, K] and W [N, K] OCP E4M3 codes (row
+// strides lda, ldw in bytes = elements), d_a [M], d_w [N] float32 dequantisation scales, bias
+// bf16 [N] or null, out bf16 [M, N]; epi EPI_NONE or EPI_GELU (from column gelu_from).
+// K % 128 == 0; A, W 16-byte aligned with lda, ldw % 16 == 0.
+struct Fp8GemmArgs {
+  int64_t M, N, K;
+  const void* A; int64_t lda; const float* d_a;
+  const void* W; int64_t ldw; const float* d_w;
+  const void* bias;
+  void* out; int64_t ldo;
+  int epi; int64_t gelu_from;
+};
+int gemm_fp8(const Fp8GemmArgs& a, hipStream_t s);
+
+// Row quantisation to OCP E4M3: amax = max |x[r, :]|, codes = RNE(x * fl32(448 / amax)),
+// d[r] = fl32(amax / 448) (zero rows: codes 0, d 0).  x of dtype [rows, cols] (stride ldx),
+// q uint8 [rows, cols] (stride ldq); cols, ldx, ldq % 8 == 0, 16-byte aligned.
+int quantize_fp8(int dtype, const void* x, int64_t ldx, void* q, int64_t ldq, float* d, int64_t rows, int64_t cols,
+                 hipStream_t s);
+
 // out[b, n] (+)= sum_k W[n, k] * act(in[b, k]) + bias[n]; in/out float32, W of dtype.
 enum Act : int { ACT_NONE = 0, ACT_SILU = 1, ACT_GELU = 2 };
 struct SkinnyArgs {

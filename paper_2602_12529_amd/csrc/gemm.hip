@@ -16,8 +16,15 @@
 // Epilogues fuse the bias, GELU-tanh (from a column on, for the fused
 // single-stream projection) and the adaLN-gated residual X + g * (.).
 //
+// fp8: the same 256 x 256 ping-pong kernel on OCP E4M3 codes (gemm_fp8_pp):
+// 128-wide K slabs (the same 128-byte LDS rows), the unscaled MFMA 32x32x64, and
+// the per-row / per-column dequantisation scales applied in the epilogue before
+// the bias.
+//
 // f32: a plain LDS-tiled FMA kernel with the same epilogues, for the float32
 // configurations.
+#include <type_traits>
+
 #include "dev.h"
 #include "ff_internal.h"
 
@@ -27,6 +34,7 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef int i32x8_t __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) void lds_t;
 typedef __attribute__((address_space(1))) void glb_t;
 
@@ -52,6 +60,8 @@ struct GemmParams {
   const bf16_t* q_w; const bf16_t* k_w; const float2* rope;
   int64_t hidden, n_joint, tok_offset, rope_from;
   int heads; float eps;
+  // fp8: out = epi(row_scale[m] * col_scale[n] * acc + bias)
+  const float* row_scale; const float* col_scale;
 };
 
 template <bool BF16, int EPI>
@@ -206,13 +216,14 @@ __device__ __forceinline__ void transpose_blocks(const f32x16_t& a0, const f32x1
   }
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 }
-template <int EPI, int FM, int I = 0>
-__device__ __forceinline__ void transpose_pair(const f32x16_t (&acc)[FM][2], float* scratch, int lane, float (&v)[4][8]) {
-  transpose_blocks(acc[I][0], acc[I][1], scratch, lane, v);
+template <int EPI, int FM, int FN, int JP, int I = 0>
+__device__ __forceinline__ void transpose_pair(const f32x16_t (&acc)[FM][FN], float* scratch, int lane, float (&v)[4][8]) {
+  transpose_blocks(acc[I][2 * JP], acc[I][2 * JP + 1], scratch, lane, v);
 }
 
-template <int EPI, int FM>
-__device__ __forceinline__ void epilogue_pairs(const GemmParams& p, const f32x16_t (&acc)[FM][2], int64_t mw, int64_t nw,
+// Columns 64 JP .. 64 JP + 63 of the wave's FM x FN block grid (blocks 2 JP and 2 JP + 1 of each row).
+template <int EPI, int FM, int FN = 2, int JP = 0, bool SCALED = false>
+__device__ __forceinline__ void epilogue_pairs(const GemmParams& p, const f32x16_t (&acc)[FM][FN], int64_t mw, int64_t nw,
                                                float* scratch, int lane) {
   static_assert(FM <= 4, "pairs per wave");
   const int rr = lane >> 3, cc = (lane & 7) * 8;
@@ -223,6 +234,14 @@ __device__ __forceinline__ void epilogue_pairs(const GemmParams& p, const f32x16
   const bool vec = p.vec_ok && n + 8 <= p.N;
   float bv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   if (vec && p.bias) ld8<true>(p.bias, n, bv);
+  float cs[8];        // fp8: the lane's eight column scales
+  if constexpr (SCALED) {
+    if (vec) {
+      const float4 c0 = *reinterpret_cast<const float4*>(p.col_scale + n);
+      const float4 c1 = *reinterpret_cast<const float4*>(p.col_scale + n + 4);
+      cs[0] = c0.x; cs[1] = c0.y; cs[2] = c0.z; cs[3] = c0.w; cs[4] = c1.x; cs[5] = c1.y; cs[6] = c1.z; cs[7] = c1.w;
+    }
+  }
   uint4 rs[2][4];     // residual rows of two pairs in flight (bf16)
   auto load_resid = [&](int i, uint4 (&dst)[4]) {
     if (!vec) return;
@@ -251,14 +270,20 @@ __device__ __forceinline__ void epilogue_pairs(const GemmParams& p, const f32x16
   float v[4][8];
 #define FF_PAIR(I)                                                                                   \
   if constexpr (I < FM) {                                                                            \
-    transpose_pair<EPI, FM, I>(acc, scratch, lane, v);                                               \
+    transpose_pair<EPI, FM, FN, JP, I>(acc, scratch, lane, v);                                       \
     for (int q = 0; q < 4; ++q) {                                                                    \
       const int64_t m = mw + 32 * (I) + rr + 8 * q;                                                  \
       if (!vec) {                                                                                    \
         for (int e = 0; e < 8; ++e)                                                                  \
-          if (m < p.M && n + e < p.N) epi_store<true, EPI>(p, m, n + e, v[q][e]);                    \
+          if (m < p.M && n + e < p.N) {                                                              \
+            float a = v[q][e];                                                                       \
+            if constexpr (SCALED) a *= p.row_scale[m] * p.col_scale[n + e];                          \
+            epi_store<true, EPI>(p, m, n + e, a);                                                    \
+          }                                                                                          \
         continue;                                                                                    \
       }                                                                                              \
+      float rsm = 1.f;                                                                               \
+      if constexpr (SCALED) rsm = p.row_scale[m < p.M ? m : p.M - 1];                                \
       float g[8], r8[8];                                                                             \
       if constexpr (EPI == EPI_GATED) {                                                              \
         const uint32_t w[4] = {rs[(I) & 1][q].x, rs[(I) & 1][q].y, rs[(I) & 1][q].z, rs[(I) & 1][q].w};  \
@@ -277,7 +302,9 @@ __device__ __forceinline__ void epilogue_pairs(const GemmParams& p, const f32x16
         }                                                                                            \
       }                                                                                              \
       for (int e = 0; e < 8; ++e) {                                                                  \
-        float x = v[q][e] + bv[e];                                                                   \
+        float x = v[q][e];                                                                           \
+        if constexpr (SCALED) x *= rsm * cs[e];                                                      \
+        x += bv[e];                                                                                  \
         if constexpr (EPI == EPI_GELU) {                                                             \
           if (n + e >= p.gelu_from) x = gelu_tanh_f(x);                                              \
         } else if constexpr (EPI == EPI_GATED) {                                                     \
@@ -604,11 +631,16 @@ __device__ __forceinline__ void dma_buf16(const u32x4_t& rsrc, uint32_t voff, ui
 
 // LAYOUT 0: each wave a 128 x 64 block (wm = w4 / 2, wn = 2 grp + w4 % 2); LAYOUT 1: a 64 x 128
 // block (wm = w4, wn = grp), one whole 128-column head, for the fused QKV epilogue.  The two
-// waves of a SIMD (same w4) always share their A rows.
-template <int EPI, int LAYOUT>
-__global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
-  constexpr int BM = 256, BN = 256, KS = 64, ROWB = KS * 2;   // 128-byte LDS rows
+// waves of a SIMD (same w4) always share their A rows.  F8: operands are E4M3 codes; a slab is
+// 128 of them, read as two k64 steps of 32 bytes per lane (lane half h takes bytes 32 h ..
+// 32 h + 31 of the step, for A and W alike) into the unscaled MFMA 32x32x64.
+template <int EPI, int LAYOUT, bool F8>
+__device__ __forceinline__ void pp_body(const GemmBatch& batch) {
+  constexpr int ES = F8 ? 1 : 2;                              // bytes per element
+  constexpr int BM = 256, BN = 256, ROWB = 128, KS = ROWB / ES;   // 128-byte LDS rows
   constexpr int STAGE = (BM + BN) * ROWB;                     // 64 KB
+  constexpr int KSTEPS = F8 ? 2 : 4;                          // MFMA k steps per slab
+  static_assert(!F8 || (EPI == EPI_NONE || EPI == EPI_GELU), "fp8 epilogues: bias, GELU");
   constexpr int TM = LAYOUT == 0 ? 128 : 64, TN = LAYOUT == 0 ? 64 : 128;
   constexpr int FM = TM / 32, FN = TN / 32;
   static_assert((EPI != EPI_QKV && EPI != EPI_QKV_GELU) || LAYOUT == 1, "the fused QKV epilogue needs a head per wave");
@@ -640,16 +672,16 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
   // A may come from two sources (the two-part K of the fused single-stream projection):
   // slabs [0, KT1) from A1, the rest from A2.
   const bool two = KT1 > 0 && KT1 < KT;
-  const char* a1_tile = reinterpret_cast<const char*>(static_cast<const bf16_t*>(p.A1) + m0 * p.lda1);
-  const char* a2_tile = reinterpret_cast<const char*>(static_cast<const bf16_t*>(p.A2) + m0 * p.lda2);
-  const int64_t a1_bytes = rows_a * p.lda1 * 2, a2_bytes = rows_a * p.lda2 * 2;
-  const uint32_t a1_off = static_cast<uint32_t>((lrow * p.lda1 + lck * 8) * 2);
-  const uint32_t a2_off = static_cast<uint32_t>((lrow * p.lda2 + lck * 8) * 2);
-  const uint32_t a1_step = static_cast<uint32_t>(32 * p.lda1 * 2), a2_step = static_cast<uint32_t>(32 * p.lda2 * 2);
-  const char* b_tile = reinterpret_cast<const char*>(static_cast<const bf16_t*>(p.W) + n0 * p.ldw);
-  const int64_t b_bytes = rows_b * p.ldw * 2;
-  const uint32_t b_off = static_cast<uint32_t>((lrow * p.ldw + lck * 8) * 2);
-  const uint32_t b_step = static_cast<uint32_t>(32 * p.ldw * 2);
+  const char* a1_tile = static_cast<const char*>(p.A1) + m0 * p.lda1 * ES;
+  const char* a2_tile = static_cast<const char*>(p.A2) + m0 * p.lda2 * ES;
+  const int64_t a1_bytes = rows_a * p.lda1 * ES, a2_bytes = rows_a * p.lda2 * ES;
+  const uint32_t a1_off = static_cast<uint32_t>(lrow * p.lda1 * ES + lck * 16);
+  const uint32_t a2_off = static_cast<uint32_t>(lrow * p.lda2 * ES + lck * 16);
+  const uint32_t a1_step = static_cast<uint32_t>(32 * p.lda1 * ES), a2_step = static_cast<uint32_t>(32 * p.lda2 * ES);
+  const char* b_tile = static_cast<const char*>(p.W) + n0 * p.ldw * ES;
+  const int64_t b_bytes = rows_b * p.ldw * ES;
+  const uint32_t b_off = static_cast<uint32_t>(lrow * p.ldw * ES + lck * 16);
+  const uint32_t b_step = static_cast<uint32_t>(32 * p.ldw * ES);
   const uint32_t smem_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
   auto rsrc_b = [&](int s) {
     const int64_t db = static_cast<int64_t>(s) * ROWB;
@@ -676,31 +708,51 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
   const int frow = lane & 31, fhalf = lane >> 5;
   const int key = (frow >> 1) & 7;
   const int a_frag0 = (wm * TM + frow) * ROWB, b_frag0 = BM * ROWB + (wn * TN + frow) * ROWB;
-  bf16x8_t fa[4][FM], fb[4][FN];   // one slab of fragments: [k16 step][block]
+  // One slab of fragments, [k step][block]: 16 bytes per lane (bf16, k16 steps) or 32 (fp8, k64).
+  typedef typename std::conditional<F8, i32x8_t, bf16x8_t>::type frag_t;
+  frag_t fa[KSTEPS][FM], fb[KSTEPS][FN];
   auto read_frags = [&](int s) {
     const char* S = smem + (s & 1) * STAGE;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const int coff = ((ks * 2 + fhalf) ^ key) << 4;
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+      if constexpr (F8) {
+        const int c0 = ((ks * 4 + fhalf * 2) ^ key) << 4, c1 = ((ks * 4 + fhalf * 2 + 1) ^ key) << 4;
+        auto rd32 = [&](int off) {
+          const u32x4_t lo = *reinterpret_cast<const u32x4_t*>(S + off + c0);
+          const u32x4_t hi = *reinterpret_cast<const u32x4_t*>(S + off + c1);
+          return i32x8_t{int(lo.x), int(lo.y), int(lo.z), int(lo.w), int(hi.x), int(hi.y), int(hi.z), int(hi.w)};
+        };
 #pragma unroll
-      for (int i = 0; i < FM; ++i) fa[ks][i] = *reinterpret_cast<const bf16x8_t*>(S + a_frag0 + i * 32 * ROWB + coff);
+        for (int i = 0; i < FM; ++i) fa[ks][i] = rd32(a_frag0 + i * 32 * ROWB);
 #pragma unroll
-      for (int j = 0; j < FN; ++j) fb[ks][j] = *reinterpret_cast<const bf16x8_t*>(S + b_frag0 + j * 32 * ROWB + coff);
+        for (int j = 0; j < FN; ++j) fb[ks][j] = rd32(b_frag0 + j * 32 * ROWB);
+      } else {
+        const int coff = ((ks * 2 + fhalf) ^ key) << 4;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) fa[ks][i] = *reinterpret_cast<const bf16x8_t*>(S + a_frag0 + i * 32 * ROWB + coff);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) fb[ks][j] = *reinterpret_cast<const bf16x8_t*>(S + b_frag0 + j * 32 * ROWB + coff);
+      }
     }
   };
-  // The 32 MFMAs of a slab; with `rb` set, the W rows of a later slab are loaded between them.
+  // The MFMAs of a slab (32 bf16 or 16 fp8); with `rb` set, the eight W-row loads of a later
+  // slab are spread between them.
   auto compute = [&](const u32x4_t* rb, uint32_t lds_b) {
+    constexpr int PER = KSTEPS * FM * FN / 8;   // MFMAs per W-row load
+    static_assert(KSTEPS * FM * FN == 8 * PER, "eight loads per compute phase");
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
+    for (int ks = 0; ks < KSTEPS; ++ks)
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks][i], fb[ks][j], acc[i][j], 0, 0, 0);
-          constexpr int PER = FM * FN / 2;   // one W-row load after every fourth MFMA
-          if (rb != nullptr && ((i * FN + j) & 3) == 3) {
-            const int q = ks * 2 + (i * FN + j) / 4;
-            static_assert(PER == 4, "eight loads per compute phase");
+          if constexpr (F8)   // zero scale operands: the compiler emits the unscaled v_mfma_f32_32x32x64_f8f6f4
+            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa[ks][i], fb[ks][j], acc[i][j], 0, 0, 0, 0, 0, 0);
+          else
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks][i], fb[ks][j], acc[i][j], 0, 0, 0);
+          const int idx = (ks * FM + i) * FN + j;
+          if (rb != nullptr && idx % PER == PER - 1) {
+            const int q = idx / PER;
             dma_buf16(*rb, b_off + q * b_step, lds_b + q * 4096);
           }
           __builtin_amdgcn_sched_barrier(0);
@@ -802,15 +854,23 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
       epilogue_qkv<FM, FN>(p, acc, mw, nw, smem + wave * QKV_SCRATCH, lane);
     } else {
       float* fs = reinterpret_cast<float*>(smem + wave * QKV_SCRATCH);
-      const f32x16_t lo[FM][2] = {{acc[0][0], acc[0][1]}, {acc[1][0], acc[1][1]}};
-      epilogue_pairs<EPI_GELU, FM>(p, lo, mw, nw, fs, lane);
-      const f32x16_t hi[FM][2] = {{acc[0][2], acc[0][3]}, {acc[1][2], acc[1][3]}};
-      epilogue_pairs<EPI_GELU, FM>(p, hi, mw, nw + 64, fs, lane);
+      epilogue_pairs<EPI_GELU, FM, FN, 0>(p, acc, mw, nw, fs, lane);
+      epilogue_pairs<EPI_GELU, FM, FN, 1>(p, acc, mw, nw + 64, fs, lane);
     }
   } else {
     static_assert(FN == 2 && 8 * 32 * PAIR_LD * 4 <= 2 * STAGE, "epilogue scratch fits the LDS ring");
-    epilogue_pairs<EPI, FM>(p, acc, m0 + wm * TM, n0 + wn * TN, reinterpret_cast<float*>(smem) + wave * 32 * PAIR_LD, lane);
+    epilogue_pairs<EPI, FM, FN, 0, F8>(p, acc, m0 + wm * TM, n0 + wn * TN,
+                                       reinterpret_cast<float*>(smem) + wave * 32 * PAIR_LD, lane);
   }
+}
+
+template <int EPI, int LAYOUT>
+__global__ __launch_bounds__(512, 1) void gemm_bf16_pp(GemmBatch batch) {
+  pp_body<EPI, LAYOUT, false>(batch);
+}
+template <int EPI>
+__global__ __launch_bounds__(512, 1) void gemm_fp8_pp(GemmBatch batch) {
+  pp_body<EPI, 0, true>(batch);
 }
 
 // ------------------------------------------------------------------ float32
@@ -898,6 +958,25 @@ int launch_pp_batch(const GemmBatch& b, hipStream_t s, const char* name, double 
 }
 
 int64_t tiles256(const GemmParams& p) { return ((p.M + 255) / 256) * ((p.N + 255) / 256); }
+
+template <int EPI>
+int launch_fp8(const GemmParams& p, hipStream_t s, const char* name, double flops, double bytes) {
+  constexpr int smem = 2 * 512 * 128;
+  static bool attr_set = false;
+  if (!attr_set) {
+    FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_fp8_pp<EPI>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, smem),
+                 "gemm smem attribute");
+    attr_set = true;
+  }
+  GemmBatch b{};
+  b.p[0] = p;
+  b.p[1] = p;
+  b.tiles0 = b.tiles = tiles256(p);
+  LaunchScope ls(name, s, flops, bytes);
+  hipLaunchKernelGGL((gemm_fp8_pp<EPI>), dim3(static_cast<unsigned>(b.tiles)), dim3(512), smem, s, b);
+  return ls.status();
+}
 
 const char* const kGemmNames[5] = {"gemm_bf16", "gemm_bf16_gelu", "gemm_bf16_gated", "gemm_bf16_qkv",
                                    "gemm_bf16_qkv_gelu"};
@@ -1002,6 +1081,24 @@ int gemm(const GemmArgs& a, hipStream_t s) {
     case EPI_GELU: return dispatch_f32<EPI_GELU>(p, s, flops, bytes);
     default: return dispatch_f32<EPI_GATED>(p, s, flops, bytes);
   }
+}
+
+int gemm_fp8(const Fp8GemmArgs& a, hipStream_t s) {
+  if (a.M == 0 || a.N == 0) return FF_OK;
+  if (a.K % 128 != 0) return fail(FF_EUNSUPPORTED, "gemm_fp8: K=%lld must be a multiple of 128", (long long)a.K);
+  GemmParams p{};
+  p.M = a.M; p.N = a.N; p.K = a.K;
+  p.A1 = a.A; p.lda1 = a.lda; p.K1 = a.K; p.A2 = a.A; p.lda2 = a.lda;
+  p.W = a.W; p.ldw = a.ldw; p.bias = a.bias;
+  p.out = a.out; p.ldo = a.ldo; p.gelu_from = a.gelu_from;
+  p.rows_per_sample = a.M;
+  p.row_scale = a.d_a; p.col_scale = a.d_w;
+  p.vec_ok = a.ldo % 8 == 0 && aligned16(a.out) && (!a.bias || aligned16(a.bias)) && aligned16(a.d_w);
+  const double flops = 2.0 * a.M * a.N * a.K;
+  const double bytes = static_cast<double>(a.M) * a.K + static_cast<double>(a.N) * a.K + 2.0 * a.M * a.N +
+                       4.0 * (a.M + a.N);
+  if (a.epi == EPI_GELU) return launch_fp8<EPI_GELU>(p, s, "gemm_fp8_gelu", flops, bytes);
+  return launch_fp8<EPI_NONE>(p, s, "gemm_fp8", flops, bytes);
 }
 
 int gemm2(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {

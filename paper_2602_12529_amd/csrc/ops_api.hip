@@ -143,4 +143,40 @@ int ff_skinny_linear(const float* in, const void* W, const void* bias, float* ou
   return skinny_linear(a, static_cast<hipStream_t>(stream));
 }
 
+int ff_quantize_fp8(const void* x, int64_t ldx, uint8_t* q, int64_t ldq, float* d, int64_t rows, int64_t cols,
+                    int32_t dtype, void* stream) {
+  const char* fn = "ff_quantize_fp8";
+  FF_TRY(check_dtype(fn, dtype));
+  if (rows < 0 || cols < 0) return fail(FF_EINVAL, "%s: bad shape rows=%lld cols=%lld", fn, (long long)rows, (long long)cols);
+  if (rows == 0) return FF_OK;
+  if (!x || !q || !d) return fail(FF_EINVAL, "%s: null x, q or d", fn);
+  if (ldx < cols || ldq < cols) return fail(FF_EINVAL, "%s: ldx or ldq < cols", fn);
+  if (cols % 8 || ldx % 8 || ldq % 8) return fail(FF_EUNSUPPORTED, "%s: cols, ldx and ldq must be multiples of 8", fn);
+  if (!aligned16(x) || !aligned16(q)) return fail(FF_EINVAL, "%s: x and q must be 16-byte aligned", fn);
+  return quantize_fp8(dtype, x, ldx, q, ldq, d, rows, cols, static_cast<hipStream_t>(stream));
+}
+
+int ff_linear_fp8(const uint8_t* A, int64_t lda, const float* d_a, const uint8_t* W, int64_t ldw, const float* d_w,
+                  const void* bias, void* out, int64_t ldo, int64_t M, int64_t N, int64_t K, int32_t epi,
+                  int64_t gelu_from, void* stream) {
+  const char* fn = "ff_linear_fp8";
+  if (M < 0 || N < 0 || K < 1) return fail(FF_EINVAL, "%s: bad shape M=%lld N=%lld K=%lld", fn, (long long)M, (long long)N, (long long)K);
+  if (M == 0 || N == 0) return FF_OK;
+  if (!A || !W || !d_a || !d_w || !out) return fail(FF_EINVAL, "%s: null A, W, d_a, d_w or out", fn);
+  if (lda < K || ldw < K || ldo < N) return fail(FF_EINVAL, "%s: lda or ldw < K, or ldo < N", fn);
+  if (epi != FF_EPI_BIAS && epi != FF_EPI_GELU) return fail(FF_EINVAL, "%s: epilogue %d (bias or GELU only)", fn, epi);
+  if (K % 128) return fail(FF_EUNSUPPORTED, "%s: K %% 128 != 0 (K=%lld)", fn, (long long)K);
+  if (lda % 16 || ldw % 16 || ldo % 8) return fail(FF_EINVAL, "%s: lda, ldw %% 16 and ldo %% 8 must be 0", fn);
+  if (!aligned16(A) || !aligned16(W) || !aligned16(out) || !aligned16(d_w) || (bias && !aligned16(bias)))
+    return fail(FF_EINVAL, "%s: A, W, out, bias and d_w must be 16-byte aligned", fn);
+  Fp8GemmArgs g{};
+  g.M = M; g.N = N; g.K = K;
+  g.A = A; g.lda = lda; g.d_a = d_a;
+  g.W = W; g.ldw = ldw; g.d_w = d_w;
+  g.bias = bias; g.out = out; g.ldo = ldo;
+  g.epi = epi == FF_EPI_GELU ? EPI_GELU : EPI_NONE;
+  g.gelu_from = gelu_from;
+  return gemm_fp8(g, static_cast<hipStream_t>(stream));
+}
+
 }  // extern "C"

@@ -5,6 +5,9 @@ Subcommands (python -m paper_2602_12529_amd.profiling ...):
   copy --bytes N --reps R
       A plain device-to-device copy of N bytes, R times: the calibration kernel
       whose FETCH_SIZE / WRITE_SIZE counters are compared with the known N.
+  linear --M --N --K --precision bf16|fp8 [--gelu] --reps R
+      One linear layer on random device data, R times, timed per launch by the
+      library's events (fp8: the activation quantiser and the FP8 GEMM).
   stats CSV OUT --title T --cmd C
       kernel_stats.csv of `rocprofv3 --kernel-trace --stats` -> markdown table.
   traffic --fetch CSV --write CSV --copy-fetch CSV --copy-write CSV --copy-bytes N
@@ -87,6 +90,56 @@ def run_copy(nbytes: int, reps: int) -> None:
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_bytes": nbytes, "reps": reps}), flush=True)
+
+
+def run_linear(M: int, N: int, K: int, precision: str, gelu: bool, reps: int) -> dict:
+    """Times one linear layer (bf16 ff_linear, or fp8 ff_quantize_fp8 of the activations plus
+    ff_linear_fp8) on random device data with the library's own per-launch events."""
+    import torch
+
+    from . import api
+
+    if not torch.cuda.is_available():
+        raise SystemExit("linear timing needs a GPU")
+    g = torch.Generator(device="cuda").manual_seed(0)
+    x = torch.randn((M, K), device="cuda", generator=g).to(torch.bfloat16)
+    w = (torch.randn((N, K), device="cuda", generator=g) * 0.02).to(torch.bfloat16)
+    b = (torch.randn((N,), device="cuda", generator=g) * 0.1).to(torch.bfloat16)
+    out = torch.empty((M, N), device="cuda", dtype=torch.bfloat16)
+    epi = api.EPI_GELU if gelu else api.EPI_BIAS
+    if precision == "fp8":
+        wq, wd = api.quantize_fp8(w)
+        xq = torch.empty((M, K), device="cuda", dtype=torch.uint8)
+        xd = torch.empty((M,), device="cuda", dtype=torch.float32)
+
+        def step():
+            api.quantize_fp8(x, xq, xd)
+            api.linear_fp8(xq, xd, wq, wd, b, out, epi=epi)
+    else:
+        def step():
+            api.linear(x, w, b, out, epi=epi)
+    for _ in range(3):
+        step()
+    torch.cuda.synchronize()
+    api.profile_reset()
+    api.profile_enable(True)
+    for _ in range(reps):
+        step()
+    torch.cuda.synchronize()
+    api.profile_enable(False)
+    prof = api.profile_read()
+    res = {"M": M, "N": N, "K": K, "precision": precision, "gelu": gelu, "reps": reps, "kernels": {}}
+    peak = 5000.0 if precision == "fp8" else 2500.0
+    for name, r in prof.items():
+        k = {"avg_us": 1e3 * r["ms"] / r["launches"]}
+        if r["flops"] > 0:
+            k["tflops"] = r["flops"] / (r["ms"] * 1e-3) / 1e12
+            k["frac_of_dense_peak"] = k["tflops"] / peak
+        elif r["bytes"] > 0:
+            k["gbs"] = r["bytes"] / (r["ms"] * 1e-3) / 1e9
+        res["kernels"][name] = k
+    print(json.dumps(res), flush=True)
+    return res
 
 
 # ---------------------------------------------------------------------------- summaries
@@ -197,6 +250,13 @@ def main(argv=None) -> int:
     c = sub.add_parser("copy")
     c.add_argument("--bytes", type=int, default=1 << 30)
     c.add_argument("--reps", type=int, default=4)
+    li = sub.add_parser("linear")
+    li.add_argument("--M", type=int, default=36864)
+    li.add_argument("--N", type=int, default=12288)
+    li.add_argument("--K", type=int, default=3072)
+    li.add_argument("--precision", choices=["bf16", "fp8"], default="fp8")
+    li.add_argument("--gelu", action="store_true")
+    li.add_argument("--reps", type=int, default=20)
     s = sub.add_parser("stats")
     s.add_argument("csv")
     s.add_argument("out")
@@ -213,6 +273,8 @@ def main(argv=None) -> int:
     a = ap.parse_args(argv)
     if a.action == "copy":
         run_copy(a.bytes, a.reps)
+    elif a.action == "linear":
+        run_linear(a.M, a.N, a.K, a.precision, a.gelu, a.reps)
     elif a.action == "stats":
         stats_md(a.csv, a.out, a.title, a.cmd)
     else:

@@ -17,7 +17,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 def declared_symbols():
     names = set()
-    for h in ("ff.h", "ff_ops.h", "ff_loss.h"):
+    for h in sorted(f for f in os.listdir(os.path.join(ROOT, "include")) if f.endswith(".h")):
         text = open(os.path.join(ROOT, "include", h)).read()
         names |= set(re.findall(r"^\s*(?:int|const char\*)\s+(ff_\w+)\s*\(", text, re.M))
     return names
@@ -110,6 +110,34 @@ def test_loss_argument_validation():
     _err(lib.ff_grpo_loss(f, f, f, None, 0, 3, 0.2, f, None, None), _lib.FF_EINVAL)
     _err(lib.ff_grpo_loss(f, f, f, None, 40000, 3, 0.2, f, None, None), _lib.FF_EUNSUPPORTED)
     _err(lib.ff_grpo_loss(None, f, f, None, 8, 3, 0.2, f, None, None), _lib.FF_EINVAL)
+
+
+def test_fp8_argument_validation():
+    """Host-side checks of the FP8 quantiser and linear layer: rejected calls return before any launch."""
+    lib = _lib.load()
+    f = c_void_p(8192)
+    # quantiser: dtype, nulls, strides below the row, widths not a multiple of 8, misalignment, empty
+    _err(lib.ff_quantize_fp8(f, 64, f, 64, f, 4, 64, 7, None), _lib.FF_EINVAL)
+    _err(lib.ff_quantize_fp8(None, 64, f, 64, f, 4, 64, 1, None), _lib.FF_EINVAL)
+    _err(lib.ff_quantize_fp8(f, 32, f, 64, f, 4, 64, 1, None), _lib.FF_EINVAL)
+    _err(lib.ff_quantize_fp8(f, 60, f, 60, f, 4, 60, 1, None), _lib.FF_EUNSUPPORTED)
+    _err(lib.ff_quantize_fp8(c_void_p(8200), 64, f, 64, f, 4, 64, 1, None), _lib.FF_EINVAL)
+    assert lib.ff_quantize_fp8(f, 64, f, 64, f, 0, 64, 1, None) == 0
+    # linear: K % 128, epilogue kind, nulls, strides, alignment, empty
+    args = dict(A=f, lda=256, d_a=f, W=f, ldw=256, d_w=f, bias=None, out=f, ldo=64, M=8, N=64, K=256, epi=0)
+
+    def call(**kw):
+        a = {**args, **kw}
+        return lib.ff_linear_fp8(a["A"], a["lda"], a["d_a"], a["W"], a["ldw"], a["d_w"], a["bias"], a["out"],
+                                 a["ldo"], a["M"], a["N"], a["K"], a["epi"], 0, None)
+    _err(call(K=192, lda=192, ldw=192), _lib.FF_EUNSUPPORTED)
+    _err(call(epi=2), _lib.FF_EINVAL)
+    _err(call(d_a=None), _lib.FF_EINVAL)
+    _err(call(lda=128), _lib.FF_EINVAL)
+    _err(call(lda=264), _lib.FF_EINVAL)
+    _err(call(W=c_void_p(8200)), _lib.FF_EINVAL)
+    _err(call(K=0), _lib.FF_EINVAL)
+    assert call(M=0) == 0
 
 
 def test_advantage_argument_validation():
