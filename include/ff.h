@@ -234,6 +234,9 @@ int ff_dit_forward(const ff_dit* m, const void* x, const void* txt, const int32_
  * and the algorithmic flops and bytes of those launches).
  * ------------------------------------------------------------------------ */
 int ff_profile_enable(int32_t on);
+/* Restricts the timing to launches of one kernel name (the string is copied; NULL or "" times
+ * every kernel again), so that a timed run pays for the events of that kernel only. */
+int ff_profile_filter(const char* name);
 int ff_profile_reset(void);
 int ff_profile_count(int32_t* n /* host, out: distinct kernel names */);
 int ff_profile_read(int32_t i, char* name, size_t name_cap, int64_t* launches, double* total_ms,

@@ -54,6 +54,7 @@ _SIGS = {
                                  c_void_p]),
     "ff_profile_enable": (c_int32, [c_int32]),
     "ff_profile_reset": (c_int32, []),
+    "ff_profile_filter": (c_int32, [c_char_p]),
     "ff_profile_count": (c_int32, [POINTER(c_int32)]),
     "ff_profile_read": (c_int32, [c_int32, c_char_p, c_size_t, POINTER(c_int64), POINTER(c_double),
                                   POINTER(c_double), POINTER(c_double)]),

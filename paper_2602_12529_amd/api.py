@@ -316,6 +316,11 @@ def profile_enable(on: bool = True):
     check(load().ff_profile_enable(1 if on else 0), "ff_profile_enable")
 
 
+def profile_filter(name: Optional[str] = None):
+    """Time only the launches of kernel `name` (None: every kernel)."""
+    check(load().ff_profile_filter(name.encode() if name else None), "ff_profile_filter")
+
+
 def profile_reset():
     check(load().ff_profile_reset(), "ff_profile_reset")
 

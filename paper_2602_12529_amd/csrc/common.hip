@@ -40,6 +40,7 @@ struct Totals {
 };
 std::mutex g_mu;
 bool g_on = false;
+std::string g_filter;   // empty: every kernel
 std::vector<Pending> g_pending;
 std::vector<hipEvent_t> g_pool;
 std::map<std::string, Totals> g_totals;
@@ -79,6 +80,7 @@ LaunchScope::LaunchScope(const char* name, hipStream_t s, double flops, double b
     : name_(name), stream_(s), flops_(flops), bytes_(bytes), slot_(-1) {
   std::lock_guard<std::mutex> lk(g_mu);
   if (!g_on) return;
+  if (!g_filter.empty() && g_filter != name_) return;
   hipEvent_t a = get_event(), b = get_event();
   if (!a || !b) return;
   if (hipEventRecord(a, stream_) != hipSuccess) return;
@@ -111,6 +113,12 @@ const char* ff_version(void) { return "ff 0.1 gfx950"; }
 int ff_profile_enable(int32_t on) {
   std::lock_guard<std::mutex> lk(g_mu);
   g_on = on != 0;
+  return FF_OK;
+}
+
+int ff_profile_filter(const char* name) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  g_filter = name ? name : "";
   return FF_OK;
 }
 

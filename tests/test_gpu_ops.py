@@ -206,3 +206,29 @@ def test_skinny_linear_parity(gpu_lib, B, N, K, dt, act):
     xa = {0: xa, 1: odit.silu(xa), 2: odit.gelu_tanh(xa)}[act]
     ref = xa @ odit.f64(w).T + odit.f64(b)
     assert rel(host(out), ref) <= 1e-5
+
+
+def test_profile_filter_times_one_kernel(gpu_lib):
+    """With a name filter only that kernel's launches are timed; without one, every launch is."""
+    A = torch.randn(512, 256, device="cuda").to(torch.bfloat16)
+    W = torch.randn(512, 256, device="cuda").to(torch.bfloat16)
+    out = torch.empty(512, 512, device="cuda", dtype=torch.bfloat16)
+    x = torch.randn(64, 256, device="cuda").to(torch.bfloat16)
+    y = torch.empty_like(x)
+    try:
+        for filt, expect in (("gemm_bf16", {"gemm_bf16"}), (None, {"gemm_bf16", "norm_modulate"})):
+            gpu_lib.profile_filter(filt)
+            gpu_lib.profile_reset()
+            gpu_lib.profile_enable(True)
+            gpu_lib.linear(A, W, None, out)
+            gpu_lib.norm_modulate(x, y)
+            gpu_lib.linear(A, W, None, out)
+            torch.cuda.synchronize()
+            gpu_lib.profile_enable(False)
+            prof = gpu_lib.profile_read()
+            assert set(prof) == expect, (filt, sorted(prof))
+            assert prof["gemm_bf16"]["launches"] == 2 and prof["gemm_bf16"]["ms"] > 0
+    finally:
+        gpu_lib.profile_enable(False)
+        gpu_lib.profile_filter(None)
+        gpu_lib.profile_reset()
