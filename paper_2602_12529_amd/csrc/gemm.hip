@@ -14,7 +14,9 @@
 // rows in L2.
 //
 // Epilogues fuse the bias, GELU-tanh (from a column on, for the fused
-// single-stream projection) and the adaLN-gated residual X + g * (.).
+// single-stream projection), the adaLN-gated residual X + g * (.) and, on the
+// QKV projections, the per-head QK norm, rotation and head-major relayout of
+// the attention operands (epilogue_qkv).
 //
 // fp8: the same 256 x 256 ping-pong kernel on OCP E4M3 codes (gemm_fp8_pp):
 // 128-wide K slabs (the same 128-byte LDS rows), the unscaled MFMA 32x32x64, and
