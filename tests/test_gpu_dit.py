@@ -270,6 +270,43 @@ def test_flux_dual_block_full_size(gpu_lib):
         assert abs(lp[b] - lr[0]) <= LOGP_ABS
 
 
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("shape", ["qwen", "flux-stack"])
+def test_dual_block_full_size_other_shapes(gpu_lib, shape):
+    """One dual-stream block at the other headline shapes, hidden 3072, 24 heads, MLP 12288, bf16:
+    the Qwen-Image stack's (B=8, 4096 image + 256 text tokens) and the Flux stack's (B=16, 1024 +
+    512), one SDE step; the fused QKV epilogue runs; the oracle recomputes two whole samples."""
+    base = C.FLUX_BLOCK
+    if shape == "qwen":
+        kw = dict(group=8, grid=(1, 64, 64), n_txt=256, index=18)
+    else:
+        kw = dict(group=16, grid=(1, 32, 32), n_txt=512, index=19)
+    w = C.Workload(**{**base.__dict__, "name": f"dual-block-{shape}", **kw})
+    m = w.model
+    say(shape, "dual block: generating inputs")
+    W, txt, cond, x0, eps = _inputs(w)
+    Wd, T, Cd, X0, E = _device(w, W, txt, cond, x0, eps)
+    dit = api.Dit(m, Wd)
+    ro = R.Rollout(w, dit)
+    api.profile_reset()
+    api.profile_enable(True)
+    try:
+        res = ro.run(X0, T, E, cond=Cd)
+        torch.cuda.synchronize()
+    finally:
+        api.profile_enable(False)
+    prof = api.profile_read()
+    api.profile_reset()
+    assert prof.get("gemm_bf16_qkv", {}).get("launches", 0) == 1, sorted(prof)
+    v = host(res.vs[0])
+    for b in (0, w.batch - 1):
+        say("oracle sample", b)
+        img, _ = odit.forward(m, W, x0[b:b + 1], txt[b:b + 1], cond=cond[b:b + 1], grid=w.grid)
+        e_v = rel(v[b:b + 1], img)
+        say("  rel v", e_v)
+        assert e_v <= TOL[C.BF16]
+
+
 @pytest.mark.parametrize("n_dual,n_single,kernel", [(1, 0, "gemm_bf16_qkv"), (0, 1, "gemm_bf16_qkv_gelu")])
 def test_fused_qkv_epilogue_ragged_streams(gpu_lib, n_dual, n_single, kernel):
     """A dual-stream block (text and image QKV projections grouped in one launch) or a single-stream
