@@ -192,3 +192,13 @@ def test_dit_validation_and_workspace_plan():
     _err(lib.ff_dit_num_tensors(byref(cfg2), byref(n)), _lib.FF_EINVAL)
     cfg3 = api.dit_config(m.replace(rope_axes=(16, 56, 54)))
     _err(lib.ff_dit_num_tensors(byref(cfg3), byref(n)), _lib.FF_EINVAL)
+
+
+def test_missing_library_fails_loudly(tmp_path, monkeypatch):
+    """Without the HIP library the binding raises instead of falling back to anything else."""
+    monkeypatch.setattr(_lib, "_lib", None)
+    monkeypatch.setattr(_lib, "LIB_PATH", str(tmp_path / "libff.so"))
+    with pytest.raises(RuntimeError, match="no non-HIP implementation"):
+        _lib.load()
+    with pytest.raises(RuntimeError):
+        api.profile_reset()
