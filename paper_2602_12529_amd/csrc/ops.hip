@@ -24,6 +24,23 @@ __device__ __forceinline__ float act_apply(int act, float x) {
   return x;
 }
 
+// Step ST of the halving exchange of V per-lane values (compile-time trip counts throughout, so
+// the values stay in registers): lanes whose bit (32 >> ST) is set keep the upper half.
+template <int V, int ST, int S>
+__device__ __forceinline__ void halve_steps(float (&a)[V], int lane) {
+  if constexpr (ST < S) {
+    constexpr int o = 32 >> ST, half = V >> (ST + 1);
+    const bool up = (lane & o) != 0;
+#pragma unroll
+    for (int i = 0; i < half; ++i) {
+      const float send = up ? a[i] : a[i + half];
+      const float keep = up ? a[i + half] : a[i];
+      a[i] = keep + __shfl_xor(send, o, 64);
+    }
+    halve_steps<V, ST + 1, S>(a, lane);
+  }
+}
+
 template <bool BF16, int BC, int R>
 __global__ __launch_bounds__(256) void skinny_kernel(const float* __restrict__ in, int64_t ldi, int act_in,
                                                      const void* __restrict__ W, const void* __restrict__ bias,
@@ -96,33 +113,30 @@ __global__ __launch_bounds__(256) void skinny_kernel(const float* __restrict__ i
     }
   }
   if (!active) return;
-  // Lane b finishes sample b: the bias and accumulate loads of all R rows are issued together,
-  // one round trip per wave rather than one per (row, sample).
-  float mine[R];
+  // Wave-wide sums of the R x BC partial sums by halving exchanges: at each step a lane keeps the
+  // half of its values that its lane bit selects and adds the partner's copy of that half, so the
+  // V = R x BCP values (BCP = BC rounded up to a power of two, padded with zeros) need V - 1
+  // shuffles instead of V x 6.  Afterwards lane l holds the full sum of value l >> (6 - S),
+  // i.e. one (row, sample) per lane, and stores it.
+  constexpr int BCP = BC <= 1 ? 1 : BC <= 2 ? 2 : BC <= 4 ? 4 : BC <= 8 ? 8 : 16;
+  constexpr int V = R * BCP;
+  constexpr int S = V <= 1 ? 0 : V <= 2 ? 1 : V <= 4 ? 2 : V <= 8 ? 3 : V <= 16 ? 4 : V <= 32 ? 5 : 6;
+  static_assert((1 << S) == V && S <= 6, "R x BCP must be a power of two up to 64");
+  float a[V];
 #pragma unroll
-  for (int r = 0; r < R; ++r) {
-    mine[r] = 0.f;
+  for (int r = 0; r < R; ++r)
 #pragma unroll
-    for (int b = 0; b < BC; ++b) {
-      const float s = wave_sum(acc[r][b]);
-      mine[r] = lane == b ? s : mine[r];
-    }
-  }
-  if (lane < BC) {
-    float bv[R], ov[R];
+    for (int b = 0; b < BCP; ++b) a[r * BCP + b] = b < BC ? acc[r][b] : 0.f;
+  halve_steps<V, 0, S>(a, lane);
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const int64_t n = n0 + r < N ? n0 + r : N - 1;
-      bv[r] = bias ? ld1<BF16>(bias, n) : 0.f;
-      ov[r] = accumulate ? out[lane * ldo + n] : 0.f;
-    }
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-      if (n0 + r < N) {
-        float v = act_apply(act_out, mine[r] + bv[r]);
-        if (accumulate) v += ov[r];
-        out[lane * ldo + n0 + r] = v;
-      }
+  for (int o = 32 >> S; o > 0; o >>= 1) a[0] += __shfl_xor(a[0], o, 64);
+  const int v = lane >> (6 - S);
+  const int r = v / BCP, b = v % BCP;
+  if (b < BC && n0 + r < N && (lane & ((1 << (6 - S)) - 1)) == 0) {
+    const int64_t n = n0 + r;
+    float y = act_apply(act_out, a[0] + (bias ? ld1<BF16>(bias, n) : 0.f));
+    if (accumulate) y += out[b * ldo + n];
+    out[b * ldo + n] = y;
   }
 }
 
