@@ -326,8 +326,10 @@ __device__ __forceinline__ void epilogue_pairs(const GemmParams& p, const f32x16
 // tokens of one stream (the QK norm and the rotation of the attention input, done while the
 // projection is still in registers instead of by a second pass over the packed output).
 //   Q, K: x = acc + bias; RMS over the head's 128 columns (a row's columns sit in 8 lanes of the
-//         wave); y = x / rms * w; each column pair (2j, 2j + 1) is rotated by the token's
-//         (cos, sin) of pair j; rows go to [B, heads, n_joint, 128] at tok_offset + token.
+//         wave); y = x / rms * w; each column pair (2j, 2j + 1) of a token at or past rope_from
+//         is rotated by (cos, sin) of pair j in table row token - rope_from (earlier tokens, the
+//         text of a joint sequence, are not rotated); rows go to [B, heads, n_joint, 128] at
+//         tok_offset + token.
 //   V:    x = acc + bias, written transposed to [B, heads, 128, n_joint] through a per-wave
 //         128 x 68 bf16 LDS scratch, so each head row leaves as 128 contiguous bytes.
 // The norm is taken of the float32 projection (the two-pass path reads it back rounded to bf16).
