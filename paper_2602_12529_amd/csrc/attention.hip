@@ -368,13 +368,8 @@ int attention(const AttnArgs& a, hipStream_t s) {
                  static_cast<bf16_t*>(a.out0), static_cast<bf16_t*>(a.out1), a.split, a.ldo,
                  static_cast<float>(a.scale * 1.4426950408889634), qbs, qhs, qrs};
     constexpr int WAVES = 8, STAGES = 4, smem = STAGES * (K_STAGE + V_STAGE);
-    static bool attr_set = false;
-    if (!attr_set) {
-      FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_bf16_d128<WAVES, STAGES>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, smem),
-                   "attention smem attribute");
-      attr_set = true;
-    }
+    static std::atomic<uint64_t> limit_set{0};
+    FF_TRY(ensure_smem_limit(reinterpret_cast<const void*>(&attn_bf16_d128<WAVES, STAGES>), smem, limit_set));
     const int64_t tiles = (a.n_q + 32 * WAVES - 1) / (32 * WAVES) * a.B * a.heads;
     LaunchScope ls("attn_bf16_d128", s, flops, bytes);
     hipLaunchKernelGGL((attn_bf16_d128<WAVES, STAGES>), dim3(static_cast<unsigned>(tiles)), dim3(64 * WAVES), smem, s, p);

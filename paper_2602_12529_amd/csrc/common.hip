@@ -27,6 +27,17 @@ int hip_status(hipError_t e, const char* what) {
   return fail(FF_EHIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+int ensure_smem_limit(const void* kernel, int bytes, std::atomic<uint64_t>& done) {
+  int dev = 0;
+  FF_CHECK_HIP(hipGetDevice(&dev), "hipGetDevice");
+  if (dev < 0 || dev >= 64) return fail(FF_EUNSUPPORTED, "device ordinal %d above 63", dev);
+  const uint64_t bit = uint64_t(1) << dev;
+  if (done.load(std::memory_order_acquire) & bit) return FF_OK;
+  FF_CHECK_HIP(hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes), "kernel LDS limit");
+  done.fetch_or(bit, std::memory_order_acq_rel);
+  return FF_OK;
+}
+
 // ----------------------------------------------------------------- profiler
 namespace {
 struct Pending {

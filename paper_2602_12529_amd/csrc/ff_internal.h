@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 #include <hip/hip_bf16.h>
 
+#include <atomic>
 #include <cstdint>
 #include <cstdio>
 #include <string>
@@ -36,6 +37,10 @@ inline size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // Wraps one kernel launch: records events when profiling is enabled and
 // checks the launch status.  `flops` / `bytes` are the launch's algorithmic
 // work, accumulated per kernel name.
+// Raises a kernel's dynamic-LDS limit to `bytes` on the current device, once per device (the
+// attribute belongs to the device; `done` is the caller's per-kernel mask of device ordinals 0..63).
+int ensure_smem_limit(const void* kernel, int bytes, std::atomic<uint64_t>& done);
+
 struct LaunchScope {
   LaunchScope(const char* name, hipStream_t s, double flops, double bytes);
   ~LaunchScope();

@@ -929,13 +929,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmParams p) {
 template <int BM, int BN, int WM, int WN, int EPI>
 int launch_bf16(const GemmParams& p, hipStream_t s, const char* name, double flops, double bytes) {
   constexpr int smem = 2 * (BM + BN) * BK * 2;
-  static bool attr_set = false;
-  if (!attr_set) {
-    FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<BM, BN, WM, WN, EPI>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, smem),
-                 "gemm smem attribute");
-    attr_set = true;
-  }
+  static std::atomic<uint64_t> limit_set{0};
+  FF_TRY(ensure_smem_limit(reinterpret_cast<const void*>(&gemm_bf16_kernel<BM, BN, WM, WN, EPI>), smem, limit_set));
   const int64_t tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
   LaunchScope ls(name, s, flops, bytes);
   hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, EPI>), dim3(static_cast<unsigned>(tiles)),
@@ -949,13 +944,8 @@ int launch_pp_batch(const GemmBatch& b, hipStream_t s, const char* name, double 
   constexpr int LAYOUT = qkv ? 1 : 0;
   constexpr int ring = 2 * 512 * 64 * 2;
   constexpr int smem = qkv && 8 * QKV_SCRATCH > ring ? 8 * QKV_SCRATCH : ring;
-  static bool attr_set = false;
-  if (!attr_set) {
-    FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_pp<EPI, LAYOUT>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, smem),
-                 "gemm smem attribute");
-    attr_set = true;
-  }
+  static std::atomic<uint64_t> limit_set{0};
+  FF_TRY(ensure_smem_limit(reinterpret_cast<const void*>(&gemm_bf16_pp<EPI, LAYOUT>), smem, limit_set));
   LaunchScope ls(name, s, flops, bytes);
   hipLaunchKernelGGL((gemm_bf16_pp<EPI, LAYOUT>), dim3(static_cast<unsigned>(b.tiles)), dim3(512), smem, s, b);
   return ls.status();
@@ -966,13 +956,8 @@ int64_t tiles256(const GemmParams& p) { return ((p.M + 255) / 256) * ((p.N + 255
 template <int EPI>
 int launch_fp8(const GemmParams& p, hipStream_t s, const char* name, double flops, double bytes) {
   constexpr int smem = 2 * 512 * 128;
-  static bool attr_set = false;
-  if (!attr_set) {
-    FF_CHECK_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_fp8_pp<EPI>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, smem),
-                 "gemm smem attribute");
-    attr_set = true;
-  }
+  static std::atomic<uint64_t> limit_set{0};
+  FF_TRY(ensure_smem_limit(reinterpret_cast<const void*>(&gemm_fp8_pp<EPI>), smem, limit_set));
   GemmBatch b{};
   b.p[0] = p;
   b.p[1] = p;
