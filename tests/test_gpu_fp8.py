@@ -87,7 +87,8 @@ def _check(out, ref, a_q, a_d, w_q, w_d, tag=""):
 
 
 @pytest.mark.parametrize("M,N,K,gelu", [(1, 8, 128, False), (100, 64, 128, True), (549, 360, 384, False),
-                                        (1030, 2104, 640, True), (4096, 3072, 3072, False)])
+                                        (1030, 2104, 640, True), (4096, 3072, 3072, False),
+                                        (3, 296, 15360, False), (520, 1032, 15360, True)])
 def test_linear_fp8_parity(gpu_lib, M, N, K, gelu):
     a_q, a_d = _codes(M * 7 + 1, M, K)
     w_q, w_d = _codes(N * 11 + 2, N, K)
