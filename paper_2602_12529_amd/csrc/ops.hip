@@ -278,6 +278,15 @@ __global__ __launch_bounds__(256) void norm_lds_kernel(NormArgs a) {
   const int64_t b = r0 / a.rows_per_sample;
   float* mul_s = mod_s;
   float* add_s = mod_s + H;
+  const float invH = 1.0f / static_cast<float>(H);
+  const bf16_t* __restrict__ xp = static_cast<const bf16_t*>(a.x);
+  bf16_t* __restrict__ yp = static_cast<bf16_t*>(a.y);
+  const int64_t rw = r0 + wave * RPW;
+  float v[NCH][8], nx[NCH][8];
+  if (rw < a.rows) {   // the first row is in flight while the modulation vectors are staged
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) ld8<true>(xp, rw * a.ldx + (c * 64 + lane) * 8, v[c]);
+  }
   for (int64_t j = threadIdx.x * 4; j < H; j += 1024) {
     float4 sc = a.scale ? *reinterpret_cast<const float4*>(a.scale + b * a.mod_ld + j) : make_float4(0.f, 0.f, 0.f, 0.f);
     float4 sh = a.shift ? *reinterpret_cast<const float4*>(a.shift + b * a.mod_ld + j) : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -285,15 +294,6 @@ __global__ __launch_bounds__(256) void norm_lds_kernel(NormArgs a) {
     *reinterpret_cast<float4*>(add_s + j) = sh;
   }
   __syncthreads();
-  const float invH = 1.0f / static_cast<float>(H);
-  const bf16_t* __restrict__ xp = static_cast<const bf16_t*>(a.x);
-  bf16_t* __restrict__ yp = static_cast<bf16_t*>(a.y);
-  const int64_t rw = r0 + wave * RPW;
-  float v[NCH][8], nx[NCH][8];
-  if (rw < a.rows) {
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) ld8<true>(xp, rw * a.ldx + (c * 64 + lane) * 8, v[c]);
-  }
   for (int rr = 0; rr < RPW; ++rr) {
     const int64_t row = rw + rr;
     if (row >= a.rows) break;
@@ -350,7 +350,7 @@ int norm_dispatch(const NormArgs& a, hipStream_t s) {
   const bool fits = a.H % 512 == 0 && a.ldx % 8 == 0 && a.ldy % 8 == 0 && aligned16(a.x) && aligned16(a.y) && mod_ok;
   if (BF16 && fits) nch = static_cast<int>(a.H / 512);
   if (nch > 8) nch = 0;
-  const int64_t block_rows = a.rows >= 32 * 512 ? 32 : 8;   // at least ~2 blocks per CU
+  const int64_t block_rows = a.rows >= 64 * 512 ? 64 : a.rows >= 32 * 512 ? 32 : 8;
   const bool one_sample_blocks = a.rows_per_sample % block_rows == 0 || a.rows <= a.rows_per_sample;
   if (BF16 && nch > 0 && nch <= 6 && one_sample_blocks && !a.w && !a.bias) {
     const dim3 grid(static_cast<unsigned>((a.rows + block_rows - 1) / block_rows));
@@ -359,6 +359,7 @@ int norm_dispatch(const NormArgs& a, hipStream_t s) {
 #define FF_NL(N, R) case N * 100 + R: hipLaunchKernelGGL((norm_lds_kernel<N, R / 4>), grid, dim3(256), shm, s, a); return FF_OK;
       FF_NL(1, 32) FF_NL(2, 32) FF_NL(3, 32) FF_NL(4, 32) FF_NL(5, 32) FF_NL(6, 32)
       FF_NL(1, 8) FF_NL(2, 8) FF_NL(3, 8) FF_NL(4, 8) FF_NL(5, 8) FF_NL(6, 8)
+      FF_NL(1, 64) FF_NL(2, 64) FF_NL(3, 64) FF_NL(4, 64) FF_NL(5, 64) FF_NL(6, 64)
 #undef FF_NL
     }
   }
