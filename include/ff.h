@@ -227,6 +227,27 @@ int ff_dit_forward(const ff_dit* m, const void* x, const void* txt, const int32_
                    int64_t B, int64_t n_txt, void* v_out, void* txt_out,
                    void* workspace, size_t ws_bytes, void* stream);
 
+/* WAN models only (others: FF_EUNSUPPORTED).  The cross-attention keys and values of every WAN block
+ * depend on the text context alone, which stays fixed along a trajectory (the condition c of
+ * Sec. 3.1), so a rollout computes them once:
+ *   ff_dit_context_size     bytes of the per-block store for B samples and n_txt text tokens
+ *   ff_dit_prepare_context  fills `context` (device, caller-owned, 16-byte aligned) from txt,
+ *                           txt_index and n_prompts as ff_dit_forward takes them; the workspace is
+ *                           sized by ff_dit_workspace_size for the same B, grid, n_txt, n_prompts
+ *   ff_dit_forward_ctx      ff_dit_forward with the text path replaced by that store: the same
+ *                           results as ff_dit_forward on the text the store was prepared from;
+ *                           any workspace sized by ff_dit_workspace_size for B, grid, n_txt serves
+ * Layout of the store: for block i, K [B, heads, n_txt, d] then V (bf16: transposed to
+ * [B, heads, d, n_txt]; float32: [B, heads, n_txt, d]), each padded to 256 bytes.  Errors as for
+ * ff_dit_forward; a store or workspace too small -> FF_EWORKSPACE. */
+int ff_dit_context_size(const ff_dit* m, int64_t B, int64_t n_txt, size_t* bytes /* host, out */);
+int ff_dit_prepare_context(const ff_dit* m, const void* txt, const int32_t* txt_index, int64_t n_prompts,
+                           const int32_t grid[3] /* host */, int64_t B, int64_t n_txt, void* context,
+                           size_t context_bytes, void* workspace, size_t ws_bytes, void* stream);
+int ff_dit_forward_ctx(const ff_dit* m, const void* x, const void* context, size_t context_bytes, const float* t,
+                       const int32_t grid[3] /* host */, int64_t B, int64_t n_txt, void* v_out,
+                       void* workspace, size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------------------
  * Kernel timing.  When enabled, every kernel the library launches is
  * bracketed by HIP events on its stream; ff_profile_read synchronises those

@@ -52,6 +52,11 @@ _SIGS = {
     "ff_dit_forward": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_int64, c_void_p, c_void_p,
                                  POINTER(c_int32), c_int64, c_int64, c_void_p, c_void_p, c_void_p, c_size_t,
                                  c_void_p]),
+    "ff_dit_context_size": (c_int32, [c_void_p, c_int64, c_int64, POINTER(c_size_t)]),
+    "ff_dit_prepare_context": (c_int32, [c_void_p, c_void_p, c_void_p, c_int64, POINTER(c_int32), c_int64, c_int64,
+                                         c_void_p, c_size_t, c_void_p, c_size_t, c_void_p]),
+    "ff_dit_forward_ctx": (c_int32, [c_void_p, c_void_p, c_void_p, c_size_t, c_void_p, POINTER(c_int32), c_int64,
+                                     c_int64, c_void_p, c_void_p, c_size_t, c_void_p]),
     "ff_profile_enable": (c_int32, [c_int32]),
     "ff_profile_reset": (c_int32, []),
     "ff_profile_filter": (c_int32, [c_char_p]),

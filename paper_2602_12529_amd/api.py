@@ -304,6 +304,32 @@ class Dit:
                                     _p(v_out), _p(txt_out), _p(ws), ws.numel(), _stream()), "ff_dit_forward")
         return v_out
 
+    # WAN: the per-block cross-attention K / V of a fixed text context, prepared once per rollout.
+    def context_size(self, B: int, n_txt: int) -> int:
+        n = c_size_t()
+        check(load().ff_dit_context_size(self._h, B, n_txt, byref(n)), "ff_dit_context_size")
+        return n.value
+
+    def prepare_context(self, txt, grid, B, txt_index=None, ws=None, context=None):
+        n_prompts, n_txt = txt.shape[0], txt.shape[1]
+        if context is None:
+            context = workspace(self.context_size(B, n_txt), txt.device)
+        if ws is None:
+            ws = workspace(self.workspace_size(B, grid, n_txt, n_prompts), txt.device)
+        g = (c_int32 * 3)(*grid)
+        check(load().ff_dit_prepare_context(self._h, _p(txt), _p(txt_index), n_prompts, g, B, n_txt, _p(context),
+                                            context.numel(), _p(ws), ws.numel(), _stream()), "ff_dit_prepare_context")
+        return context
+
+    def forward_ctx(self, x, context, n_txt, grid, v_out, t, ws=None):
+        B = x.shape[0]
+        if ws is None:
+            ws = workspace(self.workspace_size(B, grid, n_txt, 1), x.device)
+        g = (c_int32 * 3)(*grid)
+        check(load().ff_dit_forward_ctx(self._h, _p(x), _p(context), context.numel(), _p(t), g, B, n_txt, _p(v_out),
+                                        _p(ws), ws.numel(), _stream()), "ff_dit_forward_ctx")
+        return v_out
+
 
 def upload_weights(w: C.Workload, device="cuda") -> Dict[str, torch.Tensor]:
     from . import synth

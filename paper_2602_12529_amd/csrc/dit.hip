@@ -427,8 +427,14 @@ int relayout(const ff_dit_config& c, const Plan& p, const void* q, const void* k
   return qk_norm_rope(a, s);
 }
 
-// One WAN block on X [B*N_img, H] in place; ctx [B*N_txt, H]; mods [B, 6H].
-int wan_block(const ff_dit& m, const Plan& p, void* ws, int i, const void* ctx, void* X, hipStream_t s) {
+// Block i's cross-attention keys and values from the text context ctx [B*N_txt, H]: one GEMM to
+// [K | V], the RMSNorm of K over all of H, and the relayout to K [B, h, N_txt, d] and V^T.
+int wan_cross_kv(const ff_dit& m, const Plan& p, void* ws, int i, const void* ctx, void* K, void* Vt, hipStream_t s);
+
+// One WAN block on X [B*N_img, H] in place; mods [B, 6H].  The cross-attention reads K / V^T from
+// ctx_k / ctx_vt when given (prepared once per rollout), else computes them from ctx [B*N_txt, H].
+int wan_block(const ff_dit& m, const Plan& p, void* ws, int i, const void* ctx, const void* ctx_k,
+              const void* ctx_vt, void* X, hipStream_t s) {
   const ff_dit_config& c = m.cfg;
   const int64_t H = c.hidden, F = c.mlp_hidden;
   const size_t es = dtype_size(c.dtype);
@@ -470,16 +476,17 @@ int wan_block(const ff_dit& m, const Plan& p, void* ws, int i, const void* ctx, 
   }
   FF_TRY(gemm(gemm_args(c.dtype, rows, H, H, Y, H, wb.cq, QKV, H, EPI_NONE), s));
   FF_TRY(rms_rows(c, QKV, rows, H, wb.cqn, s));
-  char* KV = at(ws, p.kvc);
-  FF_TRY(gemm(gemm_args(c.dtype, crow, 2 * H, H, ctx, H, wb.ckv, KV, 2 * H, EPI_NONE), s));
-  FF_TRY(rms_rows(c, KV, crow, 2 * H, wb.ckn, s));
-  FF_TRY(relayout(c, p, KV, KV, KV + H * es, 2 * H, p.Nt, nullptr, at(ws, p.qd), at(ws, p.kc), at(ws, p.vct), s));
+  if (!ctx_k) {
+    FF_TRY(wan_cross_kv(m, p, ws, i, ctx, at(ws, p.kc), at(ws, p.vct), s));
+    ctx_k = at(ws, p.kc);
+    ctx_vt = at(ws, p.vct);
+  }
   {
     AttnArgs a{};
     a.dtype = c.dtype;
     a.B = p.B; a.heads = c.heads; a.d = c.head_dim;
     a.n_q = p.Ni; a.n_kv = p.Nt;
-    a.Q = QKV; a.K = at(ws, p.kc); a.Vt = at(ws, p.vct);
+    a.Q = QKV; a.K = ctx_k; a.Vt = ctx_vt;
     a.q_bs = p.Ni * H; a.q_hs = c.head_dim; a.q_rs = H;
     a.out0 = O; a.out1 = O; a.split = p.Ni; a.ldo = H;
     a.scale = scale;
@@ -497,8 +504,38 @@ int wan_block(const ff_dit& m, const Plan& p, void* ws, int i, const void* ctx, 
   return gemm(g2, s);
 }
 
+int wan_cross_kv(const ff_dit& m, const Plan& p, void* ws, int i, const void* ctx, void* K, void* Vt, hipStream_t s) {
+  const ff_dit_config& c = m.cfg;
+  const int64_t H = c.hidden;
+  const size_t es = dtype_size(c.dtype);
+  const Wan& wb = m.wan[i];
+  const int64_t crow = p.B * p.Nt;
+  char* KV = at(ws, p.kvc);
+  FF_TRY(gemm(gemm_args(c.dtype, crow, 2 * H, H, ctx, H, wb.ckv, KV, 2 * H, EPI_NONE), s));
+  FF_TRY(rms_rows(c, KV, crow, 2 * H, wb.ckn, s));
+  return relayout(c, p, KV, KV, KV + H * es, 2 * H, p.Nt, nullptr, at(ws, p.qd), K, Vt, s);
+}
+
+// Bytes of one block's prepared cross-attention K and V^T, and the text context of a WAN forward:
+// the embedding MLP of the prompts' text and the per-sample gather, into the workspace's xtxt.
+size_t wan_kv_block_bytes(const ff_dit_config& c, int64_t B, int64_t n_txt) {
+  return round_up(static_cast<size_t>(B) * n_txt * c.hidden * dtype_size(c.dtype), 256);
+}
+
+int wan_text_context(const ff_dit& m, const Plan& p, const void* txt, const int32_t* txt_index, void* ws,
+                     hipStream_t s) {
+  const ff_dit_config& c = m.cfg;
+  const int64_t H = c.hidden;
+  char* c1 = at(ws, p.ctx1);
+  char* cp = at(ws, p.ctxp);
+  FF_TRY(gemm(gemm_args(c.dtype, p.P * p.Nt, H, c.txt_dim, txt, c.txt_dim, m.txt1, c1, H, EPI_GELU), s));
+  FF_TRY(gemm(gemm_args(c.dtype, p.P * p.Nt, H, H, c1, H, m.txt2, cp, H, EPI_NONE), s));
+  return gather_rows(c.dtype, cp, txt_index, p.P, at(ws, p.xtxt), p.B, p.Nt, H, s);
+}
+
+// store: the prepared per-block cross-attention K / V^T (then txt is not read), or null.
 int forward_wan(const ff_dit& m, const Plan& p, const void* x, const void* txt, const int32_t* txt_index,
-                const float* t, const int32_t grid[3], void* v_out, void* ws, hipStream_t s) {
+                const float* t, const int32_t grid[3], void* v_out, void* ws, const char* store, hipStream_t s) {
   const ff_dit_config& c = m.cfg;
   const int64_t H = c.hidden;
   float* temb = reinterpret_cast<float*>(at(ws, p.c));
@@ -509,15 +546,15 @@ int forward_wan(const ff_dit& m, const Plan& p, const void* x, const void* txt, 
   FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, H, 256, te, ACT_NONE, m.temb1, tmp), s));
   FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, H, H, tmp, ACT_SILU, m.temb2, temb), s));
   FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 6 * H, H, temb, ACT_SILU, m.temb_proj, reinterpret_cast<float*>(at(ws, p.e6))), s));
-  char* c1 = at(ws, p.ctx1);
-  char* cp = at(ws, p.ctxp);
-  FF_TRY(gemm(gemm_args(c.dtype, p.P * p.Nt, H, c.txt_dim, txt, c.txt_dim, m.txt1, c1, H, EPI_GELU), s));
-  FF_TRY(gemm(gemm_args(c.dtype, p.P * p.Nt, H, H, c1, H, m.txt2, cp, H, EPI_NONE), s));
   char* ctx = at(ws, p.xtxt);
-  FF_TRY(gather_rows(c.dtype, cp, txt_index, p.P, ctx, p.B, p.Nt, H, s));
+  if (!store) FF_TRY(wan_text_context(m, p, txt, txt_index, ws, s));
   char* X = at(ws, p.ximg);
   FF_TRY(gemm(gemm_args(c.dtype, p.B * p.Ni, H, c.in_channels, x, c.in_channels, m.x_in, X, H, EPI_NONE), s));
-  for (int i = 0; i < c.n_wan; ++i) FF_TRY(wan_block(m, p, ws, i, ctx, X, s));
+  const size_t kvb = wan_kv_block_bytes(c, p.B, p.Nt);
+  for (int i = 0; i < c.n_wan; ++i) {
+    const char* k = store ? store + 2 * i * kvb : nullptr;
+    FF_TRY(wan_block(m, p, ws, i, ctx, k, store ? k + kvb : nullptr, X, s));
+  }
   float* mods = reinterpret_cast<float*>(at(ws, p.mods));
   FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 2 * H, H, temb, ACT_SILU, m.final_mod, mods), s));
   char* Y = at(ws, p.y);
@@ -743,8 +780,59 @@ int ff_dit_forward(const ff_dit* m, const void* x, const void* txt, const int32_
     return fail(FF_EWORKSPACE, "ff_dit_forward: workspace of %zu bytes needed, %zu given", p.total, workspace ? ws_bytes : 0);
   if (!aligned16(workspace)) return fail(FF_EINVAL, "ff_dit_forward: workspace must be 16-byte aligned");
   if (c.model == FF_MODEL_WAN)
-    return forward_wan(*m, p, x, txt, txt_index, t, grid, v_out, workspace, static_cast<hipStream_t>(stream));
+    return forward_wan(*m, p, x, txt, txt_index, t, grid, v_out, workspace, nullptr, static_cast<hipStream_t>(stream));
   return forward_mmdit(*m, p, x, txt, txt_index, cond, t, grid, v_out, txt_out, workspace, static_cast<hipStream_t>(stream));
+}
+
+int ff_dit_context_size(const ff_dit* m, int64_t B, int64_t n_txt, size_t* bytes) {
+  if (!m || !bytes) return fail(FF_EINVAL, "ff_dit_context_size: null model or output");
+  if (m->cfg.model != FF_MODEL_WAN) return fail(FF_EUNSUPPORTED, "ff_dit_context_size: WAN models only");
+  if (B < 1 || B > 65535 || n_txt < 1) return fail(FF_EINVAL, "ff_dit_context_size: bad B or n_txt");
+  *bytes = static_cast<size_t>(2 * m->cfg.n_wan) * wan_kv_block_bytes(m->cfg, B, n_txt);
+  return FF_OK;
+}
+
+int ff_dit_prepare_context(const ff_dit* m, const void* txt, const int32_t* txt_index, int64_t n_prompts,
+                           const int32_t grid[3], int64_t B, int64_t n_txt, void* context, size_t context_bytes,
+                           void* workspace, size_t ws_bytes, void* stream) {
+  FF_TRY(check_forward_shape(m, B, grid, n_txt, n_prompts));
+  if (m->cfg.model != FF_MODEL_WAN) return fail(FF_EUNSUPPORTED, "ff_dit_prepare_context: WAN models only");
+  if (!txt || !context) return fail(FF_EINVAL, "ff_dit_prepare_context: null txt or context");
+  if (!aligned16(txt) || !aligned16(context)) return fail(FF_EINVAL, "ff_dit_prepare_context: txt and context must be 16-byte aligned");
+  if (!txt_index && n_prompts != B) return fail(FF_EINVAL, "ff_dit_prepare_context: txt_index NULL needs n_prompts == B");
+  const size_t kvb = wan_kv_block_bytes(m->cfg, B, n_txt);
+  if (context_bytes < 2 * m->cfg.n_wan * kvb)
+    return fail(FF_EWORKSPACE, "ff_dit_prepare_context: context of %zu bytes needed, %zu given", 2 * m->cfg.n_wan * kvb, context_bytes);
+  Plan p = plan(*m, B, grid, n_txt, n_prompts);
+  if (!workspace || ws_bytes < p.total)
+    return fail(FF_EWORKSPACE, "ff_dit_prepare_context: workspace of %zu bytes needed, %zu given", p.total, workspace ? ws_bytes : 0);
+  if (!aligned16(workspace)) return fail(FF_EINVAL, "ff_dit_prepare_context: workspace must be 16-byte aligned");
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  FF_TRY(wan_text_context(*m, p, txt, txt_index, workspace, s));
+  char* store = static_cast<char*>(context);
+  for (int i = 0; i < m->cfg.n_wan; ++i)
+    FF_TRY(wan_cross_kv(*m, p, workspace, i, at(workspace, p.xtxt), store + 2 * i * kvb, store + (2 * i + 1) * kvb, s));
+  return FF_OK;
+}
+
+int ff_dit_forward_ctx(const ff_dit* m, const void* x, const void* context, size_t context_bytes, const float* t,
+                       const int32_t grid[3], int64_t B, int64_t n_txt, void* v_out, void* workspace, size_t ws_bytes,
+                       void* stream) {
+  FF_TRY(check_forward_shape(m, B, grid, n_txt, 1));
+  if (m->cfg.model != FF_MODEL_WAN) return fail(FF_EUNSUPPORTED, "ff_dit_forward_ctx: WAN models only");
+  if (!x || !context || !t || !v_out) return fail(FF_EINVAL, "ff_dit_forward_ctx: null x, context, t or v_out");
+  if (!aligned16(x) || !aligned16(context) || !aligned16(v_out))
+    return fail(FF_EINVAL, "ff_dit_forward_ctx: tensors must be 16-byte aligned");
+  if (v_out == x || v_out == context) return fail(FF_EINVAL, "ff_dit_forward_ctx: v_out may not alias an input");
+  const size_t kvb = wan_kv_block_bytes(m->cfg, B, n_txt);
+  if (context_bytes < 2 * m->cfg.n_wan * kvb)
+    return fail(FF_EWORKSPACE, "ff_dit_forward_ctx: context of %zu bytes needed, %zu given", 2 * m->cfg.n_wan * kvb, context_bytes);
+  Plan p = plan(*m, B, grid, n_txt, 1);   // the prompts' text buffers are not used here
+  if (!workspace || ws_bytes < p.total)
+    return fail(FF_EWORKSPACE, "ff_dit_forward_ctx: workspace of %zu bytes needed, %zu given", p.total, workspace ? ws_bytes : 0);
+  if (!aligned16(workspace)) return fail(FF_EINVAL, "ff_dit_forward_ctx: workspace must be 16-byte aligned");
+  return forward_wan(*m, p, x, nullptr, nullptr, t, grid, v_out, workspace, static_cast<const char*>(context),
+                     static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

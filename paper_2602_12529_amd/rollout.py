@@ -97,10 +97,17 @@ class Rollout:
         B = w.batch
         x = x0
         xs, vs, logp = [x0], [], {}
+        # WAN: the text context is fixed along the trajectory, so its per-block cross-attention K / V
+        # are prepared once and every step's forward reads them.
+        context = None
+        if m.model == C.MODEL_WAN:
+            context = self.dit.prepare_context(txt, w.grid, B, txt_index=txt_index, ws=self.ws_dit)
         for k in range(len(self.ts) - 1):
             t, tn, sigma = self.ts[k], self.ts[k + 1], self.sigmas[k]
             v = torch.empty(self.shape, dtype=self.dt, device=self.device)
-            if m.io_mode == C.IO_LATENT:
+            if context is not None:
+                self.dit.forward_ctx(x, context, w.n_txt, w.grid, v, self.t_steps[k], ws=self.ws_dit)
+            elif m.io_mode == C.IO_LATENT:
                 self.dit.forward(x, txt, w.grid, v, t=self.t_steps[k], cond=cond, txt_index=txt_index,
                                  ws=self.ws_dit)
             else:

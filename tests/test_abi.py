@@ -186,6 +186,14 @@ def test_dit_validation_and_workspace_plan():
     bad = (c_int32 * 3)(1, 63, 63)
     _err(lib.ff_dit_forward(h, f, c_void_p(2 << 20), None, 8, c_void_p(5 << 20), None, bad, 8, 512,
                             c_void_p(3 << 20), None, c_void_p(4 << 20), ws.value, None), _lib.FF_EUNSUPPORTED)
+    # the prepared WAN text context: other models are rejected before any launch
+    cs = c_size_t()
+    _err(lib.ff_dit_context_size(h, 8, 512, byref(cs)), _lib.FF_EUNSUPPORTED)
+    _err(lib.ff_dit_context_size(None, 8, 512, byref(cs)), _lib.FF_EINVAL)
+    _err(lib.ff_dit_prepare_context(h, c_void_p(2 << 20), None, 8, grid, 8, 512, c_void_p(6 << 20), 1 << 30,
+                                    c_void_p(4 << 20), ws.value, None), _lib.FF_EUNSUPPORTED)
+    _err(lib.ff_dit_forward_ctx(h, f, c_void_p(6 << 20), 1 << 30, c_void_p(7 << 20), grid, 8, 512,
+                                c_void_p(3 << 20), c_void_p(4 << 20), ws.value, None), _lib.FF_EUNSUPPORTED)
     assert lib.ff_dit_destroy(h) == 0
     # bad configs
     cfg2 = api.dit_config(m.replace(heads=7))

@@ -404,6 +404,27 @@ def test_wan_rollout_teacher_forced(gpu_lib, dt):
         assert np.max(np.abs(host(res.logp[k]) - lp_ref)) <= LOGP_ABS
 
 
+@pytest.mark.parametrize("dt", [C.F32, C.BF16])
+def test_wan_prepared_context_matches_forward(gpu_lib, dt):
+    """The per-block cross-attention K / V prepared once from the text (ff_dit_prepare_context) give
+    ff_dit_forward_ctx exactly the velocities of ff_dit_forward, with prompts shared by samples."""
+    w = _small_wan(dt)
+    m = w.model
+    W, txt, cond, x0, eps = _inputs(w)
+    Wd, T, Cd, X0, E = _device(w, W, txt, cond, x0, eps)
+    dit = api.Dit(m, Wd)
+    tidx = torch.from_numpy(synth.txt_index(w)).cuda()
+    t = torch.full((w.batch,), 0.75, dtype=torch.float32, device="cuda")
+    v_ref = torch.empty_like(X0)
+    dit.forward(X0, T, w.grid, v_ref, t=t, txt_index=tidx)
+    ctx = dit.prepare_context(T, w.grid, w.batch, txt_index=tidx)
+    assert ctx.numel() == dit.context_size(w.batch, w.n_txt)
+    v = torch.empty_like(X0)
+    dit.forward_ctx(X0, ctx, w.n_txt, w.grid, v, t)
+    torch.cuda.synchronize()
+    assert torch.equal(v, v_ref)
+
+
 @pytest.mark.timeout(900)
 def test_wan_block_full_size_sampled_rows(gpu_lib):
     """One WAN block at full size (B=1, 21x30x52 = 32760 video tokens, 512 text tokens, H=1536, bf16):
