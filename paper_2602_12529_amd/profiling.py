@@ -5,6 +5,9 @@ Subcommands (python -m paper_2602_12529_amd.profiling ...):
   copy --bytes N --reps R
       A plain device-to-device copy of N bytes, R times: the calibration kernel
       whose FETCH_SIZE / WRITE_SIZE counters are compared with the known N.
+  sde-sweep OUT --title T --cmd C [--reps R]
+      The SDE step with log-prob over 1 MB .. 2 GB of traffic, warm and cold (rotating
+      buffer sets beyond the MALL), per-launch HIP events -> markdown table.
   linear --M --N --K --precision bf16|fp8 [--gelu] --reps R
       One linear layer on random device data, R times, timed per launch by the
       library's events (fp8: the activation quantiser and the FP8 GEMM).
@@ -142,6 +145,68 @@ def run_linear(M: int, N: int, K: int, precision: str, gelu: bool, reps: int) ->
     return res
 
 
+def run_sde_sweep(out_md: str, title: str, cmds: List[str], reps: int = 20) -> List[dict]:
+    """The SDE step with log-prob (ff_sde_step, bf16, B = 8) over sizes of 1 MB to 2 GB of algorithmic
+    traffic (x, v, eps read, x' written: 8 bytes per element), each timed per launch with HIP events
+    (median of `reps`): warm, re-running on one buffer set (the 256 MB MALL holds the small ones),
+    and cold, rotating over enough buffer sets to cover at least twice the MALL (at least four)."""
+    import statistics
+
+    import torch
+
+    from . import api
+
+    if not torch.cuda.is_available():
+        raise SystemExit("the SDE size sweep needs a GPU")
+    B, mall = 8, 256 << 20
+    rows = []
+    sizes = [1 << 20, 4 << 20, 16 << 20, 64 << 20, 256 << 20, 805306368, 1 << 30, 2 << 30]
+    g = torch.Generator(device="cuda").manual_seed(0)
+    for total in sizes:
+        D = max(2048, total // (8 * B) // 2048 * 2048)
+        nbytes = 8 * B * D
+        sets = max(4, -(-2 * mall // nbytes))
+        bufs = []
+        for _ in range(sets):
+            x = torch.randn((B, D), device="cuda", generator=g).to(torch.bfloat16)
+            v = torch.randn((B, D), device="cuda", generator=g).to(torch.bfloat16)
+            e = torch.randn((B, D), device="cuda", generator=g).to(torch.bfloat16)
+            bufs.append((x, v, e, torch.empty_like(x), torch.empty(B, dtype=torch.float64, device="cuda")))
+        ws = api.workspace(api.sde_workspace_size(B, D))
+        res = {"bytes": nbytes, "elements_per_sample": D, "cold_sets": sets}
+        for mode in ("warm", "cold"):
+            times = []
+            for i in range(reps + 3):
+                x, v, e, xn, lp = bufs[0] if mode == "warm" else bufs[i % sets]
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                api.sde_step(x, v, e, xn, 0.6, 0.5, 0.9, logp=lp, ws=ws)
+                e1.record()
+                e1.synchronize()
+                if i >= 3:
+                    times.append(e0.elapsed_time(e1) * 1e-3)
+            med = statistics.median(times)
+            res[mode + "_us"] = med * 1e6
+            res[mode + "_tbs"] = nbytes / med / 1e12
+        rows.append(res)
+        print(json.dumps(res), flush=True)
+        del bufs
+        torch.cuda.empty_cache()
+    out = _header(title, cmds)
+    out += ["ff_sde_step with its log-prob, bf16, B = 8; median of %d launches, each bracketed by HIP events "
+            "on the launch stream. Warm: one buffer set re-run; cold: rotating over the stated number of "
+            "sets (together at least twice the 256 MB MALL). Peak HBM 8 TB/s." % reps, "",
+            "| bytes per launch | elements per sample | warm µs | warm TB/s | cold sets | cold µs | cold TB/s | cold / 8 TB/s |",
+            "|---|---|---|---|---|---|---|---|"]
+    for r in rows:
+        out.append(f"| {r['bytes'] / 1e6:.1f} MB | {r['elements_per_sample']} | {r['warm_us']:.1f} | "
+                   f"{r['warm_tbs']:.2f} | {r['cold_sets']} | {r['cold_us']:.1f} | {r['cold_tbs']:.2f} | "
+                   f"{r['cold_tbs'] / 8.0:.2f} |")
+    with open(out_md, "w") as f:
+        f.write("\n".join(out) + "\n")
+    return rows
+
+
 # ---------------------------------------------------------------------------- summaries
 def _header(title: str, cmds: List[str]) -> List[str]:
     out = [f"# {title}", "", "Commands (run from the repository root on one MI355X):", "", "```"]
@@ -257,6 +322,11 @@ def main(argv=None) -> int:
     li.add_argument("--precision", choices=["bf16", "fp8"], default="fp8")
     li.add_argument("--gelu", action="store_true")
     li.add_argument("--reps", type=int, default=20)
+    sw = sub.add_parser("sde-sweep")
+    sw.add_argument("out")
+    sw.add_argument("--title", required=True)
+    sw.add_argument("--cmd", action="append", required=True)
+    sw.add_argument("--reps", type=int, default=20)
     s = sub.add_parser("stats")
     s.add_argument("csv")
     s.add_argument("out")
@@ -275,6 +345,8 @@ def main(argv=None) -> int:
         run_copy(a.bytes, a.reps)
     elif a.action == "linear":
         run_linear(a.M, a.N, a.K, a.precision, a.gelu, a.reps)
+    elif a.action == "sde-sweep":
+        run_sde_sweep(a.out, a.title, a.cmd, a.reps)
     elif a.action == "stats":
         stats_md(a.csv, a.out, a.title, a.cmd)
     else:
