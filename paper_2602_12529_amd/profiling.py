@@ -13,6 +13,8 @@ Subcommands (python -m paper_2602_12529_amd.profiling ...):
       library's events (fp8: the activation quantiser and the FP8 GEMM).
   stats CSV OUT --title T --cmd C
       kernel_stats.csv of `rocprofv3 --kernel-trace --stats` -> markdown table.
+  counter CSV OUT --counter NAME --title T --cmd C [--note N]
+      one counter of a `rocprofv3 --pmc` run (e.g. the derived MfmaUtil) per kernel.
   traffic --fetch CSV --write CSV --copy-fetch CSV --copy-write CSV --copy-bytes N
           --key NAME=PATTERN OUT --title T --cmd C [--cmd C ...]
       counter_collection.csv files of four `rocprofv3 --pmc` runs (FETCH_SIZE,
@@ -289,6 +291,19 @@ def traffic_md(fetch_csv: str, write_csv: str, copy_fetch_csv: str, copy_write_c
     return {"records": records}
 
 
+def counter_md(csv_path: str, counter: str, out_md: str, title: str, cmds: List[str], note: str = "") -> None:
+    """One counter of a rocprofv3 --pmc run, per kernel: dispatches, mean, min and max."""
+    vals = _counter_per_kernel(csv_path, counter)
+    out = _header(title, cmds)
+    if note:
+        out += [note, ""]
+    out += [f"| kernel | dispatches | mean {counter} | min | max |", "|---|---|---|---|---|"]
+    for name, v in sorted(vals.items(), key=lambda kv: -len(kv[1]) * sum(kv[1]) / max(len(kv[1]), 1)):
+        out.append(f"| `{short_name(name)}` | {len(v)} | {sum(v) / len(v):.1f} | {min(v):.1f} | {max(v):.1f} |")
+    with open(out_md, "w") as f:
+        f.write("\n".join(out) + "\n")
+
+
 def lookup_traffic(kernel: str) -> Optional[dict]:
     """The committed traffic record of `kernel` whose sources still hash the same, else None."""
     if not os.path.isdir(PROFILES):
@@ -327,6 +342,13 @@ def main(argv=None) -> int:
     sw.add_argument("--title", required=True)
     sw.add_argument("--cmd", action="append", required=True)
     sw.add_argument("--reps", type=int, default=20)
+    cn = sub.add_parser("counter")
+    cn.add_argument("csv")
+    cn.add_argument("out")
+    cn.add_argument("--counter", required=True)
+    cn.add_argument("--title", required=True)
+    cn.add_argument("--cmd", action="append", required=True)
+    cn.add_argument("--note", default="")
     s = sub.add_parser("stats")
     s.add_argument("csv")
     s.add_argument("out")
@@ -347,6 +369,8 @@ def main(argv=None) -> int:
         run_linear(a.M, a.N, a.K, a.precision, a.gelu, a.reps)
     elif a.action == "sde-sweep":
         run_sde_sweep(a.out, a.title, a.cmd, a.reps)
+    elif a.action == "counter":
+        counter_md(a.csv, a.counter, a.out, a.title, a.cmd, a.note)
     elif a.action == "stats":
         stats_md(a.csv, a.out, a.title, a.cmd)
     else:
