@@ -70,3 +70,14 @@ def test_committed_traffic_summary_parses():
     assert {"gemm_bf16_gated", "sde_step", "attn_bf16_d128"} <= names
     for r in recs:
         assert r["traffic_bytes_per_launch"] > 0 and len(r["sources_sha256"]) == 64
+
+
+def test_counter_summary_per_kernel(tmp_path):
+    k = "void ff::(anonymous namespace)::attn_bf16_d128<8, 4>(ff::(anonymous namespace)::AttnParams)"
+    _write_counters(tmp_path / "m.csv", [(k, "MfmaUtil", 40.0), (k, "MfmaUtil", 50.0), ("copy", "MfmaUtil", 0.0),
+                                         (k, "GRBM_GUI_ACTIVE", 9.0)])
+    out = tmp_path / "m.md"
+    P.counter_md(str(tmp_path / "m.csv"), "MfmaUtil", str(out), "title", ["cmd"], note="a note")
+    text = out.read_text()
+    assert "| `attn_bf16_d128<8, 4>` | 2 | 45.0 | 40.0 | 50.0 |" in text
+    assert "| `copy` | 1 | 0.0 | 0.0 | 0.0 |" in text and "a note" in text and "GRBM" not in text
