@@ -291,15 +291,22 @@ def traffic_md(fetch_csv: str, write_csv: str, copy_fetch_csv: str, copy_write_c
     return {"records": records}
 
 
-def counter_md(csv_path: str, counter: str, out_md: str, title: str, cmds: List[str], note: str = "") -> None:
-    """One counter of a rocprofv3 --pmc run, per kernel: dispatches, mean, min and max."""
-    vals = _counter_per_kernel(csv_path, counter)
+def counter_md(csv_path: str, counters: List[str], out_md: str, title: str, cmds: List[str], note: str = "") -> None:
+    """Counters of a rocprofv3 --pmc run (e.g. the derived MfmaUtil), per kernel: dispatches and, per
+    counter, the mean over dispatches (the first counter also min and max)."""
+    vals = {c: _counter_per_kernel(csv_path, c) for c in counters}
+    first = vals[counters[0]]
     out = _header(title, cmds)
     if note:
         out += [note, ""]
-    out += [f"| kernel | dispatches | mean {counter} | min | max |", "|---|---|---|---|---|"]
-    for name, v in sorted(vals.items(), key=lambda kv: -len(kv[1]) * sum(kv[1]) / max(len(kv[1]), 1)):
-        out.append(f"| `{short_name(name)}` | {len(v)} | {sum(v) / len(v):.1f} | {min(v):.1f} | {max(v):.1f} |")
+    head = ["kernel", "dispatches", f"mean {counters[0]}", "min", "max"] + [f"mean {c}" for c in counters[1:]]
+    out += ["| " + " | ".join(head) + " |", "|" + "---|" * len(head)]
+    for name, v in sorted(first.items(), key=lambda kv: -sum(kv[1]) / max(len(kv[1]), 1)):
+        cells = [f"`{short_name(name)}`", str(len(v)), f"{sum(v) / len(v):.1f}", f"{min(v):.1f}", f"{max(v):.1f}"]
+        for c in counters[1:]:
+            w = vals[c].get(name, [])
+            cells.append(f"{sum(w) / len(w):.1f}" if w else "")
+        out.append("| " + " | ".join(cells) + " |")
     with open(out_md, "w") as f:
         f.write("\n".join(out) + "\n")
 
@@ -345,7 +352,7 @@ def main(argv=None) -> int:
     cn = sub.add_parser("counter")
     cn.add_argument("csv")
     cn.add_argument("out")
-    cn.add_argument("--counter", required=True)
+    cn.add_argument("--counter", action="append", required=True)
     cn.add_argument("--title", required=True)
     cn.add_argument("--cmd", action="append", required=True)
     cn.add_argument("--note", default="")

@@ -77,7 +77,9 @@ def test_counter_summary_per_kernel(tmp_path):
     _write_counters(tmp_path / "m.csv", [(k, "MfmaUtil", 40.0), (k, "MfmaUtil", 50.0), ("copy", "MfmaUtil", 0.0),
                                          (k, "GRBM_GUI_ACTIVE", 9.0)])
     out = tmp_path / "m.md"
-    P.counter_md(str(tmp_path / "m.csv"), "MfmaUtil", str(out), "title", ["cmd"], note="a note")
+    P.counter_md(str(tmp_path / "m.csv"), ["MfmaUtil"], str(out), "title", ["cmd"], note="a note")
     text = out.read_text()
     assert "| `attn_bf16_d128<8, 4>` | 2 | 45.0 | 40.0 | 50.0 |" in text
     assert "| `copy` | 1 | 0.0 | 0.0 | 0.0 |" in text and "a note" in text and "GRBM" not in text
+    P.counter_md(str(tmp_path / "m.csv"), ["MfmaUtil", "GRBM_GUI_ACTIVE"], str(out), "title", ["cmd"])
+    assert "| `attn_bf16_d128<8, 4>` | 2 | 45.0 | 40.0 | 50.0 | 9.0 |" in out.read_text()
