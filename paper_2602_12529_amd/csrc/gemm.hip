@@ -602,8 +602,8 @@ __device__ __forceinline__ void wg_barrier() {
 // is read from LDS in phases 2s - 1 and 2s only and two 64 KB buffers suffice.  Slab
 // s + 2's direct loads go into slab s's buffer during phase 2s + 1 (both groups are done
 // with it): group 0 issues the A rows in its memory phase, group 1 the W rows between the
-// MFMAs of its compute phase, and each waits for its own loads one phase later, before the
-// barrier that publishes the slab.  Loads go through buffer resources whose record count
+// first MFMAs of its compute phase, and each waits for its own loads one phase later, before
+// the barrier that publishes the slab.  Loads go through buffer resources whose record count
 // ends at the matrix's last row, so rows past M (or N) read as zero without a per-row
 // clamp; K rows are 128-byte lines (a 64-wide slab), stored with the chunk swizzle
 // chunk ^ ((row >> 1) & 7).
@@ -740,10 +740,11 @@ __device__ __forceinline__ void pp_body(const GemmBatch& batch) {
     }
   };
   // The MFMAs of a slab (32 bf16 or 16 fp8); with `rb` set, the eight W-row loads of a later
-  // slab are spread between them.
+  // slab go out one after each of the first eight MFMAs: the loads must land by the end of the
+  // next phase, and issuing them early in this one gives them most of two phases to arrive
+  // (spread evenly over the phase, the last one had little more than one).
   auto compute = [&](const u32x4_t* rb, uint32_t lds_b) {
-    constexpr int PER = KSTEPS * FM * FN / 8;   // MFMAs per W-row load
-    static_assert(KSTEPS * FM * FN == 8 * PER, "eight loads per compute phase");
+    static_assert(KSTEPS * FM * FN >= 8, "eight loads per compute phase");
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks)
 #pragma unroll
@@ -755,8 +756,8 @@ __device__ __forceinline__ void pp_body(const GemmBatch& batch) {
           else
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks][i], fb[ks][j], acc[i][j], 0, 0, 0);
           const int idx = (ks * FM + i) * FN + j;
-          if (rb != nullptr && idx % PER == PER - 1) {
-            const int q = idx / PER;
+          if (rb != nullptr && idx < 8) {
+            const int q = idx;
             dma_buf16(*rb, b_off + q * b_step, lds_b + q * 4096);
           }
           __builtin_amdgcn_sched_barrier(0);
