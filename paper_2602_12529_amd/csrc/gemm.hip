@@ -633,6 +633,23 @@ __device__ __forceinline__ void dma_buf16(const u32x4_t& rsrc, uint32_t voff, ui
 }
 #pragma clang diagnostic pop
 
+// For outputs whose tile columns come in whole sixteens: within each group of 16 tile rows, runs
+// of 256 launch slots cover a 16 x 16 block of tiles, and the 32 slots of one XCD (consecutive
+// slots go to consecutive XCDs) a 4 x 8 part of it, so the tiles an XCD runs at once share 4 A and
+// 8 W panels in its L2 instead of 2 and 16.  Measured 2% faster than the plain walk on the
+// 12288-wide MLP-up output and 2% slower on 3072- and 9216-wide ones, which keep the plain walk.
+__device__ __forceinline__ void xcd_block_order(int64_t lid, int64_t num_m, int64_t num_n, int64_t& tm, int64_t& tn) {
+  const int64_t in_group = 16 * num_n;
+  const int64_t first_m = lid / in_group * 16;
+  if (num_m - first_m < 16) {
+    group_order<16>(lid, num_m, num_n, tm, tn);
+    return;
+  }
+  const int64_t r = lid % in_group, st = r >> 8, q = r & 255, x = q & 7, j = q >> 3;
+  tm = first_m + 4 * (x & 3) + (j & 3);
+  tn = 16 * st + 8 * (x >> 2) + (j >> 2);
+}
+
 // LAYOUT 0: each wave a 128 x 64 block (wm = w4 / 2, wn = 2 grp + w4 % 2); LAYOUT 1: a 64 x 128
 // block (wm = w4, wn = grp), one whole 128-column head, for the fused QKV epilogue.  The two
 // waves of a SIMD (same w4) always share their A rows.  F8: operands are E4M3 codes; a slab is
@@ -653,13 +670,16 @@ __device__ __forceinline__ void pp_body(const GemmBatch& batch) {
 
   // Plain launch order (consecutive tiles on different XCDs) walking 16 tile rows at a time:
   // measured faster than giving each XCD a contiguous range, or 4, 8 or 32 rows, on the DiT's
-  // shapes.
+  // shapes; XCD blocks where the tile columns come in sixteens.
   const int64_t lid = blockIdx.x;
   const int which = lid >= batch.tiles0 ? 1 : 0;
   const GemmParams& p = batch.p[which];
   const int64_t num_m = (p.M + BM - 1) / BM, num_n = (p.N + BN - 1) / BN;
   int64_t tm, tn;
-  group_order<16>(lid - (which ? batch.tiles0 : 0), num_m, num_n, tm, tn);
+  if (num_n % 16 == 0)
+    xcd_block_order(lid - (which ? batch.tiles0 : 0), num_m, num_n, tm, tn);
+  else
+    group_order<16>(lid - (which ? batch.tiles0 : 0), num_m, num_n, tm, tn);
   const int64_t m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);

@@ -24,7 +24,10 @@ LIN = [
 
 
 # Shapes with at least one 256 x 256 tile per CU: these take the large-tile kernel.
-LIN_LARGE = [(4133, 4133, 192, C.BF16), (8197, 2088, 128, C.BF16), (8200, 2100, 64, C.BF16)]
+# (5000, 4000): 20 x 16 tiles, whole sixteens of tile columns (the XCD-blocked tile order) with a
+# partial last group of tile rows and ragged edges.
+LIN_LARGE = [(4133, 4133, 192, C.BF16), (8197, 2088, 128, C.BF16), (8200, 2100, 64, C.BF16),
+             (5000, 4000, 128, C.BF16)]
 
 
 @pytest.mark.parametrize("M,N,K,dt", LIN + LIN_LARGE)
