@@ -226,11 +226,18 @@ def single_block(x, c, W, j: int, cfg, n_txt: int, img_angles):
     return x + g[:, None, :] * linear(np.concatenate([o, u], axis=-1), W, p + "lin2")
 
 
-def wan_block(x, ctx, e6, W, i: int, cfg, angles):
-    """One WAN block.  x [B, N, H]; ctx [B, N_txt, H]; e6 [B, 6, H] time modulation."""
+def wan_block(x, ctx, e6, W, i: int, cfg, angles, rows=None):
+    """One WAN block.  x [B, N, H]; ctx [B, N_txt, H]; e6 [B, 6, H] time modulation.
+
+    With ``rows`` (token indices) the keys and values of the self-attention are still taken
+    over all N tokens, but only the listed query rows are carried through the block: the
+    result is x_out[:, rows], the same values as those rows of the whole block (every other
+    step is row-local), at a fraction of the cost on long sequences.
+    """
     h, eps = cfg.heads, cfg.norm_eps
     x = f64(x)
     p = f"wan.{i}."
+    sel = slice(None) if rows is None else np.asarray(rows, dtype=np.int64)
     mod = f64(W[p + "mod"])[None, :, :] + f64(e6)
     sh1, sc1, g1, sh2, sc2, g2 = (mod[:, n, :] for n in range(6))
     y = modulate(layer_norm(x, eps), sh1, sc1)
@@ -239,10 +246,10 @@ def wan_block(x, ctx, e6, W, i: int, cfg, angles):
     q = rms_norm(qkv[..., :H], eps) * f64(W[p + "sa.q_norm.w"])
     k = rms_norm(qkv[..., H:2 * H], eps) * f64(W[p + "sa.k_norm.w"])
     v = qkv[..., 2 * H:]
-    q = apply_rope(split_heads(q, h), angles)
+    q = apply_rope(split_heads(q, h), angles)[:, :, sel]
     k = apply_rope(split_heads(k, h), angles)
     o = merge_heads(attention(q, k, split_heads(v, h)))
-    x = x + g1[:, None, :] * linear(o, W, p + "sa.o")
+    x = x[:, sel] + g1[:, None, :] * linear(o, W, p + "sa.o")
     y = layer_norm(x, eps) * f64(W[p + "ca.norm.w"]) + f64(W[p + "ca.norm.b"])
     q = rms_norm(linear(y, W, p + "ca.q"), eps) * f64(W[p + "ca.q_norm.w"])
     kv = linear(ctx, W, p + "ca.kv")
@@ -261,7 +268,7 @@ def final_layer(x_img, c, W, cfg):
     return linear(modulate(norm(f64(x_img), cfg.norm_kind, cfg.norm_eps), sh, sc), W, "final.proj")
 
 
-def forward(cfg, W, x, txt, t=None, cond=None, txt_index=None, grid=(1, 1, 1)):
+def forward(cfg, W, x, txt, t=None, cond=None, txt_index=None, grid=(1, 1, 1), rows=None):
     """v_theta for a batch.
 
     LATENT mode: x [B, N_img, C] latents, txt [P, N_txt, d_txt] prompt embeddings,
@@ -270,6 +277,9 @@ def forward(cfg, W, x, txt, t=None, cond=None, txt_index=None, grid=(1, 1, 1)):
 
     HIDDEN mode (block stack only): x [B, N_img, H] image hidden, txt [B, N_txt, H]
     text hidden, cond [B, H] conditioning vector.  Returns (img_out, txt_out).
+
+    ``rows`` (WAN with one block only): the velocity of the listed latent tokens,
+    v[:, rows], computed with the block's sampled-row form.
     """
     x = f64(x)
     angles = rope_angles(grid_positions(grid), cfg.rope_axes, cfg.rope_theta)
@@ -280,6 +290,8 @@ def forward(cfg, W, x, txt, t=None, cond=None, txt_index=None, grid=(1, 1, 1)):
     txt_index = np.asarray(txt_index, dtype=np.int64)
 
     if cfg.model == MODEL_MMDIT:
+        if rows is not None:
+            raise ValueError("sampled rows are implemented for the one-block WAN model only")
         if latent:
             c = mlp2(timestep_sinusoid(t), W, "temb.fc1", "temb.fc2", silu)
             if cfg.pooled_dim:
@@ -308,6 +320,10 @@ def forward(cfg, W, x, txt, t=None, cond=None, txt_index=None, grid=(1, 1, 1)):
         e6 = linear(silu(temb), W, "temb.proj").reshape(B, 6, -1)
         ctx = mlp2(txt, W, "txt_in.fc1", "txt_in.fc2", gelu_tanh)[txt_index]
         xh = linear(x, W, "x_in")
+        if rows is not None:
+            if cfg.n_wan != 1:
+                raise ValueError("sampled rows need a one-block WAN model")
+            return final_layer(wan_block(xh, ctx, e6, W, 0, cfg, angles, rows=rows), temb, W, cfg)
         for i in range(cfg.n_wan):
             xh = wan_block(xh, ctx, e6, W, i, cfg, angles)
         return final_layer(xh, temb, W, cfg)
