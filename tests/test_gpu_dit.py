@@ -22,7 +22,7 @@ from paper_2602_12529_amd import configs as C
 from paper_2602_12529_amd import rollout as R
 from paper_2602_12529_amd import synth
 
-from gpu_util import LOGP_ABS, TOL, dev, host, rel, say
+from gpu_util import LOGP_ABS, TOL, check, dev, host, model_stages, rel, say
 
 pytestmark = pytest.mark.gpu
 
@@ -60,9 +60,8 @@ def test_tiny_rollout_end_to_end(gpu_lib):
     assert res.ts == pytest.approx(list(ref["ts"]), abs=0)
     assert res.sigmas == pytest.approx(list(ref["sigmas"]), rel=1e-15)
     for k in range(w.steps):
-        say("step", k, rel(host(res.vs[k]), ref["vs"][k]), rel(host(res.xs[k + 1]), ref["xs"][k + 1]))
-        assert rel(host(res.vs[k]), ref["vs"][k]) <= TOL[C.F32]
-        assert rel(host(res.xs[k + 1]), ref["xs"][k + 1]) <= TOL[C.F32]
+        check(host(res.vs[k]), ref["vs"][k], C.F32, what=f"tiny v step {k}")
+        check(host(res.xs[k + 1]), ref["xs"][k + 1], C.F32, what=f"tiny x step {k}")
         assert np.max(np.abs(host(res.logp[k]) - ref["logp"][k])) <= LOGP_ABS
         # the GRPO ratio of the rollout policy to itself is exactly 1
         lp2 = torch.empty_like(res.logp[k])
@@ -91,7 +90,7 @@ def test_tiny_rollout_dance_sde_and_mixgrpo(gpu_lib):
     assert res.sigmas == [0.0, w.eta, 0.0, w.eta]
     assert sorted(res.logp) == sorted(ref["logp"]) == [1, 3]
     for k in range(w.steps):
-        assert rel(host(res.xs[k + 1]), ref["xs"][k + 1]) <= TOL[C.F32]
+        check(host(res.xs[k + 1]), ref["xs"][k + 1], C.F32, what=f"tiny dance/mix x step {k}")
     for k in (1, 3):
         assert np.max(np.abs(host(res.logp[k]) - ref["logp"][k])) <= LOGP_ABS
 
@@ -117,9 +116,8 @@ def test_bf16_hidden_blocks(gpu_lib, n_dual, n_single):
     dit.forward(X0, T, w.grid, v, cond=Cd, txt_out=tout)
     torch.cuda.synchronize()
     img, tx = odit.forward(m, W, x0, txt, cond=cond, grid=w.grid)
-    say("  rel img", rel(host(v), img), "txt", rel(host(tout), tx))
-    assert rel(host(v), img) <= TOL[C.BF16]
-    assert rel(host(tout), tx) <= TOL[C.BF16]
+    check(host(v), img, C.BF16, model_stages(m), what=f"hidden blocks {n_dual}+{n_single} img")
+    check(host(tout), tx, C.BF16, model_stages(m), what=f"hidden blocks {n_dual}+{n_single} txt")
     # the blocks did act on the streams
     assert rel(img, x0) > 1e-3
 
@@ -141,10 +139,9 @@ def test_bf16_latent_with_single_blocks_and_pooled(gpu_lib):
         xk = host(res.xs[k])
         v_ref = odit.forward(m, W, xk, txt, t=np.full(w.batch, res.ts[k]), cond=cond, txt_index=synth.txt_index(w),
                              grid=w.grid)
-        say("step", k, rel(host(res.vs[k]), v_ref))
-        assert rel(host(res.vs[k]), v_ref) <= TOL[C.BF16]
+        check(host(res.vs[k]), v_ref, C.BF16, model_stages(m), what=f"small latent v step {k}")
         xn_ref = osde.sde_step(xk, host(res.vs[k]), eps[k], res.ts[k], res.ts[k + 1], res.sigmas[k])
-        assert rel(host(res.xs[k + 1]), xn_ref) <= TOL[C.BF16]
+        check(host(res.xs[k + 1]), xn_ref, C.BF16, 0, what=f"small latent x step {k}")
         lp_ref = osde.step_log_prob(xk, host(res.vs[k]), host(res.xs[k + 1]), res.ts[k], res.ts[k + 1], res.sigmas[k])
         assert np.max(np.abs(host(res.logp[k]) - lp_ref)) <= LOGP_ABS
 
@@ -196,8 +193,7 @@ def test_grpo_policy_update_forward(gpu_lib):
         xk, xk1 = host(res.xs[k]), host(res.xs[k + 1])
         v_ref = odit.forward(m, W2, xk, txt, t=np.full(w.batch, res.ts[k]), cond=cond,
                              txt_index=synth.txt_index(w), grid=w.grid)
-        say("step", k, "rel v", rel(host(v), v_ref))
-        assert rel(host(v), v_ref) <= TOL[C.BF16]
+        check(host(v), v_ref, C.BF16, model_stages(m), what=f"grpo recompute v step {k}")
         lp_ref = osde.step_log_prob(xk, host(v), xk1, res.ts[k], res.ts[k + 1], res.sigmas[k])
         assert np.max(np.abs(lp_new[i] - lp_ref)) <= LOGP_ABS
     old = np.stack([host(res.logp[k]) for k in ro2.sde_step_ids()])
@@ -229,11 +225,10 @@ def test_awm_training_forward(gpu_lib):
     per2, loss2 = gpu_lib.awm_loss(v, Ed, X0, Ad)
     torch.cuda.synchronize()
     assert torch.equal(per, per2) and torch.equal(loss, loss2)
-    assert rel(host(xt), olosses.flow_noise(x0, e, t.astype(np.float64))) <= TOL[C.BF16]
+    check(host(xt), olosses.flow_noise(x0, e, t.astype(np.float64)), C.BF16, 0, what="awm noised x_t")
     v_ref = odit.forward(m, W, host(xt), txt, t=t.astype(np.float64), cond=cond, txt_index=synth.txt_index(w),
                          grid=w.grid)
-    say("awm v rel", rel(host(v), v_ref))
-    assert rel(host(v), v_ref) <= TOL[C.BF16]
+    check(host(v), v_ref, C.BF16, model_stages(m), what="awm v")
     ref_per, ref_loss = olosses.awm_loss(host(v), e, x0, adv)
     np.testing.assert_allclose(host(per), ref_per, rtol=1e-5, atol=1e-9)
     assert host(loss)[0] == pytest.approx(ref_loss, rel=1e-5)
@@ -261,11 +256,9 @@ def test_flux_dual_block_full_size(gpu_lib):
     for b in (0, 5):
         say("oracle sample", b)
         img, _ = odit.forward(m, W, x0[b:b + 1], txt[b:b + 1], cond=cond[b:b + 1], grid=w.grid)
-        e_v = rel(v[b:b + 1], img)
-        say("  rel v", e_v)
-        assert e_v <= TOL[C.BF16]
+        check(v[b:b + 1], img, C.BF16, model_stages(m), what=f"flux block v sample {b}")
         xr = osde.sde_step(x0[b:b + 1], v[b:b + 1], eps[0][b:b + 1], t, tn, sigma)
-        assert rel(xn[b:b + 1], xr) <= TOL[C.BF16]
+        check(xn[b:b + 1], xr, C.BF16, 0, what=f"flux block x' sample {b}")
         lr = osde.step_log_prob(x0[b:b + 1], v[b:b + 1], xn[b:b + 1], t, tn, sigma)
         assert abs(lp[b] - lr[0]) <= LOGP_ABS
 
@@ -302,9 +295,7 @@ def test_dual_block_full_size_other_shapes(gpu_lib, shape):
     for b in (0, w.batch - 1):
         say("oracle sample", b)
         img, _ = odit.forward(m, W, x0[b:b + 1], txt[b:b + 1], cond=cond[b:b + 1], grid=w.grid)
-        e_v = rel(v[b:b + 1], img)
-        say("  rel v", e_v)
-        assert e_v <= TOL[C.BF16]
+        check(v[b:b + 1], img, C.BF16, model_stages(m), what=f"{w.name} v sample {b}")
 
 
 @pytest.mark.parametrize("n_dual,n_single,kernel", [(1, 0, "gemm_bf16_qkv"), (0, 1, "gemm_bf16_qkv_gelu")])
@@ -339,9 +330,7 @@ def test_fused_qkv_epilogue_ragged_streams(gpu_lib, n_dual, n_single, kernel):
     for b in (0, 3):
         say("oracle sample", b)
         img, _ = odit.forward(m, W, x0[b:b + 1], txt[b:b + 1], cond=cond[b:b + 1], grid=w.grid)
-        e_v = rel(v[b:b + 1], img)
-        say("  rel v", e_v)
-        assert e_v <= TOL[C.BF16]
+        check(v[b:b + 1], img, C.BF16, model_stages(m), what=f"{w.name} v sample {b}")
 
 
 @pytest.mark.timeout(900)
@@ -365,9 +354,7 @@ def test_flux_single_block_full_width(gpu_lib):
     for b in (0, 3):
         say("oracle sample", b)
         img, _ = odit.forward(m, W, x0[b:b + 1], txt[b:b + 1], cond=cond[b:b + 1], grid=w.grid)
-        e_v = rel(v[b:b + 1], img)
-        say("  rel v", e_v)
-        assert e_v <= TOL[C.BF16]
+        check(v[b:b + 1], img, C.BF16, model_stages(m), what=f"{w.name} v sample {b}")
 
 
 def _small_wan(dtype):
@@ -398,8 +385,7 @@ def test_wan_rollout_teacher_forced(gpu_lib, dt):
     for k in range(w.steps):
         xk = host(res.xs[k])
         v_ref = odit.forward(m, W, xk, txt, t=np.full(w.batch, res.ts[k]), txt_index=synth.txt_index(w), grid=w.grid)
-        say("wan step", k, rel(host(res.vs[k]), v_ref))
-        assert rel(host(res.vs[k]), v_ref) <= TOL[dt]
+        check(host(res.vs[k]), v_ref, dt, model_stages(m), what=f"{w.name} v step {k}")
         lp_ref = osde.step_log_prob(xk, host(res.vs[k]), host(res.xs[k + 1]), res.ts[k], res.ts[k + 1], res.sigmas[k])
         assert np.max(np.abs(host(res.logp[k]) - lp_ref)) <= LOGP_ABS
 
@@ -426,53 +412,68 @@ def test_wan_prepared_context_matches_forward(gpu_lib, dt):
 
 
 @pytest.mark.timeout(900)
-def test_wan_block_full_size_sampled_rows(gpu_lib):
-    """One WAN block at full size (B=1, 21x30x52 = 32760 video tokens, 512 text tokens, H=1536, bf16):
-    the oracle recomputes K/V for all tokens and everything else for 48 sampled query tokens."""
+@pytest.mark.parametrize("path", ["forward", "forward_ctx"])
+def test_wan_block_full_size_sampled_rows(gpu_lib, path):
+    """One WAN block at full size (B=1, 21x30x52 = 32760 video tokens, 512 text tokens, H=1536, bf16),
+    through ff_dit_forward or through the path the WAN rollout takes (the text context's cross K / V
+    prepared once by ff_dit_prepare_context, then ff_dit_forward_ctx); the oracle's sampled-row forward
+    recomputes keys and values for all tokens and everything else for 48 query tokens."""
     base = C.WAN_STACK
     m = base.model.replace(n_wan=1)
     w = C.Workload(**{**base.__dict__, "model": m, "steps": 1})
-    say("full wan block: generating inputs")
+    say("full wan block", path, ": generating inputs")
     W, txt, cond, x0, eps = _inputs(w)
     Wd, T, Cd, X0, E = _device(w, W, txt, cond, x0, eps)
     dit = api.Dit(m, Wd)
     v = torch.empty_like(X0)
     t = torch.full((1,), 0.6, dtype=torch.float32, device="cuda")
     tidx = torch.zeros(1, dtype=torch.int32, device="cuda")
-    dit.forward(X0, T, w.grid, v, t=t, txt_index=tidx)
+    if path == "forward":
+        dit.forward(X0, T, w.grid, v, t=t, txt_index=tidx)
+    else:
+        ctx = dit.prepare_context(T, w.grid, 1, txt_index=tidx)
+        dit.forward_ctx(X0, ctx, w.n_txt, w.grid, v, t)
     torch.cuda.synchronize()
-    vg = host(v)[0]
-    # oracle, sampled rows
-    f = odit.f64
-    eps_n, H, h = m.norm_eps, m.hidden, m.heads
     rows = np.linspace(0, w.n_img - 1, 48).astype(int)
-    temb = odit.mlp2(odit.timestep_sinusoid(np.array([0.6])), W, "temb.fc1", "temb.fc2", odit.silu)
-    e6 = odit.linear(odit.silu(temb), W, "temb.proj").reshape(1, 6, H)
-    ctx = odit.mlp2(txt, W, "txt_in.fc1", "txt_in.fc2", odit.gelu_tanh)[0]
-    xh = odit.linear(x0[0], W, "x_in")
-    mod = f(W["wan.0.mod"]) + e6[0]
-    sh1, sc1, g1, sh2, sc2, g2 = (mod[n] for n in range(6))
-    y = odit.layer_norm(xh, eps_n) * (1 + sc1) + sh1
-    qkv = odit.linear(y, W, "wan.0.sa.qkv")
-    ang = odit.rope_angles(odit.grid_positions(w.grid), m.rope_axes, m.rope_theta)
-    k = odit.rms_norm(qkv[:, H:2 * H], eps_n) * f(W["wan.0.sa.k_norm.w"])
-    vv = qkv[:, 2 * H:]
-    k = odit.apply_rope(k.reshape(-1, h, 128).transpose(1, 0, 2), ang)
-    q = odit.rms_norm(qkv[rows, :H], eps_n) * f(W["wan.0.sa.q_norm.w"])
-    q = odit.apply_rope(q.reshape(-1, h, 128).transpose(1, 0, 2), ang[rows])
-    o = odit.attention(q, k, vv.reshape(-1, h, 128).transpose(1, 0, 2)).transpose(1, 0, 2).reshape(len(rows), H)
-    xr = xh[rows] + g1 * odit.linear(o, W, "wan.0.sa.o")
-    yc = odit.layer_norm(xr, eps_n) * f(W["wan.0.ca.norm.w"]) + f(W["wan.0.ca.norm.b"])
-    qc = odit.rms_norm(odit.linear(yc, W, "wan.0.ca.q"), eps_n) * f(W["wan.0.ca.q_norm.w"])
-    kv = odit.linear(ctx, W, "wan.0.ca.kv")
-    kc = odit.rms_norm(kv[:, :H], eps_n) * f(W["wan.0.ca.k_norm.w"])
-    oc = odit.attention(qc.reshape(-1, h, 128).transpose(1, 0, 2), kc.reshape(-1, h, 128).transpose(1, 0, 2),
-                        kv[:, H:].reshape(-1, h, 128).transpose(1, 0, 2)).transpose(1, 0, 2).reshape(len(rows), H)
-    xr = xr + odit.linear(oc, W, "wan.0.ca.o")
-    y2 = odit.layer_norm(xr, eps_n) * (1 + sc2) + sh2
-    xr = xr + g2 * odit.mlp2(y2, W, "wan.0.ffn1", "wan.0.ffn2", odit.gelu_tanh)
-    fm = odit.linear(odit.silu(temb), W, "final.mod")[0]
-    v_ref = odit.linear(odit.layer_norm(xr, eps_n) * (1 + fm[H:]) + fm[:H], W, "final.proj")
-    err = rel(vg[rows], v_ref)
-    say("  rel v (sampled rows)", err)
-    assert err <= TOL[C.BF16]
+    say("  oracle rows")
+    v_ref = odit.forward(m, W, x0, txt, t=np.array([0.6]), txt_index=np.zeros(1, dtype=np.int64), grid=w.grid,
+                         rows=rows)
+    check(host(v)[:, rows], v_ref, C.BF16, model_stages(m), what=f"wan block full size ({path}) sampled rows")
+
+
+@pytest.mark.timeout(900)
+def test_qwen_shaped_latent_rollout_mixgrpo(gpu_lib):
+    """The Qwen-Image stack's latent model at full width (hidden 3072, 24 heads, MLP 12288, text width
+    3584) cut to 2 dual blocks and 1024 + 256 tokens, B = 2, in its 10-step rollout with SDE only on
+    1-indexed steps 2-4 (0-indexed {1, 2, 3}, MixGRPO): the sigma schedule and the log-prob steps
+    against the oracle's schedule; per step the next latent against Eq. 1 (or the ODE step) on the
+    GPU's own velocity and noise, and the log-prob of the stored latent; the velocity itself against
+    the oracle's forward at the GPU's stored x_k (teacher-forced) on the steps either side of the SDE
+    block and inside it."""
+    base = C.QWEN_STACK
+    m = base.model.replace(n_dual=2)
+    w = C.Workload(**{**base.__dict__, "name": "qwen-2dual-1024img", "index": 20, "model": m, "group": 2,
+                      "grid": (1, 32, 32)})
+    say("qwen-shaped latent rollout: generating inputs")
+    W, txt, cond, x0, eps = _inputs(w)
+    Wd, T, Cd, X0, E = _device(w, W, txt, cond, x0, eps)
+    tidx = torch.from_numpy(synth.txt_index(w)).cuda()
+    ro = R.Rollout(w, api.Dit(m, Wd))
+    res = ro.run(X0, T, E, cond=Cd, txt_index=tidx)
+    torch.cuda.synchronize()
+    ref_sig = osde.schedule_sigmas(osde.time_grid(w.steps), w.eta, "flow", w.sde_steps)
+    assert res.sigmas == pytest.approx(list(ref_sig), rel=1e-15)
+    assert [k for k, s in enumerate(res.sigmas) if s > 0] == [1, 2, 3]
+    assert sorted(res.logp) == [1, 2, 3]
+    for k in range(w.steps):
+        xk, vk = host(res.xs[k]), host(res.vs[k])
+        xn_ref = osde.sde_step(xk, vk, eps[k], res.ts[k], res.ts[k + 1], res.sigmas[k])
+        check(host(res.xs[k + 1]), xn_ref, C.BF16, 0, what=f"qwen-shaped x step {k}")
+        if k in res.logp:
+            lp_ref = osde.step_log_prob(xk, vk, host(res.xs[k + 1]), res.ts[k], res.ts[k + 1], res.sigmas[k])
+            assert np.max(np.abs(host(res.logp[k]) - lp_ref)) <= LOGP_ABS
+    for k in (0, 1, 3, 4):
+        say("  oracle forward, step", k)
+        v_ref = odit.forward(m, W, host(res.xs[k])[1:], txt, t=np.full(1, res.ts[k]), cond=cond,
+                             txt_index=synth.txt_index(w)[1:], grid=w.grid)
+        check(host(res.vs[k])[1:], v_ref, C.BF16, model_stages(m), what=f"qwen-shaped v step {k} sample 1")
