@@ -62,7 +62,7 @@ class Rollout:
     def __init__(self, w: C.Workload, dit: api.Dit, device="cuda", keep_velocities: bool = True,
                  noise_seed: Optional[int] = None):
         """noise_seed: draw each step's noise on the device (Philox4x32-10, counter = (element, sample,
-        step)) instead of reading the eps tensors passed to run()."""
+        step), key = noise_key(rollout index)) instead of reading the eps tensors passed to run()."""
         self.w = w
         self.noise_seed = noise_seed
         self.dit = dit
@@ -91,12 +91,28 @@ class Rollout:
         self.unit_weights = torch.ones(w.n_rewards, dtype=torch.float32, device=device)
         # per-step time vectors t_k for all samples, uploaded once
         self.t_steps = torch.tensor([[t] * B for t in self.ts[:-1]], dtype=torch.float32, device=device)
+        self.rollouts_started = 0
 
-    def run(self, x0, txt, eps_steps, cond=None, txt_index=None, txt_out=None) -> RolloutResult:
+    def noise_key(self, rollout_index: int) -> int:
+        """The 64-bit Philox key of one rollout's on-device noise: the seed advanced by a Weyl step
+        per rollout, so successive rollouts of one object draw independent noise (the counter
+        already separates elements, samples and steps within a rollout)."""
+        return (int(self.noise_seed) + rollout_index * 0x9E3779B97F4A7C15) & 0xFFFFFFFFFFFFFFFF
+
+    def iter_steps(self, x0, txt, eps_steps, cond=None, txt_index=None, txt_out=None, result=None):
+        """The rollout one denoising step at a time: a generator that issues step k (DiT forward,
+        then the SDE or ODE step with its log-prob) and yields k.  ``result`` (a RolloutResult with
+        empty lists) collects the latents, velocities and log-probs as they are produced."""
         w, m = self.w, self.w.model
         B = w.batch
         x = x0
-        xs, vs, logp = [x0], [], {}
+        res = result if result is not None else RolloutResult(xs=[], vs=[], logp={}, ts=list(self.ts),
+                                                               sigmas=list(self.sigmas))
+        res.xs.append(x0)
+        key = None
+        if self.noise_seed is not None:
+            key = self.noise_key(self.rollouts_started)
+        self.rollouts_started += 1
         # WAN: the text context is fixed along the trajectory, so its per-block cross-attention K / V
         # are prepared once and every step's forward reads them.
         context = None
@@ -116,16 +132,22 @@ class Rollout:
             lp = None
             if sigma > 0.0:
                 lp = torch.empty(B, dtype=torch.float64, device=self.device)
-                logp[k] = lp
-            if self.noise_seed is None:
+                res.logp[k] = lp
+            if key is None:
                 api.sde_step(x, v, eps_steps[k], x_next, t, tn, sigma, logp=lp, ws=self.ws_sde)
             else:
-                api.sde_step_philox(x, v, x_next, t, tn, sigma, self.noise_seed, k, logp=lp, ws=self.ws_sde)
+                api.sde_step_philox(x, v, x_next, t, tn, sigma, key, k, logp=lp, ws=self.ws_sde)
             if self.keep_v:
-                vs.append(v)
-            xs.append(x_next)
+                res.vs.append(v)
+            res.xs.append(x_next)
             x = x_next
-        return RolloutResult(xs=xs, vs=vs, logp=logp, ts=list(self.ts), sigmas=list(self.sigmas))
+            yield k
+
+    def run(self, x0, txt, eps_steps, cond=None, txt_index=None, txt_out=None) -> RolloutResult:
+        res = RolloutResult(xs=[], vs=[], logp={}, ts=list(self.ts), sigmas=list(self.sigmas))
+        for _ in self.iter_steps(x0, txt, eps_steps, cond=cond, txt_index=txt_index, txt_out=txt_out, result=res):
+            pass
+        return res
 
     def sde_step_ids(self) -> List[int]:
         return [k for k, s in enumerate(self.sigmas) if s > 0.0]
