@@ -1,35 +1,37 @@
 """Throughput of the Flow-GRPO rollout hot path on one MI355X.
 
-One step = one pass of the whole hot path over one batch: the DiT velocity
-forward (here one Flux-shaped dual-stream block, B = 8 samples of 4096 image
-+ 512 text tokens, hidden 3072, bf16), the SDE step with its per-sample
-log-probability, and the group-normalised advantages.  Inputs are synthetic
-(seeded, N(0, 0.02) weights, N(0, 1) activations) and resident in HBM before
-timing starts.
+Default workload: the Qwen-Image-shaped stack (60 dual-stream blocks, hidden 3072, 24 heads x 128,
+MLP 12288, B = 8 samples of 4096 image + 256 text tokens, bf16) in its 10-step rollout on the
+uniform grid with the SDE step only on 1-indexed steps 2-4 (MixGRPO) and ODE steps elsewhere.
 
-Prints one JSON line: steps/s (and latent tokens/s), the roofline of the
-dominant kernel measured with HIP events on its launch stream over the timed
-region, and the plain CPU oracle timed on a bounded sample of the same work.
-The per-kernel breakdown comes from an untimed pass in which every launch is
-bracketed by events; in the timed region only the dominant kernel's launches
-are, since events around every launch cost about 1% of a step.
+One step = one denoising step of the whole batch: the DiT velocity forward (embedders, the 60
+blocks, the final layer), then the SDE step with its per-sample log-probability (or the ODE step),
+and, on the step that ends a rollout, the group-normalised advantages.  --steps K times exactly K
+such steps, walking through successive rollouts (20 steps = two rollouts' worth, every window of
+10 consecutive steps holds the three SDE steps).  Weights are drawn on the device (N(0, 0.02^2),
+norm weights 1 + N(0, 0.02^2)); prompt embeddings, x_1 and the SDE noise are seeded host draws;
+everything is resident in HBM before timing starts.
 
-The other workloads (--workload flux-stack | qwen-stack | wan) run whole
-rollouts of the full model: 19 dual + 38 single Flux blocks (B = 16, 1024 +
-512 tokens, 10 SDE steps), 60 Qwen-Image-shaped dual blocks (B = 8, 4096 +
-256 tokens, 10 steps with SDE on steps 2-4) or 30 WAN blocks (B = 1, 32760 +
-512 tokens, 8 steps).  Their weights are drawn on the device (N(0, 0.02),
-norm weights 1 + N(0, 0.02)); a step is one denoising step of the batch, and
---steps / --warmup count whole rollouts.  Two training-side workloads run on
-the Flux stack: grpo-flux-stack times the GRPO policy-update forward over a
-stored rollout (a DiT forward and a log-prob recompute per SDE step, then the
-clipped-ratio objective; a step is one recomputed SDE step), awm-flux-stack
-the AWM training forward (noising at per-sample t, DiT forward, Eq. 3 loss; a
-step is one forward of the batch).  The oracle is timed on the default
-workload only.
+Prints one JSON line: steps/s (and latent tokens/s), the roofline of the dominant kernel measured
+with HIP events on its launch stream over the timed region, and the plain CPU oracle.  The
+per-kernel breakdown comes from an untimed pass of one rollout in which every launch is bracketed
+by events; in the timed region only the dominant kernel's launches are, since events around
+every launch cost about 1% of a step.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
-                       [--workload flux-block|flux-stack|qwen-stack|wan|tiny]
+The CPU oracle (float64 numpy) is timed on the host in the same run.  For the stacks it times one
+block of each kind at full shape with one sample (WAN: sampled query rows, extrapolated linearly
+in the row count), the embedders and final layer, the SDE step and log-prob at full size and the
+advantages, and extrapolates to a batch step by block count x samples; the line says
+"extrapolated".  The one-block and tiny workloads are timed in full.
+
+Other workloads (--workload): flux-block (one Flux-shaped dual-stream block, B = 8, 4096 + 512
+tokens, one SDE step t = 0.6 -> 0.5 on the block's hidden state), flux-stack (19 dual + 38 single
+blocks, B = 16, 1024 + 512 tokens, 10 SDE steps), wan (30 WAN blocks, B = 1, 32760 + 512 tokens,
+8 steps), tiny, and two training-side workloads on the Flux stack: grpo-flux-stack (the GRPO
+policy-update forward over a stored rollout; a step is one recomputed SDE step) and
+awm-flux-stack (noising, DiT forward, Eq. 3 loss; a step is one forward of the batch).
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 """
 from __future__ import annotations
 
@@ -40,6 +42,23 @@ import os
 import sys
 import time
 
+
+def _host_threads() -> int:
+    """Host threads for the oracle: the CPUs this process may run on, capped by an OMP_NUM_THREADS
+    the environment already sets (a shared box's per-GPU CPU share)."""
+    n = len(os.sched_getaffinity(0))
+    share = os.environ.get("OMP_NUM_THREADS", "")
+    if share.isdigit() and int(share) > 0:
+        n = min(n, int(share))
+    return n
+
+
+# The BLAS thread pools are sized when numpy is first imported, so this runs before any import
+# that loads it (torch does).
+HOST_THREADS = _host_threads()
+for _var in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS"):
+    os.environ[_var] = str(HOST_THREADS)
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -47,12 +66,13 @@ METRIC = "SDE rollout steps/sec and latent tokens/sec per GPU; % bf16 MFMA peak"
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3       # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+TARGET_MFMA, TARGET_HBM = 0.50, 0.70
 
-# workload name -> (configs attribute, default timed units, default warmup units); the one-block
-# and tiny workloads time single steps, the stacks whole rollouts.
-WORKLOADS = {"flux-block": ("FLUX_BLOCK", 20, 3), "tiny": ("TINY", 20, 3), "flux-stack": ("FLUX_STACK", 2, 1),
-             "qwen-stack": ("QWEN_STACK", 1, 1), "wan": ("WAN_STACK", 2, 1),
+# workload name -> (configs attribute, default timed steps, default warmup steps)
+WORKLOADS = {"qwen-stack": ("QWEN_STACK", 20, 5), "flux-block": ("FLUX_BLOCK", 20, 5), "tiny": ("TINY", 20, 5),
+             "flux-stack": ("FLUX_STACK", 20, 5), "wan": ("WAN_STACK", 16, 4),
              "grpo-flux-stack": ("FLUX_STACK", 2, 1), "awm-flux-stack": ("FLUX_STACK", 10, 2)}
+DEVICE_DRAWN = ("flux-stack", "qwen-stack", "wan", "grpo-flux-stack", "awm-flux-stack")
 
 
 def parse():
@@ -60,12 +80,15 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=None)
-    ap.add_argument("--workload", default="flux-block", choices=list(WORKLOADS))
+    ap.add_argument("--workload", default="qwen-stack", choices=list(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--noise", default="stored", choices=["stored", "philox"],
                     help="read each step's noise from HBM (default) or draw it in the SDE kernel")
-    ap.add_argument("--cpu-samples", type=int, default=3, help="samples of the batch the oracle times")
     return ap.parse_args()
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
 
 
 def main() -> int:
@@ -96,8 +119,8 @@ def main() -> int:
     m = w.model
     dt = api.torch_dtype(m.dtype)
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda().to(dt)
-    print(f"[bench] workload {w.name}: generating inputs", file=sys.stderr, flush=True)
-    device_drawn = args.workload in ("flux-stack", "qwen-stack", "wan", "grpo-flux-stack", "awm-flux-stack")
+    log(f"workload {w.name}: generating inputs")
+    device_drawn = args.workload in DEVICE_DRAWN
     if device_drawn:
         W = None
         Wd = device_weights(m, 1000 + w.index, dt)
@@ -113,21 +136,31 @@ def main() -> int:
     dit = api.Dit(m, Wd)
     ro = R.Rollout(w, dit, keep_velocities=False, noise_seed=(3000 + w.index) if args.noise == "philox" else None)
     txt_out = torch.empty_like(T) if m.io_mode == C.IO_HIDDEN else None
-    steps_per_unit = len(ro.sigmas)     # denoising steps in one timed unit (a rollout, or the one step)
+    K = len(ro.sigmas)                  # denoising steps of one rollout
+    steps_per_rollout = K
+    state = {"it": None}
 
     def step():
-        res = ro.run(X0, T, E, cond=Cd, txt_index=tidx, txt_out=txt_out)
-        ro.advantages(rewards)
-        return res
+        """One denoising step of the batch, continuing the current rollout (a new one starts after the
+        last step; the step that ends a rollout also computes the advantages)."""
+        if state["it"] is None:
+            state["it"] = ro.iter_steps(X0, T, E, cond=Cd, txt_index=tidx, txt_out=txt_out)
+        k = next(state["it"])
+        if k == K - 1:
+            ro.advantages(rewards)
+            state["it"] = None
 
+    timed_unit = "denoising step of the batch (DiT forward, SDE/ODE step with log-prob; advantages at rollout end)"
     if args.workload == "grpo-flux-stack":
-        print("[bench] storing one rollout for the policy update", file=sys.stderr, flush=True)
-        stored = step()
+        log("storing one rollout for the policy update")
+        stored = ro.run(X0, T, E, cond=Cd, txt_index=tidx)
+        ro.advantages(rewards)
         adv_stored = ro.adv.clone()
-        steps_per_unit = len(ro.sde_step_ids())
-        step_w = torch.ones(steps_per_unit, dtype=torch.float32, device="cuda")
+        steps_per_rollout = len(ro.sde_step_ids())
+        step_w = torch.ones(steps_per_rollout, dtype=torch.float32, device="cuda")
+        timed_unit = "GRPO update forward over a stored rollout (a step is one recomputed SDE step)"
 
-        def step():  # noqa: F811 -- the timed unit of this workload
+        def step():  # noqa: F811 -- the timed unit of this workload: a whole update, counted as its SDE steps
             return ro.grpo_objective(stored, adv_stored, T, cond=Cd, txt_index=tidx, step_w=step_w)
     elif args.workload == "awm-flux-stack":
         g = torch.Generator(device="cuda")
@@ -135,27 +168,32 @@ def main() -> int:
         t_awm = torch.rand(w.batch, generator=g, device="cuda", dtype=torch.float32)
         eps_awm = torch.randn(X0.shape, generator=g, device="cuda", dtype=torch.float32).to(dt)
         adv_awm = torch.randn(w.batch, generator=g, device="cuda", dtype=torch.float32)
-        steps_per_unit = 1
+        steps_per_rollout = 1
+        timed_unit = "AWM training forward of the batch"
 
         def step():  # noqa: F811 -- the timed unit of this workload
             return ro.awm_objective(X0, eps_awm, t_awm, T, adv_awm, cond=Cd, txt_index=tidx)
+    calls_per_step = steps_per_rollout if args.workload == "grpo-flux-stack" else 1
+    n_calls = max(1, args.steps // calls_per_step) if calls_per_step > 1 else args.steps
+    n_warm = max(1, args.warmup // calls_per_step) if calls_per_step > 1 else args.warmup
 
-    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
+    log(f"warmup {args.warmup} steps")
+    for _ in range(n_warm):
         step()
     torch.cuda.synchronize()
-    # Per-kernel breakdown: an untimed pass with every launch bracketed by HIP events (the events
-    # cost ~1% of a step, so the timed region below brackets the dominant kernel only).
-    bd_units = 1 if steps_per_unit > 1 else min(args.steps, 5)
+    # Per-kernel breakdown: an untimed pass over one rollout's worth of steps with every launch
+    # bracketed by HIP events (the events cost ~1% of a step, so the timed region below brackets
+    # the dominant kernel only).
+    bd_calls = 1 if calls_per_step > 1 else max(K, 1)
     api.profile_filter(None)
     api.profile_reset()
     api.profile_enable(True)
-    for _ in range(bd_units):
+    for _ in range(bd_calls):
         step()
     torch.cuda.synchronize()
     api.profile_enable(False)
     prof = api.profile_read()
-    bd_steps = bd_units * steps_per_unit
+    bd_steps = bd_calls * calls_per_step
     dominant = max(prof, key=lambda n: prof[n]["ms"])
     # Timed region: events around the dominant kernel's launches only.
     api.profile_reset()
@@ -163,21 +201,22 @@ def main() -> int:
     api.profile_enable(True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(args.steps):
+    for i in range(n_calls):
         step()
-        if steps_per_unit > 1:
-            print(f"[bench] rollout {i + 1}/{args.steps} issued", file=sys.stderr, flush=True)
+        if (i + 1) % 10 == 0:
+            log(f"{i + 1}/{n_calls} issued")
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     api.profile_enable(False)
     prof_timed = api.profile_read()
     api.profile_filter(None)
-    print(f"[bench] timed {args.steps} steps in {elapsed:.3f} s", file=sys.stderr, flush=True)
+    n_steps = n_calls * calls_per_step
+    log(f"timed {n_steps} steps in {elapsed:.3f} s")
 
-    n_steps = args.steps * steps_per_unit
     ms_per_step = 1e3 * elapsed / n_steps
     steps_per_s = n_steps / elapsed
     latent_tok_s = steps_per_s * w.batch * w.n_img
+    peak_mfma = PEAK_BF16_TFLOPS if m.dtype == C.BF16 else PEAK_FP32_TFLOPS
 
     # Per-kernel achieved rates from the breakdown pass's HIP events.
     kernels = {}
@@ -187,35 +226,51 @@ def main() -> int:
              "ms_per_step": p["ms"] / bd_steps}
         if p["flops"] > 0 and name.startswith(("gemm", "attn")):
             k["tflops"] = p["flops"] / (p["ms"] * 1e-3) / 1e12
-            k["mfma_frac"] = k["tflops"] / (PEAK_BF16_TFLOPS if m.dtype == C.BF16 else PEAK_FP32_TFLOPS)
+            k["mfma_frac"] = k["tflops"] / peak_mfma
         elif p["bytes"] > 0:
             k["gbs"] = p["bytes"] / (p["ms"] * 1e-3) / 1e9
             k["hbm_frac"] = k["gbs"] / PEAK_HBM_GBS
         kernels[name] = k
-    block_flops = sum(p["flops"] for n, p in prof.items() if n.startswith(("gemm", "attn"))) / bd_steps
+    model_flops = sum(p["flops"] for n, p in prof.items() if n.startswith(("gemm", "attn"))) / bd_steps
     dp = prof_timed[dominant]   # the dominant kernel, timed live over the timed region
     per_launch = {"flops": dp["flops"] / dp["launches"], "algorithmic_bytes": dp["bytes"] / dp["launches"],
-                  "avg_us": 1e3 * dp["ms"] / dp["launches"]}
-    # HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE summary of this kernel,
-    # null when there is none or the kernel's sources have changed since it was taken.
-    rec = profiling.lookup_traffic(dominant)
+                  "avg_us": 1e3 * dp["ms"] / dp["launches"], "launches_timed": dp["launches"]}
+    # HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE summary of this kernel on this
+    # workload, null when there is none or the kernel's sources have changed since it was taken.
+    rec = profiling.lookup_traffic(dominant, w.name)
     traffic = rec["traffic_bytes_per_launch"] if rec else None
     if rec:
         per_launch["traffic_source"] = rec["summary"]
-    compute_bound = dp["flops"] > 0 and dominant.startswith(("gemm", "attn"))
-    if compute_bound:
-        peak = PEAK_BF16_TFLOPS if m.dtype == C.BF16 else PEAK_FP32_TFLOPS
+    if dp["flops"] > 0 and dominant.startswith(("gemm", "attn")):
         achieved = dp["flops"] / (dp["ms"] * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
-                "traffic": traffic, "kernel": dominant, "per_launch": per_launch}
+        roof = {"bound": "mfma", "achieved": achieved, "peak": peak_mfma, "unit": "TFLOP/s",
+                "frac": achieved / peak_mfma, "traffic": traffic, "kernel": dominant, "per_launch": per_launch}
     else:
         achieved = dp["bytes"] / (dp["ms"] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": achieved / PEAK_HBM_GBS, "traffic": traffic, "kernel": dominant, "per_launch": per_launch}
 
+    # Each kernel family against its own bar: MFMA kernels >= 50% of the bf16 peak, the HBM-bound
+    # SDE / log-prob kernels >= 70% of 8 TB/s.  A miss is reported as a miss.
+    def family(prefix, key):
+        sel = {n: p for n, p in prof.items() if n.startswith(prefix)}
+        tot_ms = sum(p["ms"] for p in sel.values())
+        if not sel or tot_ms <= 0:
+            return None
+        if key == "flops":
+            frac = sum(p["flops"] for p in sel.values()) / (tot_ms * 1e-3) / 1e12 / peak_mfma
+            return {"frac_of_peak": frac, "target": TARGET_MFMA, "met": frac >= TARGET_MFMA,
+                    "share_of_step": tot_ms / bd_steps / ms_per_step}
+        frac = sum(p["bytes"] for p in sel.values()) / (tot_ms * 1e-3) / 1e9 / PEAK_HBM_GBS
+        return {"frac_of_peak": frac, "target": TARGET_HBM, "met": frac >= TARGET_HBM,
+                "share_of_step": tot_ms / bd_steps / ms_per_step}
+    targets = {"gemm": family("gemm", "flops"), "attention": family("attn", "flops"),
+               "sde_step": family("sde_step", "bytes"),
+               "model_mfma_frac": model_flops / (ms_per_step * 1e-3) / 1e12 / peak_mfma}
+
     cpu = None
-    if not args.no_cpu_baseline and W is not None:
-        cpu = cpu_baseline(w, W, txt, cond, x0, eps, args.cpu_samples)
+    if not args.no_cpu_baseline and args.workload not in ("grpo-flux-stack", "awm-flux-stack"):
+        cpu = cpu_baseline(w, W)
 
     out = {
         "metric": METRIC,
@@ -223,7 +278,7 @@ def main() -> int:
         "unit": "steps/s",
         "n_gpus": 1,
         "steps": n_steps,
-        "warmup": args.warmup * steps_per_unit,
+        "warmup": n_warm * calls_per_step,
         "ms_per_step": ms_per_step,
         "higher_is_better": True,
         "scaling": "weak",
@@ -233,19 +288,17 @@ def main() -> int:
         "config": {"workload": w.name, "batch": w.batch, "img_tokens": w.n_img, "txt_tokens": w.n_txt,
                    "hidden": m.hidden, "heads": m.heads, "head_dim": m.head_dim, "mlp_hidden": m.mlp_hidden,
                    "dual_blocks": m.n_dual, "single_blocks": m.n_single, "wan_blocks": m.n_wan,
-                   "denoising_steps": len(ro.sigmas), "sde_steps": sum(1 for s in ro.sigmas if s > 0),
-                   "timed_unit": {"grpo-flux-stack": "GRPO update forward over a stored rollout",
-                                  "awm-flux-stack": "AWM training forward of the batch"}.get(
-                       args.workload, "rollout" if steps_per_unit > 1 else "step"),
+                   "denoising_steps_per_rollout": K, "sde_steps_per_rollout": sum(1 for s in ro.sigmas if s > 0),
+                   "sde_step_ids": [k for k, s in enumerate(ro.sigmas) if s > 0],
+                   "timed_unit": timed_unit,
                    "weights": "device-drawn N(0,0.02)" if device_drawn else "host-drawn N(0,0.02), seeded",
-                   "noise": "Philox4x32-10 in the SDE kernel" if args.noise == "philox" else "stored eps tensors",
-                   "t": ro.ts[0], "t_next": ro.ts[1], "sigma": ro.sigmas[0]},
+                   "noise": "Philox4x32-10 in the SDE kernel" if args.noise == "philox" else "stored eps tensors"},
         "latent_tokens_per_s": latent_tok_s,
         "sample_steps_per_s": steps_per_s * w.batch,
-        "model_tflops": block_flops / (ms_per_step * 1e-3) / 1e12,
-        "model_mfma_frac": block_flops / (ms_per_step * 1e-3) / 1e12 /
-                           (PEAK_BF16_TFLOPS if m.dtype == C.BF16 else PEAK_FP32_TFLOPS),
+        "model_tflops": model_flops / (ms_per_step * 1e-3) / 1e12,
+        "model_mfma_frac": targets["model_mfma_frac"],
         "roofline": roof,
+        "targets": targets,
         "kernels": kernels,
         "cpu_baseline": cpu,
     }
@@ -270,9 +323,16 @@ def device_weights(m, seed: int, dt):
     return out
 
 
-def cpu_baseline(w, W, txt, cond, x0, eps, n_samples: int):
-    """The oracle (as it stands) on a bounded sample of the step: n_samples of the batch's samples
-    through the DiT forward, the SDE step and its log-prob, plus the advantages; scaled to steps/s."""
+def _timed(fn):
+    t0 = time.perf_counter()
+    r = fn()
+    return time.perf_counter() - t0, r
+
+
+def cpu_baseline(w, W):
+    """The oracle (as it stands, float64 numpy) on the host cores.  One-block and tiny workloads: the
+    whole step.  Stacks: one block of each kind at full shape with one sample, the embedders and
+    final layer, the SDE step, log-prob and advantages at full size; extrapolated to a batch step."""
     import numpy as np
 
     from oracle import dit as odit
@@ -284,33 +344,102 @@ def cpu_baseline(w, W, txt, cond, x0, eps, n_samples: int):
 
     try:
         from threadpoolctl import threadpool_info
-        threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+        blas_threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
     except Exception:  # pragma: no cover
-        threads = 1
+        blas_threads = HOST_THREADS
     m = w.model
     ts = [w.fixed_step[0], w.fixed_step[1]] if w.fixed_step else R.time_grid(w.steps)
-    n = min(n_samples, w.batch)
-    print(f"[bench] cpu baseline: oracle on {n} of {w.batch} samples, {threads} threads", file=sys.stderr, flush=True)
-    t0 = time.perf_counter()
-    x = x0[:n].astype(np.float64)
-    tidx = synth.txt_index(w)[:n]
-    for k in range(len(ts) - 1):
-        t, tn = ts[k], ts[k + 1]
-        sigma = (w.eta * math.sqrt(t / (1 - t))) if w.fixed_step else R.sigma_schedule(ts, w.eta, w.dynamics, w.sde_steps)[k]
-        if m.io_mode == C.IO_HIDDEN:
-            v, _ = odit.forward(m, W, x, txt[:n], cond=cond[:n], grid=w.grid)
-        else:
-            v = odit.forward(m, W, x, txt, t=np.full(n, t), cond=cond, txt_index=tidx, grid=w.grid)
-        xn = osde.sde_step(x, v, eps[k][:n], t, tn, sigma)
-        if sigma > 0:
-            osde.step_log_prob(x, v, xn, t, tn, sigma)
-        x = xn
-    orollout.advantages_for(synth.rewards(w), w.group)
-    el = time.perf_counter() - t0
-    per_step = el * (w.batch / n)
-    return {"value": 1.0 / per_step, "unit": "steps/s", "cores": threads, "kind": "oracle",
-            "sample": f"{n} of {w.batch} samples of one step (DiT forward fp64, SDE step, log-prob, advantages), "
-                      f"{el:.1f} s measured, scaled by {w.batch}/{n} to the full batch"}
+    if w.fixed_step:
+        sigmas = [w.eta * math.sqrt(ts[0] / (1 - ts[0]))]
+    else:
+        sigmas = R.sigma_schedule(ts, w.eta, w.dynamics, w.sde_steps)
+    K = len(sigmas)
+    txt, cond, x0 = synth.text_input(w), synth.cond_input(w), synth.x0(w)
+    x0d = x0.astype(np.float64)
+    eps0 = synth.sde_noise(w, 0)
+    log(f"cpu baseline: oracle on {HOST_THREADS} host threads ({blas_threads} BLAS threads)")
+
+    # the SDE / ODE step (and log-prob on SDE steps) and the advantages at full size
+    t_sde = 0.0
+    for k in range(K):
+        tk, tn, s = ts[k], ts[k + 1], sigmas[k]
+        dt_, xn = _timed(lambda: osde.sde_step(x0d, x0d, eps0, tk, tn, s))
+        t_sde += dt_
+        if s > 0:
+            t_sde += _timed(lambda: osde.step_log_prob(x0d, x0d, xn, tk, tn, s))[0]
+    t_adv = _timed(lambda: orollout.advantages_for(synth.rewards(w), w.group))[0]
+    update_per_step = t_sde / K + t_adv / K
+
+    if W is not None:
+        # one-block / tiny workloads: the whole step (or rollout) on the full batch
+        def full():
+            x = x0d
+            tidx = synth.txt_index(w)
+            for k in range(K):
+                if m.io_mode == C.IO_HIDDEN:
+                    v, _ = odit.forward(m, W, x, txt, cond=cond, grid=w.grid)
+                else:
+                    v = odit.forward(m, W, x, txt, t=np.full(w.batch, ts[k]), cond=cond, txt_index=tidx, grid=w.grid)
+                xn = osde.sde_step(x, v, synth.sde_noise(w, k), ts[k], ts[k + 1], sigmas[k])
+                if sigmas[k] > 0:
+                    osde.step_log_prob(x, v, xn, ts[k], ts[k + 1], sigmas[k])
+                x = xn
+            orollout.advantages_for(synth.rewards(w), w.group)
+        el = _timed(full)[0]
+        per_step = el / K
+        return {"value": 1.0 / per_step, "unit": "steps/s", "cores": HOST_THREADS, "kind": "oracle",
+                "extrapolated": False,
+                "sample": f"the whole {'step' if K == 1 else f'{K}-step rollout'} of the batch ({w.batch} samples: "
+                          f"DiT forward, SDE steps, log-probs, advantages) in float64, {el:.1f} s measured"}
+
+    # stacks: one block of each kind at full shape, B = 1, on seeded host weights of block 0
+    one = {"n_dual": 1 if m.n_dual else 0, "n_single": 1 if m.n_single else 0, "n_wan": 1 if m.n_wan else 0}
+    w1 = C.Workload(**{**w.__dict__, "model": m.replace(**one), "prompts": 1, "group": 1})
+    W1 = synth.weights(w1)
+    x1 = x0d[:1]
+    tid = np.zeros(1, dtype=np.int64)
+    t_mid = np.array([ts[1]])
+    ang = odit.rope_angles(odit.grid_positions(w.grid), m.rope_axes, m.rope_theta)
+    parts = {}
+    if m.model == C.MODEL_MMDIT:
+        c = odit.mlp2(odit.timestep_sinusoid(t_mid), W1, "temb.fc1", "temb.fc2", odit.silu)
+        if m.pooled_dim:
+            c = c + odit.mlp2(odit.f64(cond)[tid], W1, "pooled.fc1", "pooled.fc2", odit.silu)
+        x_img = odit.linear(x1, W1, "x_in")
+        x_txt = odit.linear(txt, W1, "txt_in")[tid]
+        t_edge = _timed(lambda: odit.forward(w1.model.replace(n_dual=0, n_single=0), W1, x1, txt, t=t_mid,
+                                             cond=cond, txt_index=tid, grid=w.grid))[0]
+        if m.n_dual:
+            parts["dual"] = (_timed(lambda: odit.dual_block(x_img, x_txt, c, W1, 0, m, ang))[0], m.n_dual)
+        if m.n_single:
+            xj = np.concatenate([x_txt, x_img], axis=1)
+            parts["single"] = (_timed(lambda: odit.single_block(xj, c, W1, 0, m, w.n_txt, ang))[0], m.n_single)
+        how = "one block of each kind timed in full"
+    else:
+        temb = odit.mlp2(odit.timestep_sinusoid(t_mid), W1, "temb.fc1", "temb.fc2", odit.silu)
+        e6 = odit.linear(odit.silu(temb), W1, "temb.proj").reshape(1, 6, -1)
+        ctx = odit.mlp2(txt, W1, "txt_in.fc1", "txt_in.fc2", odit.gelu_tanh)[tid]
+        xh = odit.linear(x1, W1, "x_in")
+        t_edge = _timed(lambda: odit.final_layer(xh, temb, W1, m))[0]
+        t_edge += _timed(lambda: odit.linear(x1, W1, "x_in"))[0]
+        # the sampled-row block is linear in the row count: keys / values of all tokens plus each row
+        r1, r2 = 64, 192
+        rows1 = np.linspace(0, w.n_img - 1, r1).astype(np.int64)
+        rows2 = np.linspace(0, w.n_img - 1, r2).astype(np.int64)
+        ta = _timed(lambda: odit.wan_block(xh, ctx, e6, W1, 0, m, ang, rows=rows1))[0]
+        tb = _timed(lambda: odit.wan_block(xh, ctx, e6, W1, 0, m, ang, rows=rows2))[0]
+        per_row = max(tb - ta, 0.0) / (r2 - r1)
+        t_block = ta + per_row * (w.n_img - r1)
+        parts["wan"] = (t_block, m.n_wan)
+        how = (f"one WAN block on {r1} and {r2} sampled query rows ({ta:.1f} s, {tb:.1f} s), "
+               f"extrapolated linearly to {w.n_img} rows")
+    per_step = w.batch * (t_edge + sum(t * n for t, n in parts.values())) + update_per_step
+    detail = ", ".join(f"{k} block {t:.2f} s x {n}" for k, (t, n) in parts.items())
+    return {"value": 1.0 / per_step, "unit": "steps/s", "cores": HOST_THREADS, "kind": "oracle",
+            "extrapolated": True,
+            "sample": f"float64 oracle, one sample: {detail} ({how}); embedders + final layer {t_edge:.2f} s; "
+                      f"x {w.batch} samples; plus SDE/ODE steps, log-probs and advantages at full size "
+                      f"({update_per_step * 1e3:.1f} ms per step); extrapolated to {per_step:.0f} s per batch step"}
 
 
 if __name__ == "__main__":

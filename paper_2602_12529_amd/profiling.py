@@ -16,7 +16,7 @@ Subcommands (python -m paper_2602_12529_amd.profiling ...):
   counter CSV OUT --counter NAME --title T --cmd C [--note N]
       one counter of a `rocprofv3 --pmc` run (e.g. the derived MfmaUtil) per kernel.
   traffic --fetch CSV --write CSV --copy-fetch CSV --copy-write CSV --copy-bytes N
-          --key NAME=PATTERN OUT --title T --cmd C [--cmd C ...]
+          --workload W --key NAME=PATTERN OUT --title T --cmd C [--cmd C ...]
       counter_collection.csv files of four `rocprofv3 --pmc` runs (FETCH_SIZE,
       then WRITE_SIZE, over the workload and over the copy) -> per-kernel HBM
       bytes per launch.  Each counter is scaled by N / (its value for the copy),
@@ -24,8 +24,9 @@ Subcommands (python -m paper_2602_12529_amd.profiling ...):
       interface.  NAME is the library's profiler name of the kernel the bench
       reports (gemm_bf16_gated, attn_bf16, ...), PATTERN a substring of
       rocprofv3's kernel name; the summary stores NAME's traffic per launch
-      with the hash of the sources the kernel is built from, and bench.py
-      reports it only while that hash still matches.
+      with the workload's name and the hash of the sources the kernel is built
+      from, and bench.py reports it for that workload only while that hash
+      still matches.
 """
 from __future__ import annotations
 
@@ -252,7 +253,7 @@ def _copy_factor(path: str, counter: str, nbytes: int) -> float:
 
 
 def traffic_md(fetch_csv: str, write_csv: str, copy_fetch_csv: str, copy_write_csv: str, copy_bytes: int,
-               keys: Dict[str, str], out_md: str, title: str, cmds: List[str]) -> dict:
+               keys: Dict[str, str], out_md: str, title: str, cmds: List[str], workload: str) -> dict:
     ff_ = _copy_factor(copy_fetch_csv, "FETCH_SIZE", copy_bytes)
     fw_ = _copy_factor(copy_write_csv, "WRITE_SIZE", copy_bytes)
     fetch = _counter_per_kernel(fetch_csv, "FETCH_SIZE")
@@ -280,7 +281,7 @@ def traffic_md(fetch_csv: str, write_csv: str, copy_fetch_csv: str, copy_write_c
         if len(match) != 1:
             raise SystemExit(f"pattern {pattern!r} matches {len(match)} kernels")
         name, n, af, aw, rb, wb = match[0]
-        records.append({"kernel": lib_name, "rocprof_kernel": short_name(name), "launches": n,
+        records.append({"kernel": lib_name, "workload": workload, "rocprof_kernel": short_name(name), "launches": n,
                         "fetch_bytes_per_launch": rb, "write_bytes_per_launch": wb,
                         "traffic_bytes_per_launch": rb + wb, "copy_factor_fetch": ff_, "copy_factor_write": fw_,
                         "sources_sha256": sources_sha256(lib_name)})
@@ -311,8 +312,8 @@ def counter_md(csv_path: str, counters: List[str], out_md: str, title: str, cmds
         f.write("\n".join(out) + "\n")
 
 
-def lookup_traffic(kernel: str) -> Optional[dict]:
-    """The committed traffic record of `kernel` whose sources still hash the same, else None."""
+def lookup_traffic(kernel: str, workload: str) -> Optional[dict]:
+    """The committed traffic record of `kernel` on `workload` whose sources still hash the same, else None."""
     if not os.path.isdir(PROFILES):
         return None
     want = sources_sha256(kernel)
@@ -326,7 +327,7 @@ def lookup_traffic(kernel: str) -> Optional[dict]:
             except ValueError:
                 continue
             for r in recs if isinstance(recs, list) else []:
-                if r.get("kernel") == kernel and r.get("sources_sha256") == want:
+                if r.get("kernel") == kernel and r.get("workload") == workload and r.get("sources_sha256") == want:
                     return dict(r, summary=os.path.join("profiles", fn))
     return None
 
@@ -365,6 +366,7 @@ def main(argv=None) -> int:
     for k in ("fetch", "write", "copy_fetch", "copy_write"):
         t.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
     t.add_argument("--copy-bytes", type=int, required=True)
+    t.add_argument("--workload", required=True, help="workload name the records belong to")
     t.add_argument("--key", action="append", default=[], help="NAME=PATTERN")
     t.add_argument("out")
     t.add_argument("--title", required=True)
@@ -382,7 +384,8 @@ def main(argv=None) -> int:
         stats_md(a.csv, a.out, a.title, a.cmd)
     else:
         keys = dict(kv.split("=", 1) for kv in a.key)
-        traffic_md(a.fetch, a.write, a.copy_fetch, a.copy_write, a.copy_bytes, keys, a.out, a.title, a.cmd)
+        traffic_md(a.fetch, a.write, a.copy_fetch, a.copy_write, a.copy_bytes, keys, a.out, a.title, a.cmd,
+                   a.workload)
     return 0
 
 

@@ -35,7 +35,7 @@ def test_traffic_scaling_and_lookup(tmp_path, monkeypatch):
     out = tmp_path / "prof.md"
     res = P.traffic_md(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), str(tmp_path / "cf.csv"),
                        str(tmp_path / "cw.csv"), copy_bytes, {"gemm_bf16_gated": "gemm_bf16_pp<2, 3>"}, str(out),
-                       "title", ["cmd"])
+                       "title", ["cmd"], "qwen-60dual")
     rec = res["records"][0]
     assert rec["copy_factor_fetch"] == 2048.0 and rec["copy_factor_write"] == 1024.0
     assert rec["fetch_bytes_per_launch"] == 200.0 * 2048 and rec["write_bytes_per_launch"] == 50.0 * 1024
@@ -43,12 +43,13 @@ def test_traffic_scaling_and_lookup(tmp_path, monkeypatch):
     assert rec["sources_sha256"] == P.sources_sha256("gemm_bf16_gated")
     # bench.py's lookup finds the record while the sources hash the same, and not otherwise
     monkeypatch.setattr(P, "PROFILES", str(tmp_path))
-    got = P.lookup_traffic("gemm_bf16_gated")
+    got = P.lookup_traffic("gemm_bf16_gated", "qwen-60dual")
     assert got is not None and got["traffic_bytes_per_launch"] == rec["traffic_bytes_per_launch"]
-    assert P.lookup_traffic("attn_bf16_d128") is None
+    assert P.lookup_traffic("attn_bf16_d128", "qwen-60dual") is None
+    assert P.lookup_traffic("gemm_bf16_gated", "flux-block") is None      # another workload's shapes
     stale = out.read_text().replace(rec["sources_sha256"], "0" * 64)
     out.write_text(stale)
-    assert P.lookup_traffic("gemm_bf16_gated") is None
+    assert P.lookup_traffic("gemm_bf16_gated", "qwen-60dual") is None
 
 
 def test_sources_hash_follows_kernel_family():
