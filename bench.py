@@ -267,6 +267,10 @@ def main() -> int:
     targets = {"gemm": family("gemm", "flops"), "attention": family("attn", "flops"),
                "sde_step": family("sde_step", "bytes"),
                "model_mfma_frac": model_flops / (ms_per_step * 1e-3) / 1e12 / peak_mfma}
+    if targets["sde_step"] is not None:
+        # below ~64 MB per call the step is launch-latency bound (~10-20 us) and fits the 256 MB MALL;
+        # its bandwidth bar applies to calls of hundreds of MB (the size sweep under profiles/)
+        targets["sde_step"]["bytes_per_call"] = w.batch * w.latent_dim * 4 * (2 if m.dtype == C.BF16 else 4)
 
     cpu = None
     if not args.no_cpu_baseline and args.workload not in ("grpo-flux-stack", "awm-flux-stack"):

@@ -30,15 +30,17 @@ def rel(a, b):
 
 
 # Element-wise bound of a parity check: |got - ref| <= a |ref| + b rms(ref), with
-#   a = 2 u_out                 the output's own rounding to its storage type (u_out = 2^-9 for
-#                               bf16 round-to-nearest-even, 2^-24 for float32), doubled;
+#   a = 2 u                     the output's own rounding to bf16 (unit roundoff u = 2^-8 of an
+#                               8-bit significand, round to nearest even) and one more rounding of
+#                               the same element upstream (the residual stream is stored in bf16
+#                               between the two halves of a block);
 #   b = Z sqrt(S s^2 + K u32^2) the error carried in from upstream: S storage roundings on the path
-#                               from the (identical) inputs to this output, each a relative error
-#                               uniform in +-u_store (standard deviation s = u_store / sqrt(3)) that
-#                               a random-weight layer passes on at the scale of its output's rms,
-#                               plus the float32 accumulation of a K-term contraction (u32 = 2^-24
-#                               per addition, a random walk of K steps); Z = 7 standard deviations
-#                               is above the largest of 1e9 Gaussian draws (6.3).
+#                               from the (identical) inputs to this output, each a relative error of
+#                               at most u (standard deviation s = u / sqrt(3), the uniform case)
+#                               that a random-weight layer passes on at the scale of its output's
+#                               rms, plus the float32 accumulation of a K-term contraction
+#                               (u32 = 2^-24 per addition, a random walk of K steps); Z = 7
+#                               standard deviations is above the largest of 1e9 Gaussian draws (6.3).
 # float32 paths carry no storage rounding worth modelling against their accumulation and the
 # hardware transcendental approximations, so they take the per-element form of the normwise
 # bound instead: b = the normwise tolerance 1e-4, a = 1e-5.
@@ -57,7 +59,7 @@ def model_stages(m):
     return s + (STAGES_EMBED + STAGES_FINAL if m.io_mode == C.IO_LATENT else 0)
 
 
-U_BF16 = 2.0 ** -9
+U_BF16 = 2.0 ** -8
 U_F32 = 2.0 ** -24
 Z_MAX = 7.0
 ELEM_F32 = (1e-5, 1e-4)

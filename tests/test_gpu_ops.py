@@ -11,6 +11,7 @@ import torch
 
 from oracle import dit as odit
 from paper_2602_12529_amd import configs as C
+from paper_2602_12529_amd import synth
 
 from gpu_util import TOL, check, dev, host, normal, rel, say
 
@@ -160,7 +161,10 @@ def test_qk_norm_rope_parity(gpu_lib, dt):
     n_joint = n_tok + n_txt
     H = heads * d
     qkv = normal(50, (B, n_tok, 3 * H), dt)
-    qw, kw = normal(51, (d,), dt, 0.02) + 1, normal(52, (d,), dt, 0.02) + 1
+    # norm weights 1 + N(0, 0.02^2), held in the storage dtype on both sides
+    qw, kw = normal(51, (d,), C.F32, 0.02) + 1, normal(52, (d,), C.F32, 0.02) + 1
+    if dt == C.BF16:
+        qw, kw = synth.bf16_round(qw), synth.bf16_round(kw)
     QKV = dev(qkv, dt)
     Qo = torch.zeros((B, heads, n_joint, d), dtype=QKV.dtype, device="cuda")
     Ko = torch.zeros_like(Qo)
