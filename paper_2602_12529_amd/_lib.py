@@ -35,6 +35,8 @@ _SIGS = {
     "ff_sde_workspace_size": (c_int32, [c_int64, c_int64, POINTER(c_size_t)]),
     "ff_sde_step": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_double,
                               c_double, c_double, c_int32, c_void_p, c_size_t, c_void_p]),
+    "ff_sde_step_noalloc": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_double,
+                                      c_double, c_double, c_int32, c_void_p]),
     "ff_logprob": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_double, c_double,
                              c_double, c_int32, c_void_p, c_size_t, c_void_p]),
     "ff_sde_step_philox": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_double, c_double,

@@ -77,6 +77,13 @@ def logprob(x, v, x_next, logp, t: float, t_next: float, sigma: float, ws=None):
                             ws.numel(), _stream()), "ff_logprob")
 
 
+def sde_step_noalloc(x, v, eps, x_next, t: float, t_next: float, sigma: float, logp=None):
+    """ff_sde_step without a workspace: the library's own device scratch holds the partial sums."""
+    B, D = x.shape[0], x[0].numel()
+    check(load().ff_sde_step_noalloc(_p(x), _p(v), _p(eps), _p(x_next), _p(logp), B, D, t, t_next, sigma,
+                                     dtype_code(x), _stream()), "ff_sde_step_noalloc")
+
+
 def sde_step_philox(x, v, x_next, t: float, t_next: float, sigma: float, seed: int, step: int, logp=None, ws=None):
     """The SDE step with its noise drawn on the device (Philox4x32-10, Box-Muller)."""
     B, D = x.shape[0], x[0].numel()

@@ -89,6 +89,7 @@ int drain_locked() {
 
 LaunchScope::LaunchScope(const char* name, hipStream_t s, double flops, double bytes)
     : name_(name), stream_(s), flops_(flops), bytes_(bytes), slot_(-1) {
+  if (!name_) return;   // an unprofiled launch (no events, no allocation)
   std::lock_guard<std::mutex> lk(g_mu);
   if (!g_on) return;
   if (!g_filter.empty() && g_filter != name_) return;
@@ -107,7 +108,7 @@ LaunchScope::~LaunchScope() {
 
 int LaunchScope::status() {
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return fail(FF_EHIP, "launch of %s: %s", name_, hipGetErrorString(e));
+  if (e != hipSuccess) return fail(FF_EHIP, "launch of %s: %s", name_ ? name_ : "kernel", hipGetErrorString(e));
   return FF_OK;
 }
 

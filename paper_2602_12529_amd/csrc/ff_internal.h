@@ -41,6 +41,8 @@ inline size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // attribute belongs to the device; `done` is the caller's per-kernel mask of device ordinals 0..63).
 int ensure_smem_limit(const void* kernel, int bytes, std::atomic<uint64_t>& done);
 
+// Brackets a launch with profiler events while profiling is on; a null name marks a launch that
+// is never profiled (it records no events and allocates nothing).
 struct LaunchScope {
   LaunchScope(const char* name, hipStream_t s, double flops, double bytes);
   ~LaunchScope();

@@ -11,6 +11,7 @@
 // groups, lanes, waves and blocks in a fixed order, so the result is bitwise
 // reproducible and identical between ff_sde_step and ff_logprob.
 #include <cmath>
+#include <mutex>
 
 #include "dev.h"
 #include "ff_internal.h"
@@ -233,7 +234,7 @@ __global__ __launch_bounds__(256) void logp_finalize(const double* __restrict__ 
 template <int MODE>
 int launch_sde(int dtype, const void* x, const void* v, const void* third, void* x_next, double* logp,
                int64_t B, int64_t D, float a, float b, float c, double inv_2var, double cst,
-               void* ws, hipStream_t s, NoiseKey nk = {0, 0, 0}) {
+               void* ws, hipStream_t s, NoiseKey nk = {0, 0, 0}, bool profile = true) {
   RowPlan p = row_plan(B, D);
   dim3 grid(static_cast<unsigned>(p.bps), static_cast<unsigned>(B));
   double* partial = static_cast<double*>(ws);
@@ -242,7 +243,8 @@ int launch_sde(int dtype, const void* x, const void* v, const void* third, void*
   const double esz = static_cast<double>(dtype_size(dtype));
   const double bytes = static_cast<double>(B) * D * esz * (MODE == 0 ? 4.0 : 3.0);
   {
-    LaunchScope ls(MODE == 0 ? "sde_step" : (MODE == 2 ? "sde_step_philox" : "logprob"), s, 0.0, bytes);
+    LaunchScope ls(!profile ? nullptr : (MODE == 0 ? "sde_step" : (MODE == 2 ? "sde_step_philox" : "logprob")), s,
+                   0.0, bytes);
 #define FF_SDE_LAUNCH(BF, LP, VC)                                                                 \
   hipLaunchKernelGGL((sde_kernel<BF, MODE, LP, VC>), grid, dim3(kSdeThreads), 0, s, x, v, third, \
                      x_next, partial, D, p.chunk, a, b, c, nk)
@@ -257,7 +259,7 @@ int launch_sde(int dtype, const void* x, const void* v, const void* third, void*
     FF_TRY(ls.status());
   }
   if (lp) {
-    LaunchScope ls("logp_finalize", s, 0.0, static_cast<double>(B) * p.bps * 8.0);
+    LaunchScope ls(profile ? "logp_finalize" : nullptr, s, 0.0, static_cast<double>(B) * p.bps * 8.0);
     hipLaunchKernelGGL(logp_finalize, dim3(static_cast<unsigned>(B)), dim3(256), 0, s, partial, p.bps,
                        logp, inv_2var, cst);
     FF_TRY(ls.status());
@@ -317,6 +319,34 @@ Coef coefficients(double t, double t_next, double sigma, int64_t D) {
   return k;
 }
 
+// Allocation-free variant: the per-block float64 partial sums of the log-probability live in a
+// file-scope device array instead of a caller workspace.  B x blocks-per-sample never exceeds
+// max(B, 2048 + B - 1) (the row plan aims at 2048 blocks in all, one per sample at least), so
+// 65536 doubles (512 KiB per device) cover every B <= 65535.
+constexpr int64_t kScratchDoubles = 65536;
+__device__ __align__(256) double scratch[kScratchDoubles];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+double* g_scratch_dev[kMaxDevices] = {};
+
+// The current device's address of `scratch`, looked up once per device with that device current
+// (the host-side symbol is not a device address; each device holds its own copy of the array).
+int scratch_address(double** out) {
+  int dev = 0;
+  FF_CHECK_HIP(hipGetDevice(&dev), "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(FF_EUNSUPPORTED, "device ordinal %d above %d", dev, kMaxDevices - 1);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    FF_CHECK_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(FF_EHIP, "hipGetSymbolAddress(scratch) returned null");
+    g_scratch_dev[dev] = static_cast<double*>(p);
+  }
+  *out = g_scratch_dev[dev];
+  return FF_OK;
+}
+
 }  // namespace
 }  // namespace ff
 
@@ -346,6 +376,28 @@ int ff_sde_step(const void* x, const void* v, const void* eps, void* x_next, dou
   Coef k = coefficients(t, t_next, sigma, D);
   return launch_sde<0>(dtype, x, v, eps, x_next, logp, B, D, k.a, k.b, k.c, k.inv_2var, k.cst, workspace,
                        static_cast<hipStream_t>(stream));
+}
+
+int ff_sde_step_noalloc(const void* x, const void* v, const void* eps, void* x_next, double* logp, int64_t B,
+                        int64_t D, double t, double t_next, double sigma, int32_t dtype, void* stream) {
+  const char* fn = "ff_sde_step_noalloc";
+  FF_TRY(check_sde_args(fn, x, v, eps, x_next, B, D, t, t_next, sigma, dtype));
+  if (sigma == 0.0 && logp) return fail(FF_EDOMAIN, "%s: an ODE step (sigma=0) has no log-probability", fn);
+  if (B == 0 || D == 0) return FF_OK;
+  if (!x_next) return fail(FF_EINVAL, "%s: null x_next", fn);
+  if (x_next == x || x_next == v || x_next == eps) return fail(FF_EINVAL, "%s: x_next aliases an input", fn);
+  if (logp && (reinterpret_cast<uintptr_t>(logp) & 7u) != 0) return fail(FF_EINVAL, "%s: logp misaligned", fn);
+  double* partial = nullptr;
+  if (logp) {
+    const int64_t need = B * row_plan(B, D).bps;
+    if (need > kScratchDoubles)
+      return fail(FF_EUNSUPPORTED, "%s: %lld partial sums exceed the %lld-entry scratch", fn, (long long)need,
+                  (long long)kScratchDoubles);
+    FF_TRY(scratch_address(&partial));
+  }
+  Coef k = coefficients(t, t_next, sigma, D);
+  return launch_sde<0>(dtype, x, v, eps, x_next, logp, B, D, k.a, k.b, k.c, k.inv_2var, k.cst, partial,
+                       static_cast<hipStream_t>(stream), NoiseKey{0, 0, 0}, /*profile=*/false);
 }
 
 int ff_logprob(const void* x, const void* v, const void* x_next, double* logp, int64_t B, int64_t D,

@@ -68,6 +68,21 @@ def test_sde_argument_validation():
     assert lib.ff_sde_workspace_size(0, 5, byref(n)) == 0 and n.value == 0
 
 
+def test_sde_noalloc_argument_validation():
+    """The allocation-free SDE step validates like ff_sde_step, before any device call."""
+    lib = _lib.load()
+    fake = c_void_p(4096)
+    out, lp = c_void_p(16384), c_void_p(24576)
+    _err(lib.ff_sde_step_noalloc(fake, fake, fake, out, None, 2, 8, 0.5, 0.6, 1.0, 1, None), _lib.FF_EDOMAIN)
+    _err(lib.ff_sde_step_noalloc(fake, fake, fake, out, lp, 2, 8, 0.5, 0.4, 0.0, 1, None), _lib.FF_EDOMAIN)
+    _err(lib.ff_sde_step_noalloc(fake, fake, fake, out, None, 2, 8, 0.5, 0.4, 1.0, 7, None), _lib.FF_EINVAL)
+    _err(lib.ff_sde_step_noalloc(None, fake, fake, out, None, 2, 8, 0.5, 0.4, 1.0, 1, None), _lib.FF_EINVAL)
+    _err(lib.ff_sde_step_noalloc(fake, fake, fake, fake, None, 2, 8, 0.5, 0.4, 1.0, 1, None), _lib.FF_EINVAL)
+    _err(lib.ff_sde_step_noalloc(fake, fake, fake, out, c_void_p(24580), 2, 8, 0.5, 0.4, 1.0, 1, None), _lib.FF_EINVAL)
+    _err(lib.ff_sde_step_noalloc(fake, fake, fake, out, None, 70000, 8, 0.5, 0.4, 1.0, 1, None), _lib.FF_EUNSUPPORTED)
+    assert lib.ff_sde_step_noalloc(None, None, None, None, None, 0, 8, 0.5, 0.4, 1.0, 1, None) == 0
+
+
 def test_philox_argument_validation():
     lib = _lib.load()
     f = c_void_p(8192)
