@@ -28,11 +28,19 @@ enum { FF_EPI_BIAS = 0, FF_EPI_GELU = 1, FF_EPI_GATED = 2 };
  *                 adaLN-gated residual; gate float32 [*, gate_ld] or NULL for a
  *                 plain residual (gate = 1), resid [M, N] (row stride ldr) may
  *                 alias out.
- * Accumulation is float32.  bf16 requires K % 64 == 0 and lda, ldo, ldr % 8 == 0. */
+ * Accumulation is float32.  bf16 requires K % 64 == 0 and lda, ldo, ldr % 8 == 0.
+ * workspace (device, 16-byte aligned, ff_linear_workspace_size bytes) or NULL: with it, a bf16
+ * launch whose 256 x 256 tiles leave a last, partly filled round of the GPU's compute units splits
+ * that round's tiles along K (float32 partial sums in the workspace, added in a fixed order, so the
+ * result is deterministic); without it nothing is split.  The workspace holds nothing between
+ * calls; calls that overlap on one workspace race. */
 int ff_linear(const void* A, int64_t lda, const void* W, const void* bias, void* out, int64_t ldo,
               int64_t M, int64_t N, int64_t K, int32_t epi, int64_t gelu_from, const float* gate,
               int64_t gate_ld, const void* resid, int64_t ldr, int64_t rows_per_sample, int32_t dtype,
-              void* stream);
+              void* workspace, size_t ws_bytes, void* stream);
+
+/* Workspace bytes of ff_linear's split-K tail (the same for every shape). */
+int ff_linear_workspace_size(size_t* bytes);
 
 /* Attention O = softmax(Q K^T / sqrt(d)) V, no mask.
  *   Q [B, heads, n_q, d], K [B, heads, n_kv, d];

@@ -66,7 +66,9 @@ _SIGS = {
     "ff_profile_read": (c_int32, [c_int32, c_char_p, c_size_t, POINTER(c_int64), POINTER(c_double),
                                   POINTER(c_double), POINTER(c_double)]),
     "ff_linear": (c_int32, [c_void_p, c_int64, c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_int64, c_int64,
-                            c_int32, c_int64, c_void_p, c_int64, c_void_p, c_int64, c_int64, c_int32, c_void_p]),
+                            c_int32, c_int64, c_void_p, c_int64, c_void_p, c_int64, c_int64, c_int32, c_void_p,
+                            c_size_t, c_void_p]),
+    "ff_linear_workspace_size": (c_int32, [POINTER(c_size_t)]),
     "ff_attention": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_int64, c_int64,
                                c_int64, c_int32, c_void_p]),
     "ff_norm_modulate": (c_int32, [c_void_p, c_void_p, c_int64, c_int64, c_void_p, c_void_p, c_int64, c_int64,

@@ -169,12 +169,20 @@ def grpo_loss(logp_new, logp_old, adv, step_w=None, clip_eps: float = 0.2, loss=
 
 
 # ------------------------------------------------------------------ kernel-level ops
-def linear(A, W, bias, out, epi=EPI_BIAS, gelu_from=0, gate=None, gate_ld=0, resid=None, rows_per_sample=0):
+def linear_workspace_size() -> int:
+    n = c_size_t()
+    check(load().ff_linear_workspace_size(byref(n)), "ff_linear_workspace_size")
+    return n.value
+
+
+def linear(A, W, bias, out, epi=EPI_BIAS, gelu_from=0, gate=None, gate_ld=0, resid=None, rows_per_sample=0, ws=None):
+    """ws: optional workspace (linear_workspace_size bytes) that lets the last round split along K."""
     M, K = A.shape
     N = W.shape[0]
     check(load().ff_linear(_p(A), A.stride(0), _p(W), _p(bias), _p(out), out.stride(0), M, N, K, epi, gelu_from,
                            _p(gate), gate_ld, _p(resid), resid.stride(0) if resid is not None else 0,
-                           rows_per_sample, dtype_code(A), _stream()), "ff_linear")
+                           rows_per_sample, dtype_code(A), _p(ws), ws.numel() if ws is not None else 0, _stream()),
+          "ff_linear")
     return out
 
 

@@ -173,7 +173,7 @@ namespace {
 struct Plan {
   int64_t B, Ni, Nt, N, P;
   size_t rope, temb_in, c, tmp, condB, cond32, mods, ximg, xtxt, joint, y, qkv, q, k, vt, o, u, txth;
-  size_t e6, ctx1, ctxp, kvc, kc, vct, qd, total;
+  size_t e6, ctx1, ctxp, kvc, kc, vct, qd, splitk, splitk_bytes, total;
 };
 
 Plan plan(const ff_dit& m, int64_t B, const int32_t grid[3], int64_t n_txt, int64_t n_prompts) {
@@ -215,6 +215,8 @@ Plan plan(const ff_dit& m, int64_t B, const int32_t grid[3], int64_t n_txt, int6
   p.kc = take(wan ? static_cast<size_t>(B) * p.Nt * H * es : 0);
   p.vct = take(wan ? static_cast<size_t>(B) * p.Nt * H * es : 0);
   p.qd = take(wan ? static_cast<size_t>(B) * p.Nt * H * es : 0);
+  p.splitk_bytes = c.dtype == FF_BF16 ? gemm_split_bytes() : 0;
+  p.splitk = take(p.splitk_bytes);
   p.total = round_up(cv.off, 256);
   return p;
 }
@@ -234,6 +236,17 @@ GemmArgs gemm_args(int dtype, int64_t M, int64_t N, int64_t K, const void* A, in
   g.epi = epi;
   g.gelu_from = 0;
   g.rows_per_sample = M;
+  return g;
+}
+
+// The same, with the workspace's split-K scratch for the launch's last round.
+GemmArgs gemm_args_ws(const Plan& p, void* ws, int dtype, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
+                      Lin l, void* out, int64_t ldo, int epi) {
+  GemmArgs g = gemm_args(dtype, M, N, K, A, lda, l, out, ldo, epi);
+  if (p.splitk_bytes > 0 && dtype == FF_BF16) {
+    g.split_ws = at(ws, p.splitk);
+    g.split_bytes = p.splitk_bytes;
+  }
   return g;
 }
 
@@ -332,14 +345,14 @@ int dual_block(const ff_dit& m, const Plan& p, void* ws, int i, const float* c32
   GemmArgs gq[2];
   for (int k = 0; k < 2; ++k) {
     qa[k] = qkv_args(c, p, ws, qkv_k[k], 3 * H, ntok[k], 0, ntok[k], k == 0 ? 0 : p.Nt, st[k]->qn, st[k]->kn, k == 1);
-    gq[k] = gemm_args(c.dtype, rows[k], 3 * H, H, Y + y_off[k] * es, H, st[k]->qkv, qkv_k[k], 3 * H, EPI_QKV);
+    gq[k] = gemm_args_ws(p, ws, c.dtype, rows[k], 3 * H, H, Y + y_off[k] * es, H, st[k]->qkv, qkv_k[k], 3 * H, EPI_QKV);
     gq[k].qkv = &qa[k];
   }
   FF_TRY(gemm2(gq[0], gq[1], s));
   FF_TRY(attention_joint(c, p, ws, O, O + p.B * p.Nt * H * es, s));
   GemmArgs go[2], g1[2], g2[2];
   for (int k = 0; k < 2; ++k) {
-    go[k] = gemm_args(c.dtype, rows[k], H, H, O + y_off[k] * es, H, st[k]->o, dst[k], H, EPI_GATED);
+    go[k] = gemm_args_ws(p, ws, c.dtype, rows[k], H, H, O + y_off[k] * es, H, st[k]->o, dst[k], H, EPI_GATED);
     go[k].gate = mods[k] + 2 * H; go[k].gate_ld = 6 * H;
     go[k].resid = cur[k]; go[k].ldr = H;
     go[k].rows_per_sample = ntok[k];
@@ -347,8 +360,8 @@ int dual_block(const ff_dit& m, const Plan& p, void* ws, int i, const float* c32
   FF_TRY(gemm2(go[0], go[1], s));
   for (int k = 0; k < 2; ++k) {
     FF_TRY(norm_modulate(norm_args(c, rows[k], dst[k], Y + y_off[k] * es, mods[k] + 3 * H, mods[k] + 4 * H, 6 * H, ntok[k]), s));
-    g1[k] = gemm_args(c.dtype, rows[k], F, H, Y + y_off[k] * es, H, st[k]->mlp1, U[k], F, EPI_GELU);
-    g2[k] = gemm_args(c.dtype, rows[k], H, F, U[k], F, st[k]->mlp2, dst[k], H, EPI_GATED);
+    g1[k] = gemm_args_ws(p, ws, c.dtype, rows[k], F, H, Y + y_off[k] * es, H, st[k]->mlp1, U[k], F, EPI_GELU);
+    g2[k] = gemm_args_ws(p, ws, c.dtype, rows[k], H, F, U[k], F, st[k]->mlp2, dst[k], H, EPI_GATED);
     g2[k].gate = mods[k] + 5 * H; g2[k].gate_ld = 6 * H;
     g2[k].resid = dst[k]; g2[k].ldr = H;
     g2[k].rows_per_sample = ntok[k];
@@ -375,7 +388,7 @@ int single_block(const ff_dit& m, const Plan& p, void* ws, int j, const float* c
   // (text tokens unrotated, image tokens rotated by their grid position), GELU from column 3H.
   QkvArgs qa = qkv_args(c, p, ws, H1, W1, p.N, 0, p.N, 0, sb.qn, sb.kn, true);
   qa.rope_from = p.Nt;
-  GemmArgs g1 = gemm_args(c.dtype, rows, W1, H, Y, H, sb.lin1, H1, W1, EPI_QKV);
+  GemmArgs g1 = gemm_args_ws(p, ws, c.dtype, rows, W1, H, Y, H, sb.lin1, H1, W1, EPI_QKV);
   g1.gelu_from = 3 * H;
   g1.qkv = &qa;
   FF_TRY(gemm(g1, s));
@@ -387,7 +400,7 @@ int single_block(const ff_dit& m, const Plan& p, void* ws, int j, const float* c
   a.out0 = O; a.out1 = O; a.split = p.N; a.ldo = H;
   a.scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(c.head_dim)));
   FF_TRY(attention(a, s));
-  GemmArgs g2 = gemm_args(c.dtype, rows, H, H + F, O, H, sb.lin2, X, H, EPI_GATED);
+  GemmArgs g2 = gemm_args_ws(p, ws, c.dtype, rows, H, H + F, O, H, sb.lin2, X, H, EPI_GATED);
   g2.K1 = H;
   g2.A2 = H1 + 3 * H * es; g2.lda2 = W1;
   g2.gate = mods + 2 * H; g2.gate_ld = 3 * H;
@@ -449,7 +462,7 @@ int wan_block(const ff_dit& m, const Plan& p, void* ws, int i, const void* ctx, 
   FF_TRY(add_table(wb.mod, c.dtype, e6, mods, p.B, 6 * H, s));
   // self-attention
   FF_TRY(norm_modulate(norm_args(c, rows, X, Y, mods, mods + H, 6 * H, p.Ni), s));
-  FF_TRY(gemm(gemm_args(c.dtype, rows, 3 * H, H, Y, H, wb.qkv, QKV, 3 * H, EPI_NONE), s));
+  FF_TRY(gemm(gemm_args_ws(p, ws, c.dtype, rows, 3 * H, H, Y, H, wb.qkv, QKV, 3 * H, EPI_NONE), s));
   FF_TRY(rms_rows(c, QKV, rows, 3 * H, wb.qn, s));
   FF_TRY(rms_rows(c, QKV + H * es, rows, 3 * H, wb.kn, s));
   FF_TRY(relayout(c, p, QKV, QKV + H * es, QKV + 2 * H * es, 3 * H, p.Ni,
@@ -464,7 +477,7 @@ int wan_block(const ff_dit& m, const Plan& p, void* ws, int i, const void* ctx, 
     a.scale = scale;
     FF_TRY(attention(a, s));
   }
-  GemmArgs go = gemm_args(c.dtype, rows, H, H, O, H, wb.o, X, H, EPI_GATED);
+  GemmArgs go = gemm_args_ws(p, ws, c.dtype, rows, H, H, O, H, wb.o, X, H, EPI_GATED);
   go.gate = mods + 2 * H; go.gate_ld = 6 * H; go.resid = X; go.ldr = H; go.rows_per_sample = p.Ni;
   FF_TRY(gemm(go, s));
   // cross-attention to the text context (K/V from ctx; Q read token-major)
@@ -474,7 +487,7 @@ int wan_block(const ff_dit& m, const Plan& p, void* ws, int i, const void* ctx, 
     na.w = wb.can_w; na.bias = wb.can_b;
     FF_TRY(norm_modulate(na, s));
   }
-  FF_TRY(gemm(gemm_args(c.dtype, rows, H, H, Y, H, wb.cq, QKV, H, EPI_NONE), s));
+  FF_TRY(gemm(gemm_args_ws(p, ws, c.dtype, rows, H, H, Y, H, wb.cq, QKV, H, EPI_NONE), s));
   FF_TRY(rms_rows(c, QKV, rows, H, wb.cqn, s));
   if (!ctx_k) {
     FF_TRY(wan_cross_kv(m, p, ws, i, ctx, at(ws, p.kc), at(ws, p.vct), s));
@@ -492,14 +505,14 @@ int wan_block(const ff_dit& m, const Plan& p, void* ws, int i, const void* ctx, 
     a.scale = scale;
     FF_TRY(attention(a, s));
   }
-  GemmArgs gc = gemm_args(c.dtype, rows, H, H, O, H, wb.co, X, H, EPI_GATED);
+  GemmArgs gc = gemm_args_ws(p, ws, c.dtype, rows, H, H, O, H, wb.co, X, H, EPI_GATED);
   gc.gate = nullptr; gc.resid = X; gc.ldr = H; gc.rows_per_sample = p.Ni;
   FF_TRY(gemm(gc, s));
   // FFN
   FF_TRY(norm_modulate(norm_args(c, rows, X, Y, mods + 3 * H, mods + 4 * H, 6 * H, p.Ni), s));
   char* U = at(ws, p.u);
-  FF_TRY(gemm(gemm_args(c.dtype, rows, F, H, Y, H, wb.ffn1, U, F, EPI_GELU), s));
-  GemmArgs g2 = gemm_args(c.dtype, rows, H, F, U, F, wb.ffn2, X, H, EPI_GATED);
+  FF_TRY(gemm(gemm_args_ws(p, ws, c.dtype, rows, F, H, Y, H, wb.ffn1, U, F, EPI_GELU), s));
+  GemmArgs g2 = gemm_args_ws(p, ws, c.dtype, rows, H, F, U, F, wb.ffn2, X, H, EPI_GATED);
   g2.gate = mods + 5 * H; g2.gate_ld = 6 * H; g2.resid = X; g2.ldr = H; g2.rows_per_sample = p.Ni;
   return gemm(g2, s);
 }
@@ -511,7 +524,7 @@ int wan_cross_kv(const ff_dit& m, const Plan& p, void* ws, int i, const void* ct
   const Wan& wb = m.wan[i];
   const int64_t crow = p.B * p.Nt;
   char* KV = at(ws, p.kvc);
-  FF_TRY(gemm(gemm_args(c.dtype, crow, 2 * H, H, ctx, H, wb.ckv, KV, 2 * H, EPI_NONE), s));
+  FF_TRY(gemm(gemm_args_ws(p, ws, c.dtype, crow, 2 * H, H, ctx, H, wb.ckv, KV, 2 * H, EPI_NONE), s));
   FF_TRY(rms_rows(c, KV, crow, 2 * H, wb.ckn, s));
   return relayout(c, p, KV, KV, KV + H * es, 2 * H, p.Nt, nullptr, at(ws, p.qd), K, Vt, s);
 }
@@ -528,8 +541,8 @@ int wan_text_context(const ff_dit& m, const Plan& p, const void* txt, const int3
   const int64_t H = c.hidden;
   char* c1 = at(ws, p.ctx1);
   char* cp = at(ws, p.ctxp);
-  FF_TRY(gemm(gemm_args(c.dtype, p.P * p.Nt, H, c.txt_dim, txt, c.txt_dim, m.txt1, c1, H, EPI_GELU), s));
-  FF_TRY(gemm(gemm_args(c.dtype, p.P * p.Nt, H, H, c1, H, m.txt2, cp, H, EPI_NONE), s));
+  FF_TRY(gemm(gemm_args_ws(p, ws, c.dtype, p.P * p.Nt, H, c.txt_dim, txt, c.txt_dim, m.txt1, c1, H, EPI_GELU), s));
+  FF_TRY(gemm(gemm_args_ws(p, ws, c.dtype, p.P * p.Nt, H, H, c1, H, m.txt2, cp, H, EPI_NONE), s));
   return gather_rows(c.dtype, cp, txt_index, p.P, at(ws, p.xtxt), p.B, p.Nt, H, s);
 }
 
@@ -549,7 +562,7 @@ int forward_wan(const ff_dit& m, const Plan& p, const void* x, const void* txt, 
   char* ctx = at(ws, p.xtxt);
   if (!store) FF_TRY(wan_text_context(m, p, txt, txt_index, ws, s));
   char* X = at(ws, p.ximg);
-  FF_TRY(gemm(gemm_args(c.dtype, p.B * p.Ni, H, c.in_channels, x, c.in_channels, m.x_in, X, H, EPI_NONE), s));
+  FF_TRY(gemm(gemm_args_ws(p, ws, c.dtype, p.B * p.Ni, H, c.in_channels, x, c.in_channels, m.x_in, X, H, EPI_NONE), s));
   const size_t kvb = wan_kv_block_bytes(c, p.B, p.Nt);
   for (int i = 0; i < c.n_wan; ++i) {
     const char* k = store ? store + 2 * i * kvb : nullptr;
@@ -559,7 +572,7 @@ int forward_wan(const ff_dit& m, const Plan& p, const void* x, const void* txt, 
   FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 2 * H, H, temb, ACT_SILU, m.final_mod, mods), s));
   char* Y = at(ws, p.y);
   FF_TRY(norm_modulate(norm_args(c, p.B * p.Ni, X, Y, mods, mods + H, 2 * H, p.Ni), s));
-  return gemm(gemm_args(c.dtype, p.B * p.Ni, c.in_channels, H, Y, H, m.final_proj, v_out, c.in_channels, EPI_NONE), s);
+  return gemm(gemm_args_ws(p, ws, c.dtype, p.B * p.Ni, c.in_channels, H, Y, H, m.final_proj, v_out, c.in_channels, EPI_NONE), s);
 }
 
 int forward_mmdit(const ff_dit& m, const Plan& p, const void* x, const void* txt, const int32_t* txt_index,
@@ -588,9 +601,9 @@ int forward_mmdit(const ff_dit& m, const Plan& p, const void* x, const void* txt
       FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, H, H, tmp, ACT_SILU, m.pooled2, c32, 1), s));
     }
     char* ximg = at(ws, p.ximg);
-    FF_TRY(gemm(gemm_args(c.dtype, p.B * p.Ni, H, c.in_channels, x, c.in_channels, m.x_in, ximg, H, EPI_NONE), s));
+    FF_TRY(gemm(gemm_args_ws(p, ws, c.dtype, p.B * p.Ni, H, c.in_channels, x, c.in_channels, m.x_in, ximg, H, EPI_NONE), s));
     char* txth = at(ws, p.txth);
-    FF_TRY(gemm(gemm_args(c.dtype, p.P * p.Nt, H, c.txt_dim, txt, c.txt_dim, m.txt_in, txth, H, EPI_NONE), s));
+    FF_TRY(gemm(gemm_args_ws(p, ws, c.dtype, p.P * p.Nt, H, c.txt_dim, txt, c.txt_dim, m.txt_in, txth, H, EPI_NONE), s));
     FF_TRY(gather_rows(c.dtype, txth, txt_index, p.P, at(ws, p.xtxt), p.B, p.Nt, H, s));
     cur[0] = at(ws, p.xtxt);
     cur[1] = ximg;
@@ -632,7 +645,7 @@ int forward_mmdit(const ff_dit& m, const Plan& p, const void* x, const void* txt
     FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 2 * H, H, c32, ACT_SILU, m.final_mod, mods), s));
     char* Y = at(ws, p.y);
     FF_TRY(norm_modulate(norm_args(c, p.B * p.Ni, cur[1], Y, mods, mods + H, 2 * H, p.Ni), s));
-    FF_TRY(gemm(gemm_args(c.dtype, p.B * p.Ni, c.in_channels, H, Y, H, m.final_proj, v_out, c.in_channels, EPI_NONE), s));
+    FF_TRY(gemm(gemm_args_ws(p, ws, c.dtype, p.B * p.Ni, c.in_channels, H, Y, H, m.final_proj, v_out, c.in_channels, EPI_NONE), s));
   }
   return FF_OK;
 }

@@ -107,7 +107,13 @@ struct GemmArgs {
   int64_t rows_per_sample;
   const QkvArgs* qkv = nullptr;         // EPI_QKV: where Q, K and V^T go (out still names the packed
                                         // [Q | K | V] buffer, used when the fused path does not apply)
+  // Scratch for split-K partial sums of a launch's last round (null: never split); see
+  // gemm_split_bytes.  Launches on one stream may share it (each finishes before the next starts).
+  void* split_ws = nullptr;
+  size_t split_bytes = 0;
 };
+// Scratch bytes that let any launch split its last round: 255 tile partials of 256 KB and flags.
+size_t gemm_split_bytes();
 int gemm(const GemmArgs& a, hipStream_t s);
 // Two GEMMs with the same epilogue kind, launched together when both are large bf16 problems.
 int gemm2(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s);

@@ -102,9 +102,20 @@ __device__ __forceinline__ void tile_coords(int64_t pid, int64_t num_m, int64_t 
 
 // Up to two GEMM problems with the same tile kernel in one launch (the text and
 // image streams of a dual-stream block): tiles [0, tiles0) belong to p[0].
+//
+// Split-K tail: when the tile count leaves a last round that fills only part of the GPU, the
+// tiles from split_from on are each split into `parts` K ranges (work units split_from + S t + j,
+// j = 0 .. S - 1).  Units j < S - 1 write their float32 partial sums to `partial` and publish them
+// by storing `epoch` into their flag; unit S - 1, which is dispatched after them, waits for the
+// flags, adds the partial sums and runs the epilogue.  split_from == tiles: no split.
 struct GemmBatch {
   GemmParams p[2];
   int64_t tiles0, tiles;
+  int64_t split_from;
+  int parts;
+  float4* partial;           // [split tiles][parts - 1][32 float4][512 threads]
+  uint64_t* flags;           // [split tiles][parts - 1]
+  uint64_t epoch;
 };
 
 constexpr int BK = 64;
@@ -671,7 +682,14 @@ __device__ __forceinline__ void pp_body(const GemmBatch& batch) {
   // Plain launch order (consecutive tiles on different XCDs) walking 16 tile rows at a time:
   // measured faster than giving each XCD a contiguous range, or 4, 8 or 32 rows, on the DiT's
   // shapes; XCD blocks where the tile columns come in sixteens.
-  const int64_t lid = blockIdx.x;
+  const int64_t unit = blockIdx.x;
+  int part = 0, parts = 1;
+  int64_t lid = unit;
+  if (unit >= batch.split_from) {
+    parts = batch.parts;
+    lid = batch.split_from + (unit - batch.split_from) / parts;
+    part = static_cast<int>((unit - batch.split_from) % parts);
+  }
   const int which = lid >= batch.tiles0 ? 1 : 0;
   const GemmParams& p = batch.p[which];
   const int64_t num_m = (p.M + BM - 1) / BM, num_n = (p.N + BN - 1) / BN;
@@ -685,7 +703,10 @@ __device__ __forceinline__ void pp_body(const GemmBatch& batch) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave >> 2, w4 = wave & 3;
   const int wm = LAYOUT == 0 ? w4 >> 1 : w4, wn = LAYOUT == 0 ? grp * 2 + (w4 & 1) : grp;
-  const int KT = static_cast<int>(p.K / KS), KT1 = static_cast<int>(p.K1 / KS);
+  // This unit's slabs: [s_begin, s_begin + KT) of the tile's p.K / KS (all of them when unsplit).
+  const int KT_all = static_cast<int>(p.K / KS), KT1 = static_cast<int>(p.K1 / KS);
+  const int s_begin = part * KT_all / parts;
+  const int KT = (part + 1) * KT_all / parts - s_begin;
 
   // Load q of a wave fills LDS rows 32 q + 8 w4 .. + 7 of its matrix; lane l lands at
   // row + l / 8, stored chunk l % 8, so it fetches logical chunk (l % 8) ^ ((row >> 1) & 7),
@@ -695,7 +716,7 @@ __device__ __forceinline__ void pp_body(const GemmBatch& batch) {
   const int64_t rows_a = p.M - m0, rows_b = p.N - n0;
   // A may come from two sources (the two-part K of the fused single-stream projection):
   // slabs [0, KT1) from A1, the rest from A2.
-  const bool two = KT1 > 0 && KT1 < KT;
+  const bool two = KT1 > 0 && KT1 < KT_all;
   const char* a1_tile = static_cast<const char*>(p.A1) + m0 * p.lda1 * ES;
   const char* a2_tile = static_cast<const char*>(p.A2) + m0 * p.lda2 * ES;
   const int64_t a1_bytes = rows_a * p.lda1 * ES, a2_bytes = rows_a * p.lda2 * ES;
@@ -707,13 +728,14 @@ __device__ __forceinline__ void pp_body(const GemmBatch& batch) {
   const uint32_t b_off = static_cast<uint32_t>(lrow * p.ldw * ES + lck * 16);
   const uint32_t b_step = static_cast<uint32_t>(32 * p.ldw * ES);
   const uint32_t smem_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
-  auto rsrc_b = [&](int s) {
-    const int64_t db = static_cast<int64_t>(s) * ROWB;
+  auto rsrc_b = [&](int s) {   // s counts this unit's slabs
+    const int64_t db = static_cast<int64_t>(s_begin + s) * ROWB;
     return buffer_rsrc(b_tile + db, static_cast<uint64_t>(b_bytes - db));
   };
-  auto issue_a = [&](int s, int dst) {   // slab s's A rows into the buffer of slab dst
-    const bool second = two && s >= KT1;
-    const int64_t da = static_cast<int64_t>(second ? s - KT1 : s) * ROWB;
+  auto issue_a = [&](int s, int dst) {   // this unit's slab s's A rows into the buffer of its slab dst
+    const int sa = s_begin + s;
+    const bool second = two && sa >= KT1;
+    const int64_t da = static_cast<int64_t>(second ? sa - KT1 : sa) * ROWB;
     const u32x4_t r = buffer_rsrc((second ? a2_tile : a1_tile) + da, static_cast<uint64_t>((second ? a2_bytes : a1_bytes) - da));
     const uint32_t off = second ? a2_off : a1_off, step = second ? a2_step : a1_step;
     const uint32_t lds = smem_base + (dst & 1) * STAGE + w4 * 1024;
@@ -870,6 +892,55 @@ __device__ __forceinline__ void pp_body(const GemmBatch& batch) {
     compute(nullptr, 0);
     __builtin_amdgcn_sched_barrier(0);
   }
+  if (parts > 1) {
+    // Split tile: float4 q of thread tid's accumulators is (block q / 4 of the wave's FM x FN grid,
+    // elements 4 (q % 4) ..); partial block b holds it at [q][tid], so each store and load of a
+    // wave covers 1 KB contiguously.
+    constexpr int NQ = FM * FN * 4;
+    const int64_t st = lid - batch.split_from;
+    uint64_t* flag = batch.flags + st * (parts - 1);
+    float4* blocks = batch.partial + st * (parts - 1) * (NQ * 512);
+    if (part < parts - 1) {
+      float4* dst = blocks + static_cast<int64_t>(part) * (NQ * 512) + tid;
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const f32x16_t& a = acc[(q >> 2) / FN][(q >> 2) % FN];
+        dst[q * 512] = make_float4(a[4 * (q & 3)], a[4 * (q & 3) + 1], a[4 * (q & 3) + 2], a[4 * (q & 3) + 3]);
+      }
+      // Every thread's stores have reached the XCD's L2; one release by thread 0 then writes the L2
+      // back and publishes the flag (a fence per wave would write it back eight times).
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+      if (tid == 0) __hip_atomic_store(flag + part, batch.epoch, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+      return;
+    }
+    // The last part: wait for the others (they have lower unit ids, so they were dispatched
+    // first; the spin is bounded so a wave always finishes), then add their sums in part order.
+    // The polls are relaxed loads (an acquire per poll would invalidate the XCD's L2 under the
+    // tiles still computing there); one acquire after the last poll orders the partial loads.
+    if (tid < parts - 1) {
+      for (int spin = 0; spin < (1 << 22); ++spin) {
+        if (__hip_atomic_load(flag + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == batch.epoch) break;
+        __builtin_amdgcn_s_sleep(2);
+      }
+    }
+    if (tid < 64) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    __syncthreads();
+    for (int j = 0; j < parts - 1; ++j) {
+      const float4* src = blocks + static_cast<int64_t>(j) * (NQ * 512) + tid;
+      // four loads in flight at a time: all of them at once would not fit beside the accumulators
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const float4 v = src[q * 512];
+        f32x16_t& a = acc[(q >> 2) / FN][(q >> 2) % FN];
+        a[4 * (q & 3)] += v.x;
+        a[4 * (q & 3) + 1] += v.y;
+        a[4 * (q & 3) + 2] += v.z;
+        a[4 * (q & 3) + 3] += v.w;
+        if ((q & 3) == 3) __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  }
   if constexpr (EPI == EPI_QKV) {
     epilogue_qkv<FM, FN>(p, acc, m0 + wm * TM, n0 + wn * TN, smem + wave * QKV_SCRATCH, lane);
   } else if constexpr (EPI == EPI_QKV_GELU) {
@@ -959,16 +1030,69 @@ int launch_bf16(const GemmParams& p, hipStream_t s, const char* name, double flo
   return ls.status();
 }
 
+// Compute units of the current device (one 256 x 256 tile runs per CU at a time).
+int device_cus(int* out) {
+  static std::atomic<int> cus[64] = {};
+  int dev = 0;
+  FF_CHECK_HIP(hipGetDevice(&dev), "hipGetDevice");
+  if (dev < 0 || dev >= 64) return fail(FF_EUNSUPPORTED, "device ordinal %d above 63", dev);
+  int n = cus[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
+    FF_CHECK_HIP(hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev), "CU count");
+    cus[dev].store(n, std::memory_order_relaxed);
+  }
+  *out = n;
+  return FF_OK;
+}
+
+// Split-K plan of a launch: the tiles of a last, partly filled round are split into S K ranges
+// so that the round's work units fill the CUs, S = min(CUs / tail, slabs / 8, 8), when the
+// workspace holds the partial sums, both problems have the same number of slabs and K has at
+// least 96 slabs.  Measured on the DiT's shapes with 1632 tiles (6.375 rounds): the K = 12288
+// projection gains 3.5%; at K = 3072 half a tile is too short for the fixup (partial sums through
+// memory, an L2 write-back) to pay, and those launches were 0-1.5% slower, so they are not split.
+constexpr int kSplitMinSlabs = 8, kSplitMaxParts = 8, kSplitMinK = 96;
+constexpr size_t kSplitBlockBytes = 512 * 128 * 4;   // one tile's partial sums (512 threads x 128 floats)
+std::atomic<uint64_t> g_split_epoch{0x5EED000000000000ull};
+
+void plan_split(GemmBatch& b, int cus, void* ws, size_t ws_bytes, int slab_k) {
+  b.split_from = b.tiles;
+  b.parts = 1;
+  const int64_t tail = cus > 0 ? b.tiles % cus : 0;
+  if (!ws || tail == 0 || b.p[0].K != b.p[1].K || b.tiles < cus) return;
+  const int64_t slabs = b.p[0].K / slab_k;
+  if (slabs < kSplitMinK) return;
+  int64_t S = cus / tail;
+  if (S > slabs / kSplitMinSlabs) S = slabs / kSplitMinSlabs;
+  if (S > kSplitMaxParts) S = kSplitMaxParts;
+  if (S < 2) return;
+  const size_t n_blocks = static_cast<size_t>(tail) * (S - 1);
+  const size_t flag_bytes = round_up(n_blocks * sizeof(uint64_t), 256);
+  if (flag_bytes + n_blocks * kSplitBlockBytes > ws_bytes) return;
+  b.split_from = b.tiles - tail;
+  b.parts = static_cast<int>(S);
+  b.flags = static_cast<uint64_t*>(ws);
+  b.partial = reinterpret_cast<float4*>(static_cast<char*>(ws) + flag_bytes);
+  b.epoch = g_split_epoch.fetch_add(1, std::memory_order_relaxed) + 1;
+}
+
+int64_t split_units(const GemmBatch& b) { return b.split_from + (b.tiles - b.split_from) * b.parts; }
+
 template <int EPI>
-int launch_pp_batch(const GemmBatch& b, hipStream_t s, const char* name, double flops, double bytes) {
+int launch_pp_batch(const GemmBatch& b0, hipStream_t s, const char* name, double flops, double bytes, void* ws = nullptr,
+                    size_t ws_bytes = 0) {
   constexpr bool qkv = EPI == EPI_QKV || EPI == EPI_QKV_GELU;
   constexpr int LAYOUT = qkv ? 1 : 0;
   constexpr int ring = 2 * 512 * 64 * 2;
   constexpr int smem = qkv && 8 * QKV_SCRATCH > ring ? 8 * QKV_SCRATCH : ring;
   static std::atomic<uint64_t> limit_set{0};
   FF_TRY(ensure_smem_limit(reinterpret_cast<const void*>(&gemm_bf16_pp<EPI, LAYOUT>), smem, limit_set));
+  GemmBatch b = b0;
+  int cus = 0;
+  FF_TRY(device_cus(&cus));
+  plan_split(b, cus, ws, ws_bytes, BK);
   LaunchScope ls(name, s, flops, bytes);
-  hipLaunchKernelGGL((gemm_bf16_pp<EPI, LAYOUT>), dim3(static_cast<unsigned>(b.tiles)), dim3(512), smem, s, b);
+  hipLaunchKernelGGL((gemm_bf16_pp<EPI, LAYOUT>), dim3(static_cast<unsigned>(split_units(b))), dim3(512), smem, s, b);
   return ls.status();
 }
 
@@ -983,6 +1107,8 @@ int launch_fp8(const GemmParams& p, hipStream_t s, const char* name, double flop
   b.p[0] = p;
   b.p[1] = p;
   b.tiles0 = b.tiles = tiles256(p);
+  b.split_from = b.tiles;   // no split-K
+  b.parts = 1;
   LaunchScope ls(name, s, flops, bytes);
   hipLaunchKernelGGL((gemm_fp8_pp<EPI>), dim3(static_cast<unsigned>(b.tiles)), dim3(512), smem, s, b);
   return ls.status();
@@ -994,13 +1120,13 @@ const char* const kGemmNames[5] = {"gemm_bf16", "gemm_bf16_gelu", "gemm_bf16_gat
 // Problems with at least one 256 x 256 tile per CU take the 256 x 256 kernel;
 // smaller ones the 128 x 128 tile, which fills more CUs.
 template <int EPI>
-int dispatch_bf16(const GemmParams& p, hipStream_t s, double flops, double bytes) {
+int dispatch_bf16(const GemmParams& p, hipStream_t s, double flops, double bytes, void* ws, size_t ws_bytes) {
   if (tiles256(p) >= 256) {
     GemmBatch b{};
     b.p[0] = p;
     b.p[1] = p;
     b.tiles0 = b.tiles = tiles256(p);
-    return launch_pp_batch<EPI>(b, s, kGemmNames[EPI], flops, bytes);
+    return launch_pp_batch<EPI>(b, s, kGemmNames[EPI], flops, bytes, ws, ws_bytes);
   }
   return launch_bf16<128, 128, 2, 2, EPI>(p, s, kGemmNames[EPI], flops, bytes);
 }
@@ -1055,6 +1181,11 @@ double gemm_bytes(const GemmArgs& a) {
 }
 }  // namespace
 
+size_t gemm_split_bytes() {
+  constexpr size_t max_blocks = 255;   // tail x (S - 1) < 256 CUs
+  return round_up(max_blocks * sizeof(uint64_t), 256) + max_blocks * kSplitBlockBytes;
+}
+
 int gemm(const GemmArgs& a, hipStream_t s) {
   if (a.M == 0 || a.N == 0) return FF_OK;
   if (a.epi == EPI_QKV) {
@@ -1065,8 +1196,11 @@ int gemm(const GemmArgs& a, hipStream_t s) {
       b.p[0] = p;
       b.p[1] = p;
       b.tiles0 = b.tiles = tiles256(p);
-      if (tail) return launch_pp_batch<EPI_QKV_GELU>(b, s, kGemmNames[EPI_QKV_GELU], gemm_flops(a), gemm_bytes(a));
-      return launch_pp_batch<EPI_QKV>(b, s, kGemmNames[EPI_QKV], gemm_flops(a), gemm_bytes(a));
+      if (tail)
+        return launch_pp_batch<EPI_QKV_GELU>(b, s, kGemmNames[EPI_QKV_GELU], gemm_flops(a), gemm_bytes(a), a.split_ws,
+                                             a.split_bytes);
+      return launch_pp_batch<EPI_QKV>(b, s, kGemmNames[EPI_QKV], gemm_flops(a), gemm_bytes(a), a.split_ws,
+                                      a.split_bytes);
     }
     GemmArgs plain = a;   // two passes: the packed projection, then the norm / rotation / relayout
     plain.epi = tail ? EPI_GELU : EPI_NONE;
@@ -1081,9 +1215,9 @@ int gemm(const GemmArgs& a, hipStream_t s) {
       return fail(FF_EUNSUPPORTED, "gemm: bf16 K=%lld (K1=%lld) must be a multiple of %d", (long long)a.K,
                   (long long)a.K1, BK);
     switch (a.epi) {
-      case EPI_NONE: return dispatch_bf16<EPI_NONE>(p, s, flops, bytes);
-      case EPI_GELU: return dispatch_bf16<EPI_GELU>(p, s, flops, bytes);
-      default: return dispatch_bf16<EPI_GATED>(p, s, flops, bytes);
+      case EPI_NONE: return dispatch_bf16<EPI_NONE>(p, s, flops, bytes, a.split_ws, a.split_bytes);
+      case EPI_GELU: return dispatch_bf16<EPI_GELU>(p, s, flops, bytes, a.split_ws, a.split_bytes);
+      default: return dispatch_bf16<EPI_GATED>(p, s, flops, bytes, a.split_ws, a.split_bytes);
     }
   }
   switch (a.epi) {
@@ -1127,7 +1261,7 @@ int gemm2(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
     if (a0.epi == EPI_QKV && a1.epi == EPI_QKV && qkv_fusable(a0) && qkv_fusable(a1) && a0.K % BK == 0 &&
         a1.K % BK == 0 && b.tiles >= 256)
       return launch_pp_batch<EPI_QKV>(b, s, kGemmNames[EPI_QKV], gemm_flops(a0) + gemm_flops(a1),
-                                      gemm_bytes(a0) + gemm_bytes(a1));
+                                      gemm_bytes(a0) + gemm_bytes(a1), a0.split_ws, a0.split_bytes);
     GemmArgs p0 = a0, p1 = a1;   // two passes for both streams
     if (p0.epi == EPI_QKV) { p0.epi = EPI_NONE; p0.qkv = nullptr; }
     if (p1.epi == EPI_QKV) { p1.epi = EPI_NONE; p1.qkv = nullptr; }
@@ -1154,9 +1288,9 @@ int gemm2(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
   }
   const double flops = gemm_flops(a0) + gemm_flops(a1), bytes = gemm_bytes(a0) + gemm_bytes(a1);
   switch (a0.epi) {
-    case EPI_NONE: return launch_pp_batch<EPI_NONE>(b, s, kGemmNames[EPI_NONE], flops, bytes);
-    case EPI_GELU: return launch_pp_batch<EPI_GELU>(b, s, kGemmNames[EPI_GELU], flops, bytes);
-    default: return launch_pp_batch<EPI_GATED>(b, s, kGemmNames[EPI_GATED], flops, bytes);
+    case EPI_NONE: return launch_pp_batch<EPI_NONE>(b, s, kGemmNames[EPI_NONE], flops, bytes, a0.split_ws, a0.split_bytes);
+    case EPI_GELU: return launch_pp_batch<EPI_GELU>(b, s, kGemmNames[EPI_GELU], flops, bytes, a0.split_ws, a0.split_bytes);
+    default: return launch_pp_batch<EPI_GATED>(b, s, kGemmNames[EPI_GATED], flops, bytes, a0.split_ws, a0.split_bytes);
   }
 }
 

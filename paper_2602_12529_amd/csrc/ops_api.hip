@@ -17,7 +17,8 @@ extern "C" {
 
 int ff_linear(const void* A, int64_t lda, const void* W, const void* bias, void* out, int64_t ldo, int64_t M,
               int64_t N, int64_t K, int32_t epi, int64_t gelu_from, const float* gate, int64_t gate_ld,
-              const void* resid, int64_t ldr, int64_t rows_per_sample, int32_t dtype, void* stream) {
+              const void* resid, int64_t ldr, int64_t rows_per_sample, int32_t dtype, void* workspace,
+              size_t ws_bytes, void* stream) {
   const char* fn = "ff_linear";
   FF_TRY(check_dtype(fn, dtype));
   if (M < 0 || N < 0 || K < 1) return fail(FF_EINVAL, "%s: bad shape M=%lld N=%lld K=%lld", fn, (long long)M, (long long)N, (long long)K);
@@ -43,7 +44,18 @@ int ff_linear(const void* A, int64_t lda, const void* W, const void* bias, void*
   g.epi = epi; g.gelu_from = gelu_from;
   g.gate = gate; g.gate_ld = gate_ld; g.resid = resid; g.ldr = ldr;
   g.rows_per_sample = rows_per_sample > 0 ? rows_per_sample : M;
+  if (workspace) {
+    if (!aligned16(workspace)) return fail(FF_EINVAL, "%s: workspace must be 16-byte aligned", fn);
+    g.split_ws = workspace;
+    g.split_bytes = ws_bytes;
+  }
   return gemm(g, static_cast<hipStream_t>(stream));
+}
+
+int ff_linear_workspace_size(size_t* bytes) {
+  if (!bytes) return fail(FF_EINVAL, "ff_linear_workspace_size: null output");
+  *bytes = gemm_split_bytes();
+  return FF_OK;
 }
 
 int ff_attention(const void* Q, const void* K, const void* V, void* out, int64_t B, int64_t heads, int64_t n_q,

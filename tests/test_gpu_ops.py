@@ -66,6 +66,49 @@ def test_linear_parity(gpu_lib, M, N, K, dt, epi):
     check(host(out), ref, dt, 0, K, what=f"linear {M}x{N}x{K} {epi}", norm_tol=2e-6 if dt == C.F32 else 6e-3)
 
 
+# 256 x 256 tiles leaving a partly filled last round on 256 CUs, K of at least 96 slabs of 64:
+# (17 x 16 = 272 tiles, tail 16, split in 8), (17 x 17 = 289, tail 33, split in 7), (33 x 9 = 297
+# with ragged edges, tail 41, split in 6).
+LIN_SPLIT = [(4352, 4096, 6144), (4352, 4352, 12288), (8200, 2100, 6144)]
+
+
+@pytest.mark.parametrize("M,N,K", LIN_SPLIT)
+@pytest.mark.parametrize("epi", ["bias", "gelu", "gated"])
+def test_linear_split_k_tail(gpu_lib, M, N, K, epi):
+    """With a workspace the last round's tiles are split along K and their float32 partial sums added
+    in a fixed order: the result matches the oracle element-wise, repeats bit for bit, and differs
+    (in rounding only) from the unsplit launch, which shows the split path ran."""
+    assert torch.cuda.get_device_properties(0).multi_processor_count == 256
+    say("linear split-K", M, N, K, epi)
+    a = normal(70, (M, K), C.BF16)
+    w = normal(71, (N, K), C.BF16, 0.05)
+    b = normal(72, (N,), C.BF16, 0.1)
+    A, W, Bv = dev(a, C.BF16), dev(w, C.BF16), dev(b, C.BF16)
+    z = odit.f64(a) @ odit.f64(w).T + odit.f64(b)
+    kw, code = {}, gpu_lib.EPI_BIAS
+    if epi == "gelu":
+        ref, code = odit.gelu_tanh(z), gpu_lib.EPI_GELU
+    elif epi == "gated":
+        rps = (M + 3) // 4
+        gate = normal(73, (4, N), C.F32)
+        resid = normal(74, (M, N), C.BF16)
+        kw = dict(gate=dev(gate, C.F32), gate_ld=N, resid=dev(resid, C.BF16), rows_per_sample=rps)
+        ref, code = resid + gate[np.arange(M) // rps] * z, gpu_lib.EPI_GATED
+    else:
+        ref = z
+    ws = torch.empty(gpu_lib.linear_workspace_size(), dtype=torch.uint8, device="cuda")
+    outs = []
+    for use_ws in (True, True, False):
+        out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+        gpu_lib.linear(A, W, Bv, out, epi=code, ws=ws if use_ws else None, **kw)
+        outs.append(out)
+    torch.cuda.synchronize()
+    check(host(outs[0]), ref, C.BF16, 0, K, what=f"linear split-K {M}x{N}x{K} {epi}", norm_tol=6e-3)
+    assert torch.equal(outs[0], outs[1])
+    assert not torch.equal(outs[0], outs[2])
+    check(host(outs[2]), ref, C.BF16, 0, K, what=f"linear unsplit {M}x{N}x{K} {epi}", norm_tol=6e-3)
+
+
 def test_linear_in_place_gated_residual(gpu_lib):
     M, N, K = 256, 384, 128
     a, w = normal(6, (M, K), C.BF16), normal(7, (N, K), C.BF16, 0.05)
