@@ -25,7 +25,8 @@ advantages, and extrapolates to a batch step by block count x samples; the line 
 "extrapolated".  The one-block and tiny workloads are timed in full.
 
 Other workloads (--workload): flux-block (one Flux-shaped dual-stream block, B = 8, 4096 + 512
-tokens, one SDE step t = 0.6 -> 0.5 on the block's hidden state), flux-stack (19 dual + 38 single
+tokens, one SDE step t = 0.6 -> 0.5 on the block's hidden state), qwen-block (the same with the
+Qwen stack's block shape, 4096 + 256 tokens: its launches are the stack's), flux-stack (19 dual + 38 single
 blocks, B = 16, 1024 + 512 tokens, 10 SDE steps), wan (30 WAN blocks, B = 1, 32760 + 512 tokens,
 8 steps), tiny, and two training-side workloads on the Flux stack: grpo-flux-stack (the GRPO
 policy-update forward over a stored rollout; a step is one recomputed SDE step) and
@@ -70,6 +71,7 @@ TARGET_MFMA, TARGET_HBM = 0.50, 0.70
 
 # workload name -> (configs attribute, default timed steps, default warmup steps)
 WORKLOADS = {"qwen-stack": ("QWEN_STACK", 20, 5), "flux-block": ("FLUX_BLOCK", 20, 5), "tiny": ("TINY", 20, 5),
+             "qwen-block": ("QWEN_BLOCK", 20, 5),
              "flux-stack": ("FLUX_STACK", 20, 5), "wan": ("WAN_STACK", 16, 4),
              "grpo-flux-stack": ("FLUX_STACK", 2, 1), "awm-flux-stack": ("FLUX_STACK", 10, 2)}
 DEVICE_DRAWN = ("flux-stack", "qwen-stack", "wan", "grpo-flux-stack", "awm-flux-stack")

@@ -120,6 +120,19 @@ FLUX_STACK = Workload(
     prompts=1, group=16, grid=(1, 32, 32), n_txt=512, steps=10, eta=0.7, reward_kind="normal",
 )
 
+# One dual-stream block of the Qwen-Image-shaped stack on its hidden state (B=8, 4096 image + 256
+# text tokens, one SDE step): the block's GEMM, attention and norm launches have exactly the stack's
+# shapes, so their per-launch counters stand for the stack's.
+QWEN_BLOCK = Workload(
+    name="qwen-dual-block-bf16-B8-4096img-256txt",
+    index=5,
+    model=ModelConfig(model=MODEL_MMDIT, io_mode=IO_HIDDEN, dtype=BF16, n_dual=1, n_single=0,
+                      hidden=3072, heads=24, head_dim=128, mlp_hidden=12288, in_channels=64,
+                      txt_dim=3072, rope_axes=(16, 56, 56)),
+    prompts=1, group=8, grid=(1, 64, 64), n_txt=256, steps=1, eta=0.7,
+    reward_kind="uniform", fixed_step=(0.6, 0.5),
+)
+
 QWEN_STACK = Workload(
     name="qwen-60dual-bf16-B8-4096img-256txt",
     index=3,
