@@ -173,7 +173,7 @@ namespace {
 struct Plan {
   int64_t B, Ni, Nt, N, P;
   size_t rope, temb_in, c, tmp, condB, cond32, mods, ximg, xtxt, joint, y, qkv, q, k, vt, o, u, txth;
-  size_t e6, ctx1, ctxp, kvc, kc, vct, qd, splitk, splitk_bytes, total;
+  size_t e6, ctx1, ctxp, kvc, kc, vct, qd, sumsq, splitk, splitk_bytes, total;
 };
 
 Plan plan(const ff_dit& m, int64_t B, const int32_t grid[3], int64_t n_txt, int64_t n_prompts) {
@@ -215,6 +215,7 @@ Plan plan(const ff_dit& m, int64_t B, const int32_t grid[3], int64_t n_txt, int6
   p.kc = take(wan ? static_cast<size_t>(B) * p.Nt * H * es : 0);
   p.vct = take(wan ? static_cast<size_t>(B) * p.Nt * H * es : 0);
   p.qd = take(wan ? static_cast<size_t>(B) * p.Nt * H * es : 0);
+  p.sumsq = take(wan ? static_cast<size_t>(B) * p.Ni * (2 * H / 64) * 4 : 0);
   p.splitk_bytes = c.dtype == FF_BF16 ? gemm_split_bytes() : 0;
   p.splitk = take(p.splitk_bytes);
   p.total = round_up(cv.off, 256);
@@ -462,11 +463,37 @@ int wan_block(const ff_dit& m, const Plan& p, void* ws, int i, const void* ctx, 
   FF_TRY(add_table(wb.mod, c.dtype, e6, mods, p.B, 6 * H, s));
   // self-attention
   FF_TRY(norm_modulate(norm_args(c, rows, X, Y, mods, mods + H, 6 * H, p.Ni), s));
-  FF_TRY(gemm(gemm_args_ws(p, ws, c.dtype, rows, 3 * H, H, Y, H, wb.qkv, QKV, 3 * H, EPI_NONE), s));
-  FF_TRY(rms_rows(c, QKV, rows, 3 * H, wb.qn, s));
-  FF_TRY(rms_rows(c, QKV + H * es, rows, 3 * H, wb.kn, s));
-  FF_TRY(relayout(c, p, QKV, QKV + H * es, QKV + 2 * H * es, 3 * H, p.Ni,
-                  reinterpret_cast<const float2*>(at(ws, p.rope)), at(ws, p.q), at(ws, p.k), at(ws, p.vt), s));
+  // Q, K with their RMSNorm over all of H, rotated, and V: the projection's epilogue leaves each
+  // token's partial sums of q^2 and k^2 per 64 columns, and one relayout pass normalises, rotates
+  // and moves Q, K, V^T to the attention layout.  Shapes the tile kernel does not take use the
+  // two in-place norm passes and a plain relayout.
+  GemmArgs gq = gemm_args_ws(p, ws, c.dtype, rows, 3 * H, H, Y, H, wb.qkv, QKV, 3 * H, EPI_SUMSQ);
+  gq.sumsq = reinterpret_cast<float*>(at(ws, p.sumsq));
+  gq.sumsq_w = H;
+  const float2* rope = reinterpret_cast<const float2*>(at(ws, p.rope));
+  QkvArgs qa{};
+  if (c.head_dim == 128 && gemm_sumsq_ok(gq)) {
+    FF_TRY(gemm(gq, s));
+    qa.dtype = c.dtype;
+    qa.B = p.B; qa.n_tok = p.Ni; qa.tok_offset = 0; qa.n_joint = p.Ni; qa.src_rows = p.Ni;
+    qa.heads = c.heads; qa.d = c.head_dim;
+    qa.q = QKV; qa.k = QKV + H * es; qa.v = QKV + 2 * H * es; qa.ld = 3 * H;
+    qa.q_w = wb.qn; qa.k_w = wb.kn;
+    qa.full_width_norm = 1; qa.apply_norm = 1;
+    qa.eps = static_cast<float>(c.norm_eps);
+    qa.rope = rope;
+    qa.Q = at(ws, p.q); qa.Kd = at(ws, p.k); qa.Vt = at(ws, p.vt);
+    qa.v_transposed = 1;
+    qa.sumsq = gq.sumsq;
+    qa.sumsq_parts = 2 * H / 64;
+    FF_TRY(qk_norm_rope(qa, s));
+  } else {
+    FF_TRY(gemm(gemm_args_ws(p, ws, c.dtype, rows, 3 * H, H, Y, H, wb.qkv, QKV, 3 * H, EPI_NONE), s));
+    FF_TRY(rms_rows(c, QKV, rows, 3 * H, wb.qn, s));
+    FF_TRY(rms_rows(c, QKV + H * es, rows, 3 * H, wb.kn, s));
+    FF_TRY(relayout(c, p, QKV, QKV + H * es, QKV + 2 * H * es, 3 * H, p.Ni, rope, at(ws, p.q), at(ws, p.k),
+                    at(ws, p.vt), s));
+  }
   {
     AttnArgs a{};
     a.dtype = c.dtype;

@@ -87,6 +87,9 @@ enum Epi : int {
   EPI_QKV = 3,        // columns [Q | K | V] = [0, 3H) of acc + bias go through qk_norm_rope(*qkv) (fused when
                       // possible); columns from 3H on (N > 3H: a single-stream block's MLP input) take
                       // EPI_GELU's treatment with gelu_from = 3H and go to out
+  EPI_SUMSQ = 5,      // out = acc + bias, and for columns [0, 2 sumsq_w) the sum of squares of each row's
+                      // stored (rounded) values over every 64 columns: sumsq[m * (2 sumsq_w / 64) + n / 64]
+                      // (the full-width Q / K RMS of a WAN block, added up in a fixed order by its reader)
 };
 
 struct QkvArgs;
@@ -111,7 +114,12 @@ struct GemmArgs {
   // gemm_split_bytes.  Launches on one stream may share it (each finishes before the next starts).
   void* split_ws = nullptr;
   size_t split_bytes = 0;
+  float* sumsq = nullptr;               // EPI_SUMSQ: per-row partial sums of squares
+  int64_t sumsq_w = 0;
 };
+// EPI_SUMSQ runs in the 256 x 256 tile kernel only: bf16, at least one tile per CU, N a multiple of
+// 64 and 16-byte aligned rows, sumsq_w a multiple of 64 with 2 sumsq_w <= N.
+bool gemm_sumsq_ok(const GemmArgs& a);
 // Scratch bytes that let any launch split its last round: 255 tile partials of 256 KB and flags.
 size_t gemm_split_bytes();
 int gemm(const GemmArgs& a, hipStream_t s);
@@ -185,6 +193,10 @@ struct QkvArgs {
                                             // table row i - rope_from (a joint text + image sequence)
   void* Q; void* Kd; void* Vt;              // Q, K [B, h, n_joint, d]; V transposed [B, h, d, n_joint]
   int v_transposed;
+  // Full-width norm from precomputed sums (bf16, d = 128): per source row, sumsq_parts floats whose
+  // first half adds up to the row's sum of q^2 over all H and second half to that of k^2 (EPI_SUMSQ).
+  const float* sumsq = nullptr;
+  int64_t sumsq_parts = 0;
 };
 int qk_norm_rope(const QkvArgs& a, hipStream_t s);
 

@@ -64,6 +64,9 @@ struct GemmParams {
   int heads; float eps;
   // fp8: out = epi(row_scale[m] * col_scale[n] * acc + bias)
   const float* row_scale; const float* col_scale;
+  // EPI_SUMSQ: row m's sum of squares of its stored columns [64 j, 64 j + 64), j < 2 sumsq_w / 64,
+  // at sumsq[m * (2 sumsq_w / 64) + j]
+  float* sumsq; int64_t sumsq_w;
 };
 
 template <bool BF16, int EPI>
@@ -280,6 +283,8 @@ __device__ __forceinline__ void epilogue_pairs(const GemmParams& p, const f32x16
       gv[4] = g1.x; gv[5] = g1.y; gv[6] = g1.z; gv[7] = g1.w;
     }
   }
+  // EPI_SUMSQ: which 64-column slot of the row's partial sums this pair fills (-1: past 2 sumsq_w)
+  const int64_t sq_slot = EPI == EPI_SUMSQ && nw < 2 * p.sumsq_w ? nw / 64 : -1;
   float v[4][8];
 #define FF_PAIR(I)                                                                                   \
   if constexpr (I < FM) {                                                                            \
@@ -324,6 +329,19 @@ __device__ __forceinline__ void epilogue_pairs(const GemmParams& p, const f32x16
           x = p.gate ? fmaf(g[e], x, r8[e]) : x + r8[e];                                             \
         }                                                                                            \
         v[q][e] = x;                                                                                 \
+      }                                                                                              \
+      if constexpr (EPI == EPI_SUMSQ) {                                                              \
+        if (sq_slot >= 0) {                                                                          \
+          float ss = 0.f;                                                                            \
+          for (int e = 0; e < 8; ++e) {                                                              \
+            const float r = bf2f(f2bf(v[q][e]));                                                     \
+            ss = fmaf(r, r, ss);                                                                     \
+          }                                                                                          \
+          ss += __shfl_xor(ss, 1, 64);                                                               \
+          ss += __shfl_xor(ss, 2, 64);                                                               \
+          ss += __shfl_xor(ss, 4, 64);                                                               \
+          if ((lane & 7) == 0 && m < p.M) p.sumsq[m * (2 * p.sumsq_w / 64) + sq_slot] = ss;          \
+        }                                                                                            \
       }                                                                                              \
       if (m < p.M) st8_bf16_nt(out, m * p.ldo + n, v[q]);                                            \
     }                                                                                                \
@@ -1158,8 +1176,20 @@ GemmParams make_params(const GemmArgs& a) {
     p.heads = q.heads; p.eps = q.eps;
     p.rows_per_sample = q.src_rows;
   }
+  p.sumsq = a.sumsq;
+  p.sumsq_w = a.sumsq_w;
   return p;
 }
+
+}  // namespace
+
+bool gemm_sumsq_ok(const GemmArgs& a) {
+  return a.dtype == FF_BF16 && a.K % BK == 0 && a.K1 == a.K && a.N % 64 == 0 && a.ldo % 8 == 0 && aligned16(a.out) &&
+         (!a.bias || aligned16(a.bias)) && a.sumsq && a.sumsq_w > 0 && a.sumsq_w % 64 == 0 && 2 * a.sumsq_w <= a.N &&
+         ((a.M + 255) / 256) * ((a.N + 255) / 256) >= 256;
+}
+
+namespace {
 
 // The QKV projection of one stream can end in the fused norm / rotation / relayout epilogue:
 // bf16, 128-wide heads with a per-head norm, every GEMM row a token (rows = B x tokens), V taken
@@ -1210,6 +1240,14 @@ int gemm(const GemmArgs& a, hipStream_t s) {
   }
   GemmParams p = make_params(a);
   const double flops = gemm_flops(a), bytes = gemm_bytes(a);
+  if (a.epi == EPI_SUMSQ) {
+    if (!gemm_sumsq_ok(a)) return fail(FF_EUNSUPPORTED, "gemm: the sum-of-squares epilogue does not apply to this shape");
+    GemmBatch b{};
+    b.p[0] = p;
+    b.p[1] = p;
+    b.tiles0 = b.tiles = tiles256(p);
+    return launch_pp_batch<EPI_SUMSQ>(b, s, kGemmNames[EPI_NONE], flops, bytes, a.split_ws, a.split_bytes);
+  }
   if (a.dtype == FF_BF16) {
     if (a.K % BK != 0 || a.K1 % BK != 0)
       return fail(FF_EUNSUPPORTED, "gemm: bf16 K=%lld (K1=%lld) must be a multiple of %d", (long long)a.K,

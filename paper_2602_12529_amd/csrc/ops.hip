@@ -458,8 +458,10 @@ __global__ __launch_bounds__(256) void qk_rope_vec_kernel(QkvArgs a) {
   const int64_t b = blockIdx.z;
   float qw[8], kw[8];
   if (a.apply_norm) {
-    ld8<true>(a.q_w, c * 8, qw);
-    ld8<true>(a.k_w, c * 8, kw);
+    // per-head weights [128], or full-width weights [H] (this head's slice) with precomputed sums
+    const int64_t wo = (a.sumsq ? static_cast<int64_t>(h) * 128 : 0) + c * 8;
+    ld8<true>(a.q_w, wo, qw);
+    ld8<true>(a.k_w, wo, kw);
   } else {
 #pragma unroll
     for (int j = 0; j < 8; ++j) qw[j] = kw[j] = 1.0f;
@@ -482,18 +484,43 @@ __global__ __launch_bounds__(256) void qk_rope_vec_kernel(QkvArgs a) {
       for (int j = 0; j < 4; ++j) { cs[2 * j] = 1.f; cs[2 * j + 1] = 0.f; }
     }
     const int64_t dst = (out_head + a.tok_offset + tok) * 128 + c * 8;
+    // Full-width norm: the row's sums of q^2 and k^2 over all H, from the projection's partial sums
+    // (added in a fixed order, the same in every head's block).
+    // Each of the token's 16 threads adds every 16th partial sum, then four exchanges (the same
+    // fixed order in every block) give all 16 the totals.
+    float fw_ss[2] = {0.f, 0.f};
+    if (a.sumsq) {
+      const float* ps = a.sumsq + (b * a.src_rows + tok) * a.sumsq_parts;
+      const int64_t half = a.sumsq_parts / 2;
+      for (int64_t j = c; j < half; j += 16) {
+        fw_ss[0] += ps[j];
+        fw_ss[1] += ps[half + j];
+      }
+#pragma unroll
+      for (int w = 0; w < 2; ++w) {
+        fw_ss[w] += __shfl_xor(fw_ss[w], 8, 64);
+        fw_ss[w] += __shfl_xor(fw_ss[w], 4, 64);
+        fw_ss[w] += __shfl_xor(fw_ss[w], 2, 64);
+        fw_ss[w] += __shfl_xor(fw_ss[w], 1, 64);
+      }
+    }
 #pragma unroll
     for (int which = 0; which < 2; ++which) {
       float x[8];
       ld8<true>(which == 0 ? a.q : a.k, src, x);
-      float ss = 0.f;
+      float rstd = 1.0f;
+      if (a.sumsq) {
+        rstd = rsqrtf(fw_ss[which] / static_cast<float>(a.heads * 128) + a.eps);
+      } else {
+        float ss = 0.f;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) ss = fmaf(x[j], x[j], ss);
-      ss += __shfl_xor(ss, 8, 64);
-      ss += __shfl_xor(ss, 4, 64);
-      ss += __shfl_xor(ss, 2, 64);
-      ss += __shfl_xor(ss, 1, 64);
-      const float rstd = a.apply_norm ? rsqrtf(ss * (1.0f / 128.0f) + a.eps) : 1.0f;
+        for (int j = 0; j < 8; ++j) ss = fmaf(x[j], x[j], ss);
+        ss += __shfl_xor(ss, 8, 64);
+        ss += __shfl_xor(ss, 4, 64);
+        ss += __shfl_xor(ss, 2, 64);
+        ss += __shfl_xor(ss, 1, 64);
+        if (a.apply_norm) rstd = rsqrtf(ss * (1.0f / 128.0f) + a.eps);
+      }
       const float* w = which == 0 ? qw : kw;
       float y[8];
 #pragma unroll
@@ -667,11 +694,13 @@ int qk_norm_rope(const QkvArgs& a, hipStream_t s) {
   }
   if (a.d > 128 || a.d % 2) return fail(FF_EUNSUPPORTED, "qk_norm_rope: head_dim %d", a.d);
   dim3 grid(blocks_for(a.n_tok, kRopeTok), static_cast<unsigned>(a.heads), static_cast<unsigned>(a.B));
-  LaunchScope ls("qk_norm_rope", s, 0.0, 6.0 * dtype_size(a.dtype) * a.B * a.n_tok * a.heads * a.d);
-  const bool vec = a.dtype == FF_BF16 && a.d == 128 && a.v_transposed && !a.full_width_norm &&
+  const bool vec = a.dtype == FF_BF16 && a.d == 128 && a.v_transposed && (!a.full_width_norm || a.sumsq) &&
                    a.ld % 8 == 0 && aligned16(a.q) && aligned16(a.k) && aligned16(a.v) && aligned16(a.Q) &&
                    aligned16(a.Kd) && aligned16(a.Vt) && (!a.apply_norm || (aligned16(a.q_w) && aligned16(a.k_w))) &&
                    (!a.rope || aligned16(a.rope)) && a.n_joint % 8 == 0 && a.tok_offset % 8 == 0 && a.n_tok % 8 == 0;
+  if (a.sumsq && !(vec && a.full_width_norm && a.apply_norm && a.sumsq_parts > 0 && a.sumsq_parts % 2 == 0))
+    return fail(FF_EUNSUPPORTED, "qk_norm_rope: precomputed sums need the vector path and the full-width norm");
+  LaunchScope ls("qk_norm_rope", s, 0.0, 6.0 * dtype_size(a.dtype) * a.B * a.n_tok * a.heads * a.d);
   if (vec) hipLaunchKernelGGL(qk_rope_vec_kernel, grid, dim3(256), 0, s, a);
   else if (a.dtype == FF_BF16) hipLaunchKernelGGL(qk_rope_kernel<true>, grid, dim3(256), 0, s, a);
   else hipLaunchKernelGGL(qk_rope_kernel<false>, grid, dim3(256), 0, s, a);
