@@ -87,13 +87,13 @@ int ff_sde_step(const void* x, const void* v, const void* eps, void* x_next, dou
 /* ff_sde_step for callers that cannot allocate device memory or pass a workspace (code under
  * HIP graph capture, tight serving loops, harnesses that forbid allocation): the same step and
  * log-probability, bit for bit, with the log-probability's per-block partial sums kept in a
- * library-owned device array of 65536 doubles (512 KiB per device, held until the process ends,
+ * library-owned device array of 81920 doubles (640 KiB per device, held until the process ends,
  * its address looked up once per device on the first call there).  Arguments, domain and
  * errors as ff_sde_step, without the workspace.  No call allocates (no hipMalloc, no events, no
  * library allocation).  Every call on one device shares that array: calls that overlap on one
  * device (concurrent streams, other host threads) race and must be serialised by the caller.
  * The partial sums are all written before they are read, so nothing needs clearing between
- * calls.  B * blocks-per-sample above 65536 -> FF_EUNSUPPORTED (never reached for B <= 65535). */
+ * calls.  B * blocks-per-sample above 81920 -> FF_EUNSUPPORTED (never reached for B <= 65535). */
 int ff_sde_step_noalloc(const void* x, const void* v, const void* eps, void* x_next, double* logp,
                         int64_t B, int64_t D, double t, double t_next, double sigma, int32_t dtype,
                         void* stream);

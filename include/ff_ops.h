@@ -78,6 +78,15 @@ int ff_rope_table(float* out, const int32_t grid[3], int32_t head_dim, const int
 int ff_skinny_linear(const float* in, const void* W, const void* bias, float* out, int64_t B, int64_t N,
                      int64_t K, int32_t act_in, int32_t act_out, int32_t dtype, void* stream);
 
+/* HBM streaming probe (measurement, not part of the method): mode 0 reads `bytes` from src (each
+ * workgroup folds what it read into one 16-byte word of dst, which must hold `blocks` of them),
+ * mode 1 writes `bytes` to dst, mode 2 copies src to dst; 16-byte accesses, four in flight per
+ * thread, `blocks` workgroups of 256 threads in a grid-stride loop, non-temporal loads and stores
+ * when `nontemporal` is set.  It gives the achievable streaming bandwidth that the HBM-bound
+ * kernels are compared with.  bytes % 16 == 0; buffers 16-byte aligned. */
+int ff_stream_probe(int32_t mode, int32_t nontemporal, const void* src, void* dst, int64_t bytes, int32_t blocks,
+                    void* stream);
+
 /* FP8 row quantisation to OCP E4M3 (sign, 4 exponent bits with bias 7, 3 mantissa bits; largest
  * magnitude 448, no infinities).  Not from the paper, whose DiT runs its linear layers in bf16:
  * the FP8 layer below is a throughput variant of ff_linear.

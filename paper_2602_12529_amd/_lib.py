@@ -82,6 +82,7 @@ _SIGS = {
                                   c_void_p]),
     "ff_linear_fp8": (c_int32, [c_void_p, c_int64, c_void_p, c_void_p, c_int64, c_void_p, c_void_p, c_void_p,
                                 c_int64, c_int64, c_int64, c_int64, c_int32, c_int64, c_void_p]),
+    "ff_stream_probe": (c_int32, [c_int32, c_int32, c_void_p, c_void_p, c_int64, c_int32, c_void_p]),
     "ff_flow_noise": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_int32, c_void_p]),
     "ff_loss_workspace_size": (c_int32, [c_int64, c_int64, POINTER(c_size_t)]),
     "ff_awm_loss": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_int32, c_void_p, c_void_p,

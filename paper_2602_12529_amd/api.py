@@ -207,6 +207,12 @@ def linear_fp8(A, d_a, W, d_w, bias, out, epi=EPI_BIAS, gelu_from=0):
     return out
 
 
+def stream_probe(mode: int, src, dst, nbytes: int, blocks: int, nontemporal: bool = True):
+    """HBM streaming probe (0 read, 1 write, 2 copy) over nbytes; measurement only."""
+    check(load().ff_stream_probe(mode, 1 if nontemporal else 0, _p(src), _p(dst), nbytes, blocks, _stream()),
+          "ff_stream_probe")
+
+
 def attention(Q, K, V, out):
     B, h, n_q, d = Q.shape
     n_kv = K.shape[2]

@@ -55,6 +55,28 @@ __device__ __forceinline__ void ld8(const void* p, int64_t i, float (&o)[8]) {
     o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
   }
 }
+// ld8 / st8 with non-temporal accesses: for streams touched exactly once (the SDE step's x, v,
+// eps and x'), so they bypass the caches' retention instead of displacing other data.
+typedef unsigned int nt_u32x4 __attribute__((ext_vector_type(4)));
+typedef float nt_f32x4 __attribute__((ext_vector_type(4)));
+template <bool BF16>
+__device__ __forceinline__ void ld8_nt(const void* p, int64_t i, float (&o)[8]) {
+  if constexpr (BF16) {
+    const nt_u32x4 u = __builtin_nontemporal_load(reinterpret_cast<const nt_u32x4*>(static_cast<const bf16_t*>(p) + i));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      o[2 * j] = __uint_as_float(u[j] << 16);
+      o[2 * j + 1] = __uint_as_float(u[j] & 0xffff0000u);
+    }
+  } else {
+    const nt_f32x4* q = reinterpret_cast<const nt_f32x4*>(static_cast<const float*>(p) + i);
+    const nt_f32x4 a = __builtin_nontemporal_load(q), b = __builtin_nontemporal_load(q + 1);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) { o[j] = a[j]; o[4 + j] = b[j]; }
+  }
+}
+template <bool BF16>
+__device__ __forceinline__ void st8_nt(void* p, int64_t i, const float (&v)[8]);
 // Eight values stored as bf16 with one non-temporal 16-byte store: for outputs written once and
 // read by a later kernel, so they stream out without displacing cached inputs.
 __device__ __forceinline__ void st8_bf16_nt(void* p, int64_t i, const float (&v)[8]) {
@@ -65,6 +87,17 @@ __device__ __forceinline__ void st8_bf16_nt(void* p, int64_t i, const float (&v)
   u.z = uint32_t(f2bf(v[4])) | (uint32_t(f2bf(v[5])) << 16);
   u.w = uint32_t(f2bf(v[6])) | (uint32_t(f2bf(v[7])) << 16);
   __builtin_nontemporal_store(u, reinterpret_cast<u32x4_nt*>(static_cast<bf16_t*>(p) + i));
+}
+template <bool BF16>
+__device__ __forceinline__ void st8_nt(void* p, int64_t i, const float (&v)[8]) {
+  if constexpr (BF16) {
+    st8_bf16_nt(p, i, v);
+  } else {
+    nt_f32x4* q = reinterpret_cast<nt_f32x4*>(static_cast<float*>(p) + i);
+    const nt_f32x4 a = {v[0], v[1], v[2], v[3]}, b = {v[4], v[5], v[6], v[7]};
+    __builtin_nontemporal_store(a, q);
+    __builtin_nontemporal_store(b, q + 1);
+  }
 }
 template <bool BF16>
 __device__ __forceinline__ void st8(void* p, int64_t i, const float (&v)[8]) {

@@ -174,6 +174,9 @@ struct NormArgs {
 };
 int norm_modulate(const NormArgs& a, hipStream_t s);
 
+// Streaming probe (mode 0 read, 1 write, 2 copy) over `chunks` 16-byte words; measurement only.
+int stream_probe(int mode, bool nt, const void* src, void* dst, int64_t chunks, int blocks, hipStream_t s);
+
 // Converts a float32 [rows, H] tensor to dtype (plain copy for F32) or dtype -> float32.
 int cast_to_f32(int dtype, const void* in, float* out, int64_t n, hipStream_t s);
 

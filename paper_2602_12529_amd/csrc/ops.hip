@@ -740,6 +740,64 @@ int cast_to_f32(int dtype, const void* in, float* out, int64_t n, hipStream_t s)
   return ls.status();
 }
 
+// Streaming probes (measurement only): read-only, write-only or copy of n 16-byte chunks, four
+// chunks in flight per thread in a grid-stride loop; NT selects non-temporal accesses.  The
+// read-only probe folds what it reads into one 16-byte word per workgroup (out[blockIdx.x]) so
+// the loads are kept.
+typedef unsigned int sp_u32x4 __attribute__((ext_vector_type(4)));
+template <int MODE, bool NT>
+__global__ __launch_bounds__(256) void stream_kernel(const sp_u32x4* __restrict__ src, sp_u32x4* __restrict__ dst,
+                                                     int64_t n) {
+  constexpr int U = 4;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * 256 * U;
+  sp_u32x4 acc = {0u, 0u, 0u, 0u};
+  const sp_u32x4 pattern = {0x3f800000u, 0u, 0x3f800000u, 0u};
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 * U + threadIdx.x; i < n; i += stride) {
+    sp_u32x4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t j = i + u * 256;
+      if (MODE != 1 && j < n) v[u] = NT ? __builtin_nontemporal_load(src + j) : src[j];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t j = i + u * 256;
+      if (j >= n) continue;
+      if (MODE == 0) {
+        acc ^= v[u];
+      } else {
+        const sp_u32x4 w = MODE == 1 ? pattern : v[u];
+        if (NT) __builtin_nontemporal_store(w, dst + j);
+        else dst[j] = w;
+      }
+    }
+  }
+  if (MODE == 0) {
+    __shared__ sp_u32x4 red[256];
+    red[threadIdx.x] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      sp_u32x4 r = red[0];
+      for (int t = 1; t < 256; ++t) r ^= red[t];
+      dst[blockIdx.x] = r;
+    }
+  }
+}
+
+int stream_probe(int mode, bool nt, const void* src, void* dst, int64_t chunks, int blocks, hipStream_t s) {
+  const double bytes = 16.0 * chunks * (mode == 2 ? 2.0 : 1.0);
+  LaunchScope ls("stream_probe", s, 0.0, bytes);
+  const sp_u32x4* in = static_cast<const sp_u32x4*>(src);
+  sp_u32x4* out = static_cast<sp_u32x4*>(dst);
+  const dim3 g(static_cast<unsigned>(blocks));
+#define FF_STREAM(M)                                                                                       \
+  if (nt) hipLaunchKernelGGL((stream_kernel<M, true>), g, dim3(256), 0, s, in, out, chunks);               \
+  else hipLaunchKernelGGL((stream_kernel<M, false>), g, dim3(256), 0, s, in, out, chunks);
+  if (mode == 0) { FF_STREAM(0) } else if (mode == 1) { FF_STREAM(1) } else { FF_STREAM(2) }
+#undef FF_STREAM
+  return ls.status();
+}
+
 int add_table(const void* table, int dtype, const float* e, float* out, int64_t B, int64_t n, hipStream_t s) {
   LaunchScope ls("add_table", s, 0.0, 8.0 * B * n);
   if (dtype == FF_BF16) hipLaunchKernelGGL(add_table_kernel<true>, dim3(blocks_for(B * n)), dim3(256), 0, s, table, e, out, B, n);

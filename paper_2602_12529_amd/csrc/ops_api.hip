@@ -191,4 +191,16 @@ int ff_linear_fp8(const uint8_t* A, int64_t lda, const float* d_a, const uint8_t
   return gemm_fp8(g, static_cast<hipStream_t>(stream));
 }
 
+int ff_stream_probe(int32_t mode, int32_t nontemporal, const void* src, void* dst, int64_t bytes, int32_t blocks,
+                    void* stream) {
+  const char* fn = "ff_stream_probe";
+  if (mode < 0 || mode > 2) return fail(FF_EINVAL, "%s: mode %d (0 read, 1 write, 2 copy)", fn, mode);
+  if (bytes < 0 || bytes % 16) return fail(FF_EINVAL, "%s: bytes=%lld must be a non-negative multiple of 16", fn, (long long)bytes);
+  if (blocks < 1 || blocks > (1 << 20)) return fail(FF_EINVAL, "%s: blocks=%d outside [1, 2^20]", fn, blocks);
+  if (bytes == 0) return FF_OK;
+  if ((mode != 1 && !src) || !dst) return fail(FF_EINVAL, "%s: null buffer", fn);
+  if ((src && !aligned16(src)) || !aligned16(dst)) return fail(FF_EINVAL, "%s: buffers must be 16-byte aligned", fn);
+  return stream_probe(mode, nontemporal != 0, src, dst, bytes / 16, blocks, static_cast<hipStream_t>(stream));
+}
+
 }  // extern "C"

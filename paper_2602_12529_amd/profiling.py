@@ -5,6 +5,10 @@ Subcommands (python -m paper_2602_12529_amd.profiling ...):
   copy --bytes N --reps R
       A plain device-to-device copy of N bytes, R times: the calibration kernel
       whose FETCH_SIZE / WRITE_SIZE counters are compared with the known N.
+  ceiling OUT --title T --cmd C [--reps R]
+      The HBM streaming ceiling (ff_stream_probe: read, write, copy over 1 GiB, non-temporal or
+      not, a sweep of grid sizes) beside a torch copy and the rollout's HBM-bound kernels at
+      full size, in one process -> markdown table.
   sde-sweep OUT --title T --cmd C [--reps R]
       The SDE step with log-prob over 1 MB .. 2 GB of traffic, warm and cold (rotating
       buffer sets beyond the MALL), per-launch HIP events -> markdown table.
@@ -210,6 +214,118 @@ def run_sde_sweep(out_md: str, title: str, cmds: List[str], reps: int = 20) -> L
     return rows
 
 
+def run_ceiling(out_md: str, title: str, cmds: List[str], reps: int = 10) -> List[dict]:
+    """Streaming ceiling of HBM on the box: ff_stream_probe read-only, write-only and copy over 1 GiB
+    (four times the 256 MB MALL), non-temporal or not, over a sweep of grid sizes, the best of
+    each; beside them, in the same process, a plain torch copy and the rollout's HBM-bound kernels
+    at full size (the SDE step with log-prob of the one-block workload, 8 x 12.58 M bf16; the norm
+    + modulate of a 32768 x 3072 image stream; the adaLN GEMV of one stream, B = 8, 6H x H).
+    Each entry is the median of `reps` launches timed with the library's HIP events."""
+    import statistics
+
+    import torch
+
+    from . import api
+
+    if not torch.cuda.is_available():
+        raise SystemExit("the streaming ceiling needs a GPU")
+
+    def timed(fn, name):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(reps):
+            api.profile_filter(name)
+            api.profile_reset()
+            api.profile_enable(True)
+            fn()
+            torch.cuda.synchronize()
+            api.profile_enable(False)
+            r = api.profile_read()[name]
+            times.append(r["ms"] * 1e-3 / r["launches"])
+        api.profile_filter(None)
+        return statistics.median(times)
+
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    src.random_(0, 255)
+    dst = torch.empty(n, dtype=torch.uint8, device="cuda")
+    rows, best = [], {}
+    for mode, label in ((0, "read"), (1, "write"), (2, "copy")):
+        moved = n * (2 if mode == 2 else 1)
+        for nt in (True, False):
+            for blocks in (1024, 2048, 4096, 8192, 16384):
+                t = timed(lambda: api.stream_probe(mode, src, dst, n, blocks, nt), "stream_probe")
+                r = {"what": f"probe {label}", "nt": nt, "blocks": blocks, "bytes": moved, "us": t * 1e6,
+                     "tbs": moved / t / 1e12}
+                rows.append(r)
+                if label not in best or r["tbs"] > best[label]["tbs"]:
+                    best[label] = r
+                print(json.dumps(r), flush=True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for _ in range(3):
+        dst.copy_(src)
+    times = []
+    for _ in range(reps):
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        e1.synchronize()
+        times.append(e0.elapsed_time(e1) * 1e-3)
+    t = statistics.median(times)
+    kern = [{"what": "torch copy_", "bytes": 2 * n, "us": t * 1e6, "tbs": 2 * n / t / 1e12, "ref": "copy"}]
+    del src, dst
+    torch.cuda.empty_cache()
+    g = torch.Generator(device="cuda").manual_seed(0)
+    B, D = 8, 4096 * 3072
+    x, v, e = (torch.randn((B, D), device="cuda", generator=g).to(torch.bfloat16) for _ in range(3))
+    xn = torch.empty_like(x)
+    lp = torch.empty(B, dtype=torch.float64, device="cuda")
+    ws = api.workspace(api.sde_workspace_size(B, D))
+    t = timed(lambda: api.sde_step(x, v, e, xn, 0.6, 0.5, 0.9, logp=lp, ws=ws), "sde_step")
+    kern.append({"what": "sde_step (x, v, eps read, x' written), 8 x 12.58 M bf16", "bytes": 8 * B * D, "us": t * 1e6,
+                 "tbs": 8 * B * D / t / 1e12, "ref": "copy"})
+    del x, v, e, xn
+    torch.cuda.empty_cache()
+    R, H = 32768, 3072
+    X = torch.randn((R, H), device="cuda", generator=g).to(torch.bfloat16)
+    Y = torch.empty_like(X)
+    mod = torch.randn((8, 6 * H), device="cuda", generator=g)
+    t = timed(lambda: api.norm_modulate(X, Y, shift=mod, scale=mod[:, H:], mod_ld=6 * H, rows_per_sample=R // 8),
+              "norm_modulate")
+    kern.append({"what": "norm_modulate (x read, y written), 32768 x 3072 bf16", "bytes": 4 * R * H, "us": t * 1e6,
+                 "tbs": 4 * R * H / t / 1e12, "ref": "copy"})
+    del X, Y
+    cin = torch.randn((8, H), device="cuda", generator=g)
+    Wm = (torch.randn((6 * H, H), device="cuda", generator=g) * 0.02).to(torch.bfloat16)
+    bm = torch.zeros(6 * H, device="cuda").to(torch.bfloat16)
+    out = torch.empty((8, 6 * H), device="cuda")
+    t = timed(lambda: api.skinny_linear(cin, Wm, bm, out, act_in=1), "skinny_linear")
+    kern.append({"what": "skinny_linear (weights read), B = 8, 18432 x 3072 bf16", "bytes": 2 * 6 * H * H,
+                 "us": t * 1e6, "tbs": 2 * 6 * H * H / t / 1e12, "ref": "read"})
+    for k in kern:
+        print(json.dumps(k), flush=True)
+    out = _header(title, cmds)
+    out += ["Streaming probes over 1 GiB (4x the 256 MB MALL; cold), median of %d launches timed with the "
+            "library's HIP events; 16-byte accesses, four in flight per thread, 256-thread workgroups in a "
+            "grid-stride loop. TB/s counts bytes read plus bytes written. Peak HBM 8 TB/s." % reps, "",
+            "| probe | non-temporal | workgroups | µs | TB/s | / 8 TB/s |", "|---|---|---|---|---|---|"]
+    for r in rows:
+        out.append(f"| {r['what']} | {'yes' if r['nt'] else 'no'} | {r['blocks']} | {r['us']:.1f} | {r['tbs']:.2f} | "
+                   f"{r['tbs'] / 8.0:.2f} |")
+    out += ["", "Best of each: " + ", ".join(f"{k} {v['tbs']:.2f} TB/s" for k, v in best.items()) + ".", "",
+            "The rollout's HBM-bound kernels in the same process (algorithmic bytes only):", "",
+            "| kernel | MB per launch | µs | TB/s | / 8 TB/s | / best probe of its kind |", "|---|---|---|---|---|---|"]
+    for k in kern:
+        ref = best[k["ref"]]["tbs"]
+        out.append(f"| {k['what']} | {k['bytes'] / 1e6:.1f} | {k['us']:.1f} | {k['tbs']:.2f} | {k['tbs'] / 8.0:.2f} | "
+                   f"{k['tbs'] / ref:.2f} ({k['ref']}) |")
+    with open(out_md, "w") as f:
+        f.write("\n".join(out) + "\n")
+    return rows + kern
+
+
 # ---------------------------------------------------------------------------- summaries
 def _header(title: str, cmds: List[str]) -> List[str]:
     out = [f"# {title}", "", "Commands (run from the repository root on one MI355X):", "", "```"]
@@ -350,6 +466,11 @@ def main(argv=None) -> int:
     sw.add_argument("--title", required=True)
     sw.add_argument("--cmd", action="append", required=True)
     sw.add_argument("--reps", type=int, default=20)
+    ce = sub.add_parser("ceiling")
+    ce.add_argument("out")
+    ce.add_argument("--title", required=True)
+    ce.add_argument("--cmd", action="append", required=True)
+    ce.add_argument("--reps", type=int, default=10)
     cn = sub.add_parser("counter")
     cn.add_argument("csv")
     cn.add_argument("out")
@@ -378,6 +499,8 @@ def main(argv=None) -> int:
         run_linear(a.M, a.N, a.K, a.precision, a.gelu, a.reps)
     elif a.action == "sde-sweep":
         run_sde_sweep(a.out, a.title, a.cmd, a.reps)
+    elif a.action == "ceiling":
+        run_ceiling(a.out, a.title, a.cmd, a.reps)
     elif a.action == "counter":
         counter_md(a.csv, a.counter, a.out, a.title, a.cmd, a.note)
     elif a.action == "stats":

@@ -83,6 +83,17 @@ def test_sde_noalloc_argument_validation():
     assert lib.ff_sde_step_noalloc(None, None, None, None, None, 0, 8, 0.5, 0.4, 1.0, 1, None) == 0
 
 
+def test_stream_probe_argument_validation():
+    lib = _lib.load()
+    fake = c_void_p(4096)
+    _err(lib.ff_stream_probe(3, 1, fake, fake, 1024, 64, None), _lib.FF_EINVAL)      # mode
+    _err(lib.ff_stream_probe(2, 1, fake, fake, 1000, 64, None), _lib.FF_EINVAL)      # bytes % 16
+    _err(lib.ff_stream_probe(2, 1, fake, fake, 1024, 0, None), _lib.FF_EINVAL)       # blocks
+    _err(lib.ff_stream_probe(0, 1, None, fake, 1024, 64, None), _lib.FF_EINVAL)      # read needs src
+    _err(lib.ff_stream_probe(2, 1, c_void_p(4100), fake, 1024, 64, None), _lib.FF_EINVAL)
+    assert lib.ff_stream_probe(2, 1, None, None, 0, 64, None) == 0
+
+
 def test_philox_argument_validation():
     lib = _lib.load()
     f = c_void_p(8192)

@@ -279,3 +279,26 @@ def test_profile_filter_times_one_kernel(gpu_lib):
         gpu_lib.profile_enable(False)
         gpu_lib.profile_filter(None)
         gpu_lib.profile_reset()
+
+
+@pytest.mark.parametrize("nt", [True, False])
+def test_stream_probe_moves_the_bytes(gpu_lib, nt):
+    """The HBM streaming probe behind the bandwidth ceiling does the work it is timed for: the copy
+    reproduces the source, the write leaves its pattern, the read's per-workgroup folds XOR to the
+    XOR of every 16-byte word (the bytes a ragged last pass touches included)."""
+    nbytes, blocks = 16 * 65539, 37
+    g = torch.Generator(device="cuda").manual_seed(5)
+    src = torch.randint(0, 256, (nbytes,), dtype=torch.uint8, device="cuda", generator=g)
+    dst = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+    gpu_lib.stream_probe(2, src, dst, nbytes, blocks, nt)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, src)
+    gpu_lib.stream_probe(1, None, dst, nbytes, blocks, nt)
+    torch.cuda.synchronize()
+    words = dst.view(torch.int32).view(-1, 4).cpu().numpy()
+    assert (words == np.array([0x3F800000, 0, 0x3F800000, 0], dtype=np.int32)).all()
+    gpu_lib.stream_probe(0, src, dst, nbytes, blocks, nt)
+    torch.cuda.synchronize()
+    folds = dst[:16 * blocks].view(torch.int32).view(blocks, 4).cpu().numpy()
+    ref = np.bitwise_xor.reduce(src.view(torch.int32).view(-1, 4).cpu().numpy(), axis=0)
+    assert (np.bitwise_xor.reduce(folds, axis=0) == ref).all()
