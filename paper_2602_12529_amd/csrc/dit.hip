@@ -173,7 +173,7 @@ namespace {
 struct Plan {
   int64_t B, Ni, Nt, N, P;
   size_t rope, temb_in, c, tmp, condB, cond32, mods, ximg, xtxt, joint, y, qkv, q, k, vt, o, u, txth;
-  size_t e6, ctx1, ctxp, kvc, kc, vct, qd, sumsq, splitk, splitk_bytes, total;
+  size_t e6, ctx1, ctxp, kvc, kc, vct, qd, sumsq, splitk, splitk_bytes, rowmap, total;
 };
 
 Plan plan(const ff_dit& m, int64_t B, const int32_t grid[3], int64_t n_txt, int64_t n_prompts) {
@@ -218,6 +218,7 @@ Plan plan(const ff_dit& m, int64_t B, const int32_t grid[3], int64_t n_txt, int6
   p.sumsq = take(wan ? static_cast<size_t>(B) * p.Ni * (2 * H / 64) * 4 : 0);
   p.splitk_bytes = c.dtype == FF_BF16 ? gemm_split_bytes() : 0;
   p.splitk = take(p.splitk_bytes);
+  p.rowmap = take(static_cast<size_t>(row_classes_ints(B)) * 4);
   p.total = round_up(cv.off, 256);
   return p;
 }
@@ -267,8 +268,9 @@ NormArgs norm_args(const ff_dit_config& c, int64_t rows, const void* x, void* y,
 }
 
 SkinnyArgs skinny_args(int dtype, int64_t B, int64_t N, int64_t K, const float* in, int act_in, Lin l, float* out,
-                       int accumulate = 0, int act_out = ACT_NONE) {
+                       int accumulate = 0, int act_out = ACT_NONE, const int32_t* rowmap = nullptr) {
   SkinnyArgs s{};
+  s.rowmap = rowmap;
   s.dtype = dtype;
   s.B = B; s.N = N; s.K = K;
   s.in = in; s.ldi = K; s.act_in = act_in;
@@ -326,6 +328,7 @@ int dual_block(const ff_dit& m, const Plan& p, void* ws, int i, const float* c32
   const ff_dit_config& c = m.cfg;
   const int64_t H = c.hidden, F = c.mlp_hidden;
   const size_t es = dtype_size(c.dtype);
+  const int32_t* classes = reinterpret_cast<const int32_t*>(at(ws, p.rowmap));
   const Stream* st[2] = {&m.dual_txt[i], &m.dual_img[i]};
   const int64_t rows[2] = {p.B * p.Nt, p.B * p.Ni};
   const int64_t ntok[2] = {p.Nt, p.Ni};
@@ -337,7 +340,7 @@ int dual_block(const ff_dit& m, const Plan& p, void* ws, int i, const float* c32
   char* qkv_k[2] = {QKV, QKV + p.B * p.Nt * 3 * H * es};
   char* U[2] = {at(ws, p.u), at(ws, p.u) + p.B * p.Nt * F * es};
   for (int k = 0; k < 2; ++k) {
-    FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 6 * H, H, c32, ACT_SILU, st[k]->mod, mods[k]), s));
+    FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 6 * H, H, c32, ACT_SILU, st[k]->mod, mods[k], 0, ACT_NONE, classes), s));
     FF_TRY(norm_modulate(norm_args(c, rows[k], cur[k], Y + y_off[k] * es, mods[k], mods[k] + H, 6 * H, ntok[k]), s));
   }
   // QKV projections of both streams; the QK norm, rotation and relayout run in the GEMM epilogue
@@ -377,13 +380,14 @@ int single_block(const ff_dit& m, const Plan& p, void* ws, int j, const float* c
   const ff_dit_config& c = m.cfg;
   const int64_t H = c.hidden, F = c.mlp_hidden, W1 = 3 * H + F;
   const size_t es = dtype_size(c.dtype);
+  const int32_t* classes = reinterpret_cast<const int32_t*>(at(ws, p.rowmap));
   const Single& sb = m.single[j];
   float* mods = reinterpret_cast<float*>(at(ws, p.mods));
   const int64_t rows = p.B * p.N;
   char* Y = at(ws, p.y);
   char* H1 = at(ws, p.qkv);
   char* O = at(ws, p.o);
-  FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 3 * H, H, c32, ACT_SILU, sb.mod, mods), s));
+  FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 3 * H, H, c32, ACT_SILU, sb.mod, mods, 0, ACT_NONE, classes), s));
   FF_TRY(norm_modulate(norm_args(c, rows, X, Y, mods, mods + H, 3 * H, p.N), s));
   // [Q | K | V | MLP input] in one GEMM: Q, K, V of the joint sequence go to the attention layout
   // (text tokens unrotated, image tokens rotated by their grid position), GELU from column 3H.
@@ -644,6 +648,9 @@ int forward_mmdit(const ff_dit& m, const Plan& p, const void* x, const void* txt
     dst[1] = v_out;
   }
 
+  // Samples at the same time step with the same prompt share c, hence every modulation vector:
+  // the block GEMVs compute each distinct row of c once.
+  FF_TRY(row_classes(c32, p.B, H, reinterpret_cast<int32_t*>(at(ws, p.rowmap)), s));
   for (int i = 0; i < c.n_dual; ++i) {
     FF_TRY(dual_block(m, p, ws, i, c32, cur, dst, s));
     cur[0] = dst[0];
@@ -669,7 +676,8 @@ int forward_mmdit(const ff_dit& m, const Plan& p, const void* x, const void* txt
 
   if (latent) {
     float* mods = reinterpret_cast<float*>(at(ws, p.mods));
-    FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 2 * H, H, c32, ACT_SILU, m.final_mod, mods), s));
+    FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 2 * H, H, c32, ACT_SILU, m.final_mod, mods, 0, ACT_NONE,
+                                     reinterpret_cast<const int32_t*>(at(ws, p.rowmap))), s));
     char* Y = at(ws, p.y);
     FF_TRY(norm_modulate(norm_args(c, p.B * p.Ni, cur[1], Y, mods, mods + H, 2 * H, p.Ni), s));
     FF_TRY(gemm(gemm_args_ws(p, ws, c.dtype, p.B * p.Ni, c.in_channels, H, Y, H, m.final_proj, v_out, c.in_channels, EPI_NONE), s));

@@ -157,8 +157,13 @@ struct SkinnyArgs {
   float* out; int64_t ldo;
   int accumulate;             // 1: out += result
   int act_out;                // activation applied to the result (before accumulate)
+  const int32_t* rowmap;      // row classes of `in` from row_classes (device), or null: all rows
 };
 int skinny_linear(const SkinnyArgs& a, hipStream_t s);
+// Classes of bitwise-equal rows of c [B, H] fp32 into map (device int32, row_classes_ints(B)
+// entries), for skinny_linear to compute each distinct row once.
+int64_t row_classes_ints(int64_t B);
+int row_classes(const float* c, int64_t B, int64_t H, int32_t* map, hipStream_t s);
 
 // y = Norm(x) * mul + add per row; row r belongs to sample r / rows_per_sample.
 // mul = (1 + scale[b]) (if scale) * w (if w); add = shift[b] (if shift) + bias (if bias)

@@ -11,17 +11,109 @@ namespace {
 
 // ------------------------------------------------------------------ skinny linear
 // out[b, n] = act_out(sum_k W[n,k] act_in(in[b,k]) + bias[n]) (+ out[b, n] when accumulating).
-// Weight-bandwidth bound (B <= 16 samples per pass).  A block of four waves owns 4 R output
-// rows, R per wave; lanes stride over K in 8-element chunks.  K is walked in 512-wide slices:
-// the block stages act_in(in[b, slice]) for all its samples in LDS (the activation is evaluated
-// once per block, not once per wave), and each wave holds the raw weights of the next slice in
-// flight while it multiplies the current one against the staged inputs.
-constexpr int kSkSlice = 512, kSkMaxB = 16;
+// Weight-bandwidth bound.  A block of four waves owns 4 R output rows, R per wave; lanes stride
+// over K in 8-element chunks.  K is walked in 512-wide slices: the block stages act_in(in[b,
+// slice]) for its input rows in LDS (the activation is evaluated once per block, not once per
+// wave), and each wave holds the raw weights of the next slice in flight while it multiplies the
+// current one against the staged inputs.
+//
+// Input rows are taken kSkCap at a time, one pass per blockIdx.y.  With a row map (row_classes)
+// the passes run over the classes of bitwise-equal input rows: each distinct row is computed
+// once and its result written to every sample of its class, so staging and multiply-adds scale
+// with the number of distinct rows.  A pass with L live rows runs the body compiled for exactly
+// L (a switch on L; the kernel's registers are those of the largest body).
+constexpr int kSkSlice = 512, kSkCap = 8;
+constexpr int64_t kClassMaxB = 64;   // row classes are searched for B <= 64, identity above
 
 __device__ __forceinline__ float act_apply(int act, float x) {
   if (act == ACT_SILU) return silu_f(x);
   if (act == ACT_GELU) return gelu_tanh_f(x);
   return x;
+}
+
+// Classes of bitwise-equal rows of c [B, H] (fp32).  map (int32, 2 + 3 B entries):
+//   map[0]                      U, the number of classes
+//   map[1 + j], j < U           first row of class j (ascending)
+//   map[1 + B + j], j <= U      start of class j in the member list
+//   map[2 + 2 B + m], m < B     members, grouped by class, ascending within a class
+// One block of 16 waves, one wave per row at a time.  Each row gets a 64-bit hash (a sum over
+// columns of a mixed (column, bits) word, so the order of the partial sums does not matter); a
+// row whose hash equals an earlier row's is compared with the first such row element by element
+// and joins its class only if every bit matches (a hash collision costs a missed merge, never a
+// wrong one).  For B > 64 every row is its own class (no search).
+__device__ __forceinline__ uint64_t mix64(uint64_t z) {   // splitmix64 finaliser
+  z += 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+__global__ __launch_bounds__(1024) void row_classes_kernel(const float* __restrict__ c, int64_t B, int64_t H,
+                                                           int32_t* __restrict__ map) {
+  int32_t* uniq = map + 1;
+  int32_t* offs = map + 1 + B;
+  int32_t* memb = map + 2 + 2 * B;
+  if (B > kClassMaxB) {
+    for (int64_t b = threadIdx.x; b < B; b += blockDim.x) {
+      uniq[b] = static_cast<int32_t>(b);
+      offs[b] = static_cast<int32_t>(b);
+      memb[b] = static_cast<int32_t>(b);
+    }
+    if (threadIdx.x == 0) { map[0] = static_cast<int32_t>(B); offs[B] = static_cast<int32_t>(B); }
+    return;
+  }
+  __shared__ unsigned long long hs[kClassMaxB];
+  __shared__ int rep[kClassMaxB], cls[kClassMaxB], cnt[kClassMaxB + 1];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6, waves = blockDim.x >> 6;
+  const uint32_t* cu = reinterpret_cast<const uint32_t*>(c);
+  // Lane l reads the 4-word groups l, l + 64, ... of a row (16-byte loads: H % 4 == 0 and c is
+  // 16-byte aligned, checked by the host).
+  for (int b = wave; b < B; b += waves) {
+    unsigned long long h = 0;
+#pragma unroll 12
+    for (int64_t k0 = 4 * lane; k0 < H; k0 += 256) {
+      const uint4 q = *reinterpret_cast<const uint4*>(cu + b * H + k0);
+      const uint32_t w4[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) h += mix64(static_cast<uint64_t>(k0 + i) << 32 | w4[i]);
+    }
+    for (int o = 32; o > 0; o >>= 1) h += __shfl_xor(h, o, 64);
+    if (lane == 0) hs[b] = h;
+  }
+  __syncthreads();
+  if (t < B) {
+    int r = t;
+    for (int o = 0; o < t; ++o)
+      if (hs[o] == hs[t]) { r = o; break; }
+    rep[t] = r;
+  }
+  __syncthreads();
+  for (int b = wave; b < B; b += waves) {   // confirm each candidate bit for bit
+    const int r = rep[b];
+    if (r == b) continue;
+    bool differ = false;
+#pragma unroll 12
+    for (int64_t k0 = 4 * lane; k0 < H; k0 += 256) {
+      const uint4 x = *reinterpret_cast<const uint4*>(cu + b * H + k0);
+      const uint4 y = *reinterpret_cast<const uint4*>(cu + r * H + k0);
+      differ |= x.x != y.x || x.y != y.y || x.z != y.z || x.w != y.w;
+    }
+    if (__ballot(differ) != 0 && lane == 0) rep[b] = b;
+  }
+  __syncthreads();
+  if (t == 0) {
+    int U = 0;
+    for (int b = 0; b < B; ++b) {
+      if (rep[b] == b) { uniq[U] = b; cnt[U] = 0; cls[b] = U++; }
+      else cls[b] = cls[rep[b]];
+      ++cnt[cls[b]];
+    }
+    int run = 0;
+    for (int j = 0; j < U; ++j) { offs[j] = run; const int n = cnt[j]; cnt[j] = run; run += n; }
+    offs[U] = run;
+    for (int b = 0; b < B; ++b) memb[cnt[cls[b]]++] = b;
+    map[0] = U;
+  }
 }
 
 // Step ST of the halving exchange of V per-lane values (compile-time trip counts throughout, so
@@ -41,15 +133,24 @@ __device__ __forceinline__ void halve_steps(float (&a)[V], int lane) {
   }
 }
 
+struct SkinnyPass {
+  const float* in; int64_t ldi; int act_in;
+  const void* W; const void* bias;
+  float* out; int64_t ldo; int64_t N, K;
+  int accumulate, act_out;
+  const int32_t* rowmap; int64_t B;
+};
+
+// One pass over BC input rows: slot b is class u0 + b of the row map (or sample u0 + b).
 template <bool BF16, int BC, int R>
-__global__ __launch_bounds__(256) void skinny_kernel(const float* __restrict__ in, int64_t ldi, int act_in,
-                                                     const void* __restrict__ W, const void* __restrict__ bias,
-                                                     float* __restrict__ out, int64_t ldo, int64_t N, int64_t K,
-                                                     int accumulate, int act_out) {
+__device__ __forceinline__ void skinny_pass(const SkinnyPass& a, int64_t u0, float (*xs)[kSkSlice]) {
   constexpr int WORDS = BF16 ? 4 : 8;           // 32-bit words of an 8-element chunk of a weight row
-  constexpr int XPT = BC * kSkSlice / 256;      // staged inputs per thread per slice (2 per sample)
-  static_assert(kSkSlice == 512, "two staged inputs per sample and thread");
-  __shared__ __attribute__((aligned(16))) float xs[BC][kSkSlice];
+  constexpr int XPT = BC * kSkSlice / 256;      // staged inputs per thread per slice (2 per row)
+  static_assert(kSkSlice == 512, "two staged inputs per row and thread");
+  const int64_t K = a.K, N = a.N;
+  int64_t row[BC];
+#pragma unroll
+  for (int b = 0; b < BC; ++b) row[b] = a.rowmap ? a.rowmap[1 + u0 + b] : u0 + b;
   const int lane = threadIdx.x & 63;
   const int64_t n0 = (static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6)) * R;
   const bool active = n0 < N;   // wave-uniform
@@ -65,17 +166,17 @@ __global__ __launch_bounds__(256) void skinny_kernel(const float* __restrict__ i
   auto fetch = [&](int64_t k0) {
     const int len = K - k0 < kSkSlice ? static_cast<int>(K - k0) : kSkSlice;
     if (len <= 0) return;
-    const float* src_x = in + k0 + threadIdx.x;
+    const float* src_x = a.in + k0 + threadIdx.x;
 #pragma unroll
-    for (int q = 0; q < XPT; ++q) {   // sample q / 2, column threadIdx.x + 256 (q % 2) of the slice
-      const int b = q >> 1, j = static_cast<int>(threadIdx.x) + ((q & 1) << 8);
-      xin[q] = j < len ? src_x[b * ldi + ((q & 1) << 8)] : 0.f;
+    for (int q = 0; q < XPT; ++q) {   // row q / 2, column threadIdx.x + 256 (q % 2) of the slice
+      const int j = static_cast<int>(threadIdx.x) + ((q & 1) << 8);
+      xin[q] = j < len ? src_x[row[q >> 1] * a.ldi + ((q & 1) << 8)] : 0.f;
     }
     if (!active || lane * 8 >= len) return;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const int64_t n = n0 + r < N ? n0 + r : N - 1;
-      const uint4* src = reinterpret_cast<const uint4*>(static_cast<const char*>(W) + (n * K + k0 + lane * 8) * (BF16 ? 2 : 4));
+      const uint4* src = reinterpret_cast<const uint4*>(static_cast<const char*>(a.W) + (n * K + k0 + lane * 8) * (BF16 ? 2 : 4));
 #pragma unroll
       for (int h = 0; h < WORDS / 4; ++h) {
         const uint4 u = src[h];
@@ -88,7 +189,7 @@ __global__ __launch_bounds__(256) void skinny_kernel(const float* __restrict__ i
     const int len = K - k0 < kSkSlice ? static_cast<int>(K - k0) : kSkSlice;
     __syncthreads();   // the previous slice has been consumed
 #pragma unroll
-    for (int q = 0; q < XPT; ++q) xs[q >> 1][threadIdx.x + ((q & 1) << 8)] = act_apply(act_in, xin[q]);
+    for (int q = 0; q < XPT; ++q) xs[q >> 1][threadIdx.x + ((q & 1) << 8)] = act_apply(a.act_in, xin[q]);
     float w[R][8];
 #pragma unroll
     for (int r = 0; r < R; ++r)
@@ -117,46 +218,56 @@ __global__ __launch_bounds__(256) void skinny_kernel(const float* __restrict__ i
   // half of its values that its lane bit selects and adds the partner's copy of that half, so the
   // V = R x BCP values (BCP = BC rounded up to a power of two, padded with zeros) need V - 1
   // shuffles instead of V x 6.  Afterwards lane l holds the full sum of value l >> (6 - S),
-  // i.e. one (row, sample) per lane, and stores it.
+  // i.e. one (row, slot) per lane, and stores it.  Every value is summed over the same lane
+  // tree (pairs differing in lane bit 32, then 16, ...), whatever its slot.
   constexpr int BCP = BC <= 1 ? 1 : BC <= 2 ? 2 : BC <= 4 ? 4 : BC <= 8 ? 8 : 16;
   constexpr int V = R * BCP;
   constexpr int S = V <= 1 ? 0 : V <= 2 ? 1 : V <= 4 ? 2 : V <= 8 ? 3 : V <= 16 ? 4 : V <= 32 ? 5 : 6;
   static_assert((1 << S) == V && S <= 6, "R x BCP must be a power of two up to 64");
-  float a[V];
+  float v[V];
 #pragma unroll
   for (int r = 0; r < R; ++r)
 #pragma unroll
-    for (int b = 0; b < BCP; ++b) a[r * BCP + b] = b < BC ? acc[r][b] : 0.f;
-  halve_steps<V, 0, S>(a, lane);
+    for (int b = 0; b < BCP; ++b) v[r * BCP + b] = b < BC ? acc[r][b] : 0.f;
+  halve_steps<V, 0, S>(v, lane);
 #pragma unroll
-  for (int o = 32 >> S; o > 0; o >>= 1) a[0] += __shfl_xor(a[0], o, 64);
-  const int v = lane >> (6 - S);
-  const int r = v / BCP, b = v % BCP;
+  for (int o = 32 >> S; o > 0; o >>= 1) v[0] += __shfl_xor(v[0], o, 64);
+  const int slot = lane >> (6 - S);
+  const int r = slot / BCP, b = slot % BCP;
   if (b < BC && n0 + r < N && (lane & ((1 << (6 - S)) - 1)) == 0) {
     const int64_t n = n0 + r;
-    float y = act_apply(act_out, a[0] + (bias ? ld1<BF16>(bias, n) : 0.f));
-    if (accumulate) y += out[b * ldo + n];
-    out[b * ldo + n] = y;
+    const float y = act_apply(a.act_out, v[0] + (a.bias ? ld1<BF16>(a.bias, n) : 0.f));
+    int m0 = 0, m1 = 1;
+    const int32_t* memb = nullptr;
+    if (a.rowmap) {
+      m0 = a.rowmap[1 + a.B + u0 + b];
+      m1 = a.rowmap[2 + a.B + u0 + b];
+      memb = a.rowmap + 2 + 2 * a.B;
+    }
+    for (int m = m0; m < m1; ++m) {
+      float* o = a.out + (memb ? memb[m] : u0 + b) * a.ldo + n;
+      *o = a.accumulate ? y + *o : y;
+    }
   }
 }
 
-template <bool BF16>
-int skinny_dispatch(const SkinnyArgs& a, int64_t b0, int bc, hipStream_t s) {
-  const float* in = a.in + b0 * a.ldi;
-  float* out = a.out + b0 * a.ldo;
-#define FF_SK(BCV, R)                                                                                      \
-  case BCV:                                                                                               \
-    hipLaunchKernelGGL((skinny_kernel<BF16, BCV, R>), dim3(static_cast<unsigned>((a.N + 4 * R - 1) / (4 * R))), \
-                       dim3(256), 0, s, in, a.ldi, a.act_in, a.W, a.bias, out, a.ldo, a.N, a.K, a.accumulate,   \
-                       a.act_out);                                                                        \
-    break;
-  switch (bc) {
-    FF_SK(1, 4) FF_SK(2, 4) FF_SK(3, 4) FF_SK(4, 4) FF_SK(5, 4) FF_SK(6, 4) FF_SK(7, 4) FF_SK(8, 4)
-    FF_SK(9, 4) FF_SK(10, 4) FF_SK(11, 4) FF_SK(12, 4) FF_SK(13, 4) FF_SK(14, 4) FF_SK(15, 4) FF_SK(16, 4)
-    default: return fail(FF_EUNSUPPORTED, "skinny_linear: chunk %d", bc);
+template <bool BF16, int R>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void skinny_kernel(SkinnyPass a) {
+  __shared__ __attribute__((aligned(16))) float xs[kSkCap][kSkSlice];
+  const int64_t U = a.rowmap ? a.rowmap[0] : a.B;
+  const int64_t u0 = static_cast<int64_t>(blockIdx.y) * kSkCap;
+  if (u0 >= U) return;   // uniform over the block: this pass has no rows
+  const int live = U - u0 < kSkCap ? static_cast<int>(U - u0) : kSkCap;
+  switch (live) {
+    case 1: skinny_pass<BF16, 1, R>(a, u0, xs); break;
+    case 2: skinny_pass<BF16, 2, R>(a, u0, xs); break;
+    case 3: skinny_pass<BF16, 3, R>(a, u0, xs); break;
+    case 4: skinny_pass<BF16, 4, R>(a, u0, xs); break;
+    case 5: skinny_pass<BF16, 5, R>(a, u0, xs); break;
+    case 6: skinny_pass<BF16, 6, R>(a, u0, xs); break;
+    case 7: skinny_pass<BF16, 7, R>(a, u0, xs); break;
+    default: skinny_pass<BF16, 8, R>(a, u0, xs); break;
   }
-#undef FF_SK
-  return FF_OK;
 }
 
 // ------------------------------------------------------------------ norm + modulate
@@ -646,15 +757,27 @@ __global__ __launch_bounds__(256) void quantize_fp8_kernel(const void* x, int64_
 
 }  // namespace
 
+int64_t row_classes_ints(int64_t B) { return 2 + 3 * B; }
+
+int row_classes(const float* c, int64_t B, int64_t H, int32_t* map, hipStream_t s) {
+  if (B == 0) return FF_OK;
+  if (H % 4 || !aligned16(c)) return fail(FF_EUNSUPPORTED, "row_classes: H=%lld must be a multiple of 4, c 16-byte aligned", (long long)H);
+  LaunchScope ls("row_classes", s, 0.0, 4.0 * (B * H + row_classes_ints(B)));
+  hipLaunchKernelGGL(row_classes_kernel, dim3(1), dim3(1024), 0, s, c, B, H, map);
+  return ls.status();
+}
+
 int skinny_linear(const SkinnyArgs& a, hipStream_t s) {
   if (a.B == 0 || a.N == 0) return FF_OK;
   if (a.K % 8 != 0 || a.ldi % 4 != 0) return fail(FF_EUNSUPPORTED, "skinny_linear: K=%lld must be a multiple of 8", (long long)a.K);
   LaunchScope ls("skinny_linear", s, 2.0 * a.B * a.N * a.K,
                  static_cast<double>(dtype_size(a.dtype)) * a.N * a.K + 4.0 * a.B * (a.K + a.N));
-  for (int64_t b0 = 0; b0 < a.B; b0 += kSkMaxB) {
-    const int bc = static_cast<int>(a.B - b0 < kSkMaxB ? a.B - b0 : kSkMaxB);
-    FF_TRY(a.dtype == FF_BF16 ? skinny_dispatch<true>(a, b0, bc, s) : skinny_dispatch<false>(a, b0, bc, s));
-  }
+  // R output rows per wave: 4 for bf16 weights, 2 for fp32 (twice the words per chunk).
+  const SkinnyPass k{a.in, a.ldi, a.act_in, a.W, a.bias, a.out, a.ldo, a.N, a.K, a.accumulate, a.act_out, a.rowmap, a.B};
+  const int R = a.dtype == FF_BF16 ? 4 : 2;
+  const dim3 grid(static_cast<unsigned>((a.N + 4 * R - 1) / (4 * R)), static_cast<unsigned>((a.B + kSkCap - 1) / kSkCap));
+  if (a.dtype == FF_BF16) hipLaunchKernelGGL((skinny_kernel<true, 4>), grid, dim3(256), 0, s, k);
+  else hipLaunchKernelGGL((skinny_kernel<false, 2>), grid, dim3(256), 0, s, k);
   return ls.status();
 }
 

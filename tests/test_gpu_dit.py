@@ -146,6 +146,71 @@ def test_bf16_latent_with_single_blocks_and_pooled(gpu_lib):
         assert np.max(np.abs(host(res.logp[k]) - lp_ref)) <= LOGP_ABS
 
 
+@pytest.mark.parametrize("B,n_same", [(24, 6), (8, 8), (66, 4)], ids=["21-classes", "1-class", "B66-no-search"])
+def test_modulation_row_classes(gpu_lib, B, n_same):
+    """The adaLN GEMVs compute each distinct conditioning row once and write it to every sample of
+    its class (Eq. 1's v depends on a sample's c = f(t, prompt) only).  Samples 0 .. n_same - 1 share
+    t; the rest have their own t; prompts cycle over three (one prompt when all share t), so the
+    classes are not contiguous and with B = 24 there are 21 of them (more than one 16-row pass).  B = 66 is past the class search
+    (every row its own class).  Parity against the oracle per sample, and samples with the same
+    (x, t, prompt) give bitwise equal velocities."""
+    m = C.ModelConfig(model=C.MODEL_MMDIT, io_mode=C.IO_LATENT, dtype=C.BF16, n_dual=1, n_single=1, hidden=256,
+                      heads=2, head_dim=128, mlp_hidden=512, in_channels=64, txt_dim=128, pooled_dim=64,
+                      rope_axes=(16, 56, 56))
+    w = C.Workload(name="small-latent-classes", index=17, model=m, prompts=3, group=B // 3 + (B % 3 > 0),
+                   grid=(1, 4, 8), n_txt=16, steps=1)
+    say("row classes", B, n_same)
+    W = synth.weights(w)
+    txt = synth.text_input(w)
+    cond = synth.cond_input(w)
+    x0 = synth.x0(w)[:B].copy()
+    tidx = (np.arange(B) % 3 if n_same < B else np.zeros(B)).astype(np.int32)
+    t = np.array([0.6] * n_same + list(np.linspace(0.95, 0.05, B - n_same)), dtype=np.float32)
+    x0[3] = x0[0]   # sample 3: same x, t and prompt as sample 0
+    Wd = {k: dev(v, m.dtype) for k, v in W.items()}
+    dit = api.Dit(m, Wd)
+    X = dev(x0, m.dtype)
+    v = torch.empty_like(X)
+    dit.forward(X, dev(txt, m.dtype), w.grid, v, t=torch.from_numpy(t).cuda(), cond=dev(cond, m.dtype),
+                txt_index=torch.from_numpy(tidx).cuda())
+    torch.cuda.synchronize()
+    got = host(v)
+    assert np.array_equal(got[3], got[0])
+    ref = odit.forward(m, W, x0, txt, t=t.astype(np.float64), cond=cond, txt_index=tidx, grid=w.grid)
+    check(got, ref, C.BF16, model_stages(m), what=f"row classes B={B} shared={n_same}")
+
+
+def test_modulation_row_classes_hidden_mode(gpu_lib):
+    """Hidden mode takes c per sample.  Rows 0, 1 are equal; row 2 equals row 0 except in its last
+    column (+3), and row 4 equals row 2: the classes are {0, 1}, {2, 4}, {3}, {5}.  A merge of
+    rows that differ anywhere would give samples 2 and 4 the modulation of sample 0."""
+    w = _small_hidden()
+    m = w.model.replace(n_dual=1, n_single=1)
+    w = C.Workload(**{**w.__dict__, "model": m, "group": 6})
+    W, txt, cond, x0, _ = _inputs(w)
+    cond = cond.copy(); txt = txt.copy(); x0 = x0.copy()
+    cond[1] = cond[0]
+    cond[2] = cond[0]
+    cond[2, -1] += 3.0
+    cond[4] = cond[2]
+    for a, b in ((1, 0), (4, 2)):
+        txt[a] = txt[b]
+        x0[a] = x0[b]
+    Wd, T, Cd, X0, _ = _device(w, W, txt, cond, x0, [])
+    dit = api.Dit(m, Wd)
+    v = torch.empty_like(X0)
+    tout = torch.empty_like(T)
+    dit.forward(X0, T, w.grid, v, cond=Cd, txt_out=tout)
+    torch.cuda.synchronize()
+    got = host(v)
+    assert np.array_equal(got[1], got[0]) and np.array_equal(got[4], got[2])
+    img, tx = odit.forward(m, W, x0, txt, cond=cond, grid=w.grid)
+    check(got, img, C.BF16, model_stages(m), what="row classes hidden img")
+    check(host(tout), tx, C.BF16, model_stages(m), what="row classes hidden txt")
+    # the +3 in one column of c does change the result
+    assert np.max(np.abs(img[2] - img[0])) > 1e-2
+
+
 def _small_latent_stack():
     m = C.ModelConfig(model=C.MODEL_MMDIT, io_mode=C.IO_LATENT, dtype=C.BF16, n_dual=1, n_single=1, hidden=256,
                       heads=2, head_dim=128, mlp_hidden=512, in_channels=64, txt_dim=128, pooled_dim=64,
