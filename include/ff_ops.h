@@ -93,8 +93,9 @@ int ff_stream_probe(int32_t mode, int32_t nontemporal, const void* src, void* ds
  * For each row r of x [rows, cols] (dtype, row stride ldx elements): amax = max |x[r, :]|,
  * q[r, :] = round-to-nearest-even(x[r, :] * fl32(448 / amax)) as codes (uint8, row stride ldq
  * bytes; a value that rounds to zero keeps its sign bit) and d[r] = fl32(amax / 448) (float32), so
- * that x[r, k] ~ d[r] * decode(q[r, k]); a row of zeros gets codes 0 and d = 0.  Non-finite
- * inputs give unspecified codes.  cols, ldx, ldq % 8 == 0; x and q 16-byte aligned. */
+ * that x[r, k] ~ d[r] * decode(q[r, k]).  A row with amax < 448 * 2^-126 (a row of zeros
+ * included) gets codes 0 and d = 0; a row holding an infinity or a NaN gets the NaN code 0x7f in
+ * every position and d = NaN.  cols, ldx, ldq % 8 == 0; x and q 16-byte aligned. */
 int ff_quantize_fp8(const void* x, int64_t ldx, uint8_t* q, int64_t ldq, float* d, int64_t rows, int64_t cols,
                     int32_t dtype, void* stream);
 

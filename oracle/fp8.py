@@ -17,11 +17,15 @@ bit 0 is clear), in magnitude, then the sign bit; a negative value that rounds
 to zero gives 0x80.  Magnitudes at or above 464 (halfway from 448 to the next
 binade step) are out of range: the quantiser below never produces them.
 
-Quantisation of a row x (float32 values): amax = max |x|; when amax > 0,
-mult = fl32(448 / amax), codes = encode(fl32(x * mult)) and the dequantisation
-scale is d = fl32(amax / 448); a zero row gets codes 0 and d = 0.  Every
-float32 step is one IEEE operation rounded to nearest even, so codes are
-reproducible bit for bit on any IEEE machine.
+Quantisation of a row x (float32 values): amax = max |x|; when amax >= A_MIN =
+448 * 2^-126, mult = fl32(448 / amax), codes = encode(fl32(x * mult)) and the
+dequantisation scale is d = fl32(amax / 448).  Every float32 step is one IEEE
+operation rounded to nearest even, so codes are reproducible bit for bit on any
+IEEE machine.  Two kinds of row fall outside that rule, by convention of this
+scheme: a row with amax < A_MIN (zero rows included) gets codes 0 and d = 0 (its
+entries are below 2^-117, and the bound keeps 448 / amax and amax / 448 finite
+and normal); a row holding an infinity or a NaN gets the NaN code 0x7f in every
+position and d = NaN.
 
 Linear layer: out[m, n] = epi(d_a[m] * d_w[n] * sum_k dec(A[m, k]) dec(W[n, k])
 + bias[n]) with epi the identity or GELU-tanh.  The sum is formed exactly in
@@ -33,6 +37,7 @@ from __future__ import annotations
 import numpy as np
 
 MAX_E4M3 = 448.0
+A_MIN = np.float32(448.0 * 2.0 ** -126)    # smallest amax quantised; rows below it are zero rows
 
 
 def decode_table() -> np.ndarray:
@@ -80,14 +85,16 @@ def encode(y) -> np.ndarray:
 def quantize_rows(x: np.ndarray):
     """Rows of x [R, C] -> (codes uint8 [R, C], d float32 [R]) by the scheme in the module docstring."""
     x = np.asarray(x, dtype=np.float32)
-    if not np.all(np.isfinite(x)):
-        raise ValueError("quantize_rows: non-finite input")
     R = x.shape[0]
     codes = np.zeros(x.shape, dtype=np.uint8)
     d = np.zeros(R, dtype=np.float32)
     for r in range(R):
+        if not np.all(np.isfinite(x[r])):
+            codes[r] = 0x7F
+            d[r] = np.float32(np.nan)
+            continue
         amax = np.float32(np.max(np.abs(x[r]))) if x.shape[1] else np.float32(0)
-        if amax > 0:
+        if amax >= A_MIN:
             mult = np.float32(MAX_E4M3) / amax
             codes[r] = encode(x[r] * mult)
             d[r] = amax / np.float32(MAX_E4M3)

@@ -726,21 +726,26 @@ __global__ __launch_bounds__(256) void quantize_fp8_kernel(const void* x, int64_
   const int64_t r = blockIdx.x;
   const int tid = threadIdx.x;
   const int64_t n8 = cols / 8;
-  float amax = 0.f;
+  float amax = 0.f;   // a NaN counts as +inf, so that any non-finite entry marks the row
   for (int64_t c = tid; c < n8; c += 256) {
     float v[8];
     ld8<BF16>(x, r * ldx + c * 8, v);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf(v[e]));
+    for (int e = 0; e < 8; ++e) amax = fmaxf(amax, __builtin_isnan(v[e]) ? INFINITY : fabsf(v[e]));
   }
   amax = wave_max(amax);
   if ((tid & 63) == 0) part[tid >> 6] = amax;
   __syncthreads();
   amax = fmaxf(fmaxf(part[0], part[1]), fmaxf(part[2], part[3]));
-  if (tid == 0) d[r] = amax / 448.0f;
+  // Rows below 448 * 2^-126 (zero rows included) are zero rows: codes 0, d = 0.  A row with an
+  // infinity or a NaN: NaN code 0x7f everywhere, d = NaN.
+  constexpr float kAmin = 448.0f * 0x1p-126f;
+  const bool tiny = amax < kAmin, nonfinite = amax == INFINITY;
+  if (tid == 0) d[r] = nonfinite ? __uint_as_float(0x7fc00000u) : tiny ? 0.f : amax / 448.0f;
   uint8_t* qr = q + r * ldq;
-  if (amax == 0.f) {   // a zero row: codes 0 (also for negative zeros)
-    for (int64_t c = tid; c < n8; c += 256) *reinterpret_cast<uint2*>(qr + c * 8) = make_uint2(0u, 0u);
+  if (tiny || nonfinite) {
+    const uint32_t fill = nonfinite ? 0x7f7f7f7fu : 0u;
+    for (int64_t c = tid; c < n8; c += 256) *reinterpret_cast<uint2*>(qr + c * 8) = make_uint2(fill, fill);
     return;
   }
   const float mult = 448.0f / amax;

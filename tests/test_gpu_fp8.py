@@ -24,6 +24,15 @@ def _rows(seed, R, Cn, code):
         x[2] = -0.0
         x[3, :] = 0.0
         x[3, 5] = -3.5e-3                  # a single entry: it maps to -448, the rest to zeros
+    if R > 8:                              # rows outside the ordinary rule (see oracle.fp8)
+        amin = np.float32(448.0 * 2.0 ** -126)
+        x[4] = x[4] * np.float32(1e-40)    # amax far below 448 * 2^-126: a zero row
+        x[5] = 0.0
+        x[5, 1] = amin                     # exactly at the bound: quantised, d = 2^-126
+        x[5, 2] = -amin / 4
+        x[6, 7] = np.inf
+        x[7, 0] = np.nan
+        x[8, 3] = -np.inf
     if code == C.BF16:      # the values the device holds
         x = torch.from_numpy(x).to(torch.bfloat16).to(torch.float32).numpy()
     return x

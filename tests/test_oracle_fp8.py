@@ -74,6 +74,30 @@ def test_quantize_rows_error_bound_and_edges():
         assert np.all(err <= bound)
 
 
+def test_quantize_rows_out_of_range_rows():
+    """Rows below A_MIN = 448 * 2^-126 are zero rows; at A_MIN the scale is exactly 2^-126 and
+    mult exactly 2^126 (both powers of two, so the codes are those of x * 2^126); a row holding
+    an infinity or a NaN is all NaN codes with d = NaN."""
+    amin = np.float32(448.0 * 2.0 ** -126)
+    x = np.zeros((6, 16), dtype=np.float32)
+    x[0, 3] = np.float32(1e-37)                        # below A_MIN: a zero row
+    x[1, 3] = -np.nextafter(amin, np.float32(0))       # just below, negative
+    x[2, 3] = amin                                     # the smallest row quantised
+    x[2, 7] = -amin / np.float32(4)
+    x[3] = 1.0
+    x[3, 5] = np.inf
+    x[4] = 1.0
+    x[4, 9] = np.nan
+    x[5, 0] = -np.inf
+    codes, d = F.quantize_rows(x)
+    assert np.all(codes[:2] == 0) and np.all(d[:2] == 0)
+    assert d[2] == np.float32(2.0 ** -126)
+    assert codes[2, 3] == 0x7E and codes[2, 7] == F.encode(np.float32(-112.0)) and codes[2, 7] == 0xEE
+    assert np.count_nonzero(codes[2]) == 2
+    assert np.all(codes[3:] == 0x7F) and np.all(np.isnan(d[3:]))
+    assert F.A_MIN == amin
+
+
 def test_linear_fp8_exact_on_integer_codes():
     rng = np.random.default_rng(9)
     ints = np.array([0, 1, 2, 3, 4, 6, 8, 12, 16])
