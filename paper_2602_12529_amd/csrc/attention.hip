@@ -54,12 +54,16 @@ typedef __attribute__((address_space(1))) void glb_t;
 
 // ------------------------------------------------------------------ bf16
 // Each wave's work is ordered so the matrix core and the vector ALUs overlap
-// inside one wave: while the MFMAs of S = K Q^T for tile i + 1 run, the softmax of tile i
-// (exp2, row sums, bf16 packing) is issued between them; while the MFMAs of
-// O += V P^T for tile i - 1 run, the row max of tile i is taken.  K / V^T tiles
-// come through a ring of STAGES LDS buffers filled STAGES - 1 tiles ahead by
-// direct loads; loads past the last tile replay it into a buffer that is never
-// read again, so the number of loads in flight is the same on every tile.
+// inside one wave: the softmax of tile i (exp2, bf16 packing, row sums) is split
+// evenly over the MFMAs of O += V P^T for tile i - 1 and those of S = K Q^T for
+// tile i + 1, one score per MFMA.  There is no per-score row max: P is exp2 of
+// (score - m) with a lagging running max m, and a tile whose row sum on some lane
+// exceeds 256 is redone after m moves to the tile's max (rare after the first
+// tile, which starts from its own max).  K / V^T tiles come through a ring of
+// STAGES LDS buffers filled STAGES - 1 tiles ahead by direct loads, issued one at
+// a time between the S MFMAs; loads past the last tile replay it into a buffer
+// that is never read again, so the number of loads in flight is the same on
+// every tile.
 template <int WAVES, int STAGES>
 __global__ __launch_bounds__(WAVES * 64, 1) void attn_bf16_d128(AttnParams p) {
   constexpr int K_INS = K_STAGE / 1024 / WAVES;   // 1 KB direct loads per wave per K tile
@@ -119,19 +123,22 @@ __global__ __launch_bounds__(WAVES * 64, 1) void attn_bf16_d128(AttnParams p) {
   };
 #pragma clang diagnostic pop
   const uint32_t smem_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
-  auto issue = [&](int tile) {
+  // Load j (0 .. LPW - 1) of this wave's share of tile `tile`: K loads first, then V^T.
+  auto issue_one = [&](int tile, int j) {
     const int kv0 = (tile < ntiles ? tile : ntiles - 1) * KT;
     const uint32_t base = smem_base + static_cast<uint32_t>((tile % STAGES) * STAGE);
-#pragma unroll
-    for (int i = 0; i < K_INS; ++i) {
-      const int key = kv0 + k_row[i] < n_kv ? kv0 + k_row[i] : n_kv - 1;
-      dma16(Kb + key * D + k_ck[i] * 8, __builtin_amdgcn_readfirstlane(base + (i * WAVES + wave) * 1024));
-    }
-#pragma unroll
-    for (int i = 0; i < V_INS; ++i) {
+    if (j < K_INS) {
+      const int key = kv0 + k_row[j] < n_kv ? kv0 + k_row[j] : n_kv - 1;
+      dma16(Kb + key * D + k_ck[j] * 8, __builtin_amdgcn_readfirstlane(base + (j * WAVES + wave) * 1024));
+    } else {
+      const int i = j - K_INS;
       const int col = kv0 + v_ck[i] * 8 < n_kv ? kv0 + v_ck[i] * 8 : n_kv - 8;
       dma16(Vb + v_row[i] * n_kv + col, __builtin_amdgcn_readfirstlane(base + K_STAGE + (i * WAVES + wave) * 1024));
     }
+  };
+  auto issue = [&](int tile) {
+#pragma unroll
+    for (int j = 0; j < LPW; ++j) issue_one(tile, j);
   };
 
   f32x16_t o[4];
@@ -144,7 +151,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void attn_bf16_d128(AttnParams p) {
 
   // The two halves of a tile step are written out as 16 fused steps, fenced so the
   // compiler keeps the order: each issues one MFMA, the LDS read of the fragment six
-  // steps ahead, and the vector work of two scores.
+  // steps ahead, and the softmax of one score of the current tile.
   constexpr int AHEAD = 6;
   // K fragment f = (t, kb) of S^T = K Q^T: K rows 32 kb + krow, d slots 16 t + 8 g.
   auto k_frag = [&](const char* Ks, int f) {
@@ -154,24 +161,50 @@ __global__ __launch_bounds__(WAVES * 64, 1) void attn_bf16_d128(AttnParams p) {
   auto v_frag = [&](const char* Vs, int f) {
     return *reinterpret_cast<const bf16x8_t*>(Vs + v_off(32 * (f & 3) + ql, 2 * (f >> 2) + g));
   };
-  // Score i (0..31) of a tile: s[i / 16][i % 16]; its P slot is pf[i / 8][i % 8].
-  // O += V P^T of tile `tile` with the row max of `s` (log2 units, both lane halves).
-  auto pv_max = [&](int tile, const bf16x8_t (&pf)[4], const f32x16_t (&s)[2]) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+  // Score i (0..31) of a tile: s[i / 16][i % 16]; its P slot is pf[i / 8][i % 8].  The offsets
+  // nm[g8] = -m (or -inf for a group of 8 keys past n_kv).  Odd scores pack the pair into its
+  // P slots and add both bf16 values to the tile's row sum lt (so l sums the P that O uses).
+  float e_even = 0.f;
+  auto soft = [&](int i, const f32x16_t (&s)[2], bf16x8_t (&pf)[4], const float (&nm)[4], float& lt) {
+    const float e = __builtin_amdgcn_exp2f(fmaf(s[i >> 4][i & 15], p.scale_log2, nm[i >> 3]));
+    if (i & 1) {
+      const bf16x2_t pr = {static_cast<__bf16>(e_even), static_cast<__bf16>(e)};
+      pf[i >> 3][(i & 7) - 1] = pr[0];
+      pf[i >> 3][i & 7] = pr[1];
+      lt = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, lt, false);
+    } else {
+      e_even = e;
+    }
+  };
+  auto offsets = [&](int tile, float (&nm)[4]) {
+    const int kv0 = tile * KT;
+#pragma unroll
+    for (int gi = 0; gi < 4; ++gi) nm[gi] = kv0 + 8 * (2 * gi + g) < n_kv ? -m_run : -INFINITY;
+  };
+  auto mfma_o = [](f32x16_t& acc, const bf16x8_t& a, const bf16x8_t& b) {
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
+  };
+  // O += V P^T of tile `tile` (P in pf) with the softmax of scores 0..15 of the next tile.
+  auto pv_soft = [&](int tile, const bf16x8_t (&pf)[4], const f32x16_t (&s)[2], bf16x8_t (&pn)[4],
+                     const float (&nm)[4], float& lt) {
     const char* Vs = smem + (tile % STAGES) * STAGE + K_STAGE;
     bf16x8_t vf[16];
-    float mx0 = -INFINITY, mx1 = -INFINITY;
 #pragma unroll
     for (int f = 0; f < AHEAD; ++f) vf[f] = v_frag(Vs, f);
 #pragma unroll
     for (int f = 0; f < 16; ++f) {
-      o[f & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[f], pf[f >> 2], o[f & 3], 0, 0, 0);
+      mfma_o(o[f & 3], vf[f], pf[f >> 2]);
       if (f + AHEAD < 16) vf[f + AHEAD] = v_frag(Vs, f + AHEAD);
-      mx0 = fmaxf(mx0, s[f >> 3][(2 * f) & 15]);
-      mx1 = fmaxf(mx1, s[f >> 3][(2 * f + 1) & 15]);
+      soft(f, s, pn, nm, lt);
       __builtin_amdgcn_sched_barrier(0);
     }
-    const float mx = fmaxf(mx0, mx1);
-    return fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.scale_log2;
+  };
+  auto pv = [&](int tile, const bf16x8_t (&pf)[4]) {
+    const char* Vs = smem + (tile % STAGES) * STAGE + K_STAGE;
+#pragma unroll
+    for (int f = 0; f < 16; ++f) mfma_o(o[f & 3], v_frag(Vs, f), pf[f >> 2]);
   };
   auto rowmax = [&](const f32x16_t (&s)[2]) {
     float mx = -INFINITY;
@@ -181,49 +214,25 @@ __global__ __launch_bounds__(WAVES * 64, 1) void attn_bf16_d128(AttnParams p) {
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
     return fmaxf(mx, __shfl_xor(mx, 32, 64)) * p.scale_log2;
   };
-  // Lazy rescale: O and l move to a new max only when some lane's max grew by more than 8.
-  auto rescale = [&](float mx) {
-    if (__any(mx > m_run + 8.0f)) {
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
-      l_run *= alpha;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
-    }
-  };
-  // S of tile `next` with P = exp2(S_cur scale - m) of tile `tile` into bf16 operand slots and
-  // l += row sums.  A group of 8 keys past n_kv gets the offset -inf, so its P is 0.
-  auto qk_softmax = [&](int next, f32x16_t (&s_nxt)[2], int tile, const f32x16_t (&s)[2], bf16x8_t (&pf)[4]) {
+  // S of tile `next` with the softmax of scores 16..31 of the current tile.
+  auto qk_soft = [&](int next, f32x16_t (&s_nxt)[2], const f32x16_t (&s)[2], bf16x8_t (&pf)[4],
+                     const float (&nm)[4], float& lt, int load_tile) {
     const char* Ks = smem + (next % STAGES) * STAGE;
-    const int kv0 = tile * KT;
-    float nm[4];
-#pragma unroll
-    for (int gi = 0; gi < 4; ++gi) nm[gi] = kv0 + 8 * (2 * gi + g) < n_kv ? -m_run : -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) s_nxt[kb][r] = 0.f;
     bf16x8_t kf[16];
-    float lsum0 = 0.f, lsum1 = 0.f;
 #pragma unroll
     for (int f = 0; f < AHEAD; ++f) kf[f] = k_frag(Ks, f);
 #pragma unroll
     for (int f = 0; f < 16; ++f) {
       s_nxt[f & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[f], qf[f >> 1], s_nxt[f & 1], 0, 0, 0);
       if (f + AHEAD < 16) kf[f + AHEAD] = k_frag(Ks, f + AHEAD);
-      const int i0 = 2 * f, i1 = 2 * f + 1;   // scores i0, i1: same 8-key group i0 / 8
-      const float e0 = __builtin_amdgcn_exp2f(fmaf(s[i0 >> 4][i0 & 15], p.scale_log2, nm[i0 >> 3]));
-      const float e1 = __builtin_amdgcn_exp2f(fmaf(s[i1 >> 4][i1 & 15], p.scale_log2, nm[i1 >> 3]));
-      lsum0 += e0;
-      lsum1 += e1;
-      pf[i0 >> 3][i0 & 7] = static_cast<__bf16>(e0);
-      pf[i1 >> 3][i1 & 7] = static_cast<__bf16>(e1);
+      if (f % (16 / LPW) == 1) issue_one(load_tile, f / (16 / LPW));
+      soft(16 + f, s, pf, nm, lt);
       __builtin_amdgcn_sched_barrier(0);
     }
-    l_run += lsum0 + lsum1;
   };
   auto qk = [&](int tile, f32x16_t (&s)[2]) {
     const char* Ks = smem + (tile % STAGES) * STAGE;
@@ -234,6 +243,25 @@ __global__ __launch_bounds__(WAVES * 64, 1) void attn_bf16_d128(AttnParams p) {
 #pragma unroll
     for (int f = 0; f < 16; ++f) s[f & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k_frag(Ks, f), qf[f >> 1], s[f & 1], 0, 0, 0);
   };
+  // The running max m lags: every P of a tile is exp2 of (score - m), and a tile whose row sum
+  // on some lane exceeds 256 (a score more than 8 above m, in log2 units, or enough scores near
+  // it) is redone: m moves to the tile's max, O and l are rescaled, and the tile's P recomputed.
+  // The first tile starts from its own max.
+  auto redo = [&](int tile, const f32x16_t (&s)[2], bf16x8_t (&pf)[4], float& lt) {
+    const float m_new = fmaxf(m_run, rowmax(s));
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    l_run *= alpha;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[i][r] *= alpha;
+    float nm[4];
+    offsets(tile, nm);
+    lt = 0.f;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) soft(i, s, pf, nm, lt);
+  };
   auto wait_next = [&]() {   // tile it + 1 has landed in every wave's view
     if constexpr (STAGES == 3) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     else asm volatile("s_waitcnt vmcnt(%0)" ::"n"((STAGES - 3) * LPW) : "memory");
@@ -241,17 +269,26 @@ __global__ __launch_bounds__(WAVES * 64, 1) void attn_bf16_d128(AttnParams p) {
     asm volatile("s_barrier" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
   };
-  // Tile it: [O += V P^T of tile it - 1 | row max of tile it], rescale, wait for tile it + 1,
-  // issue tile it + STAGES - 1, [S of tile it + 1 | softmax of tile it].
+  // Tile it: [O += V P^T of tile it - 1 | softmax of half of tile it], wait for tile it + 1,
+  // issue tile it + STAGES - 1, [S of tile it + 1 | softmax of the other half of tile it], check.
   auto iter = [&](int it, f32x16_t (&s_cur)[2], f32x16_t (&s_nxt)[2], const bf16x8_t (&p_prev)[4],
                   bf16x8_t (&p_cur)[4], bool first) {
-    const float mx = first ? rowmax(s_cur) : pv_max(it - 1, p_prev, s_cur);
+    float nm[4];
+    if (first) m_run = rowmax(s_cur);
+    offsets(it, nm);
+    float lt = 0.f;
+    if (first) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) soft(i, s_cur, p_cur, nm, lt);
+    } else {
+      pv_soft(it - 1, p_prev, s_cur, p_cur, nm, lt);
+    }
     __builtin_amdgcn_sched_barrier(0);
-    rescale(mx);
     wait_next();
-    issue(it + STAGES - 1);
     __builtin_amdgcn_sched_barrier(0);
-    qk_softmax(it + 1, s_nxt, it, s_cur, p_cur);   // past the last tile: replayed data, unused
+    qk_soft(it + 1, s_nxt, s_cur, p_cur, nm, lt, it + STAGES - 1);   // past the last tile: replayed data, unused
+    if (__any(lt > 256.0f)) redo(it, s_cur, p_cur, lt);
+    l_run += lt;
   };
 
 #pragma unroll
@@ -271,9 +308,9 @@ __global__ __launch_bounds__(WAVES * 64, 1) void attn_bf16_d128(AttnParams p) {
   }
   if (it < ntiles) {
     iter(it, sB, sA, pA, pB, false);
-    pv_max(it, pB, sA);
+    pv(it, pB);
   } else {
-    pv_max(ntiles - 1, pA, sA);
+    pv(ntiles - 1, pA);
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // replayed loads may still target LDS
 

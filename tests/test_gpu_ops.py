@@ -155,6 +155,40 @@ def test_attention_cross_shape(gpu_lib):
           norm_tol=1e-2)
 
 
+@pytest.mark.parametrize("pattern", ["rising", "late-spike", "flat-high", "huge"])
+def test_attention_running_max_moves(gpu_lib, pattern):
+    """The softmax keeps a lagging running max and redoes a 64-key tile whose row sum passes 256.
+    Scores that keep rising over the keys (the max moves by more than 8 in log2 units tile after
+    tile), a spike in a late tile, many keys tied near the top (row sums large with no single
+    large score) and scores in the thousands must all give the exact softmax."""
+    B, h, N, d = 1, 2, 704, 128
+    q, k, v = (normal(50 + i, (B, h, N, d), C.BF16) for i in range(3))
+    # every query gets a component along u (|u|^2 = d); key j one of beta_j, which adds about
+    # 16 beta_j to its scores in log2 units (beta_j d / sqrt(d) * log2(e))
+    u = np.ones(d)
+    q = q.astype(np.float64) + u
+    k = k.astype(np.float64)
+    beta = np.zeros(N)
+    if pattern == "rising":
+        beta = np.linspace(0.0, 6.0, N)             # the max moves ~9 per tile: redone tile after tile
+    elif pattern == "late-spike":
+        beta[600:606] = 3.0                         # ~+49 in tile 9
+    elif pattern == "flat-high":
+        beta[128:320] = 0.7                         # ~+11 on 192 keys: row sums past 256, no single P > 256
+    else:
+        q, k = q * 8.0, k * 8.0                     # scores in the thousands
+    k = k + beta[None, None, :, None] * u
+    q = synth.bf16_round(q.astype(np.float32))
+    k = synth.bf16_round(k.astype(np.float32))
+    out = torch.empty((B, N, h * d), dtype=torch.bfloat16, device="cuda")
+    gpu_lib.attention(dev(q, C.BF16), dev(k, C.BF16), dev(v, C.BF16).transpose(-1, -2).contiguous(), out)
+    torch.cuda.synchronize()
+    got = host(out)
+    assert np.all(np.isfinite(got))
+    check(got, odit.merge_heads(odit.attention(q, k, v)), C.BF16, 1, N, what=f"attention max moves ({pattern})",
+          norm_tol=1e-2)
+
+
 NORM = [(37, 3072, C.BF16), (10, 64, C.F32), (9, 200, C.BF16), (8, 1536, C.BF16), (5, 96, C.F32)]
 
 
