@@ -74,9 +74,22 @@ int ff_rope_table(float* out, const int32_t grid[3], int32_t head_dim, const int
 
 /* out[b, n] = act_out(sum_k W[n,k] act_in(in[b,k]) + bias[n]) for skinny batches
  * (the adaLN modulation and embedding MLPs).  in float32 [B, K], out float32
- * [B, N], W of dtype [N, K]; act: 0 none, 1 SiLU, 2 GELU_tanh. */
+ * [B, N], W of dtype [N, K]; act: 0 none, 1 SiLU, 2 GELU_tanh.  classes: NULL, or the row map
+ * ff_row_classes made of `in` (device): then each class is computed once and its result stored
+ * in every member's row (the same values, since members are bitwise-equal rows). */
 int ff_skinny_linear(const float* in, const void* W, const void* bias, float* out, int64_t B, int64_t N,
-                     int64_t K, int32_t act_in, int32_t act_out, int32_t dtype, void* stream);
+                     int64_t K, int32_t act_in, int32_t act_out, int32_t dtype, const int32_t* classes,
+                     void* stream);
+
+/* Classes of bitwise-equal rows of c (float32 [B, H], device, 16-byte aligned, H % 4 == 0): in a
+ * rollout step every sample of a prompt has the same conditioning c = f(t, prompt) (Eq. 1's
+ * v_theta(x_t, c, t)), so ff_dit_forward computes each adaLN modulation vector once per class.
+ * map (int32 device, 2 + 3 B entries): map[0] = U, the number of classes; map[1 + j], j < U, the
+ * first row of class j (ascending); map[1 + B + j], j <= U, the start of class j in the member
+ * list; map[2 + 2 B + m], m < B, the members grouped by class, ascending within a class.  For
+ * B > 64 every row is its own class.  Errors: FF_EINVAL (null pointers, B < 0, H < 1),
+ * FF_EUNSUPPORTED (H % 4, misaligned c). */
+int ff_row_classes(const float* c, int64_t B, int64_t H, int32_t* map, void* stream);
 
 /* HBM streaming probe (measurement, not part of the method): mode 0 reads `bytes` from src (each
  * workgroup folds what it read into one 16-byte word of dst, which must hold `blocks` of them),

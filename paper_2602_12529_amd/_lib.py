@@ -77,7 +77,8 @@ _SIGS = {
                                   c_void_p, c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_int32, c_void_p]),
     "ff_rope_table": (c_int32, [c_void_p, POINTER(c_int32), c_int32, POINTER(c_int32), c_double, c_void_p]),
     "ff_skinny_linear": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_int64, c_int64, c_int64, c_int32,
-                                   c_int32, c_int32, c_void_p]),
+                                   c_int32, c_int32, c_void_p, c_void_p]),
+    "ff_row_classes": (c_int32, [c_void_p, c_int64, c_int64, c_void_p, c_void_p]),
     "ff_quantize_fp8": (c_int32, [c_void_p, c_int64, c_void_p, c_int64, c_void_p, c_int64, c_int64, c_int32,
                                   c_void_p]),
     "ff_linear_fp8": (c_int32, [c_void_p, c_int64, c_void_p, c_void_p, c_int64, c_void_p, c_void_p, c_void_p,

@@ -244,11 +244,20 @@ def rope_table(grid: Sequence[int], head_dim: int, axes: Sequence[int], theta: f
     return out
 
 
-def skinny_linear(inp, W, bias, out, act_in=ACT_NONE, act_out=ACT_NONE):
+def skinny_linear(inp, W, bias, out, act_in=ACT_NONE, act_out=ACT_NONE, classes=None):
     B, K = inp.shape
     N = W.shape[0]
     check(load().ff_skinny_linear(_p(inp), _p(W), _p(bias), _p(out), B, N, K, act_in, act_out, dtype_code(W),
-                                  _stream()), "ff_skinny_linear")
+                                  _p(classes), _stream()), "ff_skinny_linear")
+    return out
+
+
+def row_classes(c, out=None):
+    """Classes of bitwise-equal rows of c (float32 [B, H]): the int32 map ff_row_classes documents."""
+    B, H = c.shape
+    if out is None:
+        out = torch.empty(2 + 3 * B, dtype=torch.int32, device=c.device)
+    check(load().ff_row_classes(_p(c), B, H, _p(out), _stream()), "ff_row_classes")
     return out
 
 

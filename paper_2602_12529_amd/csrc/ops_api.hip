@@ -136,7 +136,7 @@ int ff_rope_table(float* out, const int32_t grid[3], int32_t head_dim, const int
 }
 
 int ff_skinny_linear(const float* in, const void* W, const void* bias, float* out, int64_t B, int64_t N, int64_t K,
-                     int32_t act_in, int32_t act_out, int32_t dtype, void* stream) {
+                     int32_t act_in, int32_t act_out, int32_t dtype, const int32_t* classes, void* stream) {
   const char* fn = "ff_skinny_linear";
   FF_TRY(check_dtype(fn, dtype));
   if (B < 0 || N < 0 || K < 1) return fail(FF_EINVAL, "%s: bad shape", fn);
@@ -152,7 +152,16 @@ int ff_skinny_linear(const float* in, const void* W, const void* bias, float* ou
   a.W = W; a.bias = bias;
   a.out = out; a.ldo = N;
   a.accumulate = 0; a.act_out = act_out;
+  a.rowmap = classes;
   return skinny_linear(a, static_cast<hipStream_t>(stream));
+}
+
+int ff_row_classes(const float* c, int64_t B, int64_t H, int32_t* map, void* stream) {
+  const char* fn = "ff_row_classes";
+  if (B < 0 || H < 1) return fail(FF_EINVAL, "%s: bad shape B=%lld H=%lld", fn, (long long)B, (long long)H);
+  if (B == 0) return FF_OK;
+  if (!c || !map) return fail(FF_EINVAL, "%s: null pointer", fn);
+  return row_classes(c, B, H, map, static_cast<hipStream_t>(stream));
 }
 
 int ff_quantize_fp8(const void* x, int64_t ldx, uint8_t* q, int64_t ldq, float* d, int64_t rows, int64_t cols,

@@ -94,6 +94,18 @@ def test_stream_probe_argument_validation():
     assert lib.ff_stream_probe(2, 1, None, None, 0, 64, None) == 0
 
 
+def test_row_classes_argument_validation():
+    lib = _lib.load()
+    fake = c_void_p(4096)
+    _err(lib.ff_row_classes(fake, -1, 8, fake, None), _lib.FF_EINVAL)
+    _err(lib.ff_row_classes(fake, 4, 0, fake, None), _lib.FF_EINVAL)
+    _err(lib.ff_row_classes(None, 4, 8, fake, None), _lib.FF_EINVAL)
+    _err(lib.ff_row_classes(fake, 4, 8, None, None), _lib.FF_EINVAL)
+    _err(lib.ff_row_classes(fake, 4, 6, fake, None), _lib.FF_EUNSUPPORTED)          # H % 4
+    _err(lib.ff_row_classes(c_void_p(4100), 4, 8, fake, None), _lib.FF_EUNSUPPORTED)  # alignment
+    assert lib.ff_row_classes(None, 0, 8, None, None) == 0
+
+
 def test_philox_argument_validation():
     lib = _lib.load()
     f = c_void_p(8192)

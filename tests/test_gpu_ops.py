@@ -289,6 +289,90 @@ def test_skinny_linear_parity(gpu_lib, B, N, K, dt, act):
     check(host(out), ref, C.F32, what=f"skinny {B}x{N}x{K} act {act}", norm_tol=1e-5)
 
 
+def _classes_ref(c):
+    """The row map of ff_row_classes by its definition: classes of bitwise-equal rows, numbered by
+    first occurrence; members grouped by class, ascending.  B > 64: every row its own class."""
+    B = c.shape[0]
+    bits = np.ascontiguousarray(c).view(np.uint32)
+    first, cls = [], np.empty(B, dtype=np.int64)
+    for b in range(B):
+        j = next((i for i, f in enumerate(first) if B <= 64 and np.array_equal(bits[f], bits[b])), None)
+        if j is None:
+            first.append(b)
+            j = len(first) - 1
+        cls[b] = j
+    U = len(first)
+    counts = np.bincount(cls, minlength=U)
+    offs = np.concatenate([[0], np.cumsum(counts)])
+    memb = np.argsort(cls, kind="stable")
+    out = np.zeros(2 + 3 * B, dtype=np.int32)
+    out[0] = U
+    out[1:1 + U] = first
+    out[1 + B:2 + B + U] = offs
+    out[2 + 2 * B:] = memb
+    return out, U
+
+
+@pytest.mark.parametrize("pattern,B,H", [("one", 8, 3072), ("distinct", 5, 3072), ("mixed", 20, 3072),
+                                         ("last-col", 6, 3072), ("signed-zero", 4, 64), ("nan", 4, 64),
+                                         ("one", 1, 100), ("mixed", 64, 256), ("mixed", 65, 256)])
+def test_row_classes_map(gpu_lib, pattern, B, H):
+    """ff_row_classes against the definition, integer map bit for bit (U, first rows, offsets,
+    members), including a pair of rows that differ only in their last column, +0 against -0
+    (different bits: different classes) and NaN rows with equal bits (one class)."""
+    rng = np.random.default_rng(70 + B)
+    base = rng.standard_normal((4, H)).astype(np.float32)
+    if pattern == "one":
+        c = np.repeat(base[:1], B, axis=0)
+    elif pattern == "distinct":
+        c = rng.standard_normal((B, H)).astype(np.float32)
+    elif pattern == "mixed":
+        c = base[(np.arange(B) * 7 // 3) % 4].copy()
+        if B > 20:
+            c[B - 1, 0] += 1.0
+    elif pattern == "last-col":
+        c = np.repeat(base[:1], B, axis=0)
+        c[2, -1] = np.nextafter(c[2, -1], np.float32(np.inf))
+        c[4] = c[2]
+    elif pattern == "signed-zero":
+        c = np.zeros((B, H), dtype=np.float32)
+        c[1, 7] = -0.0
+        c[3, 7] = -0.0
+    else:
+        c = np.repeat(base[:1], B, axis=0)
+        c[:, 5] = np.nan
+        c[2, 6] = 1.0
+    ref, U = _classes_ref(c)
+    got = gpu_lib.row_classes(torch.from_numpy(c).cuda()).cpu().numpy()
+    torch.cuda.synchronize()
+    say("row classes", pattern, B, H, "U", U)
+    # the defined entries: U, the first rows of the U classes, U + 1 offsets, B members
+    assert got[0] == U
+    np.testing.assert_array_equal(got[1:1 + U], ref[1:1 + U])
+    np.testing.assert_array_equal(got[1 + B:2 + B + U], ref[1 + B:2 + B + U])
+    np.testing.assert_array_equal(got[2 + 2 * B:], ref[2 + 2 * B:])
+
+
+@pytest.mark.parametrize("B", [8, 20])
+def test_skinny_linear_with_classes(gpu_lib, B):
+    """The GEMV over row classes stores in every row exactly what the plain GEMV stores there."""
+    K, N = 3072, 1000
+    rng = np.random.default_rng(80 + B)
+    base = rng.standard_normal((3, K)).astype(np.float32)
+    x = base[np.arange(B) % 3 if B > 8 else np.zeros(B, dtype=np.int64)]
+    X = torch.from_numpy(np.ascontiguousarray(x)).cuda()
+    w, b = normal(81, (N, K), C.BF16, 0.02), normal(82, (N,), C.BF16, 0.02)
+    Wd, bd = dev(w, C.BF16), dev(b, C.BF16)
+    plain = torch.empty((B, N), dtype=torch.float32, device="cuda")
+    grouped = torch.full((B, N), float("nan"), dtype=torch.float32, device="cuda")
+    gpu_lib.skinny_linear(X, Wd, bd, plain, act_in=1)
+    classes = gpu_lib.row_classes(X)
+    gpu_lib.skinny_linear(X, Wd, bd, grouped, act_in=1, classes=classes)
+    torch.cuda.synchronize()
+    assert int(classes[0]) == (3 if B > 8 else 1)
+    np.testing.assert_array_equal(grouped.cpu().numpy().view(np.uint32), plain.cpu().numpy().view(np.uint32))
+
+
 def test_profile_filter_times_one_kernel(gpu_lib):
     """With a name filter only that kernel's launches are timed; without one, every launch is."""
     A = torch.randn(512, 256, device="cuda").to(torch.bfloat16)
