@@ -173,7 +173,7 @@ namespace {
 struct Plan {
   int64_t B, Ni, Nt, N, P;
   size_t rope, temb_in, c, tmp, condB, cond32, mods, ximg, xtxt, joint, y, qkv, q, k, vt, o, u, txth;
-  size_t e6, ctx1, ctxp, kvc, kc, vct, qd, sumsq, splitk, splitk_bytes, rowmap, total;
+  size_t e6, ctx1, ctxp, kvc, kc, vct, qd, sumsq, splitk, splitk_bytes, rowmap, block_mods, total;
 };
 
 Plan plan(const ff_dit& m, int64_t B, const int32_t grid[3], int64_t n_txt, int64_t n_prompts) {
@@ -219,6 +219,8 @@ Plan plan(const ff_dit& m, int64_t B, const int32_t grid[3], int64_t n_txt, int6
   p.splitk_bytes = c.dtype == FF_BF16 ? gemm_split_bytes() : 0;
   p.splitk = take(p.splitk_bytes);
   p.rowmap = take(static_cast<size_t>(row_classes_ints(B)) * 4);
+  // every dual block's two [B, 6H] and every single block's [B, 3H] modulation vectors
+  p.block_mods = take(static_cast<size_t>(B) * (c.n_dual * 12 + c.n_single * 3) * H * 4);
   p.total = round_up(cv.off, 256);
   return p;
 }
@@ -321,6 +323,33 @@ int attention_joint(const ff_dit_config& c, const Plan& p, void* ws, void* out_t
   return attention(a, s);
 }
 
+// Where block_modulations leaves the modulation vectors: dual block i, stream k (0 text, 1 image)
+// [B, 6H]; then single block j [B, 3H].
+float* dual_mods(const Plan& p, void* ws, int64_t H, int i, int k) {
+  return reinterpret_cast<float*>(at(ws, p.block_mods)) + (2 * static_cast<int64_t>(i) + k) * p.B * 6 * H;
+}
+float* single_mods(const ff_dit& m, const Plan& p, void* ws, int64_t H, int j) {
+  return reinterpret_cast<float*>(at(ws, p.block_mods)) + m.cfg.n_dual * 2 * p.B * 6 * H + static_cast<int64_t>(j) * p.B * 3 * H;
+}
+
+// All blocks' adaLN modulation vectors W_mod SiLU(c) + b from the same c, one row per class of
+// equal conditioning rows, in as few launches as there are groups of 40 weight matrices: one long
+// weight stream instead of a short launch per block and stream.
+int block_modulations(const ff_dit& m, const Plan& p, void* ws, const float* c32, hipStream_t s) {
+  const ff_dit_config& c = m.cfg;
+  const int64_t H = c.hidden;
+  std::vector<SkinnySeg> segs;
+  segs.reserve(2 * c.n_dual + c.n_single);
+  for (int i = 0; i < c.n_dual; ++i) {
+    segs.push_back({m.dual_txt[i].mod.w, m.dual_txt[i].mod.b, dual_mods(p, ws, H, i, 0), 6 * H});
+    segs.push_back({m.dual_img[i].mod.w, m.dual_img[i].mod.b, dual_mods(p, ws, H, i, 1), 6 * H});
+  }
+  for (int j = 0; j < c.n_single; ++j) segs.push_back({m.single[j].mod.w, m.single[j].mod.b, single_mods(m, p, ws, H, j), 3 * H});
+  SkinnyArgs a = skinny_args(c.dtype, p.B, 0, H, c32, ACT_SILU, Lin{}, nullptr, 0, ACT_NONE,
+                             reinterpret_cast<const int32_t*>(at(ws, p.rowmap)));
+  return skinny_linear_multi(a, segs.data(), static_cast<int>(segs.size()), s);
+}
+
 // One dual-stream block.  cur[s] is the stream's current residual (input of the block);
 // dst[s] receives the updated residual (may equal cur[s]).
 int dual_block(const ff_dit& m, const Plan& p, void* ws, int i, const float* c32, const void* cur[2], void* dst[2],
@@ -328,19 +357,17 @@ int dual_block(const ff_dit& m, const Plan& p, void* ws, int i, const float* c32
   const ff_dit_config& c = m.cfg;
   const int64_t H = c.hidden, F = c.mlp_hidden;
   const size_t es = dtype_size(c.dtype);
-  const int32_t* classes = reinterpret_cast<const int32_t*>(at(ws, p.rowmap));
   const Stream* st[2] = {&m.dual_txt[i], &m.dual_img[i]};
   const int64_t rows[2] = {p.B * p.Nt, p.B * p.Ni};
   const int64_t ntok[2] = {p.Nt, p.Ni};
   const int64_t y_off[2] = {0, p.B * p.Nt * H};    // Y / O rows: txt rows first, then img rows
-  float* mods[2] = {reinterpret_cast<float*>(at(ws, p.mods)), reinterpret_cast<float*>(at(ws, p.mods)) + p.B * 6 * H};
+  float* mods[2] = {dual_mods(p, ws, H, i, 0), dual_mods(p, ws, H, i, 1)};   // computed by block_modulations
   char* Y = at(ws, p.y);
   char* O = at(ws, p.o);
   char* QKV = at(ws, p.qkv);
   char* qkv_k[2] = {QKV, QKV + p.B * p.Nt * 3 * H * es};
   char* U[2] = {at(ws, p.u), at(ws, p.u) + p.B * p.Nt * F * es};
   for (int k = 0; k < 2; ++k) {
-    FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 6 * H, H, c32, ACT_SILU, st[k]->mod, mods[k], 0, ACT_NONE, classes), s));
     FF_TRY(norm_modulate(norm_args(c, rows[k], cur[k], Y + y_off[k] * es, mods[k], mods[k] + H, 6 * H, ntok[k]), s));
   }
   // QKV projections of both streams; the QK norm, rotation and relayout run in the GEMM epilogue
@@ -380,14 +407,12 @@ int single_block(const ff_dit& m, const Plan& p, void* ws, int j, const float* c
   const ff_dit_config& c = m.cfg;
   const int64_t H = c.hidden, F = c.mlp_hidden, W1 = 3 * H + F;
   const size_t es = dtype_size(c.dtype);
-  const int32_t* classes = reinterpret_cast<const int32_t*>(at(ws, p.rowmap));
   const Single& sb = m.single[j];
-  float* mods = reinterpret_cast<float*>(at(ws, p.mods));
+  float* mods = single_mods(m, p, ws, H, j);   // computed by block_modulations
   const int64_t rows = p.B * p.N;
   char* Y = at(ws, p.y);
   char* H1 = at(ws, p.qkv);
   char* O = at(ws, p.o);
-  FF_TRY(skinny_linear(skinny_args(c.dtype, p.B, 3 * H, H, c32, ACT_SILU, sb.mod, mods, 0, ACT_NONE, classes), s));
   FF_TRY(norm_modulate(norm_args(c, rows, X, Y, mods, mods + H, 3 * H, p.N), s));
   // [Q | K | V | MLP input] in one GEMM: Q, K, V of the joint sequence go to the attention layout
   // (text tokens unrotated, image tokens rotated by their grid position), GELU from column 3H.
@@ -651,6 +676,7 @@ int forward_mmdit(const ff_dit& m, const Plan& p, const void* x, const void* txt
   // Samples at the same time step with the same prompt share c, hence every modulation vector:
   // the block GEMVs compute each distinct row of c once.
   FF_TRY(row_classes(c32, p.B, H, reinterpret_cast<int32_t*>(at(ws, p.rowmap)), s));
+  FF_TRY(block_modulations(m, p, ws, c32, s));
   for (int i = 0; i < c.n_dual; ++i) {
     FF_TRY(dual_block(m, p, ws, i, c32, cur, dst, s));
     cur[0] = dst[0];

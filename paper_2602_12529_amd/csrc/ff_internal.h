@@ -160,6 +160,13 @@ struct SkinnyArgs {
   const int32_t* rowmap;      // row classes of `in` from row_classes (device), or null: all rows
 };
 int skinny_linear(const SkinnyArgs& a, hipStream_t s);
+// The same input rows (a.in, a.B, a.K, activations, row map) against several weight matrices in as
+// few launches as possible: segment i writes out_i [B, N_i] (row stride N_i).  a.W, a.bias, a.out,
+// a.N and a.ldo are not used.
+struct SkinnySeg {
+  const void* W; const void* bias; float* out; int64_t N;
+};
+int skinny_linear_multi(const SkinnyArgs& a, const SkinnySeg* segs, int nseg, hipStream_t s);
 // Classes of bitwise-equal rows of c [B, H] fp32 into map (device int32, row_classes_ints(B)
 // entries), for skinny_linear to compute each distinct row once.
 int64_t row_classes_ints(int64_t B);

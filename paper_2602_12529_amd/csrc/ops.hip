@@ -22,7 +22,7 @@ namespace {
 // once and its result written to every sample of its class, so staging and multiply-adds scale
 // with the number of distinct rows.  A pass with L live rows runs the body compiled for exactly
 // L (a switch on L; the kernel's registers are those of the largest body).
-constexpr int kSkSlice = 512, kSkCap = 8;
+constexpr int kSkSlice = 512, kSkCap = 8, kSkMaxSeg = 40;
 constexpr int64_t kClassMaxB = 64;   // row classes are searched for B <= 64, identity above
 
 __device__ __forceinline__ float act_apply(int act, float x) {
@@ -141,9 +141,10 @@ struct SkinnyPass {
   const int32_t* rowmap; int64_t B;
 };
 
-// One pass over BC input rows: slot b is class u0 + b of the row map (or sample u0 + b).
+// One pass over BC input rows: slot b is class u0 + b of the row map (or sample u0 + b); blk is
+// the workgroup's index among the workgroups of this weight matrix (4 R output rows each).
 template <bool BF16, int BC, int R>
-__device__ __forceinline__ void skinny_pass(const SkinnyPass& a, int64_t u0, float (*xs)[kSkSlice]) {
+__device__ __forceinline__ void skinny_pass(const SkinnyPass& a, int64_t u0, int64_t blk, float (*xs)[kSkSlice]) {
   constexpr int WORDS = BF16 ? 4 : 8;           // 32-bit words of an 8-element chunk of a weight row
   constexpr int XPT = BC * kSkSlice / 256;      // staged inputs per thread per slice (2 per row)
   static_assert(kSkSlice == 512, "two staged inputs per row and thread");
@@ -152,7 +153,7 @@ __device__ __forceinline__ void skinny_pass(const SkinnyPass& a, int64_t u0, flo
 #pragma unroll
   for (int b = 0; b < BC; ++b) row[b] = a.rowmap ? a.rowmap[1 + u0 + b] : u0 + b;
   const int lane = threadIdx.x & 63;
-  const int64_t n0 = (static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6)) * R;
+  const int64_t n0 = (blk * 4 + (threadIdx.x >> 6)) * R;
   const bool active = n0 < N;   // wave-uniform
   float acc[R][BC];
 #pragma unroll
@@ -252,22 +253,54 @@ __device__ __forceinline__ void skinny_pass(const SkinnyPass& a, int64_t u0, flo
 }
 
 template <bool BF16, int R>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void skinny_kernel(SkinnyPass a) {
-  __shared__ __attribute__((aligned(16))) float xs[kSkCap][kSkSlice];
+__device__ __forceinline__ void skinny_dispatch_live(const SkinnyPass& a, int64_t blk, float (*xs)[kSkSlice]) {
   const int64_t U = a.rowmap ? a.rowmap[0] : a.B;
   const int64_t u0 = static_cast<int64_t>(blockIdx.y) * kSkCap;
   if (u0 >= U) return;   // uniform over the block: this pass has no rows
   const int live = U - u0 < kSkCap ? static_cast<int>(U - u0) : kSkCap;
   switch (live) {
-    case 1: skinny_pass<BF16, 1, R>(a, u0, xs); break;
-    case 2: skinny_pass<BF16, 2, R>(a, u0, xs); break;
-    case 3: skinny_pass<BF16, 3, R>(a, u0, xs); break;
-    case 4: skinny_pass<BF16, 4, R>(a, u0, xs); break;
-    case 5: skinny_pass<BF16, 5, R>(a, u0, xs); break;
-    case 6: skinny_pass<BF16, 6, R>(a, u0, xs); break;
-    case 7: skinny_pass<BF16, 7, R>(a, u0, xs); break;
-    default: skinny_pass<BF16, 8, R>(a, u0, xs); break;
+    case 1: skinny_pass<BF16, 1, R>(a, u0, blk, xs); break;
+    case 2: skinny_pass<BF16, 2, R>(a, u0, blk, xs); break;
+    case 3: skinny_pass<BF16, 3, R>(a, u0, blk, xs); break;
+    case 4: skinny_pass<BF16, 4, R>(a, u0, blk, xs); break;
+    case 5: skinny_pass<BF16, 5, R>(a, u0, blk, xs); break;
+    case 6: skinny_pass<BF16, 6, R>(a, u0, blk, xs); break;
+    case 7: skinny_pass<BF16, 7, R>(a, u0, blk, xs); break;
+    default: skinny_pass<BF16, 8, R>(a, u0, blk, xs); break;
   }
+}
+
+template <bool BF16, int R>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void skinny_kernel(SkinnyPass a) {
+  __shared__ __attribute__((aligned(16))) float xs[kSkCap][kSkSlice];
+  skinny_dispatch_live<BF16, R>(a, blockIdx.x, xs);
+}
+
+// Several weight matrices against the same input rows in one launch (the modulation vectors of
+// every block of a forward): workgroup x belongs to the segment s with block0[s] <= x <
+// block0[s + 1].  One long weight stream instead of one short launch per matrix.
+struct SkinnySegs {
+  int nseg;
+  int64_t block0[kSkMaxSeg + 1];
+  const void* W[kSkMaxSeg];
+  const void* bias[kSkMaxSeg];
+  float* out[kSkMaxSeg];
+  int64_t N[kSkMaxSeg];
+};
+
+template <bool BF16, int R>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void skinny_multi_kernel(SkinnyPass a,
+                                                                                                  SkinnySegs g) {
+  __shared__ __attribute__((aligned(16))) float xs[kSkCap][kSkSlice];
+  const int64_t x = blockIdx.x;
+  int sg = 0;
+  while (sg + 1 < g.nseg && g.block0[sg + 1] <= x) ++sg;
+  a.W = g.W[sg];
+  a.bias = g.bias[sg];
+  a.out = g.out[sg];
+  a.N = g.N[sg];
+  a.ldo = g.N[sg];
+  skinny_dispatch_live<BF16, R>(a, x - g.block0[sg], xs);
 }
 
 // ------------------------------------------------------------------ norm + modulate
@@ -786,6 +819,36 @@ int skinny_linear(const SkinnyArgs& a, hipStream_t s) {
   const dim3 grid(static_cast<unsigned>((a.N + 4 * R - 1) / (4 * R)), static_cast<unsigned>((a.B + kSkCap - 1) / kSkCap));
   if (a.dtype == FF_BF16) hipLaunchKernelGGL((skinny_kernel<true, 4>), grid, dim3(256), 0, s, k);
   else hipLaunchKernelGGL((skinny_kernel<false, 2>), grid, dim3(256), 0, s, k);
+  return ls.status();
+}
+
+int skinny_linear_multi(const SkinnyArgs& a, const SkinnySeg* segs, int nseg, hipStream_t s) {
+  if (a.B == 0 || nseg == 0) return FF_OK;
+  if (a.K % 8 != 0 || a.ldi % 4 != 0) return fail(FF_EUNSUPPORTED, "skinny_linear: K=%lld must be a multiple of 8", (long long)a.K);
+  double flops = 0.0, bytes = 0.0;
+  for (int i = 0; i < nseg; ++i) {
+    flops += 2.0 * a.B * segs[i].N * a.K;
+    bytes += static_cast<double>(dtype_size(a.dtype)) * segs[i].N * a.K + 4.0 * a.B * (a.K + segs[i].N);
+  }
+  LaunchScope ls("skinny_linear", s, flops, bytes);
+  const int R = a.dtype == FF_BF16 ? 4 : 2;
+  const SkinnyPass k{a.in, a.ldi, a.act_in, nullptr, nullptr, nullptr, 0, 0, a.K, a.accumulate, a.act_out, a.rowmap, a.B};
+  for (int first = 0; first < nseg; first += kSkMaxSeg) {
+    SkinnySegs g{};
+    g.nseg = nseg - first < kSkMaxSeg ? nseg - first : kSkMaxSeg;
+    int64_t blocks = 0;
+    for (int i = 0; i < g.nseg; ++i) {
+      const SkinnySeg& sg = segs[first + i];
+      g.block0[i] = blocks;
+      g.W[i] = sg.W; g.bias[i] = sg.bias; g.out[i] = sg.out; g.N[i] = sg.N;
+      blocks += (sg.N + 4 * R - 1) / (4 * R);
+    }
+    g.block0[g.nseg] = blocks;
+    if (blocks == 0) continue;
+    const dim3 grid(static_cast<unsigned>(blocks), static_cast<unsigned>((a.B + kSkCap - 1) / kSkCap));
+    if (a.dtype == FF_BF16) hipLaunchKernelGGL((skinny_multi_kernel<true, 4>), grid, dim3(256), 0, s, k, g);
+    else hipLaunchKernelGGL((skinny_multi_kernel<false, 2>), grid, dim3(256), 0, s, k, g);
+  }
   return ls.status();
 }
 
