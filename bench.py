@@ -96,7 +96,7 @@ def log(*a):
 def main() -> int:
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(the rollout would shard by prompt groups with no communication until the advantages).",
               file=sys.stderr)
         return 2
