@@ -211,6 +211,26 @@ def test_modulation_row_classes_hidden_mode(gpu_lib):
     assert np.max(np.abs(img[2] - img[0])) > 1e-2
 
 
+def test_deep_model_modulation_launch_groups(gpu_lib):
+    """The forward computes every block's modulation vectors up front, 40 weight matrices per
+    launch: 21 dual blocks (42 matrices) and 3 single blocks give two launches with a segment
+    boundary inside a block's pair.  float32 tiny widths with per-sample t and two prompts; the
+    velocity against the oracle's whole forward."""
+    m = C.TINY.model.replace(n_dual=21, n_single=3)
+    w = C.Workload(**{**C.TINY.__dict__, "name": "tiny-deep", "index": 18, "model": m})
+    say("deep model", m.n_dual, m.n_single)
+    W, txt, cond, x0, _ = _inputs(w)
+    t = np.linspace(0.9, 0.3, w.batch).astype(np.float32)
+    tidx = synth.txt_index(w)
+    Wd, T, Cd, X0, _ = _device(w, W, txt, cond, x0, [])
+    dit = api.Dit(m, Wd)
+    v = torch.empty_like(X0)
+    dit.forward(X0, T, w.grid, v, t=torch.from_numpy(t).cuda(), cond=Cd, txt_index=torch.from_numpy(tidx).cuda())
+    torch.cuda.synchronize()
+    ref = odit.forward(m, W, x0, txt, t=t.astype(np.float64), cond=cond, txt_index=tidx, grid=w.grid)
+    check(host(v), ref, C.F32, what="deep model (21 dual + 3 single) v")
+
+
 def _small_latent_stack():
     m = C.ModelConfig(model=C.MODEL_MMDIT, io_mode=C.IO_LATENT, dtype=C.BF16, n_dual=1, n_single=1, hidden=256,
                       heads=2, head_dim=128, mlp_hidden=512, in_channels=64, txt_dim=128, pooled_dim=64,
