@@ -323,7 +323,7 @@ def test_awm_training_forward(gpu_lib):
 def test_flux_dual_block_full_size(gpu_lib):
     """One Flux-shaped dual-stream block at full size (B=8, 4096 img + 512 txt, H=3072, bf16),
     one SDE step t=0.6 -> 0.5 with log-prob, as timed by the benchmark; the oracle
-    recomputes two whole samples."""
+    recomputes two whole samples.  A second run on the same inputs is bitwise the first."""
     w = C.FLUX_BLOCK
     m = w.model
     say("full flux block: generating inputs")
@@ -336,6 +336,12 @@ def test_flux_dual_block_full_size(gpu_lib):
     v = host(res.vs[0])
     xn = host(res.xs[1])
     lp = host(res.logp[0])
+    say("full flux block: repeat run")
+    res2 = ro.run(X0, T, E, cond=Cd)
+    torch.cuda.synchronize()
+    assert torch.equal(res2.vs[0], res.vs[0]) and torch.equal(res2.xs[1], res.xs[1])
+    assert torch.equal(res2.logp[0], res.logp[0])
+    del res2
     t, tn, sigma = res.ts[0], res.ts[1], res.sigmas[0]
     assert sigma == pytest.approx(0.7 * math.sqrt(1.5), rel=1e-15)
     for b in (0, 5):
@@ -353,7 +359,9 @@ def test_flux_dual_block_full_size(gpu_lib):
 def test_dual_block_full_size_other_shapes(gpu_lib, shape):
     """One dual-stream block at the other headline shapes, hidden 3072, 24 heads, MLP 12288, bf16:
     the Qwen-Image stack's (B=8, 4096 image + 256 text tokens) and the Flux stack's (B=16, 1024 +
-    512), one SDE step; the fused QKV epilogue runs; the oracle recomputes two whole samples."""
+    512), one SDE step; the fused QKV epilogue runs; the oracle recomputes two whole samples.  Both
+    shapes split the last round of the K = 12288 projection along K (1632 and 1152 tiles on 256 CUs):
+    a second run is bitwise the first, the partial sums being added in a fixed order."""
     base = C.FLUX_BLOCK
     if shape == "qwen":
         kw = dict(group=8, grid=(1, 64, 64), n_txt=256, index=18)
@@ -376,6 +384,10 @@ def test_dual_block_full_size_other_shapes(gpu_lib, shape):
     prof = api.profile_read()
     api.profile_reset()
     assert prof.get("gemm_bf16_qkv", {}).get("launches", 0) == 1, sorted(prof)
+    res2 = ro.run(X0, T, E, cond=Cd)
+    torch.cuda.synchronize()
+    assert torch.equal(res2.vs[0], res.vs[0]) and torch.equal(res2.xs[1], res.xs[1])
+    del res2
     v = host(res.vs[0])
     for b in (0, w.batch - 1):
         say("oracle sample", b)
