@@ -79,7 +79,8 @@ int ff_sde_workspace_size(int64_t B, int64_t D, size_t* bytes /* host, out */);
  * alias x, v or eps.  logp: device float64 [B], or NULL to skip the
  * log-probability.  Domain: 0 <= t_next < t <= 1, sigma >= 0 finite, t > 0;
  * sigma = 0 requires logp == NULL (an ODE step has no density) -> FF_EDOMAIN.
- * B >= 1, D >= 1 (B = 0 or D = 0 is a no-op returning FF_OK). */
+ * B = 0 is a no-op returning FF_OK.  D = 0 (empty samples) reads no tensor and writes only
+ * logp[b] = 0 when logp is given: the log-density above with no terms. */
 int ff_sde_step(const void* x, const void* v, const void* eps, void* x_next, double* logp,
                 int64_t B, int64_t D, double t, double t_next, double sigma, int32_t dtype,
                 void* workspace, size_t ws_bytes, void* stream);
@@ -98,7 +99,7 @@ int ff_sde_step_noalloc(const void* x, const void* v, const void* eps, void* x_n
                         int64_t B, int64_t D, double t, double t_next, double sigma, int32_t dtype,
                         void* stream);
 
-/* Recomputes logp[b] for stored (x, v, x_next) exactly as ff_sde_step does.
+/* Recomputes logp[b] for stored (x, v, x_next) exactly as ff_sde_step does (D = 0: logp[b] = 0).
  * sigma must be > 0 (FF_EDOMAIN otherwise). */
 int ff_logprob(const void* x, const void* v, const void* x_next, double* logp,
                int64_t B, int64_t D, double t, double t_next, double sigma, int32_t dtype,

@@ -54,6 +54,15 @@ def workspace(nbytes: int, device="cuda") -> torch.Tensor:
 
 
 # ------------------------------------------------------------------ SDE step / log-prob
+
+def _bd(t) -> tuple:
+    """(B, D) of a [B, ...] tensor: samples, and elements per sample (also for B = 0)."""
+    d = 1
+    for n in t.shape[1:]:
+        d *= int(n)
+    return int(t.shape[0]), d
+
+
 def sde_workspace_size(B: int, D: int) -> int:
     n = c_size_t()
     check(load().ff_sde_workspace_size(B, D, byref(n)), "ff_sde_workspace_size")
@@ -61,7 +70,7 @@ def sde_workspace_size(B: int, D: int) -> int:
 
 
 def sde_step(x, v, eps, x_next, t: float, t_next: float, sigma: float, logp=None, ws=None):
-    B, D = x.shape[0], x[0].numel()
+    B, D = _bd(x)
     if ws is None and logp is not None:
         ws = workspace(sde_workspace_size(B, D), x.device)
     check(load().ff_sde_step(_p(x), _p(v), _p(eps), _p(x_next), _p(logp), B, D, t, t_next, sigma,
@@ -70,7 +79,7 @@ def sde_step(x, v, eps, x_next, t: float, t_next: float, sigma: float, logp=None
 
 
 def logprob(x, v, x_next, logp, t: float, t_next: float, sigma: float, ws=None):
-    B, D = x.shape[0], x[0].numel()
+    B, D = _bd(x)
     if ws is None:
         ws = workspace(sde_workspace_size(B, D), x.device)
     check(load().ff_logprob(_p(x), _p(v), _p(x_next), _p(logp), B, D, t, t_next, sigma, dtype_code(x), _p(ws),
@@ -79,14 +88,14 @@ def logprob(x, v, x_next, logp, t: float, t_next: float, sigma: float, ws=None):
 
 def sde_step_noalloc(x, v, eps, x_next, t: float, t_next: float, sigma: float, logp=None):
     """ff_sde_step without a workspace: the library's own device scratch holds the partial sums."""
-    B, D = x.shape[0], x[0].numel()
+    B, D = _bd(x)
     check(load().ff_sde_step_noalloc(_p(x), _p(v), _p(eps), _p(x_next), _p(logp), B, D, t, t_next, sigma,
                                      dtype_code(x), _stream()), "ff_sde_step_noalloc")
 
 
 def sde_step_philox(x, v, x_next, t: float, t_next: float, sigma: float, seed: int, step: int, logp=None, ws=None):
     """The SDE step with its noise drawn on the device (Philox4x32-10, Box-Muller)."""
-    B, D = x.shape[0], x[0].numel()
+    B, D = _bd(x)
     if ws is None and logp is not None:
         ws = workspace(sde_workspace_size(B, D), x.device)
     check(load().ff_sde_step_philox(_p(x), _p(v), _p(x_next), _p(logp), B, D, t, t_next, sigma, seed, step,
@@ -97,7 +106,7 @@ def sde_step_philox(x, v, x_next, t: float, t_next: float, sigma: float, seed: i
 def philox_normal(shape, seed: int, step: int, dtype=torch.float32, device="cuda"):
     """The noise of ff_sde_step_philox for a [B, ...] latent, materialised."""
     out = torch.empty(shape, dtype=dtype, device=device)
-    B, D = out.shape[0], out[0].numel()
+    B, D = _bd(out)
     check(load().ff_philox_normal(_p(out), B, D, seed, step, dtype_code(out), _stream()), "ff_philox_normal")
     return out
 
@@ -123,7 +132,7 @@ def group_advantage(rewards, weights, group_id, n_groups: int, mode: int = 0, ep
 # ------------------------------------------------------------------ objectives that consume the rollout
 def flow_noise(x0, eps, t, xt=None):
     """x_t = (1 - t) x0 + t eps per sample; t: float32 [B] on the device."""
-    B, D = x0.shape[0], x0[0].numel()
+    B, D = _bd(x0)
     if xt is None:
         xt = torch.empty_like(x0)
     check(load().ff_flow_noise(_p(x0), _p(eps), _p(t), _p(xt), B, D, dtype_code(x0), _stream()), "ff_flow_noise")
@@ -138,7 +147,7 @@ def loss_workspace_size(B: int, D: int) -> int:
 
 def awm_loss(v, eps, x0, adv, per_sample=None, loss=None, ws=None):
     """Eq. 3; returns (per_sample float64 [B], loss float64 [1]) on the device."""
-    B, D = v.shape[0], v[0].numel()
+    B, D = _bd(v)
     per_sample = torch.empty(B, dtype=torch.float64, device=v.device) if per_sample is None else per_sample
     loss = torch.empty(1, dtype=torch.float64, device=v.device) if loss is None else loss
     ws = workspace(loss_workspace_size(B, D), v.device) if ws is None else ws
@@ -149,7 +158,7 @@ def awm_loss(v, eps, x0, adv, per_sample=None, loss=None, ws=None):
 
 def nft_loss(v_pos, v_neg, eps, x0, r, per_sample=None, loss=None, ws=None):
     """Eq. 2; returns (per_sample float64 [B], loss float64 [1]) on the device."""
-    B, D = v_pos.shape[0], v_pos[0].numel()
+    B, D = _bd(v_pos)
     per_sample = torch.empty(B, dtype=torch.float64, device=v_pos.device) if per_sample is None else per_sample
     loss = torch.empty(1, dtype=torch.float64, device=v_pos.device) if loss is None else loss
     ws = workspace(loss_workspace_size(B, D), v_pos.device) if ws is None else ws

@@ -367,12 +367,28 @@ int ff_sde_workspace_size(int64_t B, int64_t D, size_t* bytes) {
   return FF_OK;
 }
 
+// D = 0: every sample is an empty vector, whose log-density (an empty sum, no normalising terms)
+// is 0; nothing else is read or written.
+__global__ __launch_bounds__(256) void zero_logp_kernel(double* __restrict__ logp, int64_t B) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i < B) logp[i] = 0.0;
+}
+int zero_logp(const char* fn, double* logp, int64_t B, void* stream, bool profile = true) {
+  if (!logp) return FF_OK;
+  if ((reinterpret_cast<uintptr_t>(logp) & 7u) != 0) return fail(FF_EINVAL, "%s: logp misaligned", fn);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  LaunchScope ls(profile ? "logp_zero" : nullptr, s, 0.0, 8.0 * static_cast<double>(B));
+  hipLaunchKernelGGL(zero_logp_kernel, dim3(static_cast<unsigned>((B + 255) / 256)), dim3(256), 0, s, logp, B);
+  return ls.status();
+}
+
 int ff_sde_step(const void* x, const void* v, const void* eps, void* x_next, double* logp, int64_t B,
                 int64_t D, double t, double t_next, double sigma, int32_t dtype, void* workspace,
                 size_t ws_bytes, void* stream) {
   FF_TRY(check_sde_args("ff_sde_step", x, v, eps, x_next, B, D, t, t_next, sigma, dtype));
   if (sigma == 0.0 && logp) return fail(FF_EDOMAIN, "ff_sde_step: an ODE step (sigma=0) has no log-probability");
-  if (B == 0 || D == 0) return FF_OK;
+  if (B == 0) return FF_OK;
+  if (D == 0) return zero_logp("ff_sde_step", logp, B, stream);
   if (!x_next) return fail(FF_EINVAL, "ff_sde_step: null x_next");
   if (x_next == x || x_next == v || x_next == eps) return fail(FF_EINVAL, "ff_sde_step: x_next aliases an input");
   if (logp && !aligned16(logp)) { /* doubles need 8-byte alignment only */
@@ -389,7 +405,8 @@ int ff_sde_step_noalloc(const void* x, const void* v, const void* eps, void* x_n
   const char* fn = "ff_sde_step_noalloc";
   FF_TRY(check_sde_args(fn, x, v, eps, x_next, B, D, t, t_next, sigma, dtype));
   if (sigma == 0.0 && logp) return fail(FF_EDOMAIN, "%s: an ODE step (sigma=0) has no log-probability", fn);
-  if (B == 0 || D == 0) return FF_OK;
+  if (B == 0) return FF_OK;
+  if (D == 0) return zero_logp(fn, logp, B, stream, /*profile=*/false);
   if (!x_next) return fail(FF_EINVAL, "%s: null x_next", fn);
   if (x_next == x || x_next == v || x_next == eps) return fail(FF_EINVAL, "%s: x_next aliases an input", fn);
   if (logp && (reinterpret_cast<uintptr_t>(logp) & 7u) != 0) return fail(FF_EINVAL, "%s: logp misaligned", fn);
@@ -411,8 +428,9 @@ int ff_logprob(const void* x, const void* v, const void* x_next, double* logp, i
                void* stream) {
   FF_TRY(check_sde_args("ff_logprob", x, v, x_next, nullptr, B, D, t, t_next, sigma, dtype));
   if (!(sigma > 0.0)) return fail(FF_EDOMAIN, "ff_logprob: needs sigma > 0");
-  if (B == 0 || D == 0) return FF_OK;
+  if (B == 0) return FF_OK;
   if (!logp) return fail(FF_EINVAL, "ff_logprob: null logp");
+  if (D == 0) return zero_logp("ff_logprob", logp, B, stream);
   if ((reinterpret_cast<uintptr_t>(logp) & 7u) != 0) return fail(FF_EINVAL, "ff_logprob: logp misaligned");
   FF_TRY(check_ws("ff_logprob", B, D, true, workspace, ws_bytes));
   Coef k = coefficients(t, t_next, sigma, D);
@@ -426,7 +444,8 @@ int ff_sde_step_philox(const void* x, const void* v, void* x_next, double* logp,
   const char* fn = "ff_sde_step_philox";
   FF_TRY(check_sde_args(fn, x, v, x, x_next, B, D, t, t_next, sigma, dtype));
   if (sigma == 0.0 && logp) return fail(FF_EDOMAIN, "%s: an ODE step (sigma=0) has no log-probability", fn);
-  if (B == 0 || D == 0) return FF_OK;
+  if (B == 0) return FF_OK;
+  if (D == 0) return zero_logp(fn, logp, B, stream);
   if (!x_next) return fail(FF_EINVAL, "%s: null x_next", fn);
   if (x_next == x || x_next == v) return fail(FF_EINVAL, "%s: x_next aliases an input", fn);
   if (logp && (reinterpret_cast<uintptr_t>(logp) & 7u) != 0) return fail(FF_EINVAL, "%s: logp misaligned", fn);

@@ -63,6 +63,12 @@ def test_sde_argument_validation():
     _err(lib.ff_sde_step(fake, fake, fake, c_void_p(16384), None, -1, 8, 0.5, 0.4, 1.0, 1, None, 0, None), _lib.FF_EINVAL)
     # empty batch is a no-op
     assert lib.ff_sde_step(None, None, None, None, None, 0, 8, 0.5, 0.4, 1.0, 1, None, 0, None) == 0
+    # empty samples: only logp is touched, and it is still validated (without logp: a no-op)
+    assert lib.ff_sde_step(None, None, None, None, None, 2, 0, 0.5, 0.4, 1.0, 1, None, 0, None) == 0
+    _err(lib.ff_sde_step(None, None, None, None, c_void_p(24580), 2, 0, 0.5, 0.4, 1.0, 1, None, 0, None), _lib.FF_EINVAL)
+    _err(lib.ff_logprob(None, None, None, None, 2, 0, 0.5, 0.4, 1.0, 1, None, 0, None), _lib.FF_EINVAL)
+    _err(lib.ff_logprob(None, None, None, c_void_p(24580), 2, 0, 0.5, 0.4, 1.0, 1, None, 0, None), _lib.FF_EINVAL)
+    _err(lib.ff_sde_step_noalloc(None, None, None, None, c_void_p(24580), 2, 0, 0.5, 0.4, 1.0, 1, None), _lib.FF_EINVAL)
     n = c_size_t()
     assert lib.ff_sde_workspace_size(8, 12582912, byref(n)) == 0 and n.value >= 8 * 8
     assert lib.ff_sde_workspace_size(0, 5, byref(n)) == 0 and n.value == 0

@@ -9,7 +9,7 @@ from oracle import advantage as oadv
 from oracle import sde as osde
 from paper_2602_12529_amd import configs as C
 
-from gpu_util import LOGP_ABS, TOL, check, dev, host, normal, rel, say
+from gpu_util import LOGP_ABS, TOL, check, dev, host, normal, rel, say, tdt
 
 pytestmark = pytest.mark.gpu
 
@@ -69,6 +69,35 @@ def test_logprob_at_mean_matches_closed_form(gpu_lib):
     torch.cuda.synchronize()
     closed = -0.5 * D * math.log(2 * math.pi * s * s * (t - tn))
     assert np.max(np.abs(host(lp) - closed)) <= LOGP_ABS
+
+
+@pytest.mark.parametrize("dt", [C.F32, C.BF16], ids=["f32", "bf16"])
+def test_empty_samples_and_empty_batch(gpu_lib, dt):
+    """Degenerate sizes: samples with no elements have log-density 0 (the oracle's empty sum) from
+    every step entry point and from the recomputation; an empty batch is a no-op."""
+    say("empty samples", dt)
+    B = 5
+    X = torch.empty((B, 0), dtype=tdt(dt), device="cuda")
+    ref = osde.step_log_prob(np.zeros((B, 0)), np.zeros((B, 0)), np.zeros((B, 0)), 0.6, 0.5, 0.9)
+    assert np.all(ref == 0.0)
+    calls = {
+        "sde_step": lambda lp: gpu_lib.sde_step(X, X, X, torch.empty_like(X), 0.6, 0.5, 0.9, logp=lp),
+        "logprob": lambda lp: gpu_lib.logprob(X, X, X, lp, 0.6, 0.5, 0.9),
+        "sde_step_philox": lambda lp: gpu_lib.sde_step_philox(X, X, torch.empty_like(X), 0.6, 0.5, 0.9, 7, 1, logp=lp),
+        "sde_step_noalloc": lambda lp: gpu_lib.sde_step_noalloc(X, X, X, torch.empty_like(X), 0.6, 0.5, 0.9, logp=lp),
+    }
+    for name, f in calls.items():
+        lp = torch.full((B,), float("nan"), dtype=torch.float64, device="cuda")
+        f(lp)
+        torch.cuda.synchronize()
+        assert np.array_equal(host(lp), ref), name
+    # B = 0: nothing is written (the sentinel behind the empty view stays)
+    lp = torch.full((1,), float("nan"), dtype=torch.float64, device="cuda")
+    Z = torch.empty((0, 16), dtype=tdt(dt), device="cuda")
+    gpu_lib.sde_step(Z, Z, Z, torch.empty_like(Z), 0.6, 0.5, 0.9, logp=lp[:0])
+    gpu_lib.logprob(Z, Z, Z, lp[:0], 0.6, 0.5, 0.9)
+    torch.cuda.synchronize()
+    assert torch.isnan(lp).all()
 
 
 def test_sde_full_size_flux_block_shape(gpu_lib):

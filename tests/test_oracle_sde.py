@@ -88,6 +88,24 @@ def test_logprob_one_element_matches_scipy():
         assert got == pytest.approx(ref, abs=1e-12)
 
 
+def test_logprob_sums_independent_coordinates():
+    """The noise of Eq. 1 is isotropic, so the density of a sample factorises over its elements:
+    the log-density of [a | b] is that of a plus that of b, for every split (scipy per element
+    for the one-element parts), and a sample with no elements has log-density 0."""
+    rng = np.random.default_rng(4)
+    B, D = 3, 50
+    mean = rng.standard_normal((B, D))
+    xn = mean + 0.3 * rng.standard_normal((B, D))
+    sigma, dt = 0.8, -0.15
+    whole = sde.log_prob(xn, mean, sigma, dt)
+    for cut in (1, 17, 49):
+        parts = sde.log_prob(xn[:, :cut], mean[:, :cut], sigma, dt) + sde.log_prob(xn[:, cut:], mean[:, cut:], sigma, dt)
+        np.testing.assert_allclose(whole, parts, rtol=1e-13)
+    per_elem = stats.norm.logpdf(xn, loc=mean, scale=sigma * math.sqrt(-dt)).sum(axis=1)
+    np.testing.assert_allclose(whole, per_elem, rtol=1e-12)
+    assert np.all(sde.log_prob(np.zeros((B, 0)), np.zeros((B, 0)), sigma, dt) == 0.0)
+
+
 def test_logprob_undefined_for_ode_step():
     with pytest.raises(ValueError):
         sde.log_prob(np.zeros((1, 2)), np.zeros((1, 2)), 0.0, -0.1)
