@@ -149,6 +149,12 @@ def test_group_advantage_edge_cases(gpu_lib):
     a = adv.cpu().numpy()
     assert cnt.cpu().tolist() == [3, 1, 0, 1]
     assert np.all(a[:5] == 0.0) and np.isnan(a[5])
+    # no samples: every group is empty
+    cnt = torch.full((3,), -1, dtype=torch.int32, device="cuda")
+    gpu_lib.group_advantage(torch.empty((0, 2), device="cuda"), dev(np.ones(2)), torch.empty(0, dtype=torch.int32, device="cuda"),
+                            3, 1, counts=cnt)
+    torch.cuda.synchronize()
+    assert cnt.cpu().tolist() == [0, 0, 0]
 
 
 # ------------------------------------------------------------------ counter-based noise
