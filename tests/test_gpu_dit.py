@@ -574,3 +574,52 @@ def test_qwen_shaped_latent_rollout_mixgrpo(gpu_lib):
         v_ref = odit.forward(m, W, host(res.xs[k])[1:], txt, t=np.full(1, res.ts[k]), cond=cond,
                              txt_index=synth.txt_index(w)[1:], grid=w.grid)
         check(host(res.vs[k])[1:], v_ref, C.BF16, model_stages(m), what=f"qwen-shaped v step {k} sample 1")
+
+
+@pytest.mark.timeout(900)
+def test_qwen_stack_bench_configuration(gpu_lib):
+    """The default benchmark's workload as it runs there: the Qwen-Image-shaped stack (60 dual
+    blocks, hidden 3072, 24 heads, MLP 12288, text width 3584), B = 8 samples of 4096 + 256 tokens,
+    bf16, the 10-step rollout with SDE on 1-indexed steps 2-4, weights drawn on the device.  The
+    oracle cannot run 60 such blocks, so the final projection's weights are zeroed and the velocity
+    is its bias b for every token: every velocity must be exactly b (a non-finite value anywhere in
+    the 60 blocks would reach it, 0 x NaN being NaN), every stored latent must match the oracle's SDE
+    or ODE step from the previous stored latent element by element, every log-prob the oracle's, and
+    a second rollout is bitwise the first."""
+    w = C.QWEN_STACK
+    m = w.model
+    say("qwen stack: drawing weights on the device")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(1000 + w.index)
+    Wd = {}
+    for name, shape, kind in synth.tensor_table(m):
+        t = torch.randn(shape, device="cuda", generator=g, dtype=torch.float32).mul_(0.02)
+        if kind == "norm":
+            t.add_(1.0)
+        Wd[name] = t.to(torch.bfloat16)
+    Wd["final.proj.w"].zero_()
+    b = host(Wd["final.proj.b"])
+    txt, cond, x0 = synth.text_input(w), synth.cond_input(w), synth.x0(w)
+    eps = [synth.sde_noise(w, k) for k in range(w.steps)]
+    T, X0 = dev(txt, C.BF16), dev(x0, C.BF16)
+    Cd = dev(cond, C.BF16) if cond is not None else None
+    E = [dev(e, C.BF16) for e in eps]
+    tidx = torch.from_numpy(synth.txt_index(w)).cuda()
+    ro = R.Rollout(w, api.Dit(m, Wd))
+    say("qwen stack: rollout")
+    res = ro.run(X0, T, E, cond=Cd, txt_index=tidx)
+    torch.cuda.synchronize()
+    assert sorted(res.logp) == [1, 2, 3]
+    for k in range(w.steps):
+        xk, vk = host(res.xs[k]), host(res.vs[k])
+        assert np.array_equal(vk, np.broadcast_to(b, vk.shape)), f"velocity of step {k}"
+        xn_ref = osde.sde_step(xk, vk, host(E[k]), res.ts[k], res.ts[k + 1], res.sigmas[k])
+        check(host(res.xs[k + 1]), xn_ref, C.BF16, 0, what=f"qwen stack x step {k}")
+        if k in res.logp:
+            lp_ref = osde.step_log_prob(xk, vk, host(res.xs[k + 1]), res.ts[k], res.ts[k + 1], res.sigmas[k])
+            assert np.max(np.abs(host(res.logp[k]) - lp_ref)) <= LOGP_ABS
+    say("qwen stack: repeat")
+    res2 = ro.run(X0, T, E, cond=Cd, txt_index=tidx)
+    torch.cuda.synchronize()
+    assert torch.equal(res2.xs[-1], res.xs[-1])
+    assert all(torch.equal(res2.logp[k], res.logp[k]) for k in res.logp)
