@@ -577,18 +577,20 @@ def test_qwen_shaped_latent_rollout_mixgrpo(gpu_lib):
 
 
 @pytest.mark.timeout(900)
-def test_qwen_stack_bench_configuration(gpu_lib):
-    """The default benchmark's workload as it runs there: the Qwen-Image-shaped stack (60 dual
-    blocks, hidden 3072, 24 heads, MLP 12288, text width 3584), B = 8 samples of 4096 + 256 tokens,
-    bf16, the 10-step rollout with SDE on 1-indexed steps 2-4, weights drawn on the device.  The
-    oracle cannot run 60 such blocks, so the final projection's weights are zeroed and the velocity
-    is its bias b for every token: every velocity must be exactly b (a non-finite value anywhere in
-    the 60 blocks would reach it, 0 x NaN being NaN), every stored latent must match the oracle's SDE
-    or ODE step from the previous stored latent element by element, every log-prob the oracle's, and
-    a second rollout is bitwise the first."""
-    w = C.QWEN_STACK
+@pytest.mark.parametrize("stack", ["QWEN_STACK", "FLUX_STACK", "WAN_STACK"])
+def test_stack_bench_configuration(gpu_lib, stack):
+    """The benchmark's stack workloads as they run there, weights drawn on the device: the
+    Qwen-Image-shaped stack (60 dual blocks, B = 8 of 4096 + 256 tokens, SDE on 1-indexed steps 2-4),
+    the Flux stack (19 dual + 38 single blocks, B = 16 of 1024 + 512 tokens) and WAN (30 blocks,
+    32760 tokens, cross-attention to 512), bf16, whole rollouts.  The oracle cannot run such stacks,
+    so the final projection's weights are zeroed and the velocity is its bias b for every token:
+    every velocity must be exactly b (a non-finite value anywhere in the blocks would reach it, 0 x
+    NaN being NaN), every stored latent must match the oracle's SDE or ODE step from the previous
+    stored latent element by element, every log-prob the oracle's, and a second rollout is bitwise
+    the first."""
+    w = getattr(C, stack)
     m = w.model
-    say("qwen stack: drawing weights on the device")
+    say(stack, "drawing weights on the device")
     g = torch.Generator(device="cuda")
     g.manual_seed(1000 + w.index)
     Wd = {}
@@ -606,19 +608,19 @@ def test_qwen_stack_bench_configuration(gpu_lib):
     E = [dev(e, C.BF16) for e in eps]
     tidx = torch.from_numpy(synth.txt_index(w)).cuda()
     ro = R.Rollout(w, api.Dit(m, Wd))
-    say("qwen stack: rollout")
+    say(stack, "rollout")
     res = ro.run(X0, T, E, cond=Cd, txt_index=tidx)
     torch.cuda.synchronize()
-    assert sorted(res.logp) == [1, 2, 3]
+    assert sorted(res.logp) == [k for k, sg in enumerate(res.sigmas) if sg > 0]
     for k in range(w.steps):
         xk, vk = host(res.xs[k]), host(res.vs[k])
         assert np.array_equal(vk, np.broadcast_to(b, vk.shape)), f"velocity of step {k}"
         xn_ref = osde.sde_step(xk, vk, host(E[k]), res.ts[k], res.ts[k + 1], res.sigmas[k])
-        check(host(res.xs[k + 1]), xn_ref, C.BF16, 0, what=f"qwen stack x step {k}")
+        check(host(res.xs[k + 1]), xn_ref, C.BF16, 0, what=f"{stack} x step {k}")
         if k in res.logp:
             lp_ref = osde.step_log_prob(xk, vk, host(res.xs[k + 1]), res.ts[k], res.ts[k + 1], res.sigmas[k])
             assert np.max(np.abs(host(res.logp[k]) - lp_ref)) <= LOGP_ABS
-    say("qwen stack: repeat")
+    say(stack, "repeat")
     res2 = ro.run(X0, T, E, cond=Cd, txt_index=tidx)
     torch.cuda.synchronize()
     assert torch.equal(res2.xs[-1], res.xs[-1])
