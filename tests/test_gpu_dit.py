@@ -587,7 +587,7 @@ def test_stack_bench_configuration(gpu_lib, stack):
     every velocity must be exactly b (a non-finite value anywhere in the blocks would reach it, 0 x
     NaN being NaN), every stored latent must match the oracle's SDE or ODE step from the previous
     stored latent element by element, every log-prob the oracle's, and a second rollout is bitwise
-    the first."""
+    the first.  On the Flux stack also the GRPO update and AWM forwards the benchmark times there."""
     w = getattr(C, stack)
     m = w.model
     say(stack, "drawing weights on the device")
@@ -625,3 +625,25 @@ def test_stack_bench_configuration(gpu_lib, stack):
     torch.cuda.synchronize()
     assert torch.equal(res2.xs[-1], res.xs[-1])
     assert all(torch.equal(res2.logp[k], res.logp[k]) for k in res.logp)
+    del res2
+    if stack != "FLUX_STACK":
+        return
+    # The training forwards the benchmark times on this stack.  GRPO update on the stored rollout:
+    # recomputed with the rollout's own weights every log-prob is bitwise the stored one, so the
+    # ratio is 1, nothing is clipped and the objective is -mean(A).  AWM (Eq. 3) at per-sample t:
+    # with v = b the per-sample loss is the oracle's on b, the noise and x_0.
+    say(stack, "GRPO and AWM forwards")
+    adv = torch.from_numpy(np.linspace(-1.5, 1.5, w.batch).astype(np.float32)).cuda()
+    new = ro.policy_logprobs(res, T, cond=Cd, txt_index=tidx)
+    loss, n = ro.grpo_objective(res, adv, T, cond=Cd, txt_index=tidx)
+    torch.cuda.synchronize()
+    assert torch.equal(new, torch.stack([res.logp[k] for k in ro.sde_step_ids()]))
+    assert int(n.cpu()[0]) == 0
+    assert host(loss)[0] == pytest.approx(-float(np.mean(host(adv))), rel=1e-12)
+    e = synth.normal(700, x0.shape, C.BF16)
+    t = np.linspace(0.05, 0.95, w.batch).astype(np.float32)
+    per, aloss = ro.awm_objective(X0, dev(e, C.BF16), torch.from_numpy(t).cuda(), T, adv, cond=Cd, txt_index=tidx)
+    torch.cuda.synchronize()
+    ref_per, ref_loss = olosses.awm_loss(np.broadcast_to(b, x0.shape), e, host(X0), host(adv))
+    np.testing.assert_allclose(host(per), ref_per, rtol=1e-5, atol=1e-9)
+    assert host(aloss)[0] == pytest.approx(ref_loss, rel=1e-5)
