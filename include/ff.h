@@ -165,6 +165,14 @@ int ff_group_advantage(const float* rewards, const float* weights, const int32_t
  * three bands of widths rope_axes over the token's (frame, row, col) grid
  * position; pair i of band a turns by pos_a * rope_theta^(-2i/rope_axes[a]).
  * Text tokens have position 0 (no rotation).
+ *
+ * Size limits (FF_EUNSUPPORTED beyond them, checked on the host before any
+ * allocation or launch): at most 4096 blocks of each kind; hidden <= 65536,
+ * heads <= 1024, mlp_hidden <= 262144, in_channels, txt_dim, pooled_dim <=
+ * 65536; per forward each grid axis <= 2^20, n_txt <= 2^20, n_prompts <=
+ * 65535, and N_img, B (N_img + n_txt) and n_prompts n_txt <= 2^27 token rows.
+ * No C++ exception leaves an entry point (a failed host allocation returns
+ * FF_EUNSUPPORTED).
  * ------------------------------------------------------------------------ */
 
 enum { FF_MODEL_MMDIT = 0, FF_MODEL_WAN = 1 };

@@ -4,6 +4,7 @@
 #include <cmath>
 #include <cstring>
 #include <string>
+#include <memory>
 #include <unordered_map>
 #include <vector>
 
@@ -95,6 +96,11 @@ std::vector<TensorSpec> tensor_table(const ff_dit_config& c) {
   return t;
 }
 
+// Size limits of a model and of a forward: they keep every tile count within a launch's 31-bit
+// grid and every buffer size within 2^48 bytes (far beyond the models and batches in use).
+constexpr int32_t kMaxBlocks = 4096, kMaxHidden = 1 << 16, kMaxHeads = 1024, kMaxMlp = 1 << 18, kMaxWidth = 1 << 16;
+constexpr int64_t kMaxAxis = 1 << 20, kMaxRows = int64_t(1) << 27, kMaxTxt = 1 << 20;
+
 int check_config(const ff_dit_config* c) {
   if (!c) return fail(FF_EINVAL, "ff_dit: null config");
   if (c->model != FF_MODEL_MMDIT && c->model != FF_MODEL_WAN) return fail(FF_EINVAL, "ff_dit: bad model %d", c->model);
@@ -103,6 +109,12 @@ int check_config(const ff_dit_config* c) {
   if (c->n_dual < 0 || c->n_single < 0 || c->n_wan < 0) return fail(FF_EINVAL, "ff_dit: negative block count");
   if (c->hidden <= 0 || c->heads <= 0 || c->head_dim <= 0 || c->mlp_hidden <= 0)
     return fail(FF_EINVAL, "ff_dit: non-positive size");
+  if (c->n_dual > kMaxBlocks || c->n_single > kMaxBlocks || c->n_wan > kMaxBlocks)
+    return fail(FF_EUNSUPPORTED, "ff_dit: more than %d blocks of one kind", kMaxBlocks);
+  if (c->hidden > kMaxHidden || c->heads > kMaxHeads || c->mlp_hidden > kMaxMlp || c->in_channels > kMaxWidth ||
+      c->txt_dim > kMaxWidth || c->pooled_dim > kMaxWidth)
+    return fail(FF_EUNSUPPORTED, "ff_dit: a width above its limit (hidden %d, heads %d, MLP %d, other widths %d)",
+                kMaxHidden, kMaxHeads, kMaxMlp, kMaxWidth);
   if (static_cast<int64_t>(c->heads) * c->head_dim != c->hidden)
     return fail(FF_EINVAL, "ff_dit: hidden %d != heads %d * head_dim %d", c->hidden, c->heads, c->head_dim);
   if (c->head_dim % 2) return fail(FF_EINVAL, "ff_dit: head_dim must be even");
@@ -711,96 +723,114 @@ int forward_mmdit(const ff_dit& m, const Plan& p, const void* x, const void* txt
   return FF_OK;
 }
 
+// Runs an entry point's body so that no C++ exception (a failed host allocation) leaves the C ABI.
+template <typename F>
+int guarded(const char* fn, F&& body) {
+  try {
+    return body();
+  } catch (const std::bad_alloc&) {
+    return fail(FF_EUNSUPPORTED, "%s: out of host memory", fn);
+  } catch (...) {
+    return fail(FF_EINVAL, "%s: internal error", fn);
+  }
+}
+
 }  // namespace
 
 extern "C" {
 
 int ff_dit_num_tensors(const ff_dit_config* cfg, int64_t* n) {
-  FF_TRY(check_config(cfg));
-  if (!n) return fail(FF_EINVAL, "ff_dit_num_tensors: null output");
-  *n = static_cast<int64_t>(tensor_table(*cfg).size());
-  return FF_OK;
+  return guarded("ff_dit_num_tensors", [&]() -> int {
+    FF_TRY(check_config(cfg));
+    if (!n) return fail(FF_EINVAL, "ff_dit_num_tensors: null output");
+    *n = static_cast<int64_t>(tensor_table(*cfg).size());
+    return FF_OK;
+  });
 }
 
 int ff_dit_tensor_info(const ff_dit_config* cfg, int64_t i, char* name, size_t name_cap, int64_t* shape0,
                        int64_t* shape1) {
-  FF_TRY(check_config(cfg));
-  std::vector<TensorSpec> t = tensor_table(*cfg);
-  if (i < 0 || i >= static_cast<int64_t>(t.size())) return fail(FF_EINVAL, "ff_dit_tensor_info: index %lld out of range", (long long)i);
-  if (name) {
-    if (name_cap < t[i].name.size() + 1) return fail(FF_EINVAL, "ff_dit_tensor_info: name buffer too small");
-    memcpy(name, t[i].name.c_str(), t[i].name.size() + 1);
-  }
-  if (shape0) *shape0 = t[i].s0;
-  if (shape1) *shape1 = t[i].s1;
-  return FF_OK;
+  return guarded("ff_dit_tensor_info", [&]() -> int {
+    FF_TRY(check_config(cfg));
+    std::vector<TensorSpec> t = tensor_table(*cfg);
+    if (i < 0 || i >= static_cast<int64_t>(t.size())) return fail(FF_EINVAL, "ff_dit_tensor_info: index %lld out of range", (long long)i);
+    if (name) {
+      if (name_cap < t[i].name.size() + 1) return fail(FF_EINVAL, "ff_dit_tensor_info: name buffer too small");
+      memcpy(name, t[i].name.c_str(), t[i].name.size() + 1);
+    }
+    if (shape0) *shape0 = t[i].s0;
+    if (shape1) *shape1 = t[i].s1;
+    return FF_OK;
+  });
 }
 
 int ff_dit_create(const ff_dit_config* cfg, const void* const* tensors, int64_t n_tensors, ff_dit** out) {
-  FF_TRY(check_config(cfg));
-  if (cfg->model == FF_MODEL_WAN && cfg->io_mode != FF_IO_LATENT)
-    return fail(FF_EUNSUPPORTED, "ff_dit_create: the WAN model runs in latent mode only");
-  if (!out) return fail(FF_EINVAL, "ff_dit_create: null output");
-  *out = nullptr;
-  std::vector<TensorSpec> t = tensor_table(*cfg);
-  if (n_tensors != static_cast<int64_t>(t.size()))
-    return fail(FF_EINVAL, "ff_dit_create: %lld tensors given, %zu expected", (long long)n_tensors, t.size());
-  if (!tensors) return fail(FF_EINVAL, "ff_dit_create: null tensor array");
-  std::unordered_map<std::string, const void*> by;
-  for (size_t i = 0; i < t.size(); ++i) {
-    if (!tensors[i]) return fail(FF_EINVAL, "ff_dit_create: tensor %zu (%s) is null", i, t[i].name.c_str());
-    if (!aligned16(tensors[i])) return fail(FF_EINVAL, "ff_dit_create: tensor %s not 16-byte aligned", t[i].name.c_str());
-    by[t[i].name] = tensors[i];
-  }
-  ff_dit* m = new ff_dit();
-  m->cfg = *cfg;
-  m->ptr.assign(tensors, tensors + n_tensors);
-  auto L = [&](const std::string& p) { Lin l; l.w = by[p + ".w"]; l.b = by[p + ".b"]; return l; };
-  if (cfg->io_mode == FF_IO_LATENT) {
-    m->temb1 = L("temb.fc1");
-    m->temb2 = L("temb.fc2");
-    if (cfg->model == FF_MODEL_MMDIT) {
-      if (cfg->pooled_dim) { m->pooled1 = L("pooled.fc1"); m->pooled2 = L("pooled.fc2"); }
-      m->txt_in = L("txt_in");
-    } else {
-      m->temb_proj = L("temb.proj");
-      m->txt1 = L("txt_in.fc1");
-      m->txt2 = L("txt_in.fc2");
+  return guarded("ff_dit_create", [&]() -> int {
+    FF_TRY(check_config(cfg));
+    if (cfg->model == FF_MODEL_WAN && cfg->io_mode != FF_IO_LATENT)
+      return fail(FF_EUNSUPPORTED, "ff_dit_create: the WAN model runs in latent mode only");
+    if (!out) return fail(FF_EINVAL, "ff_dit_create: null output");
+    *out = nullptr;
+    std::vector<TensorSpec> t = tensor_table(*cfg);
+    if (n_tensors != static_cast<int64_t>(t.size()))
+      return fail(FF_EINVAL, "ff_dit_create: %lld tensors given, %zu expected", (long long)n_tensors, t.size());
+    if (!tensors) return fail(FF_EINVAL, "ff_dit_create: null tensor array");
+    std::unordered_map<std::string, const void*> by;
+    for (size_t i = 0; i < t.size(); ++i) {
+      if (!tensors[i]) return fail(FF_EINVAL, "ff_dit_create: tensor %zu (%s) is null", i, t[i].name.c_str());
+      if (!aligned16(tensors[i])) return fail(FF_EINVAL, "ff_dit_create: tensor %s not 16-byte aligned", t[i].name.c_str());
+      by[t[i].name] = tensors[i];
     }
-    m->x_in = L("x_in");
-    m->final_mod = L("final.mod");
-    m->final_proj = L("final.proj");
-  }
-  for (int i = 0; i < (cfg->model == FF_MODEL_WAN ? cfg->n_wan : 0); ++i) {
-    std::string p = "wan." + std::to_string(i) + ".";
-    Wan wb;
-    wb.mod = by[p + "mod"];
-    wb.qkv = L(p + "sa.qkv"); wb.o = L(p + "sa.o");
-    wb.qn = by[p + "sa.q_norm.w"]; wb.kn = by[p + "sa.k_norm.w"];
-    wb.can_w = by[p + "ca.norm.w"]; wb.can_b = by[p + "ca.norm.b"];
-    wb.cq = L(p + "ca.q"); wb.ckv = L(p + "ca.kv"); wb.co = L(p + "ca.o");
-    wb.cqn = by[p + "ca.q_norm.w"]; wb.ckn = by[p + "ca.k_norm.w"];
-    wb.ffn1 = L(p + "ffn1"); wb.ffn2 = L(p + "ffn2");
-    m->wan.push_back(wb);
-  }
-  for (int i = 0; i < (cfg->model == FF_MODEL_MMDIT ? cfg->n_dual : 0); ++i)
-    for (int k = 0; k < 2; ++k) {
-      std::string p = "dual." + std::to_string(i) + (k == 0 ? ".img." : ".txt.");
-      Stream st;
-      st.mod = L(p + "mod"); st.qkv = L(p + "qkv"); st.o = L(p + "o");
-      st.mlp1 = L(p + "mlp1"); st.mlp2 = L(p + "mlp2");
-      st.qn = by[p + "q_norm.w"]; st.kn = by[p + "k_norm.w"];
-      (k == 0 ? m->dual_img : m->dual_txt).push_back(st);
+    std::unique_ptr<ff_dit> m(new ff_dit());
+    m->cfg = *cfg;
+    m->ptr.assign(tensors, tensors + n_tensors);
+    auto L = [&](const std::string& p) { Lin l; l.w = by[p + ".w"]; l.b = by[p + ".b"]; return l; };
+    if (cfg->io_mode == FF_IO_LATENT) {
+      m->temb1 = L("temb.fc1");
+      m->temb2 = L("temb.fc2");
+      if (cfg->model == FF_MODEL_MMDIT) {
+        if (cfg->pooled_dim) { m->pooled1 = L("pooled.fc1"); m->pooled2 = L("pooled.fc2"); }
+        m->txt_in = L("txt_in");
+      } else {
+        m->temb_proj = L("temb.proj");
+        m->txt1 = L("txt_in.fc1");
+        m->txt2 = L("txt_in.fc2");
+      }
+      m->x_in = L("x_in");
+      m->final_mod = L("final.mod");
+      m->final_proj = L("final.proj");
     }
-  for (int j = 0; j < (cfg->model == FF_MODEL_MMDIT ? cfg->n_single : 0); ++j) {
-    std::string p = "single." + std::to_string(j) + ".";
-    Single sb;
-    sb.mod = L(p + "mod"); sb.lin1 = L(p + "lin1"); sb.lin2 = L(p + "lin2");
-    sb.qn = by[p + "q_norm.w"]; sb.kn = by[p + "k_norm.w"];
-    m->single.push_back(sb);
-  }
-  *out = m;
-  return FF_OK;
+    for (int i = 0; i < (cfg->model == FF_MODEL_WAN ? cfg->n_wan : 0); ++i) {
+      std::string p = "wan." + std::to_string(i) + ".";
+      Wan wb;
+      wb.mod = by[p + "mod"];
+      wb.qkv = L(p + "sa.qkv"); wb.o = L(p + "sa.o");
+      wb.qn = by[p + "sa.q_norm.w"]; wb.kn = by[p + "sa.k_norm.w"];
+      wb.can_w = by[p + "ca.norm.w"]; wb.can_b = by[p + "ca.norm.b"];
+      wb.cq = L(p + "ca.q"); wb.ckv = L(p + "ca.kv"); wb.co = L(p + "ca.o");
+      wb.cqn = by[p + "ca.q_norm.w"]; wb.ckn = by[p + "ca.k_norm.w"];
+      wb.ffn1 = L(p + "ffn1"); wb.ffn2 = L(p + "ffn2");
+      m->wan.push_back(wb);
+    }
+    for (int i = 0; i < (cfg->model == FF_MODEL_MMDIT ? cfg->n_dual : 0); ++i)
+      for (int k = 0; k < 2; ++k) {
+        std::string p = "dual." + std::to_string(i) + (k == 0 ? ".img." : ".txt.");
+        Stream st;
+        st.mod = L(p + "mod"); st.qkv = L(p + "qkv"); st.o = L(p + "o");
+        st.mlp1 = L(p + "mlp1"); st.mlp2 = L(p + "mlp2");
+        st.qn = by[p + "q_norm.w"]; st.kn = by[p + "k_norm.w"];
+        (k == 0 ? m->dual_img : m->dual_txt).push_back(st);
+      }
+    for (int j = 0; j < (cfg->model == FF_MODEL_MMDIT ? cfg->n_single : 0); ++j) {
+      std::string p = "single." + std::to_string(j) + ".";
+      Single sb;
+      sb.mod = L(p + "mod"); sb.lin1 = L(p + "lin1"); sb.lin2 = L(p + "lin2");
+      sb.qn = by[p + "q_norm.w"]; sb.kn = by[p + "k_norm.w"];
+      m->single.push_back(sb);
+    }
+    *out = m.release();
+    return FF_OK;
+  });
 }
 
 int ff_dit_destroy(ff_dit* m) {
@@ -815,7 +845,11 @@ static int check_forward_shape(const ff_dit* m, int64_t B, const int32_t grid[3]
   if (grid[0] < 1 || grid[1] < 1 || grid[2] < 1) return fail(FF_EINVAL, "ff_dit: grid entries must be >= 1");
   if (n_txt < 1) return fail(FF_EINVAL, "ff_dit: n_txt must be >= 1");
   if (n_prompts < 1) return fail(FF_EINVAL, "ff_dit: n_prompts must be >= 1");
+  if (grid[0] > kMaxAxis || grid[1] > kMaxAxis || grid[2] > kMaxAxis || n_txt > kMaxTxt || n_prompts > 65535)
+    return fail(FF_EUNSUPPORTED, "ff_dit: grid axis, n_txt or n_prompts above its limit");
   const int64_t Ni = static_cast<int64_t>(grid[0]) * grid[1] * grid[2];
+  if (Ni > kMaxRows || B * (Ni + n_txt) > kMaxRows || n_prompts * n_txt > kMaxRows)
+    return fail(FF_EUNSUPPORTED, "ff_dit: more than %lld token rows in one forward", (long long)kMaxRows);
   if (m->cfg.dtype == FF_BF16 && (Ni % 8 || n_txt % 8))
     return fail(FF_EUNSUPPORTED, "ff_dit: bf16 token counts must be multiples of 8 (N_img=%lld, n_txt=%lld)", (long long)Ni, (long long)n_txt);
   return FF_OK;
@@ -823,39 +857,43 @@ static int check_forward_shape(const ff_dit* m, int64_t B, const int32_t grid[3]
 
 int ff_dit_workspace_size(const ff_dit* m, int64_t B, const int32_t grid[3], int64_t n_txt, int64_t n_prompts,
                           size_t* bytes) {
-  FF_TRY(check_forward_shape(m, B, grid, n_txt, n_prompts));
-  if (!bytes) return fail(FF_EINVAL, "ff_dit_workspace_size: null output");
-  *bytes = plan(*m, B, grid, n_txt, n_prompts).total;
-  return FF_OK;
+  return guarded("ff_dit_workspace_size", [&]() -> int {
+    FF_TRY(check_forward_shape(m, B, grid, n_txt, n_prompts));
+    if (!bytes) return fail(FF_EINVAL, "ff_dit_workspace_size: null output");
+    *bytes = plan(*m, B, grid, n_txt, n_prompts).total;
+    return FF_OK;
+  });
 }
 
 int ff_dit_forward(const ff_dit* m, const void* x, const void* txt, const int32_t* txt_index, int64_t n_prompts,
                    const void* cond, const float* t, const int32_t grid[3], int64_t B, int64_t n_txt, void* v_out,
                    void* txt_out, void* workspace, size_t ws_bytes, void* stream) {
-  FF_TRY(check_forward_shape(m, B, grid, n_txt, n_prompts));
-  const ff_dit_config& c = m->cfg;
-  if (!x || !txt || !v_out) return fail(FF_EINVAL, "ff_dit_forward: null x, txt or v_out");
-  if (!aligned16(x) || !aligned16(txt) || !aligned16(v_out) || (txt_out && !aligned16(txt_out)) ||
-      (cond && !aligned16(cond)))
-    return fail(FF_EINVAL, "ff_dit_forward: tensors must be 16-byte aligned");
-  if (c.io_mode == FF_IO_LATENT) {
-    if (!t) return fail(FF_EINVAL, "ff_dit_forward: latent mode needs t");
-    if (txt_out) return fail(FF_EINVAL, "ff_dit_forward: txt_out must be NULL in latent mode");
-    if (!txt_index && n_prompts != B) return fail(FF_EINVAL, "ff_dit_forward: txt_index NULL needs n_prompts == B");
-    if (c.pooled_dim && !cond) return fail(FF_EINVAL, "ff_dit_forward: pooled_dim > 0 needs cond");
-  } else {
-    if (!cond) return fail(FF_EINVAL, "ff_dit_forward: hidden mode needs cond");
-    if (txt_index || n_prompts != B) return fail(FF_EINVAL, "ff_dit_forward: hidden mode takes per-sample text (txt_index NULL, n_prompts == B)");
-  }
-  if (v_out == x || v_out == txt || (txt_out && (txt_out == x || txt_out == txt || txt_out == v_out)))
-    return fail(FF_EINVAL, "ff_dit_forward: outputs may not alias inputs");
-  Plan p = plan(*m, B, grid, n_txt, n_prompts);
-  if (!workspace || ws_bytes < p.total)
-    return fail(FF_EWORKSPACE, "ff_dit_forward: workspace of %zu bytes needed, %zu given", p.total, workspace ? ws_bytes : 0);
-  if (!aligned16(workspace)) return fail(FF_EINVAL, "ff_dit_forward: workspace must be 16-byte aligned");
-  if (c.model == FF_MODEL_WAN)
-    return forward_wan(*m, p, x, txt, txt_index, t, grid, v_out, workspace, nullptr, static_cast<hipStream_t>(stream));
-  return forward_mmdit(*m, p, x, txt, txt_index, cond, t, grid, v_out, txt_out, workspace, static_cast<hipStream_t>(stream));
+  return guarded("ff_dit_forward", [&]() -> int {
+    FF_TRY(check_forward_shape(m, B, grid, n_txt, n_prompts));
+    const ff_dit_config& c = m->cfg;
+    if (!x || !txt || !v_out) return fail(FF_EINVAL, "ff_dit_forward: null x, txt or v_out");
+    if (!aligned16(x) || !aligned16(txt) || !aligned16(v_out) || (txt_out && !aligned16(txt_out)) ||
+        (cond && !aligned16(cond)))
+      return fail(FF_EINVAL, "ff_dit_forward: tensors must be 16-byte aligned");
+    if (c.io_mode == FF_IO_LATENT) {
+      if (!t) return fail(FF_EINVAL, "ff_dit_forward: latent mode needs t");
+      if (txt_out) return fail(FF_EINVAL, "ff_dit_forward: txt_out must be NULL in latent mode");
+      if (!txt_index && n_prompts != B) return fail(FF_EINVAL, "ff_dit_forward: txt_index NULL needs n_prompts == B");
+      if (c.pooled_dim && !cond) return fail(FF_EINVAL, "ff_dit_forward: pooled_dim > 0 needs cond");
+    } else {
+      if (!cond) return fail(FF_EINVAL, "ff_dit_forward: hidden mode needs cond");
+      if (txt_index || n_prompts != B) return fail(FF_EINVAL, "ff_dit_forward: hidden mode takes per-sample text (txt_index NULL, n_prompts == B)");
+    }
+    if (v_out == x || v_out == txt || (txt_out && (txt_out == x || txt_out == txt || txt_out == v_out)))
+      return fail(FF_EINVAL, "ff_dit_forward: outputs may not alias inputs");
+    Plan p = plan(*m, B, grid, n_txt, n_prompts);
+    if (!workspace || ws_bytes < p.total)
+      return fail(FF_EWORKSPACE, "ff_dit_forward: workspace of %zu bytes needed, %zu given", p.total, workspace ? ws_bytes : 0);
+    if (!aligned16(workspace)) return fail(FF_EINVAL, "ff_dit_forward: workspace must be 16-byte aligned");
+    if (c.model == FF_MODEL_WAN)
+      return forward_wan(*m, p, x, txt, txt_index, t, grid, v_out, workspace, nullptr, static_cast<hipStream_t>(stream));
+    return forward_mmdit(*m, p, x, txt, txt_index, cond, t, grid, v_out, txt_out, workspace, static_cast<hipStream_t>(stream));
+  });
 }
 
 int ff_dit_context_size(const ff_dit* m, int64_t B, int64_t n_txt, size_t* bytes) {
@@ -869,44 +907,48 @@ int ff_dit_context_size(const ff_dit* m, int64_t B, int64_t n_txt, size_t* bytes
 int ff_dit_prepare_context(const ff_dit* m, const void* txt, const int32_t* txt_index, int64_t n_prompts,
                            const int32_t grid[3], int64_t B, int64_t n_txt, void* context, size_t context_bytes,
                            void* workspace, size_t ws_bytes, void* stream) {
-  FF_TRY(check_forward_shape(m, B, grid, n_txt, n_prompts));
-  if (m->cfg.model != FF_MODEL_WAN) return fail(FF_EUNSUPPORTED, "ff_dit_prepare_context: WAN models only");
-  if (!txt || !context) return fail(FF_EINVAL, "ff_dit_prepare_context: null txt or context");
-  if (!aligned16(txt) || !aligned16(context)) return fail(FF_EINVAL, "ff_dit_prepare_context: txt and context must be 16-byte aligned");
-  if (!txt_index && n_prompts != B) return fail(FF_EINVAL, "ff_dit_prepare_context: txt_index NULL needs n_prompts == B");
-  const size_t kvb = wan_kv_block_bytes(m->cfg, B, n_txt);
-  if (context_bytes < 2 * m->cfg.n_wan * kvb)
-    return fail(FF_EWORKSPACE, "ff_dit_prepare_context: context of %zu bytes needed, %zu given", 2 * m->cfg.n_wan * kvb, context_bytes);
-  Plan p = plan(*m, B, grid, n_txt, n_prompts);
-  if (!workspace || ws_bytes < p.total)
-    return fail(FF_EWORKSPACE, "ff_dit_prepare_context: workspace of %zu bytes needed, %zu given", p.total, workspace ? ws_bytes : 0);
-  if (!aligned16(workspace)) return fail(FF_EINVAL, "ff_dit_prepare_context: workspace must be 16-byte aligned");
-  const hipStream_t s = static_cast<hipStream_t>(stream);
-  FF_TRY(wan_text_context(*m, p, txt, txt_index, workspace, s));
-  char* store = static_cast<char*>(context);
-  for (int i = 0; i < m->cfg.n_wan; ++i)
-    FF_TRY(wan_cross_kv(*m, p, workspace, i, at(workspace, p.xtxt), store + 2 * i * kvb, store + (2 * i + 1) * kvb, s));
-  return FF_OK;
+  return guarded("ff_dit_prepare_context", [&]() -> int {
+    FF_TRY(check_forward_shape(m, B, grid, n_txt, n_prompts));
+    if (m->cfg.model != FF_MODEL_WAN) return fail(FF_EUNSUPPORTED, "ff_dit_prepare_context: WAN models only");
+    if (!txt || !context) return fail(FF_EINVAL, "ff_dit_prepare_context: null txt or context");
+    if (!aligned16(txt) || !aligned16(context)) return fail(FF_EINVAL, "ff_dit_prepare_context: txt and context must be 16-byte aligned");
+    if (!txt_index && n_prompts != B) return fail(FF_EINVAL, "ff_dit_prepare_context: txt_index NULL needs n_prompts == B");
+    const size_t kvb = wan_kv_block_bytes(m->cfg, B, n_txt);
+    if (context_bytes < 2 * m->cfg.n_wan * kvb)
+      return fail(FF_EWORKSPACE, "ff_dit_prepare_context: context of %zu bytes needed, %zu given", 2 * m->cfg.n_wan * kvb, context_bytes);
+    Plan p = plan(*m, B, grid, n_txt, n_prompts);
+    if (!workspace || ws_bytes < p.total)
+      return fail(FF_EWORKSPACE, "ff_dit_prepare_context: workspace of %zu bytes needed, %zu given", p.total, workspace ? ws_bytes : 0);
+    if (!aligned16(workspace)) return fail(FF_EINVAL, "ff_dit_prepare_context: workspace must be 16-byte aligned");
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    FF_TRY(wan_text_context(*m, p, txt, txt_index, workspace, s));
+    char* store = static_cast<char*>(context);
+    for (int i = 0; i < m->cfg.n_wan; ++i)
+      FF_TRY(wan_cross_kv(*m, p, workspace, i, at(workspace, p.xtxt), store + 2 * i * kvb, store + (2 * i + 1) * kvb, s));
+    return FF_OK;
+  });
 }
 
 int ff_dit_forward_ctx(const ff_dit* m, const void* x, const void* context, size_t context_bytes, const float* t,
                        const int32_t grid[3], int64_t B, int64_t n_txt, void* v_out, void* workspace, size_t ws_bytes,
                        void* stream) {
-  FF_TRY(check_forward_shape(m, B, grid, n_txt, 1));
-  if (m->cfg.model != FF_MODEL_WAN) return fail(FF_EUNSUPPORTED, "ff_dit_forward_ctx: WAN models only");
-  if (!x || !context || !t || !v_out) return fail(FF_EINVAL, "ff_dit_forward_ctx: null x, context, t or v_out");
-  if (!aligned16(x) || !aligned16(context) || !aligned16(v_out))
-    return fail(FF_EINVAL, "ff_dit_forward_ctx: tensors must be 16-byte aligned");
-  if (v_out == x || v_out == context) return fail(FF_EINVAL, "ff_dit_forward_ctx: v_out may not alias an input");
-  const size_t kvb = wan_kv_block_bytes(m->cfg, B, n_txt);
-  if (context_bytes < 2 * m->cfg.n_wan * kvb)
-    return fail(FF_EWORKSPACE, "ff_dit_forward_ctx: context of %zu bytes needed, %zu given", 2 * m->cfg.n_wan * kvb, context_bytes);
-  Plan p = plan(*m, B, grid, n_txt, 1);   // the prompts' text buffers are not used here
-  if (!workspace || ws_bytes < p.total)
-    return fail(FF_EWORKSPACE, "ff_dit_forward_ctx: workspace of %zu bytes needed, %zu given", p.total, workspace ? ws_bytes : 0);
-  if (!aligned16(workspace)) return fail(FF_EINVAL, "ff_dit_forward_ctx: workspace must be 16-byte aligned");
-  return forward_wan(*m, p, x, nullptr, nullptr, t, grid, v_out, workspace, static_cast<const char*>(context),
-                     static_cast<hipStream_t>(stream));
+  return guarded("ff_dit_forward_ctx", [&]() -> int {
+    FF_TRY(check_forward_shape(m, B, grid, n_txt, 1));
+    if (m->cfg.model != FF_MODEL_WAN) return fail(FF_EUNSUPPORTED, "ff_dit_forward_ctx: WAN models only");
+    if (!x || !context || !t || !v_out) return fail(FF_EINVAL, "ff_dit_forward_ctx: null x, context, t or v_out");
+    if (!aligned16(x) || !aligned16(context) || !aligned16(v_out))
+      return fail(FF_EINVAL, "ff_dit_forward_ctx: tensors must be 16-byte aligned");
+    if (v_out == x || v_out == context) return fail(FF_EINVAL, "ff_dit_forward_ctx: v_out may not alias an input");
+    const size_t kvb = wan_kv_block_bytes(m->cfg, B, n_txt);
+    if (context_bytes < 2 * m->cfg.n_wan * kvb)
+      return fail(FF_EWORKSPACE, "ff_dit_forward_ctx: context of %zu bytes needed, %zu given", 2 * m->cfg.n_wan * kvb, context_bytes);
+    Plan p = plan(*m, B, grid, n_txt, 1);   // the prompts' text buffers are not used here
+    if (!workspace || ws_bytes < p.total)
+      return fail(FF_EWORKSPACE, "ff_dit_forward_ctx: workspace of %zu bytes needed, %zu given", p.total, workspace ? ws_bytes : 0);
+    if (!aligned16(workspace)) return fail(FF_EINVAL, "ff_dit_forward_ctx: workspace must be 16-byte aligned");
+    return forward_wan(*m, p, x, nullptr, nullptr, t, grid, v_out, workspace, static_cast<const char*>(context),
+                       static_cast<hipStream_t>(stream));
+  });
 }
 
 }  // extern "C"

@@ -246,6 +246,73 @@ def test_dit_validation_and_workspace_plan():
     _err(lib.ff_dit_num_tensors(byref(cfg3), byref(n)), _lib.FF_EINVAL)
 
 
+def test_dit_size_limits():
+    """Block counts, widths and forward shapes beyond the library's limits are refused on the host
+    (the tensor table of 2^31 blocks is never built; token counts whose products would overflow a
+    launch grid or a workspace size never reach a kernel)."""
+    lib = _lib.load()
+    m = C.FLUX_BLOCK.model
+    n = c_int64()
+    for bad in (m.replace(n_dual=4097), m.replace(n_single=2 ** 31 - 1), m.replace(hidden=1 << 17, heads=1024),
+                m.replace(mlp_hidden=(1 << 18) + 64)):
+        _err(lib.ff_dit_num_tensors(byref(api.dit_config(bad)), byref(n)), _lib.FF_EUNSUPPORTED)
+    assert lib.ff_dit_num_tensors(byref(api.dit_config(m.replace(n_dual=4096))), byref(n)) == 0
+    cfg = api.dit_config(m)
+    assert lib.ff_dit_num_tensors(byref(cfg), byref(n)) == 0
+    ptrs = (c_void_p * n.value)(*[4096 * (i + 1) for i in range(n.value)])
+    h = c_void_p()
+    assert lib.ff_dit_create(byref(cfg), ptrs, n.value, byref(h)) == 0
+    ws = c_size_t()
+    for grid, B, n_txt, n_prompts in (((1, (1 << 20) + 1, 8), 8, 512, 8),    # an axis above 2^20
+                                      ((64, 1 << 15, 1 << 15), 1, 512, 1),   # 2^34 tokens
+                                      ((1, 1024, 1024), 256, 512, 256),      # B x tokens above 2^27
+                                      ((1, 64, 64), 8, (1 << 20) + 8, 8),    # text above 2^20
+                                      ((1, 64, 64), 8, 512, 65536)):         # prompts above 65535
+        _err(lib.ff_dit_workspace_size(h, B, (c_int32 * 3)(*grid), n_txt, n_prompts, byref(ws)), _lib.FF_EUNSUPPORTED)
+    assert lib.ff_dit_workspace_size(h, 1, (c_int32 * 3)(21, 30, 52), 512, 1, byref(ws)) == 0
+    assert lib.ff_dit_destroy(h) == 0
+
+
+def test_dit_entry_points_return_a_status_for_mutated_configs():
+    """Seeded mutations of valid configurations (one to three fields set to extreme or odd values):
+    every entry point returns a status, and an accepted model with an accepted shape reports a
+    workspace of at least one byte per element of its [B, N_img, hidden] activations (no size
+    wrapped around)."""
+    import random
+    lib = _lib.load()
+    vals = [-2 ** 31, -7, -1, 0, 1, 2, 3, 8, 64, 128, 130, 3072, 1 << 16, (1 << 16) + 8, 2 ** 31 - 1]
+    rng = random.Random(7)
+    bases = [C.TINY.model, C.FLUX_BLOCK.model, C.WAN_STACK.model.replace(n_wan=2)]
+    fields = [f for f, _ in _lib.DitConfig._fields_]
+    accepted = 0
+    for _ in range(400):
+        cfg = api.dit_config(rng.choice(bases))
+        for _ in range(rng.choice([1, 2, 3])):
+            f = rng.choice(fields)
+            if f == "rope_axes":
+                cfg.rope_axes[rng.randrange(3)] = rng.choice(vals)
+            elif f in ("rope_theta", "norm_eps"):
+                setattr(cfg, f, rng.choice([0.0, -1.0, float("nan"), 1e300, 1e-6]))
+            else:
+                setattr(cfg, f, rng.choice(vals))
+        n = c_int64()
+        if lib.ff_dit_num_tensors(byref(cfg), byref(n)) != 0:
+            continue
+        h = c_void_p()
+        ptrs = (c_void_p * n.value)(*[4096 * (i + 1) for i in range(n.value)])
+        if lib.ff_dit_create(byref(cfg), ptrs, n.value, byref(h)) != 0:
+            continue
+        accepted += 1
+        for _ in range(4):
+            grid = (rng.choice([1, 2, 8, 64, 1 << 20]), rng.choice([1, 8, 64]), rng.choice([8, 64, 1 << 21]))
+            B, n_txt = rng.choice([1, 8, 65535, 65536]), rng.choice([8, 256, 1 << 21])
+            ws = c_size_t()
+            if lib.ff_dit_workspace_size(h, B, (c_int32 * 3)(*grid), n_txt, B, byref(ws)) == 0:
+                assert ws.value >= B * grid[0] * grid[1] * grid[2] * cfg.hidden
+        assert lib.ff_dit_destroy(h) == 0
+    assert accepted > 20
+
+
 def test_missing_library_fails_loudly(tmp_path, monkeypatch):
     """Without the HIP library the binding raises instead of falling back to anything else."""
     monkeypatch.setattr(_lib, "_lib", None)
