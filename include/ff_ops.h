@@ -28,7 +28,9 @@ enum { FF_EPI_BIAS = 0, FF_EPI_GELU = 1, FF_EPI_GATED = 2 };
  *                 adaLN-gated residual; gate float32 [*, gate_ld] or NULL for a
  *                 plain residual (gate = 1), resid [M, N] (row stride ldr) may
  *                 alias out.
- * Accumulation is float32.  bf16 requires K % 64 == 0 and lda, ldo, ldr % 8 == 0.
+ * Accumulation is float32.  bf16 requires K % 64 == 0 and lda, ldo, ldr % 8 == 0.  Limits
+ * (FF_EUNSUPPORTED): M, N <= 2^27; K and the row strides <= 2^22 elements; at most 2^31 - 1
+ * tiles of 128 x 128.
  * workspace (device, 16-byte aligned, ff_linear_workspace_size bytes) or NULL: with it, a bf16
  * launch whose 256 x 256 tiles leave a last, partly filled round of the GPU's compute units splits
  * that round's tiles along K (float32 partial sums in the workspace, added in a fixed order, so the
@@ -46,7 +48,8 @@ int ff_linear_workspace_size(size_t* bytes);
  *   Q [B, heads, n_q, d], K [B, heads, n_kv, d];
  *   V: bf16 takes V transposed, [B, heads, d, n_kv]; f32 takes [B, heads, n_kv, d].
  *   out [B, n_q, heads*d] (token-major, heads concatenated).
- * bf16: d == 128, n_kv % 8 == 0.  f32: d <= 64. */
+ * bf16: d == 128, n_kv % 8 == 0.  f32: d <= 64, B heads <= 65535.  Limits (FF_EUNSUPPORTED):
+ * n_q, n_kv <= 2^27, heads d <= 2^22, at most 2^31 - 1 workgroups of 64 queries. */
 int ff_attention(const void* Q, const void* K, const void* V, void* out, int64_t B, int64_t heads,
                  int64_t n_q, int64_t n_kv, int64_t head_dim, int32_t dtype, void* stream);
 
@@ -117,7 +120,7 @@ int ff_quantize_fp8(const void* x, int64_t ldx, uint8_t* q, int64_t ldq, float* 
  * ff_quantize_fp8 produces them), bias bf16 [N] or NULL, out bf16 [M, N] (row stride ldo
  * elements); epi FF_EPI_BIAS or FF_EPI_GELU (GELU_tanh on columns >= gelu_from).  Products of
  * codes accumulate in float32.  K % 128 == 0; lda, ldw % 16 == 0; ldo % 8 == 0; A, W, out,
- * bias and d_w 16-byte aligned. */
+ * bias and d_w 16-byte aligned.  Size limits as ff_linear. */
 int ff_linear_fp8(const uint8_t* A, int64_t lda, const float* d_a, const uint8_t* W, int64_t ldw, const float* d_w,
                   const void* bias, void* out, int64_t ldo, int64_t M, int64_t N, int64_t K, int32_t epi,
                   int64_t gelu_from, void* stream);

@@ -413,6 +413,7 @@ int attention(const AttnArgs& a, hipStream_t s) {
     return ls.status();
   }
   if (a.d > 64) return fail(FF_EUNSUPPORTED, "attention: f32 head_dim %lld > 64", (long long)a.d);
+  if (a.B * a.heads > 65535) return fail(FF_EUNSUPPORTED, "attention: f32 needs B x heads <= 65535 (one grid row each)");
   AttnF32Params p{a.B, a.heads, a.n_q, a.n_kv, a.d,
                   static_cast<const float*>(a.Q), static_cast<const float*>(a.K), static_cast<const float*>(a.Vt),
                   static_cast<float*>(a.out0), static_cast<float*>(a.out1), a.split, a.ldo, a.scale, qbs, qhs, qrs};

@@ -1,4 +1,5 @@
 // C ABI of the kernel-level building blocks (include/ff_ops.h): validation + dispatch.
+#include <climits>
 #include <cmath>
 
 #include "../../include/ff_ops.h"
@@ -9,6 +10,17 @@ using namespace ff;
 namespace {
 int check_dtype(const char* fn, int32_t dt) {
   if (dt != FF_F32 && dt != FF_BF16) return fail(FF_EINVAL, "%s: bad dtype %d", fn, dt);
+  return FF_OK;
+}
+
+// Size limits of the linear layers and attention: row strides and K fit the 32-bit offsets of a
+// tile's buffer loads, and tile and workgroup counts fit a launch grid.
+constexpr int64_t kMaxOpRows = int64_t(1) << 27, kMaxOpStride = int64_t(1) << 22;
+int check_linear_sizes(const char* fn, int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldw, int64_t ldo,
+                       int64_t ldr, int64_t gate_ld) {
+  if (M > kMaxOpRows || N > kMaxOpRows || K > kMaxOpStride || lda > kMaxOpStride || ldw > kMaxOpStride ||
+      ldo > kMaxOpStride || ldr > kMaxOpStride || gate_ld > kMaxOpStride || ((M + 127) / 128) * ((N + 127) / 128) > INT32_MAX)
+    return fail(FF_EUNSUPPORTED, "%s: M, N above 2^27, K or a row stride above 2^22, or too many tiles", fn);
   return FF_OK;
 }
 }  // namespace
@@ -25,6 +37,7 @@ int ff_linear(const void* A, int64_t lda, const void* W, const void* bias, void*
   if (M == 0 || N == 0) return FF_OK;
   if (!A || !W || !out) return fail(FF_EINVAL, "%s: null A, W or out", fn);
   if (lda < K || ldo < N) return fail(FF_EINVAL, "%s: lda < K or ldo < N", fn);
+  FF_TRY(check_linear_sizes(fn, M, N, K, lda, K, ldo, epi == FF_EPI_GATED ? ldr : 0, gate ? gate_ld : 0));
   if (epi < FF_EPI_BIAS || epi > FF_EPI_GATED) return fail(FF_EINVAL, "%s: bad epilogue %d", fn, epi);
   if (epi == FF_EPI_GATED) {
     if (!resid) return fail(FF_EINVAL, "%s: gated epilogue needs resid", fn);
@@ -66,7 +79,9 @@ int ff_attention(const void* Q, const void* K, const void* V, void* out, int64_t
   if (B == 0 || n_q == 0) return FF_OK;
   if (!Q || !K || !V || !out) return fail(FF_EINVAL, "%s: null pointer", fn);
   if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(out)) return fail(FF_EINVAL, "%s: pointers must be 16-byte aligned", fn);
-  if (B * heads > (int64_t{1} << 31)) return fail(FF_EUNSUPPORTED, "%s: too many heads", fn);
+  if (B > kMaxOpRows || heads > kMaxOpStride || n_q > kMaxOpRows || n_kv > kMaxOpRows || heads * head_dim > kMaxOpStride ||
+      (n_q + 63) / 64 * B * heads > INT32_MAX)
+    return fail(FF_EUNSUPPORTED, "%s: n_q or n_kv above 2^27, heads x head_dim above 2^22, or too many workgroups", fn);
   AttnArgs a{};
   a.dtype = dtype;
   a.B = B; a.heads = heads; a.d = head_dim; a.n_q = n_q; a.n_kv = n_kv;
@@ -185,6 +200,7 @@ int ff_linear_fp8(const uint8_t* A, int64_t lda, const float* d_a, const uint8_t
   if (M == 0 || N == 0) return FF_OK;
   if (!A || !W || !d_a || !d_w || !out) return fail(FF_EINVAL, "%s: null A, W, d_a, d_w or out", fn);
   if (lda < K || ldw < K || ldo < N) return fail(FF_EINVAL, "%s: lda or ldw < K, or ldo < N", fn);
+  FF_TRY(check_linear_sizes(fn, M, N, K, lda, ldw, ldo, 0, 0));
   if (epi != FF_EPI_BIAS && epi != FF_EPI_GELU) return fail(FF_EINVAL, "%s: epilogue %d (bias or GELU only)", fn, epi);
   if (K % 128) return fail(FF_EUNSUPPORTED, "%s: K %% 128 != 0 (K=%lld)", fn, (long long)K);
   if (lda % 16 || ldw % 16 || ldo % 8) return fail(FF_EINVAL, "%s: lda, ldw %% 16 and ldo %% 8 must be 0", fn);

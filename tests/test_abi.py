@@ -273,6 +273,24 @@ def test_dit_size_limits():
     assert lib.ff_dit_destroy(h) == 0
 
 
+def test_linear_and_attention_size_limits():
+    """Shapes whose strides would overflow a tile's 32-bit load offsets, or whose tile or workgroup
+    counts would overflow a launch grid, are refused on the host before any launch."""
+    lib = _lib.load()
+    f = c_void_p(1 << 20)
+    big, K = 1 << 27, 3072
+    for M, N, K_, lda in ((big + 1, 64, K, K), (64, big + 1, K, K), (64, 64, (1 << 22) + 64, (1 << 22) + 64),
+                          (64, 64, K, (1 << 22) + 8), (big, big, K, K)):
+        _err(lib.ff_linear(f, lda, f, None, f, max(N, 64), M, N, K_, 0, 0, None, 0, None, 0, 0, 1, None, 0, None),
+             _lib.FF_EUNSUPPORTED)
+    _err(lib.ff_linear_fp8(f, (1 << 22) + 128, f, f, (1 << 22) + 128, f, None, f, 64, 64, 64, (1 << 22) + 128, 0, 0,
+                           None), _lib.FF_EUNSUPPORTED)
+    # attention: n_kv above 2^27, too many workgroups, f32 grid rows
+    _err(lib.ff_attention(f, f, f, f, 1, 1, 256, big + 8, 128, 1, None), _lib.FF_EUNSUPPORTED)
+    _err(lib.ff_attention(f, f, f, f, 65535, 1024, 1 << 20, 64, 128, 1, None), _lib.FF_EUNSUPPORTED)
+    _err(lib.ff_attention(f, f, f, f, 300, 300, 64, 64, 16, 0, None), _lib.FF_EUNSUPPORTED)
+
+
 def test_dit_entry_points_return_a_status_for_mutated_configs():
     """Seeded mutations of valid configurations (one to three fields set to extreme or odd values):
     every entry point returns a status, and an accepted model with an accepted shape reports a
