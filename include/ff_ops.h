@@ -79,7 +79,8 @@ int ff_rope_table(float* out, const int32_t grid[3], int32_t head_dim, const int
  * (the adaLN modulation and embedding MLPs).  in float32 [B, K], out float32
  * [B, N], W of dtype [N, K]; act: 0 none, 1 SiLU, 2 GELU_tanh.  classes: NULL, or the row map
  * ff_row_classes made of `in` (device): then each class is computed once and its result stored
- * in every member's row (the same values, since members are bitwise-equal rows). */
+ * in every member's row (the same values, since members are bitwise-equal rows).  K % 8 == 0;
+ * limits (FF_EUNSUPPORTED): B <= 65535, N <= 2^27, K <= 2^22. */
 int ff_skinny_linear(const float* in, const void* W, const void* bias, float* out, int64_t B, int64_t N,
                      int64_t K, int32_t act_in, int32_t act_out, int32_t dtype, const int32_t* classes,
                      void* stream);
@@ -111,7 +112,8 @@ int ff_stream_probe(int32_t mode, int32_t nontemporal, const void* src, void* ds
  * bytes; a value that rounds to zero keeps its sign bit) and d[r] = fl32(amax / 448) (float32), so
  * that x[r, k] ~ d[r] * decode(q[r, k]).  A row with amax < 448 * 2^-126 (a row of zeros
  * included) gets codes 0 and d = 0; a row holding an infinity or a NaN gets the NaN code 0x7f in
- * every position and d = NaN.  cols, ldx, ldq % 8 == 0; x and q 16-byte aligned. */
+ * every position and d = NaN.  cols, ldx, ldq % 8 == 0; x and q 16-byte aligned; rows <= 2^27 and
+ * ldx, ldq <= 2^22 (FF_EUNSUPPORTED). */
 int ff_quantize_fp8(const void* x, int64_t ldx, uint8_t* q, int64_t ldq, float* d, int64_t rows, int64_t cols,
                     int32_t dtype, void* stream);
 

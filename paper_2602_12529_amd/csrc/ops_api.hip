@@ -158,6 +158,8 @@ int ff_skinny_linear(const float* in, const void* W, const void* bias, float* ou
   if (B == 0 || N == 0) return FF_OK;
   if (!in || !W || !out) return fail(FF_EINVAL, "%s: null pointer", fn);
   if (K % 8) return fail(FF_EUNSUPPORTED, "%s: K must be a multiple of 8", fn);
+  if (B > 65535 || N > kMaxOpRows || K > kMaxOpStride)
+    return fail(FF_EUNSUPPORTED, "%s: B above 65535, N above 2^27 or K above 2^22", fn);
   if (act_in < 0 || act_in > 2 || act_out < 0 || act_out > 2) return fail(FF_EINVAL, "%s: bad activation", fn);
   if (!aligned16(in) || !aligned16(W)) return fail(FF_EINVAL, "%s: pointers must be 16-byte aligned", fn);
   SkinnyArgs a{};
@@ -188,6 +190,8 @@ int ff_quantize_fp8(const void* x, int64_t ldx, uint8_t* q, int64_t ldq, float* 
   if (!x || !q || !d) return fail(FF_EINVAL, "%s: null x, q or d", fn);
   if (ldx < cols || ldq < cols) return fail(FF_EINVAL, "%s: ldx or ldq < cols", fn);
   if (cols % 8 || ldx % 8 || ldq % 8) return fail(FF_EUNSUPPORTED, "%s: cols, ldx and ldq must be multiples of 8", fn);
+  if (rows > kMaxOpRows || ldx > kMaxOpStride || ldq > kMaxOpStride)
+    return fail(FF_EUNSUPPORTED, "%s: rows above 2^27 or a row stride above 2^22", fn);
   if (!aligned16(x) || !aligned16(q)) return fail(FF_EINVAL, "%s: x and q must be 16-byte aligned", fn);
   return quantize_fp8(dtype, x, ldx, q, ldq, d, rows, cols, static_cast<hipStream_t>(stream));
 }

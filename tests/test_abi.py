@@ -289,6 +289,9 @@ def test_linear_and_attention_size_limits():
     _err(lib.ff_attention(f, f, f, f, 1, 1, 256, big + 8, 128, 1, None), _lib.FF_EUNSUPPORTED)
     _err(lib.ff_attention(f, f, f, f, 65535, 1024, 1 << 20, 64, 128, 1, None), _lib.FF_EUNSUPPORTED)
     _err(lib.ff_attention(f, f, f, f, 300, 300, 64, 64, 16, 0, None), _lib.FF_EUNSUPPORTED)
+    # GEMV batch and quantiser rows
+    _err(lib.ff_skinny_linear(f, f, None, f, 65536, 64, 64, 0, 0, 1, None, None), _lib.FF_EUNSUPPORTED)
+    _err(lib.ff_quantize_fp8(f, 64, f, 64, f, big + 1, 64, 1, None), _lib.FF_EUNSUPPORTED)
 
 
 def test_dit_entry_points_return_a_status_for_mutated_configs():
