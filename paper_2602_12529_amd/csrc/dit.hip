@@ -120,7 +120,7 @@ int check_config(const ff_dit_config* c) {
   if (c->head_dim % 2) return fail(FF_EINVAL, "ff_dit: head_dim must be even");
   for (int a = 0; a < 3; ++a)
     if (c->rope_axes[a] < 0 || c->rope_axes[a] % 2) return fail(FF_EINVAL, "ff_dit: rope axis widths must be even and >= 0");
-  if (c->rope_axes[0] + c->rope_axes[1] + c->rope_axes[2] != c->head_dim)
+  if (static_cast<int64_t>(c->rope_axes[0]) + c->rope_axes[1] + c->rope_axes[2] != c->head_dim)
     return fail(FF_EINVAL, "ff_dit: rope axes must sum to head_dim");
   if (!(c->rope_theta > 0) || !(c->norm_eps > 0)) return fail(FF_EINVAL, "ff_dit: rope_theta and norm_eps must be > 0");
   if (c->norm_kind != FF_NORM_RMS && c->norm_kind != FF_NORM_LN) return fail(FF_EINVAL, "ff_dit: bad norm_kind");

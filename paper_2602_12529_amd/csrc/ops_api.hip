@@ -98,6 +98,8 @@ int ff_norm_modulate(const void* x, void* y, int64_t rows, int64_t H, const floa
   FF_TRY(check_dtype(fn, dtype));
   if (rows < 0 || H < 1) return fail(FF_EINVAL, "%s: bad shape", fn);
   if (rows == 0) return FF_OK;
+  if (rows > kMaxOpRows || H > kMaxOpStride || mod_ld > kMaxOpStride)
+    return fail(FF_EUNSUPPORTED, "%s: rows above 2^27, or H or mod_ld above 2^22", fn);
   if (!x || !y) return fail(FF_EINVAL, "%s: null x or y", fn);
   if (norm_kind != FF_NORM_RMS && norm_kind != FF_NORM_LN) return fail(FF_EINVAL, "%s: bad norm_kind", fn);
   if (!(eps > 0.f)) return fail(FF_EINVAL, "%s: eps must be > 0", fn);
@@ -122,7 +124,8 @@ int ff_qk_norm_rope(const void* qkv, int64_t B, int64_t n_tok, int64_t heads, in
     return fail(FF_EINVAL, "%s: bad shape", fn);
   if (tok_offset < 0 || tok_offset + n_tok > n_joint) return fail(FF_EINVAL, "%s: tokens outside the joint sequence", fn);
   if (B == 0 || n_tok == 0) return FF_OK;
-  if (B > 65535 || heads > 65535) return fail(FF_EUNSUPPORTED, "%s: grid too large", fn);
+  if (B > 65535 || heads > 65535 || n_joint > kMaxOpRows || heads * head_dim > kMaxOpStride)
+    return fail(FF_EUNSUPPORTED, "%s: B or heads above 65535, n_joint above 2^27 or heads x head_dim above 2^22", fn);
   if (!qkv || !q_w || !k_w || !Q || !K || !V) return fail(FF_EINVAL, "%s: null pointer", fn);
   QkvArgs a{};
   a.dtype = dtype;
@@ -143,8 +146,11 @@ int ff_rope_table(float* out, const int32_t grid[3], int32_t head_dim, const int
   const char* fn = "ff_rope_table";
   if (!out || !grid || !axes) return fail(FF_EINVAL, "%s: null pointer", fn);
   if (grid[0] < 1 || grid[1] < 1 || grid[2] < 1) return fail(FF_EINVAL, "%s: bad grid", fn);
-  if (head_dim < 2 || head_dim % 2 || axes[0] + axes[1] + axes[2] != head_dim || axes[0] % 2 || axes[1] % 2 ||
-      axes[2] % 2 || axes[0] < 0 || axes[1] < 0 || axes[2] < 0)
+  const int64_t n01 = static_cast<int64_t>(grid[0]) * grid[1];   // both factors < 2^31: no overflow
+  if (n01 > kMaxOpRows || n01 * grid[2] > kMaxOpRows || head_dim > 1024)
+    return fail(FF_EUNSUPPORTED, "%s: more than 2^27 grid positions or head_dim above 1024", fn);
+  if (head_dim < 2 || head_dim % 2 || axes[0] % 2 || axes[1] % 2 || axes[2] % 2 || axes[0] < 0 || axes[1] < 0 ||
+      axes[2] < 0 || static_cast<int64_t>(axes[0]) + axes[1] + axes[2] != head_dim)
     return fail(FF_EINVAL, "%s: axes must be even and sum to head_dim", fn);
   if (!(theta > 0)) return fail(FF_EINVAL, "%s: theta must be > 0", fn);
   return rope_table(reinterpret_cast<float2*>(out), grid, head_dim, axes, theta, static_cast<hipStream_t>(stream));

@@ -289,6 +289,18 @@ def test_linear_and_attention_size_limits():
     _err(lib.ff_attention(f, f, f, f, 1, 1, 256, big + 8, 128, 1, None), _lib.FF_EUNSUPPORTED)
     _err(lib.ff_attention(f, f, f, f, 65535, 1024, 1 << 20, 64, 128, 1, None), _lib.FF_EUNSUPPORTED)
     _err(lib.ff_attention(f, f, f, f, 300, 300, 64, 64, 16, 0, None), _lib.FF_EUNSUPPORTED)
+    # norm rows, joint sequence length, rotation table positions; axis widths whose int32 sum would wrap
+    _err(lib.ff_norm_modulate(f, f, big + 1, 3072, None, None, 0, 0, 0, 1e-6, 1, None), _lib.FF_EUNSUPPORTED)
+    _err(lib.ff_qk_norm_rope(f, 1, 8, 1, 128, f, f, 1e-6, None, f, f, f, big + 8, 0, 1, None), _lib.FF_EUNSUPPORTED)
+    I3 = c_int32 * 3
+    _err(lib.ff_rope_table(f, I3(1 << 10, 1 << 10, 1 << 10), 128, I3(16, 56, 56), 1e4, None), _lib.FF_EUNSUPPORTED)
+    _err(lib.ff_rope_table(f, I3(2 ** 31 - 1, 2 ** 31 - 1, 2 ** 31 - 1), 128, I3(16, 56, 56), 1e4, None),
+         _lib.FF_EUNSUPPORTED)
+    _err(lib.ff_rope_table(f, I3(1, 8, 8), 8, I3(2 ** 31 - 2, 2 ** 31 - 2, 12), 1e4, None), _lib.FF_EINVAL)
+    n = c_int64()
+    cfg = api.dit_config(C.FLUX_BLOCK.model)
+    cfg.rope_axes[0], cfg.rope_axes[1], cfg.rope_axes[2] = 2 ** 31 - 2, 2 ** 31 - 2, 132
+    _err(lib.ff_dit_num_tensors(byref(cfg), byref(n)), _lib.FF_EINVAL)
     # GEMV batch and quantiser rows
     _err(lib.ff_skinny_linear(f, f, None, f, 65536, 64, 64, 0, 0, 1, None, None), _lib.FF_EUNSUPPORTED)
     _err(lib.ff_quantize_fp8(f, 64, f, 64, f, big + 1, 64, 1, None), _lib.FF_EUNSUPPORTED)
