@@ -55,7 +55,8 @@ int ff_attention(const void* Q, const void* K, const void* V, void* out, int64_t
 
 /* y = Norm(x) (1 + scale[b]) + shift[b] per row, b = row / rows_per_sample.
  * x, y [rows, H]; shift, scale float32 rows of stride mod_ld (either may be NULL);
- * norm_kind FF_NORM_RMS or FF_NORM_LN (no affine), statistics in float32. */
+ * norm_kind FF_NORM_RMS or FF_NORM_LN (no affine), statistics in float32.  rows <= 2^27, H and
+ * mod_ld <= 2^22 (FF_EUNSUPPORTED). */
 int ff_norm_modulate(const void* x, void* y, int64_t rows, int64_t H, const float* shift,
                      const float* scale, int64_t mod_ld, int64_t rows_per_sample, int32_t norm_kind,
                      float eps, int32_t dtype, void* stream);
@@ -65,13 +66,15 @@ int ff_norm_modulate(const void* x, void* y, int64_t rows, int64_t H, const floa
  *   qkv [B, n_tok, 3*heads*d] (Q | K | V per row);
  *   rope: float32 pairs [n_tok, d/2, 2] = (cos, sin), or NULL for no rotation;
  *   Q, K out [B, heads, n_joint, d] at token offset tok_offset;
- *   V out transposed [B, heads, d, n_joint] (bf16) or [B, heads, n_joint, d] (f32). */
+ *   V out transposed [B, heads, d, n_joint] (bf16) or [B, heads, n_joint, d] (f32).
+ * B, heads <= 65535, n_joint <= 2^27, heads d <= 2^22 (FF_EUNSUPPORTED). */
 int ff_qk_norm_rope(const void* qkv, int64_t B, int64_t n_tok, int64_t heads, int64_t head_dim,
                     const void* q_w, const void* k_w, float eps, const float* rope, void* Q, void* K,
                     void* V, int64_t n_joint, int64_t tok_offset, int32_t dtype, void* stream);
 
 /* RoPE (cos, sin) table for a (frames, rows, cols) grid: out float32 [N, d/2, 2],
- * pair i of band a turning by pos_a * theta^(-2i/axes[a]) (float64 math). */
+ * pair i of band a turning by pos_a * theta^(-2i/axes[a]) (float64 math).  At most 2^27 grid
+ * positions and head_dim <= 1024 (FF_EUNSUPPORTED). */
 int ff_rope_table(float* out, const int32_t grid[3], int32_t head_dim, const int32_t axes[3],
                   double theta, void* stream);
 
