@@ -138,7 +138,7 @@ int ff_philox4x32(uint32_t* out, int64_t n, uint64_t ctr_base, uint32_t c2, uint
  * are float64 and summed in sample order.  adv: device float32 [N].
  * group_count: device int32 [n_groups] receiving the group sizes, or NULL.
  * A sample whose group id is out of range gets adv = NaN and is counted in
- * no group.  Limits: 1 <= K <= 16, n_groups * K <= 4096 (FF_EUNSUPPORTED).
+ * no group.  Limits: 1 <= K <= 16, n_groups * K <= 4096, N <= 2^20 (FF_EUNSUPPORTED).
  * ------------------------------------------------------------------------ */
 int ff_group_advantage(const float* rewards, const float* weights, const int32_t* group_id,
                        int64_t N, int32_t K, int32_t n_groups, int32_t mode, float eps,

@@ -299,7 +299,8 @@ int ff_grpo_loss(const double* logp_new, const double* logp_old, const float* ad
                  int32_t S, double clip_eps, double* loss, int32_t* n_clipped, void* stream) {
   const char* fn = "ff_grpo_loss";
   if (B < 1 || S < 1) return fail(FF_EINVAL, "%s: need B >= 1 and S >= 1 (B=%lld S=%d)", fn, (long long)B, S);
-  if (static_cast<int64_t>(S) * B > 65536) return fail(FF_EUNSUPPORTED, "%s: S*B=%lld exceeds 65536", fn, (long long)(S * B));
+  if (B > 65536 || static_cast<int64_t>(S) * B > 65536)
+    return fail(FF_EUNSUPPORTED, "%s: S*B exceeds 65536 (B=%lld S=%d)", fn, (long long)B, S);
   if (!(clip_eps > 0.0) || !std::isfinite(clip_eps)) return fail(FF_EDOMAIN, "%s: clip_eps must be finite and > 0", fn);
   if (!logp_new || !logp_old || !adv || !loss) return fail(FF_EINVAL, "%s: null pointer", fn);
   hipStream_t s = static_cast<hipStream_t>(stream);

@@ -567,6 +567,7 @@ extern "C" int ff_group_advantage(const float* rewards, const float* weights, co
                                   int32_t* group_count, void* stream) {
   const char* fn = "ff_group_advantage";
   if (N < 0) return fail(FF_EINVAL, "%s: negative N", fn);
+  if (N > (int64_t(1) << 20)) return fail(FF_EUNSUPPORTED, "%s: N=%lld above 2^20 samples", fn, (long long)N);
   if (K < 1 || K > kAdvMaxK) return fail(FF_EUNSUPPORTED, "%s: K=%d outside [1, %d]", fn, K, kAdvMaxK);
   if (n_groups < 1) return fail(FF_EINVAL, "%s: n_groups=%d < 1", fn, n_groups);
   if (mode != 0 && mode != 1) return fail(FF_EINVAL, "%s: mode=%d", fn, mode);

@@ -153,6 +153,7 @@ def test_loss_argument_validation():
     _err(lib.ff_grpo_loss(f, f, f, None, 8, 3, float("nan"), f, None, None), _lib.FF_EDOMAIN)
     _err(lib.ff_grpo_loss(f, f, f, None, 0, 3, 0.2, f, None, None), _lib.FF_EINVAL)
     _err(lib.ff_grpo_loss(f, f, f, None, 40000, 3, 0.2, f, None, None), _lib.FF_EUNSUPPORTED)
+    _err(lib.ff_grpo_loss(f, f, f, None, 2 ** 62, 4, 0.2, f, None, None), _lib.FF_EUNSUPPORTED)   # S*B would wrap
     _err(lib.ff_grpo_loss(None, f, f, None, 8, 3, 0.2, f, None, None), _lib.FF_EINVAL)
 
 
@@ -195,6 +196,7 @@ def test_advantage_argument_validation():
     _err(lib.ff_group_advantage(f, f, f, 8, 2, 4097, 1, 1e-4, f, None, None), _lib.FF_EUNSUPPORTED)
     _err(lib.ff_group_advantage(None, f, f, 8, 1, 2, 0, 1e-4, f, None, None), _lib.FF_EINVAL)
     assert lib.ff_group_advantage(None, None, None, 0, 1, 2, 0, 1e-4, None, None, None) == 0
+    _err(lib.ff_group_advantage(f, f, f, (1 << 20) + 1, 1, 2, 0, 1e-4, f, None, None), _lib.FF_EUNSUPPORTED)
 
 
 @pytest.mark.parametrize("w", C.WORKLOADS, ids=lambda w: w.name)
