@@ -356,3 +356,48 @@ def test_missing_library_fails_loudly(tmp_path, monkeypatch):
         _lib.load()
     with pytest.raises(RuntimeError):
         api.profile_reset()
+
+
+def test_c_program_uses_the_library(tmp_path):
+    """The headers are plain C99 (checked with -pedantic) and a C program links libff.so and calls it:
+    version, a workspace size, a model's parameter count, and an error with its message."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    lib_dir = os.path.dirname(_lib.LIB_PATH)
+    src = tmp_path / "use_ff.c"
+    src.write_text(r"""
+#include <stdio.h>
+#include <string.h>
+#include "ff.h"
+#include "ff_ops.h"
+#include "ff_loss.h"
+int main(void) {
+  size_t ws = 0;
+  int64_t n = 0;
+  ff_dit_config c;
+  memset(&c, 0, sizeof c);
+  c.model = FF_MODEL_MMDIT; c.io_mode = FF_IO_HIDDEN; c.dtype = FF_BF16; c.n_dual = 2;
+  c.hidden = 3072; c.heads = 24; c.head_dim = 128; c.mlp_hidden = 12288;
+  c.norm_kind = FF_NORM_RMS; c.rope_axes[0] = 16; c.rope_axes[1] = 56; c.rope_axes[2] = 56;
+  c.rope_theta = 10000.0; c.norm_eps = 1e-6;
+  if (ff_sde_workspace_size(8, 1000, &ws) != FF_OK || ws == 0) return 1;
+  if (ff_dit_num_tensors(&c, &n) != FF_OK) return 2;
+  c.heads = 7;
+  if (ff_dit_num_tensors(&c, &n) != FF_EINVAL || strlen(ff_last_error()) == 0) return 3;
+  printf("%s %lld\n", ff_version(), (long long)n);
+  return 0;
+}
+""")
+    exe = tmp_path / "use_ff"
+    inc = os.path.join(root, "include")
+    r = subprocess.run([cc, "-std=c99", "-Wall", "-Wextra", "-pedantic", "-Werror", "-I", inc, str(src), "-o", str(exe),
+                        "-L", lib_dir, "-lff", "-Wl,-rpath," + lib_dir], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    out = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
+    assert out.returncode == 0, (out.returncode, out.stderr)
+    version, n = out.stdout.strip().rsplit(maxsplit=1)
+    assert version and int(n) == 2 * 2 * 12   # two dual blocks, two streams, twelve tensors per stream
