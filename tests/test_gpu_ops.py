@@ -126,6 +126,7 @@ ATT = [
     # B, heads, n_q (= n_kv), dtype, d
     (1, 1, 64, C.BF16, 128), (2, 3, 200, C.BF16, 128), (1, 2, 520, C.BF16, 128), (1, 2, 24, C.BF16, 128),
     (1, 4, 4608, C.BF16, 128), (2, 4, 24, C.F32, 16), (1, 2, 77, C.F32, 64),
+    (1, 2, 128, C.BF16, 128), (2, 2, 320, C.BF16, 128),   # 2 and 5 key tiles: the ring's last loads
 ]
 
 
